@@ -1,0 +1,80 @@
+"""Pins of the tile-order oracle: a hand-traced run of the interleave rule, exact
+coverage, phase order at large lead, and deadlock freedom under lock-step
+simulation."""
+import itertools
+
+import numpy as np
+import pytest
+
+from oracle import schedule as sc
+
+
+def test_interleave_hand_traced():
+    # G=1, P=2 rows, P1=2, P2=1, D=1, traced by hand from the rule
+    s = sc.interleave_stream(0, 1, P=2, P1=2, P2=1, D=1)
+    assert s == [(1, 0, 0), (1, 0, 1), (2, 0, 0), (1, 1, 2), (1, 1, 3), (2, 1, 1)]
+
+
+def test_interleave_two_instances_hand_traced():
+    # G=2, P=2, P1=2, P2=2, D=1: instance 0 owns L1 tiles 0,2 and L2 tiles 0,2.
+    # After L1 tile 0 its L1 cursor sits at tile 2 (row 1), one row ahead of L2 row 0.
+    s0 = sc.interleave_stream(0, 2, P=2, P1=2, P2=2, D=1)
+    assert s0 == [(1, 0, 0), (2, 0, 0), (1, 1, 2), (2, 1, 2)]
+    s1 = sc.interleave_stream(1, 2, P=2, P1=2, P2=2, D=1)
+    assert s1 == [(1, 0, 1), (2, 0, 1), (1, 1, 3), (2, 1, 3)]
+
+
+@pytest.mark.parametrize("policy", ["interleave", "chunk", "wave"])
+def test_every_tile_exactly_once(policy):
+    for G, P, P1, P2 in itertools.product([1, 3, 8], [1, 4, 9], [1, 4], [2, 7]):
+        waves = [(r, min(P, r + 2)) for r in range(0, P, 2)]
+        st = sc.all_streams(policy, G, P, P1, P2, D=2, chunk=2, waves=waves)
+        l1 = sorted(k for s in st for (kind, _, k) in s if kind == 1)
+        l2 = sorted(k for s in st for (kind, _, k) in s if kind == 2)
+        assert l1 == list(range(P * P1)) and l2 == list(range(P * P2))
+        for s in st:
+            for kind, row, k in s:
+                assert row == k // (P1 if kind == 1 else P2)
+
+
+def test_large_lead_gives_phase_order():
+    for g in range(4):
+        s = sc.interleave_stream(g, 4, P=6, P1=3, P2=5, D=6)
+        kinds = [t[0] for t in s]
+        assert kinds == sorted(kinds)
+
+
+def test_chunk_caps_consecutive_l2():
+    s = sc.interleave_stream(0, 1, P=8, P1=1, P2=6, D=1, chunk=2)
+    run = 0
+    l1_left = 8
+    for kind, _, _ in s:
+        if kind == 2:
+            run += 1
+            assert run <= 2 or l1_left == 0
+        else:
+            run = 0
+            l1_left -= 1
+
+
+def test_no_deadlock_with_positive_lead():
+    rng = np.random.default_rng(0)
+    for _ in range(150):
+        G = int(rng.integers(1, 12))
+        P = int(rng.integers(1, 12))
+        P1, P2 = int(rng.integers(1, 6)), int(rng.integers(1, 6))
+        D = int(rng.integers(1, 4))
+        for policy in ("interleave", "chunk"):
+            sc.simulate(sc.all_streams(policy, G, P, P1, P2, D=D, chunk=1), P, P1)
+        waves = sc.waves_by_tiles(list(range(P)), P1, int(rng.integers(1, 8)))
+        sc.simulate(sc.all_streams("wave", G, P, P1, P2, waves=waves), P, P1)
+
+
+def test_zero_lead_can_deadlock():
+    with pytest.raises(RuntimeError):
+        sc.simulate(sc.all_streams("interleave", 1, 2, 2, 1, D=0), 2, 2)
+
+
+def test_waves_by_tiles_whole_experts():
+    row_expert = [0, 0, 1, 2, 2, 2, 3]
+    assert sc.waves_by_tiles(row_expert, P1=2, min_tiles=4) == [(0, 2), (2, 6), (6, 7)]
