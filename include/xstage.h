@@ -1,0 +1,352 @@
+/*
+ * xstage.h — C ABI of the MI355X (gfx950) fused store-path library.
+ *
+ * The library implements, at one GPU's share, the communication–computation fusion
+ * studied in "X-Stage: Modeling Post-Issue Backpressure in GPU Communication–Computation
+ * Fusion": a compute pipeline that issues one-sided stores into per-destination windows.
+ *   - expert parallelism (Sec. 4.3, Sec. 5.3): route -> dispatch -> local-expert SwiGLU
+ *     grouped GEMM -> combine-send stores (the Linear-2 epilogue bursts) -> combine-reduce;
+ *   - tensor parallelism (Sec. 4.5): GEMM whose output row blocks are stored into
+ *     per-destination windows as tiles complete;
+ *   - Ulysses sequence parallelism (Sec. 5.4, GEMM-All-to-All): QKV projection whose
+ *     epilogue stores head groups into per-destination windows;
+ *   - store pacing: the tile order of the persistent EP kernel (Expert-Wave, cross-wave
+ *     interleaving of Alg. 1, chunked bursts) and the Burst-Gap model of Sec. 3
+ *     (Eqs. 1-6) with its calibration microbenchmark (Sec. 3.1).
+ *
+ * Conventions (every entry point):
+ *   - Pointers named "device" point to GPU memory (hipMalloc / torch CUDA tensors) or, for
+ *     windows, to fine-grained host-coherent memory (hipHostMalloc coherent). Host pointers
+ *     are marked "host". bf16 tensors are passed as void* (16-bit storage, row-major).
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream). Every call is
+ *     asynchronous on that stream; it only enqueues work.
+ *   - Ownership: the caller owns every buffer; the library only borrows pointers for the
+ *     stream-ordered duration of the call and never allocates on these calls. Scratch is
+ *     passed in as `workspace` (size from the matching *_workspace_bytes query).
+ *   - Errors: the return value reports argument problems synchronously (XS_EINVAL,
+ *     XS_EUNSUPPORTED, XS_EWORKSPACE) and launch failures (XS_EHIP). Data-dependent errors
+ *     (a window over capacity, a bad expert id, a dependency wait that timed out) are
+ *     written to the caller's device word `dev_status` (first error wins, via atomic
+ *     compare-and-swap from 0). The library never clears `dev_status`: zero it before the
+ *     first call. No exception crosses the ABI and the library prints nothing.
+ *   - Calls on one stream are ordered; calls on different streams that share buffers race.
+ */
+#ifndef XSTAGE_H
+#define XSTAGE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ----------------------------------------------------------------------------- status */
+enum {
+  XS_OK = 0,
+  XS_EINVAL = 1,        /* bad argument (null pointer, k > E, E % W != 0, ...) */
+  XS_EUNSUPPORTED = 2,  /* valid but not implemented (e.g. H not a multiple of 256) */
+  XS_EHIP = 3,          /* a HIP launch or runtime call failed */
+  XS_EWORKSPACE = 4,    /* workspace missing or too small */
+  XS_ECAPACITY = 5,     /* device: a window received more rows than capacity_rows */
+  XS_ETIMEOUT = 6,      /* device: a bounded dependency wait expired */
+  XS_EBADINPUT = 7      /* device: an expert id outside [0, E) */
+};
+
+/* Text for a status code (static storage; never NULL). */
+const char* xs_strerror(int code);
+/* Library version, major * 10000 + minor * 100 + patch. */
+int xs_version(void);
+
+/* ----------------------------------------------------------------------------- windows
+ * A destination window (Sec. 2.1: the memory a one-sided store lands in). On one GPU a
+ * "remote" window is a buffer in local HBM, or in host-coherent memory for a slow sink.
+ * Row r starts at base + r * row_stride_bytes. row_stride_bytes must be a multiple of 16
+ * and at least the row size in bytes. If ready_flag is non-NULL, the call that stores into
+ * the window sets *ready_flag = 1 after its last store, behind a release fence at system
+ * scope (consumer readiness, Sec. 2.1; sender progress alone is not readiness). */
+typedef struct xs_window {
+  void* base;
+  int64_t capacity_rows;
+  int64_t row_stride_bytes;
+  uint32_t* ready_flag;
+} xs_window;
+
+#define XS_MAX_WINDOWS 64
+
+/* ----------------------------------------------------------------------------- routing
+ * Top-k softmax gating (routing is fixed by the model and unchanged by the method:
+ * Related Work, "MoE communication").
+ *   logits   device fp32 [T][E], finite.
+ *   topk_idx device int32 [T][k] out: the k largest logits in descending order, ties to
+ *            the lower expert index (selection is exact on the fp32 logits).
+ *   topk_w   device fp32 [T][k] out: softmax over all E experts taken at topk_idx; with
+ *            renormalize != 0 divided by the sum of the k weights.
+ * Requires 1 <= k <= min(E, 32), E <= 1024. */
+int xs_route_topk_softmax(const float* logits, int32_t T, int32_t E, int32_t k,
+                          int32_t renormalize, int32_t* topk_idx, float* topk_w, void* stream);
+
+/* ----------------------------------------------------------------------------- layout
+ * Destination-window layout of every (source, token, slot) (the Dispatch exchange,
+ * Sec. 2.2 and Sec. 4.3: expert-parallel tokens go to the ranks owning their experts).
+ * Expert e lives in window d(e) = e / (E / W). Rows of window d are the slots routed to
+ * its experts ordered by (expert, source, token), unpadded, one row per slot.
+ *   topk_idx       device int32 [n_src][T][k]
+ *   expert_counts  device int32 [n_src][E] out: slots of source s routed to expert e
+ *   src_base       device int32 [n_src][E] out: rows of expert e from sources < s
+ *   expert_offsets device int32 [E] out: first row of expert e inside window d(e)
+ *   dest_counts    device int32 [W] out: rows per window (may exceed cap: XS_ECAPACITY)
+ *   slot_row       device int32 [n_src][T][k] out: row of each slot inside its window
+ *   row_src        device int32 [W][cap] out: inverse map, (src << 24) | (t * k + j), for
+ *                  rows < cap (rows at or beyond cap are not recorded)
+ *   workspace      device, xs_dispatch_layout_workspace_bytes() bytes
+ * Requires E % W == 0, E <= 1024, W <= XS_MAX_WINDOWS, n_src <= 127, T * k < 2^24. */
+int xs_dispatch_layout_workspace_bytes(int32_t n_src, int32_t T, int32_t E, int64_t* bytes);
+int xs_dispatch_layout(const int32_t* topk_idx, int32_t n_src, int32_t T, int32_t k, int32_t E,
+                       int32_t W, int32_t cap, int32_t* expert_counts, int32_t* src_base,
+                       int32_t* expert_offsets, int32_t* dest_counts, int32_t* slot_row,
+                       int32_t* row_src, void* workspace, int64_t workspace_bytes,
+                       int32_t* dev_status, void* stream);
+
+/* ----------------------------------------------------------------------------- dispatch
+ * Store one source's token rows into the destination windows (one-sided stores, Sec. 2.1):
+ * window d(topk_idx[t][j]) row slot_row[t][j] <- x[t], a bit-exact bf16 copy of H values.
+ *   x        device bf16 [T][H] (row-major, rows contiguous)
+ *   topk_idx, slot_row  device int32 [T][k] of this source (a slice of the layout outputs)
+ *   win      host array of W windows (capacity_rows >= largest row + 1, else XS_ECAPACITY
+ *            and the row is skipped)
+ * Requires H % 8 == 0 (128-bit stores). */
+int xs_dispatch(const void* x, int32_t T, int32_t H, const int32_t* topk_idx,
+                const int32_t* slot_row, int32_t k, int32_t E, const xs_window* win, int32_t W,
+                int32_t* dev_status, void* stream);
+
+/* ----------------------------------------------------------------------------- EP layer
+ * One rank's share of an expert-parallel MoE layer (Sec. 4.3). Experts
+ * [e_begin, e_begin + n_experts) are computed here; they must be whole windows
+ * (e_begin and n_experts multiples of E / W). "This GPU" is source rank `src`: its
+ * tokens are dispatched and its output is reduced; routing and layout cover all n_src
+ * sources (standing in for the count exchange between ranks).
+ * Expert FFN (SwiGLU): h = bf16(silu(x Wg^T) * (x Wu^T)), y = bf16(h W2^T), fp32
+ * accumulation; W1 rows [0, I) are the gate Wg and rows [I, 2I) the up projection Wu. */
+typedef struct xs_ep_layer {
+  int32_t n_src, T, H, E, k, I, W;
+  int32_t e_begin, n_experts;
+  int32_t src;
+  int32_t renormalize;
+  int32_t expert_mode;        /* XS_EXPERT_SWIGLU, or XS_EXPERT_IDENTITY (y = x) */
+  int32_t cap;                /* capacity_rows of every dispatch window */
+  const float* logits;        /* device fp32 [n_src][T][E] */
+  const void* x;              /* device bf16 [T][H], tokens of source `src` */
+  const void* w1;             /* device bf16 [n_experts][2I][H] */
+  const void* w2;             /* device bf16 [n_experts][H][I] */
+  int32_t* topk_idx;          /* device int32 [n_src][T][k] (out of route, in to layout) */
+  float* topk_w;              /* device fp32  [n_src][T][k] */
+  int32_t* expert_counts;     /* device int32 [n_src][E] */
+  int32_t* src_base;          /* device int32 [n_src][E] */
+  int32_t* expert_offsets;    /* device int32 [E] */
+  int32_t* dest_counts;       /* device int32 [W] */
+  int32_t* slot_row;          /* device int32 [n_src][T][k] */
+  int32_t* row_src;           /* device int32 [W][cap] */
+  const xs_window* dispatch_win; /* host array [W]; rows of H bf16 */
+  const xs_window* combine_win;  /* host array [n_src]; window s holds [T*k] rows of H bf16 */
+  void* h_ws;                 /* device bf16 [h_rows][I], SwiGLU activations */
+  int64_t h_rows;             /* >= (n_experts / (E / W)) * cap */
+  void* y_ws;                 /* device bf16 [h_rows][H]; only used by the unfused path */
+  void* out;                  /* device bf16 [T][H], combined output of source `src` */
+} xs_ep_layer;
+
+enum { XS_EXPERT_SWIGLU = 0, XS_EXPERT_IDENTITY = 1 };
+
+/* Store pacing of the persistent EP kernel: the order of Linear-1 / Linear-2 tiles.
+ *   XS_POLICY_BURST      Expert-Wave (Sec. 4.3): per wave of experts, all Linear-1 tiles
+ *                        then all Linear-2 tiles (whose epilogues are the store bursts).
+ *   XS_POLICY_INTERLEAVE cross-wave interleaving (App. A.2, Alg. 1) with lead D =
+ *                        lead_rows >= 1 rows of Linear-1 over Linear-2.
+ *   XS_POLICY_CHUNK      Alg. 1 with at most chunk_tiles consecutive Linear-2 tiles before
+ *                        a ready Linear-1 tile is forced.
+ *   XS_POLICY_AUTO       CHUNK with chunk_tiles chosen from `model`: the largest run of
+ *                        aligned Linear-2 bursts per Linear-1 tile that meets the
+ *                        average-rate bound (Eq. 9) for full alignment of the producers
+ *                        (Sec. 4.2); INTERLEAVE when the bursts never outrun the drain or
+ *                        without a model.
+ * max_producers caps the persistent grid (0 = one workgroup per CU); wave_tiles is the
+ * minimum Linear-1 tile count of an expert wave (0 = the grid size); gap_ns inserts a
+ * non-injecting wait of that many nanoseconds after every Linear-2 store burst.
+ * Every policy computes the same tiles and stores the same bytes; outputs are
+ * bit-identical across policies. */
+enum { XS_POLICY_BURST = 0, XS_POLICY_INTERLEAVE = 1, XS_POLICY_CHUNK = 2, XS_POLICY_AUTO = 3 };
+
+struct xs_model;
+typedef struct xs_pacing {
+  int32_t policy;
+  int32_t lead_rows;
+  int32_t chunk_tiles;
+  int32_t max_producers;
+  int32_t wave_tiles;
+  int32_t gap_ns;
+  int32_t spin_timeout_us;        /* bound of each dependency wait; 0 = 2 s */
+  int32_t withhold_row;           /* failure-path hook: this row never signals Linear-1
+                                     completion, so its Linear-2 waits expire (-1 = none) */
+  double t_l1_us, t_l2_us;        /* AUTO: mainloop time of one Linear-1 / Linear-2 tile;
+                                     0 = estimate from the tile FLOPs */
+  const struct xs_model* model;   /* host, for XS_POLICY_AUTO; may be NULL */
+} xs_pacing;
+
+/* Optional device trace of the persistent kernels: one 32-byte record per tile,
+ *   rec[0] = kind << 56 | workgroup << 32 | tile index  (kind 1 = Linear-1, 2 = Linear-2,
+ *            3 = plain / scatter GEMM tile)
+ *   rec[1] = wall clock (s_memrealtime ticks, xs_clock_rate_hz) at tile start
+ *   rec[2] = wall clock when the mainloop finished (epilogue starts)
+ *   rec[3] = wall clock after the last store of the epilogue was issued (sender-visible
+ *            issue end: the stores are accepted, not necessarily visible)
+ * records are appended at atomicAdd(count, 1); records past `capacity` are dropped but
+ * still counted. buf and count are device memory; the caller zeroes *count. */
+typedef struct xs_trace {
+  uint64_t* buf;
+  int64_t capacity;
+  uint32_t* count;
+} xs_trace;
+
+/* Workspace of the EP calls below (layout scratch, tile tables, readiness counters). */
+int xs_ep_layer_workspace_bytes(const xs_ep_layer* L, int64_t* bytes);
+
+/* Expert FFN of the computed experts, unfused: Linear-1 + SwiGLU into h_ws, then Linear-2
+ * into y_ws, both indexed by "computed row" (window d_first's rows, then the next
+ * window's, ...). Reads the layout outputs of L. */
+int xs_expert_ffn(const xs_ep_layer* L, void* workspace, int64_t workspace_bytes,
+                  int32_t* dev_status, void* stream);
+
+/* Combine-send (the Combine exchange, Sec. 4.3): computed row r of window d goes to
+ * combine window s at row t*k+j where row_src[d][r] = (s << 24) | (t*k+j). Unfused form of
+ * the Linear-2 epilogue stores; reads y_ws. */
+int xs_combine_send(const xs_ep_layer* L, int32_t* dev_status, void* stream);
+
+/* Combine-reduce: out[t] = bf16(sum_{j<k} w[t][j] * C[t*k + j]), fp32 sum in ascending j.
+ *   cbuf device bf16 [T*k][H] (row stride cbuf_stride_bytes), topk_w device fp32 [T][k],
+ *   out device bf16 [T][H]. Requires H % 8 == 0. */
+int xs_combine_reduce(const void* cbuf, int64_t cbuf_stride_bytes, const float* topk_w,
+                      int32_t T, int32_t k, int32_t H, void* out, void* stream);
+
+/* The whole layer: route (all sources) -> layout -> dispatch (source src) -> persistent
+ * Linear-1 / Linear-2 kernel whose Linear-2 epilogue stores straight into the combine
+ * windows, in the order set by `pacing` -> combine-reduce of source src. `trace` may be
+ * NULL. Linear-2 tiles wait on per-row Linear-1 completion counters with a bounded spin
+ * (XS_ETIMEOUT in dev_status if it expires; the kernel then skips the tile and exits). */
+int xs_fused_ep_layer(const xs_ep_layer* L, const xs_pacing* pacing, const xs_trace* trace,
+                      void* workspace, int64_t workspace_bytes, int32_t* dev_status,
+                      void* stream);
+
+/* ----------------------------------------------------------------------------- GEMM
+ * C = A B^T with bf16 operands and fp32 accumulation, bf16 output.
+ *   a  device bf16 [M][K] (row stride lda elements), b device bf16 [N][K] (row stride ldb;
+ *      the weight's output-major layout), c device bf16 [M][N] (row stride ldc).
+ * Requires N % 256 == 0, K % 64 == 0, strides multiples of 8. */
+int xs_gemm(const void* a, int64_t lda, const void* b, int64_t ldb, void* c, int64_t ldc,
+            int32_t M, int32_t N, int32_t K, const xs_trace* trace, void* stream);
+
+/* GEMM with a scatter epilogue: every output tile is stored on completion into the
+ * destination windows (no separate permutation pass).
+ *   XS_SCATTER_ROW_BLOCK  (Sec. 4.5, row-parallel TP): output row m goes to window
+ *                         m / rows_per_dest, row m % rows_per_dest (N values per row).
+ *   XS_SCATTER_HEAD_GROUP (Sec. 5.4, Ulysses GEMM-All-to-All): column c of the
+ *                         [n_proj * n_heads * head_dim] output is (p, head, dd) with
+ *                         p = c / (n_heads*head_dim), head = (c / head_dim) % n_heads,
+ *                         dd = c % head_dim; it goes to window g = head / heads_per_group
+ *                         at element ((p * heads_per_group + head % heads_per_group) * M + m)
+ *                         * head_dim + dd, i.e. window g is [n_proj][hpg][M][head_dim]
+ *                         (row_stride_bytes = head_dim * 2).
+ * Requires M % rows_per_dest == 0 and rows_per_dest % 256 == 0 (ROW_BLOCK); head_dim % 8 == 0
+ * (HEAD_GROUP). Window capacity_rows must cover rows_per_dest (ROW_BLOCK) or
+ * n_proj * heads_per_group * M (HEAD_GROUP). */
+enum { XS_SCATTER_ROW_BLOCK = 0, XS_SCATTER_HEAD_GROUP = 1 };
+typedef struct xs_scatter_desc {
+  int32_t kind;
+  int32_t rows_per_dest;
+  int32_t n_proj, n_heads, head_dim, heads_per_group;
+} xs_scatter_desc;
+
+int xs_gemm_scatter(const void* a, int64_t lda, const void* b, int64_t ldb, int32_t M, int32_t N,
+                    int32_t K, const xs_scatter_desc* desc, const xs_window* win, int32_t W,
+                    const xs_trace* trace, void* stream);
+
+/* Serial counterpart of xs_gemm_scatter: a separate permutation pass that copies a plain
+ * GEMM output c [M][N] into the windows with the same mapping (the "permutation before the
+ * All-to-All" that fusion removes, Sec. 5.4). */
+int xs_scatter_copy(const void* c, int64_t ldc, int32_t M, int32_t N, const xs_scatter_desc* desc,
+                    const xs_window* win, int32_t W, void* stream);
+
+/* ----------------------------------------------------------------------------- X-Stage
+ * Burst-Gap model (Sec. 3.3-3.5). Units: bytes and microseconds.
+ *   T0(V) = t0_a_us + t0_b_us_per_byte * V   recovered issue floor at K producers
+ *   R_bytes_per_us                           effective aggregate drain rate
+ *   Q_bytes                                  effective outstanding capacity (inf allowed) */
+typedef struct xs_model {
+  double t0_a_us;
+  double t0_b_us_per_byte;
+  double R_bytes_per_us;
+  double Q_bytes;
+  int32_t K;
+  int32_t _pad;
+} xs_model;
+
+typedef struct xs_burst { double V_bytes, T0_us, G_us; } xs_burst;
+
+/* Per-burst audit: rho and delta_b (Eqs. 3-4), backlog before the burst, b_iso and the
+ * capacity guard (Eq. 6), and the predicted issue time: T0 while the guard holds, else
+ * (q + V - Q) / R (a fluid queue capped at Q); the backlog then follows
+ * q' = [q + V - R (T_iss + G)]_+, which is Eq. 5 whenever the guard holds. */
+typedef struct xs_burst_pred {
+  double rho, delta_b, q_before, b_iso, T_iss_us, stall_us;
+  int32_t guard_ok;
+  int32_t _pad;
+} xs_burst_pred;
+
+/* Host-only, synchronous. q0 is the backlog before the first burst. */
+int xs_model_predict(const xs_model* m, const xs_burst* bursts, int32_t n, double q0,
+                     xs_burst_pred* out);
+
+/* Calibration points (host arrays): recovered large-gap issue times, zero-gap periodic
+ * periods, isolated-burst issue times, each against the aggregate volume V (Sec. 3.3).
+ * T0 is a least-squares line, R the through-origin slope of period vs V, and Q the median
+ * of V - R T_iss over isolated bursts whose issue exceeds T0(V) by more than knee_excess
+ * (relative): the knee where the floor meets the stalled branch (Sec. 3.5). */
+typedef struct xs_calib {
+  const double* rec_V; const double* rec_T; int32_t n_rec;
+  const double* zg_V; const double* zg_T; int32_t n_zg;
+  const double* iso_V; const double* iso_T; int32_t n_iso;
+  int32_t K;
+  double knee_excess;
+} xs_calib;
+
+int xs_model_fit(const xs_calib* c, xs_model* out);
+
+/* Remote-store microbenchmark (Sec. 3.1): K producer workgroups each store B bytes per
+ * burst into `target` (HBM window or host-coherent sink), separated by a non-injecting
+ * gap of gap_ns nanoseconds; n_bursts bursts per producer.
+ *   mode XS_MB_PERIODIC   bursts back to back with the gap in between
+ *   mode XS_MB_COMPLETION after each burst the producer waits for its stores to complete
+ *                         (the completion-coupled counterfactual) before the gap
+ * Each producer writes one record per burst into trace->buf: [0] = producer << 32 | burst,
+ * [1] = clock at burst start, [2] = clock after the last store was issued, [3] = clock
+ * after the gap. Clocks are wall-clock ticks; xs_clock_rate_hz() converts.
+ * Producer p writes bytes [p * B * n_bursts ...) of target, wrapping at target_bytes. */
+enum { XS_MB_PERIODIC = 0, XS_MB_COMPLETION = 1 };
+typedef struct xs_microbench_args {
+  void* target;
+  int64_t target_bytes;
+  int32_t K;
+  int32_t B_bytes;        /* multiple of 1024 */
+  int32_t n_bursts;
+  int32_t gap_ns;
+  int32_t mode;
+  int32_t store_waves;    /* waves per producer issuing the stores (1..4) */
+} xs_microbench_args;
+
+int xs_xstage_microbench(const xs_microbench_args* args, const xs_trace* trace, void* stream);
+
+/* Frequency of the wall clock used by trace records (Hz), from the current device. */
+double xs_clock_rate_hz(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* XSTAGE_H */

@@ -1,0 +1,444 @@
+// Expert-parallel routing, dispatch layout, dispatch stores and combine-reduce.
+//
+// Routing: one wavefront per token; top-k by repeated wave arg-max over the fp32 logits
+// (ties to the lower expert index) and a softmax over all E experts.
+// Layout: per 256-token chunk, every wave builds a 64-bit lane mask per expert in LDS
+// (ds_or_b64), so a slot's rank among earlier tokens of the chunk routed to the same expert
+// is a popcount: a deterministic, stable slot assignment. Chunk counts are scanned per
+// source, then across sources and across the experts of each window.
+// Dispatch: one wavefront per token row; every lane holds 16-byte pieces of the row in
+// registers and stores them, 128-bit and coalesced, into the k destination rows. A row is
+// contiguous on both sides, so no LDS staging is needed to coalesce.
+#include "xs_common.hpp"
+
+namespace xs {
+
+// ------------------------------------------------------------------------------ route
+template <int EPL>
+__global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict__ logits, int T,
+                                                         int E, int k, int renorm,
+                                                         int* __restrict__ topk_idx,
+                                                         float* __restrict__ topk_w) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const float* row = logits + static_cast<int64_t>(t) * E;
+  float v[EPL];
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    int e = i * 64 + lane;
+    v[i] = e < E ? row[e] : -INFINITY;
+  }
+  // softmax denominator over all experts: lane partials in ascending i, then a butterfly
+  float m = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) m = fmaxf(m, v[i]);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < EPL; ++i)
+    if (i * 64 + lane < E) s += expf(v[i] - m);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+
+  uint32_t taken = 0;
+  int my_idx = 0;
+  float my_w = 0.f;
+  for (int j = 0; j < k; ++j) {
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      int e = i * 64 + lane;
+      bool ok = e < E && !((taken >> i) & 1u);
+      if (ok && (v[i] > bv || (v[i] == bv && e < bi))) {
+        bv = v[i];
+        bi = e;
+      }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      float ov = __shfl_xor(bv, off);
+      int oi = __shfl_xor(bi, off);
+      if (ov > bv || (ov == bv && oi < bi)) {
+        bv = ov;
+        bi = oi;
+      }
+    }
+    if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
+    if (lane == j) {
+      my_idx = bi;
+      my_w = expf(bv - m) / s;
+    }
+  }
+  if (renorm) {
+    float ws = lane < k ? my_w : 0.f;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) ws += __shfl_xor(ws, off);
+    my_w = my_w / ws;
+  }
+  if (lane < k) {
+    topk_idx[static_cast<int64_t>(t) * k + lane] = my_idx;
+    topk_w[static_cast<int64_t>(t) * k + lane] = my_w;
+  }
+}
+
+// ------------------------------------------------------------------------------ layout
+constexpr int kChunk = 256;   // tokens per layout chunk (4 waves)
+
+// Per chunk: stable rank of each slot among the chunk's earlier slots of the same expert
+// (written to slot_row as a partial value) and per-expert chunk counts.
+__global__ __launch_bounds__(256) void layout_chunk_kernel(const int* __restrict__ idx, int T,
+                                                           int k, int E, int n_chunks,
+                                                           int* __restrict__ slot_row,
+                                                           int* __restrict__ chunk_cnt,
+                                                           int* status) {
+  extern __shared__ unsigned long long masks[];   // [4][E]
+  const int s = blockIdx.y, c = blockIdx.x, tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
+  for (int i = tid; i < 4 * E; i += 256) masks[i] = 0ull;
+  __syncthreads();
+  const int t = c * kChunk + tid;
+  const int64_t base = (static_cast<int64_t>(s) * T + t) * k;
+  const unsigned long long bit = 1ull << lane;
+  if (t < T) {
+    for (int j = 0; j < k; ++j) {
+      int e = idx[base + j];
+      if (e >= 0 && e < E) atomicOr(&masks[w * E + e], bit);
+      else set_status(status, XS_EBADINPUT);
+    }
+  }
+  __syncthreads();
+  if (t < T) {
+    const unsigned long long below = bit - 1ull;
+    for (int j = 0; j < k; ++j) {
+      int e = idx[base + j];
+      if (e < 0 || e >= E) continue;
+      int r = __popcll(masks[w * E + e] & below);
+      for (int ww = 0; ww < w; ++ww) r += __popcll(masks[ww * E + e]);
+      slot_row[base + j] = r;
+    }
+  }
+  for (int e = tid; e < E; e += 256) {
+    int n = 0;
+    for (int ww = 0; ww < 4; ++ww) n += __popcll(masks[ww * E + e]);
+    chunk_cnt[(static_cast<int64_t>(s) * n_chunks + c) * E + e] = n;
+  }
+}
+
+// Per source: exclusive scan of the chunk counts of every expert, and source totals.
+__global__ __launch_bounds__(1024) void layout_source_scan_kernel(int* __restrict__ chunk_cnt,
+                                                                  int n_chunks, int E,
+                                                                  int* __restrict__ expert_counts) {
+  const int s = blockIdx.x;
+  for (int e = threadIdx.x; e < E; e += blockDim.x) {
+    int* col = chunk_cnt + static_cast<int64_t>(s) * n_chunks * E + e;
+    int run = 0;
+    int c = 0;
+    for (; c + 8 <= n_chunks; c += 8) {
+      int v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = col[static_cast<int64_t>(c + u) * E];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        col[static_cast<int64_t>(c + u) * E] = run;
+        run += v[u];
+      }
+    }
+    for (; c < n_chunks; ++c) {
+      int v = col[static_cast<int64_t>(c) * E];
+      col[static_cast<int64_t>(c) * E] = run;
+      run += v;
+    }
+    expert_counts[static_cast<int64_t>(s) * E + e] = run;
+  }
+}
+
+// Across sources and experts: src_base, expert_offsets (exclusive scan of expert totals
+// within each window), dest_counts and the capacity check.
+__global__ __launch_bounds__(1024) void layout_global_scan_kernel(
+    const int* __restrict__ expert_counts, int n_src, int E, int W, int cap,
+    int* __restrict__ src_base, int* __restrict__ expert_offsets, int* __restrict__ dest_counts,
+    int* status) {
+  __shared__ int tot[1024];
+  for (int e = threadIdx.x; e < E; e += blockDim.x) {
+    int run = 0;
+    for (int s = 0; s < n_src; ++s) {
+      src_base[static_cast<int64_t>(s) * E + e] = run;
+      run += expert_counts[static_cast<int64_t>(s) * E + e];
+    }
+    tot[e] = run;
+  }
+  __syncthreads();
+  const int epw = E / W;
+  for (int e = threadIdx.x; e < E; e += blockDim.x) {
+    int d0 = (e / epw) * epw, off = 0;
+    for (int x = d0; x < e; ++x) off += tot[x];
+    expert_offsets[e] = off;
+  }
+  for (int d = threadIdx.x; d < W; d += blockDim.x) {
+    int n = 0;
+    for (int x = d * epw; x < (d + 1) * epw; ++x) n += tot[x];
+    dest_counts[d] = n;
+    if (n > cap) set_status(status, XS_ECAPACITY);
+  }
+}
+
+// Every slot: final row = expert offset + source base + chunk base + rank in chunk;
+// records the inverse map for rows inside the capacity.
+__global__ __launch_bounds__(256) void layout_finalize_kernel(
+    const int* __restrict__ idx, int n_src, int T, int k, int E, int W, int cap, int n_chunks,
+    const int* __restrict__ chunk_base, const int* __restrict__ src_base,
+    const int* __restrict__ expert_offsets, int* __restrict__ slot_row, int* __restrict__ row_src) {
+  const int64_t n = static_cast<int64_t>(n_src) * T * k;
+  const int epw = E / W;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    int e = idx[i];
+    if (e < 0 || e >= E) continue;
+    int64_t st = i / k;
+    int j = static_cast<int>(i - st * k);
+    int s = static_cast<int>(st / T);
+    int t = static_cast<int>(st - static_cast<int64_t>(s) * T);
+    int c = t / kChunk;
+    int r = expert_offsets[e] + src_base[static_cast<int64_t>(s) * E + e] +
+            chunk_base[(static_cast<int64_t>(s) * n_chunks + c) * E + e] + slot_row[i];
+    slot_row[i] = r;
+    if (r < cap) row_src[static_cast<int64_t>(e / epw) * cap + r] = (s << 24) | (t * k + j);
+  }
+}
+
+// ------------------------------------------------------------------------------ dispatch
+// One wave per token. Lanes hold up to 8 16-byte pieces of the row per round.
+__global__ __launch_bounds__(256) void dispatch_kernel(const uint16_t* __restrict__ x, int T, int H,
+                                                       const int* __restrict__ idx,
+                                                       const int* __restrict__ slot_row, int k,
+                                                       int E, WinSet win, int* status) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const int epw = E / win.n;
+  // lane j < k resolves destination j; broadcast below with readlane
+  char* my_dst = nullptr;
+  if (lane < k) {
+    int e = idx[static_cast<int64_t>(t) * k + lane];
+    int r = slot_row[static_cast<int64_t>(t) * k + lane];
+    if (e < 0 || e >= E) {
+      set_status(status, XS_EBADINPUT);
+    } else {
+      int d = e / epw;
+      if (r < 0 || r >= win.cap[d]) set_status(status, XS_ECAPACITY);
+      else my_dst = win.base[d] + static_cast<int64_t>(r) * win.stride[d];
+    }
+  }
+  const u32x4* src = reinterpret_cast<const u32x4*>(x + static_cast<int64_t>(t) * H);
+  const int nch = H >> 3;
+  for (int c0 = 0; c0 < nch; c0 += 64 * 8) {
+    u32x4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      int c = c0 + u * 64 + lane;
+      if (c < nch) v[u] = src[c];
+    }
+    for (int j = 0; j < k; ++j) {
+      uint64_t p = __shfl(reinterpret_cast<uint64_t>(my_dst), j);
+      if (!p) continue;
+      u32x4* dst = reinterpret_cast<u32x4*>(p);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        int c = c0 + u * 64 + lane;
+        if (c < nch) dst[c] = v[u];
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------ combine
+// out[t] = bf16(sum_j w[t][j] * C[t*k + j]); one wave per token, 8 values per lane-piece.
+__global__ __launch_bounds__(256) void combine_reduce_kernel(const char* __restrict__ cbuf,
+                                                             int64_t cstride,
+                                                             const float* __restrict__ w, int T,
+                                                             int k, int H,
+                                                             uint16_t* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const float wl = lane < k ? w[static_cast<int64_t>(t) * k + lane] : 0.f;
+  const int nch = H >> 3;
+  u32x4* dst = reinterpret_cast<u32x4*>(out + static_cast<int64_t>(t) * H);
+  for (int c = lane; c < nch; c += 64) {
+    float acc[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+    for (int j = 0; j < k; ++j) {
+      float wj = __shfl(wl, j);
+      const u32x4 p = reinterpret_cast<const u32x4*>(
+          cbuf + (static_cast<int64_t>(t) * k + j) * cstride)[c];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        acc[2 * q] += wj * bf_lo(p[q]);
+        acc[2 * q + 1] += wj * bf_hi(p[q]);
+      }
+    }
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = pack_bf16x2(acc[2 * q], acc[2 * q + 1]);
+    dst[c] = o;
+  }
+}
+
+// Ready flags of windows written by the preceding kernels on the same stream: the kernel
+// boundary orders those stores before these; the system-scope release makes them visible
+// to host-coherent consumers before the flag.
+__global__ void signal_windows_kernel(WinSet win) {
+  int d = threadIdx.x;
+  if (d < win.n && win.flag[d]) {
+    __threadfence_system();
+    __hip_atomic_store(win.flag[d], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+  }
+}
+
+}  // namespace xs
+
+// ------------------------------------------------------------------------------ C ABI
+using namespace xs;
+
+namespace xs_host {
+int signal_windows(const WinSet& ws, hipStream_t st) {
+  bool any = false;
+  for (int d = 0; d < ws.n; ++d) any |= ws.flag[d] != nullptr;
+  if (!any) return XS_OK;
+  hipLaunchKernelGGL(signal_windows_kernel, dim3(1), dim3(XS_MAX_WINDOWS), 0, st, ws);
+  return launch_status();
+}
+}  // namespace xs_host
+
+extern "C" int xs_route_topk_softmax(const float* logits, int32_t T, int32_t E, int32_t k,
+                                     int32_t renormalize, int32_t* topk_idx, float* topk_w,
+                                     void* stream) {
+  if (!logits || !topk_idx || !topk_w || T < 0 || E < 1 || E > 1024 || k < 1 || k > E || k > 32)
+    return XS_EINVAL;
+  if (T == 0) return XS_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  dim3 grid((T + 3) / 4), block(256);
+  const int epl = (E + 63) / 64;
+#define XS_ROUTE(N)                                                                        \
+  case N:                                                                                  \
+    hipLaunchKernelGGL(route_topk_kernel<N>, grid, block, 0, st, logits, T, E, k, renormalize, \
+                       topk_idx, topk_w);                                                  \
+    break;
+  switch (epl) {
+    XS_ROUTE(1) XS_ROUTE(2) XS_ROUTE(3) XS_ROUTE(4) XS_ROUTE(5) XS_ROUTE(6) XS_ROUTE(7) XS_ROUTE(8)
+    XS_ROUTE(9) XS_ROUTE(10) XS_ROUTE(11) XS_ROUTE(12) XS_ROUTE(13) XS_ROUTE(14) XS_ROUTE(15)
+    XS_ROUTE(16)
+    default: return XS_EINVAL;
+  }
+#undef XS_ROUTE
+  return xs_host::launch_status();
+}
+
+static int64_t layout_ws_bytes(int32_t n_src, int32_t T, int32_t E) {
+  int64_t n_chunks = (static_cast<int64_t>(T) + kChunk - 1) / kChunk;
+  int64_t b = static_cast<int64_t>(n_src) * n_chunks * E * 4;
+  return (b + 255) & ~int64_t(255);
+}
+
+extern "C" int xs_dispatch_layout_workspace_bytes(int32_t n_src, int32_t T, int32_t E,
+                                                  int64_t* bytes) {
+  if (!bytes || n_src < 1 || T < 0 || E < 1) return XS_EINVAL;
+  *bytes = layout_ws_bytes(n_src, T, E);
+  return XS_OK;
+}
+
+namespace xs_host {
+int dispatch_layout(const int32_t* topk_idx, int32_t n_src, int32_t T, int32_t k, int32_t E,
+                    int32_t W, int32_t cap, int32_t* expert_counts, int32_t* src_base,
+                    int32_t* expert_offsets, int32_t* dest_counts, int32_t* slot_row,
+                    int32_t* row_src, void* workspace, int64_t workspace_bytes,
+                    int32_t* dev_status, hipStream_t st) {
+  if (!topk_idx || !expert_counts || !src_base || !expert_offsets || !dest_counts || !slot_row ||
+      !row_src)
+    return XS_EINVAL;
+  if (n_src < 1 || n_src > 127 || T < 0 || k < 1 || k > E || E < 1 || E > 1024 || W < 1 ||
+      W > XS_MAX_WINDOWS || E % W || cap < 0 || static_cast<int64_t>(T) * k >= (1 << 24))
+    return XS_EINVAL;
+  if (!workspace || workspace_bytes < layout_ws_bytes(n_src, T, E)) return XS_EWORKSPACE;
+  const int n_chunks = (T + kChunk - 1) / kChunk;
+  int* chunk = static_cast<int*>(workspace);
+  if (n_chunks > 0) {
+    hipLaunchKernelGGL(layout_chunk_kernel, dim3(n_chunks, n_src), dim3(256),
+                       4 * E * sizeof(unsigned long long), st, topk_idx, T, k, E, n_chunks,
+                       slot_row, chunk, dev_status);
+    if (launch_status()) return XS_EHIP;
+  }
+  hipLaunchKernelGGL(layout_source_scan_kernel, dim3(n_src), dim3(1024), 0, st, chunk, n_chunks, E,
+                     expert_counts);
+  if (launch_status()) return XS_EHIP;
+  hipLaunchKernelGGL(layout_global_scan_kernel, dim3(1), dim3(1024), 0, st, expert_counts, n_src,
+                     E, W, cap, src_base, expert_offsets, dest_counts, dev_status);
+  if (launch_status()) return XS_EHIP;
+  const int64_t n = static_cast<int64_t>(n_src) * T * k;
+  if (n > 0) {
+    int blocks = static_cast<int>(std::min<int64_t>((n + 255) / 256, 4096));
+    hipLaunchKernelGGL(layout_finalize_kernel, dim3(blocks), dim3(256), 0, st, topk_idx, n_src, T,
+                       k, E, W, cap, n_chunks, chunk, src_base, expert_offsets, slot_row, row_src);
+    if (launch_status()) return XS_EHIP;
+  }
+  return XS_OK;
+}
+
+int dispatch(const void* x, int32_t T, int32_t H, const int32_t* topk_idx, const int32_t* slot_row,
+             int32_t k, int32_t E, const WinSet& ws, int32_t* dev_status, hipStream_t st) {
+  if (T == 0) return signal_windows(ws, st);
+  hipLaunchKernelGGL(dispatch_kernel, dim3((T + 3) / 4), dim3(256), 0, st,
+                     static_cast<const uint16_t*>(x), T, H, topk_idx, slot_row, k, E, ws,
+                     dev_status);
+  if (launch_status()) return XS_EHIP;
+  return signal_windows(ws, st);
+}
+
+int combine_reduce(const void* cbuf, int64_t cstride, const float* w, int32_t T, int32_t k,
+                   int32_t H, void* out, hipStream_t st) {
+  if (T == 0) return XS_OK;
+  hipLaunchKernelGGL(combine_reduce_kernel, dim3((T + 3) / 4), dim3(256), 0, st,
+                     static_cast<const char*>(cbuf), cstride, w, T, k, H,
+                     static_cast<uint16_t*>(out));
+  return launch_status();
+}
+}  // namespace xs_host
+
+extern "C" int xs_dispatch_layout(const int32_t* topk_idx, int32_t n_src, int32_t T, int32_t k,
+                                  int32_t E, int32_t W, int32_t cap, int32_t* expert_counts,
+                                  int32_t* src_base, int32_t* expert_offsets,
+                                  int32_t* dest_counts, int32_t* slot_row, int32_t* row_src,
+                                  void* workspace, int64_t workspace_bytes, int32_t* dev_status,
+                                  void* stream) {
+  return xs_host::dispatch_layout(topk_idx, n_src, T, k, E, W, cap, expert_counts, src_base,
+                                  expert_offsets, dest_counts, slot_row, row_src, workspace,
+                                  workspace_bytes, dev_status, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int xs_dispatch(const void* x, int32_t T, int32_t H, const int32_t* topk_idx,
+                           const int32_t* slot_row, int32_t k, int32_t E, const xs_window* win,
+                           int32_t W, int32_t* dev_status, void* stream) {
+  if (!x || !topk_idx || !slot_row || T < 0 || H < 8 || k < 1 || k > 32 || k > E || E < 1 ||
+      W < 1 || E % W)
+    return XS_EINVAL;
+  if (H % 8 || (reinterpret_cast<uintptr_t>(x) & 15)) return XS_EUNSUPPORTED;
+  WinSet ws;
+  int rc = xs_host::make_winset(win, W, static_cast<int64_t>(H) * 2, &ws);
+  if (rc) return rc;
+  return xs_host::dispatch(x, T, H, topk_idx, slot_row, k, E, ws, dev_status,
+                           static_cast<hipStream_t>(stream));
+}
+
+extern "C" int xs_combine_reduce(const void* cbuf, int64_t cbuf_stride_bytes, const float* topk_w,
+                                 int32_t T, int32_t k, int32_t H, void* out, void* stream) {
+  if (!cbuf || !topk_w || !out || T < 0 || k < 1 || k > 32 || H < 8) return XS_EINVAL;
+  if (H % 8 || (cbuf_stride_bytes & 15) || cbuf_stride_bytes < static_cast<int64_t>(H) * 2 ||
+      (reinterpret_cast<uintptr_t>(cbuf) & 15) || (reinterpret_cast<uintptr_t>(out) & 15))
+    return XS_EUNSUPPORTED;
+  return xs_host::combine_reduce(cbuf, cbuf_stride_bytes, topk_w, T, k, H, out,
+                                 static_cast<hipStream_t>(stream));
+}

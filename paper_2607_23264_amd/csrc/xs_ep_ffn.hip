@@ -1,0 +1,633 @@
+// Persistent expert-FFN kernel of the EP layer (Sec. 4.3, App. A.2).
+//
+// Scheduler rows are (local expert, 256-row block) pairs in expert-major order. Each row
+// has P1 = I / 128 Linear-1 tiles (gate+up GEMM with the SwiGLU epilogue, 128 columns of h
+// each) and P2 = H / 256 Linear-2 tiles (down GEMM whose epilogue stores the output rows
+// into the combine windows of their source ranks: the remote-store bursts of Sec. 4.3).
+// A Linear-2 tile of row p reads the whole h row block, so it waits until all P1 Linear-1
+// tiles of row p have released their stores (per-row counters, agent-scope
+// release/acquire, bounded wait).
+//
+// Tile order per persistent workgroup ("scheduler instance" g of G):
+//   BURST       Expert-Wave: global list [L1 of wave 0, L2 of wave 0, L1 of wave 1, ...],
+//               instance g takes entries g, g + G, ...
+//   INTERLEAVE  Alg. 1: one cursor per tile stream, both starting at g and stepping by G; the
+//               next Linear-2 tile is taken when its row trails the Linear-1 cursor's row by
+//               at least D rows, otherwise the next Linear-1 tile.
+//   CHUNK       Alg. 1 with at most c consecutive Linear-2 tiles before a Linear-1 tile.
+// Deadlock freedom needs every workgroup resident (grid <= CUs, one workgroup per CU by
+// LDS) and D >= 1: an instance only waits on a row strictly behind its own Linear-1 cursor,
+// so the lowest row anyone waits on always has its Linear-1 owners running.
+#include <algorithm>
+#include <cmath>
+
+#include "xs_gemm.hpp"
+
+namespace xs {
+
+struct RowWin {
+  char* base[XS_MAX_WINDOWS];
+  int64_t stride[XS_MAX_WINDOWS];
+};
+
+struct EpArgs {
+  int E, epw, H, I, e_begin, n_experts, cap, d_first;
+  int n_src, tk;               // combine windows and rows per combine window (T * k)
+  int P1, P2;
+  RowWin dwin;                 // computed dispatch windows, index d - d_first
+  RowWin cwin;                 // combine windows by source rank
+  const int* expert_offsets;
+  const int* row_src;          // [W][cap]
+  const uint16_t* w1;
+  const uint16_t* w2;
+  uint16_t* h;
+  uint16_t* y;
+  const int* meta;             // [0] rows P, [1] waves, [2] wave-list length, [3] computed rows
+  const int* row_expert;
+  const int* exp_m;
+  const int* exp_rowfirst;
+  const int* exp_hrow;
+  const int* wave_pos;
+  const int* wave_row;
+  int* l1_done;
+  int mode;                    // bit 0: Linear-1 tiles, bit 1: Linear-2 tiles
+  int l2_combine;              // Linear-2 epilogue: 1 = combine windows, 0 = y rows
+  int policy, lead, chunk, withhold_row;
+  int64_t gap_ticks, timeout_ticks;
+  int* status;
+  xs_trace tr;
+};
+
+// Per-expert row counts (clipped to the rows that fit in the window), scheduler rows,
+// Expert-Wave boundaries; clears the readiness counters. One block.
+__global__ __launch_bounds__(1024) void ep_plan_kernel(const int* __restrict__ expert_counts,
+                                                       int n_src, int E, int e_begin,
+                                                       int n_experts,
+                                                       const int* __restrict__ expert_offsets,
+                                                       int cap, int P1, int P2, int wave_tiles,
+                                                       int* meta, int* row_expert, int* exp_m,
+                                                       int* exp_rowfirst, int* exp_hrow,
+                                                       int* wave_pos, int* wave_row,
+                                                       int* l1_done) {
+  __shared__ int s_m[1024], s_first[1024], s_rows;
+  const int i = threadIdx.x;
+  if (i < n_experts) {
+    const int e = e_begin + i;
+    int m = 0;
+    for (int s = 0; s < n_src; ++s) m += expert_counts[static_cast<int64_t>(s) * E + e];
+    s_m[i] = max(0, min(m, cap - expert_offsets[e]));
+  }
+  __syncthreads();
+  if (i == 0) {
+    int rows = 0, hrow = 0, nw = 0, wl1 = 0;
+    wave_row[0] = 0;
+    wave_pos[0] = 0;
+    for (int x = 0; x < n_experts; ++x) {
+      const int mt = (s_m[x] + kBM - 1) / kBM;
+      exp_m[x] = s_m[x];
+      exp_rowfirst[x] = rows;
+      s_first[x] = rows;
+      exp_hrow[x] = hrow;
+      rows += mt;
+      hrow += s_m[x];
+      wl1 += mt * P1;
+      if (wl1 >= wave_tiles && rows > wave_row[nw]) {
+        ++nw;
+        wave_row[nw] = rows;
+        wave_pos[nw] = rows * (P1 + P2);
+        wl1 = 0;
+      }
+    }
+    if (rows > wave_row[nw]) {
+      ++nw;
+      wave_row[nw] = rows;
+      wave_pos[nw] = rows * (P1 + P2);
+    }
+    meta[0] = rows;
+    meta[1] = nw;
+    meta[2] = rows * (P1 + P2);
+    meta[3] = hrow;
+    s_rows = rows;
+  }
+  __syncthreads();
+  if (i < n_experts) {
+    const int mt = (s_m[i] + kBM - 1) / kBM;
+    for (int p = s_first[i]; p < s_first[i] + mt; ++p) row_expert[p] = i;
+  }
+  for (int p = i; p < s_rows; p += blockDim.x) l1_done[p] = 0;
+}
+
+__device__ __forceinline__ void ep_l1_tile(const EpArgs& a, int p, int nt, bool fused,
+                                           uint16_t* lds, char** rowptr) {
+  const int tid = threadIdx.x;
+  const int x = a.row_expert[p];
+  const int e = a.e_begin + x;
+  const int dl = e / a.epw - a.d_first;
+  const int m0 = (p - a.exp_rowfirst[x]) * kBM;
+  const int rows = min(kBM, a.exp_m[x] - m0);
+  const uint64_t t0 = a.tr.buf ? wall_ticks() : 0;
+  const int64_t lda = a.dwin.stride[dl] / 2;
+  const uint16_t* A = reinterpret_cast<const uint16_t*>(
+      a.dwin.base[dl] + static_cast<int64_t>(a.expert_offsets[e] + m0) * a.dwin.stride[dl]);
+  const uint16_t* B = a.w1 + static_cast<int64_t>(x) * 2 * a.I * a.H;
+  f32x16 acc[4][2];
+  gemm_mainloop(A, lda, rows, B, a.H, nt * (kBN / 2), a.I, true, a.H, acc, lds);
+  const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
+  if (tid < rows)
+    rowptr[tid] = reinterpret_cast<char*>(
+        a.h + static_cast<int64_t>(a.exp_hrow[x] + m0 + tid) * a.I + nt * (kBN / 2));
+  stage_swiglu(acc, lds);
+  __syncthreads();
+  store_rows(lds, kEpiPitchH, kBN / 2, rows, rowptr);
+  if (fused) {
+    __threadfence();   // each wave: its h stores complete and visible at agent scope
+    __syncthreads();
+    if (tid == 0 && p != a.withhold_row)
+      __hip_atomic_fetch_add(&a.l1_done[p], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  } else {
+    __syncthreads();
+  }
+  if (a.tr.buf && tid == 0) {
+    uint32_t i = atomicAdd(a.tr.count, 1u);
+    if (static_cast<int64_t>(i) < a.tr.capacity) {
+      uint64_t* r = a.tr.buf + static_cast<int64_t>(i) * 4;
+      r[0] = (1ull << 56) | (static_cast<uint64_t>(blockIdx.x) << 32) |
+             static_cast<uint32_t>(p * a.P1 + nt);
+      r[1] = t0;
+      r[2] = t1;
+      r[3] = wall_ticks();
+    }
+  }
+}
+
+// Returns false if the wait for row p's Linear-1 tiles expired (the tile is then skipped).
+__device__ __forceinline__ bool ep_wait_row(const EpArgs& a, int p, int* flag) {
+  if (threadIdx.x == 0) {
+    int ok = 1;
+    if (__hip_atomic_load(&a.l1_done[p], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < a.P1) {
+      const uint64_t t0 = wall_ticks();
+      while (__hip_atomic_load(&a.l1_done[p], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) <
+             a.P1) {
+        if (wall_ticks() - t0 > static_cast<uint64_t>(a.timeout_ticks)) {
+          ok = 0;
+          set_status(a.status, XS_ETIMEOUT);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+      }
+    }
+    *flag = ok;
+  }
+  __syncthreads();
+  const bool ok = *flag != 0;
+  __syncthreads();
+  return ok;
+}
+
+__device__ __forceinline__ void ep_l2_tile(const EpArgs& a, int p, int nt, bool fused,
+                                           uint16_t* lds, char** rowptr, int* flag) {
+  const int tid = threadIdx.x;
+  const uint64_t t0 = a.tr.buf ? wall_ticks() : 0;
+  if (fused && !ep_wait_row(a, p, flag)) return;
+  const int x = a.row_expert[p];
+  const int e = a.e_begin + x;
+  const int m0 = (p - a.exp_rowfirst[x]) * kBM;
+  const int rows = min(kBM, a.exp_m[x] - m0);
+  const uint16_t* A = a.h + static_cast<int64_t>(a.exp_hrow[x] + m0) * a.I;
+  const uint16_t* B = a.w2 + static_cast<int64_t>(x) * a.H * a.I;
+  const int n0 = nt * kBN;
+  f32x16 acc[4][2];
+  gemm_mainloop(A, a.I, rows, B, a.I, n0, 0, false, a.I, acc, lds);
+  const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
+  if (tid < rows) {
+    char* ptr;
+    if (a.l2_combine) {
+      const int d = e / a.epw;
+      const int code = a.row_src[static_cast<int64_t>(d) * a.cap + a.expert_offsets[e] + m0 + tid];
+      const int src = code >> 24, slot = code & 0xffffff;
+      if (code >= 0 && src < a.n_src && slot < a.tk) {
+        ptr = a.cwin.base[src] + static_cast<int64_t>(slot) * a.cwin.stride[src] +
+              static_cast<int64_t>(n0) * 2;
+      } else {
+        ptr = nullptr;   // a row the layout never assigned (bad routing input): not stored
+        set_status(a.status, XS_EBADINPUT);
+      }
+    } else {
+      ptr = reinterpret_cast<char*>(a.y + static_cast<int64_t>(a.exp_hrow[x] + m0 + tid) * a.H + n0);
+    }
+    rowptr[tid] = ptr;
+  }
+  stage_tile(acc, lds);
+  __syncthreads();
+  store_rows(lds, kEpiPitch, kBN, rows, rowptr);
+  __syncthreads();
+  if (tid == 0) {
+    const uint64_t t2 = a.tr.buf ? wall_ticks() : 0;
+    if (a.tr.buf) {
+      uint32_t i = atomicAdd(a.tr.count, 1u);
+      if (static_cast<int64_t>(i) < a.tr.capacity) {
+        uint64_t* r = a.tr.buf + static_cast<int64_t>(i) * 4;
+        r[0] = (2ull << 56) | (static_cast<uint64_t>(blockIdx.x) << 32) |
+               static_cast<uint32_t>(p * a.P2 + nt);
+        r[1] = t0;
+        r[2] = t1;
+        r[3] = t2;
+      }
+    }
+    spin_ticks(static_cast<uint64_t>(a.gap_ticks));   // non-injecting gap after the burst
+  }
+  if (a.gap_ticks) __syncthreads();
+}
+
+__device__ __forceinline__ int xcd_instance_ep(int b, int G) {
+  return (G % 8) ? b : (b % 8) * (G / 8) + b / 8;
+}
+
+__global__ __launch_bounds__(kThreads, 1) void ep_ffn_kernel(EpArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
+  uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
+  char** rowptr = reinterpret_cast<char**>(smem + kLdsRowPtrOff);
+  int* flag = reinterpret_cast<int*>(smem + kLdsMiscOff);
+  const int P = a.meta[0];
+  const int G = gridDim.x;
+  const int g = xcd_instance_ep(blockIdx.x, G);
+  const bool fused = a.mode == 3;
+  const int n1 = (a.mode & 1) ? P * a.P1 : 0;
+  const int n2 = (a.mode & 2) ? P * a.P2 : 0;
+  if (fused && a.policy == XS_POLICY_BURST) {
+    const int nw = a.meta[1], total = a.meta[2];
+    int w = 0;
+    for (int pos = g; pos < total; pos += G) {
+      while (w + 1 < nw && a.wave_pos[w + 1] <= pos) ++w;
+      const int off = pos - a.wave_pos[w];
+      const int r0 = a.wave_row[w], nl1 = (a.wave_row[w + 1] - r0) * a.P1;
+      if (off < nl1) {
+        const int k1 = r0 * a.P1 + off;
+        ep_l1_tile(a, k1 / a.P1, k1 % a.P1, true, lds, rowptr);
+      } else {
+        const int k2 = r0 * a.P2 + (off - nl1);
+        ep_l2_tile(a, k2 / a.P2, k2 % a.P2, true, lds, rowptr, flag);
+      }
+    }
+    return;
+  }
+  const int D = a.lead, c = a.chunk;
+  int k1 = g, k2 = g, run = 0;
+  while (k1 < n1 || k2 < n2) {
+    const int p1 = k1 < n1 ? k1 / a.P1 : 0x3fffffff;
+    const int p2 = k2 / a.P2;
+    bool take2 = k2 < n2 && p2 + D <= p1;
+    if (take2 && c > 0 && run >= c && k1 < n1) take2 = false;
+    if (take2) {
+      ep_l2_tile(a, p2, k2 % a.P2, fused, lds, rowptr, flag);
+      k2 += G;
+      ++run;
+    } else {
+      ep_l1_tile(a, p1, k1 % a.P1, fused, lds, rowptr);
+      k1 += G;
+      run = 0;
+    }
+  }
+}
+
+// Prefix of the rows each computed window holds (rows past capacity were never stored).
+__device__ __forceinline__ int window_prefix(const EpArgs& a, const int* dest_counts, int n_cwin,
+                                             int* base) {
+  if (threadIdx.x == 0) {
+    base[0] = 0;
+    for (int d = 0; d < n_cwin; ++d) base[d + 1] = base[d] + min(dest_counts[a.d_first + d], a.cap);
+  }
+  __syncthreads();
+  return base[n_cwin];
+}
+
+__device__ __forceinline__ char* combine_row(const EpArgs& a, int dl, int r) {
+  const int code = a.row_src[static_cast<int64_t>(a.d_first + dl) * a.cap + r];
+  const int s = code >> 24, slot = code & 0xffffff;
+  if (code < 0 || s >= a.n_src || slot >= a.tk) {
+    set_status(a.status, XS_EBADINPUT);
+    return nullptr;
+  }
+  return a.cwin.base[s] + static_cast<int64_t>(slot) * a.cwin.stride[s];
+}
+
+// Identity experts: y = x, i.e. the computed window rows are copied to y (unfused) or
+// stored straight into the combine windows. One wave per computed row.
+__global__ __launch_bounds__(256) void ep_identity_kernel(EpArgs a, const int* __restrict__ dest_counts,
+                                                          int n_cwin, int to_combine) {
+  __shared__ int base[XS_MAX_WINDOWS + 1];
+  const int lane = threadIdx.x & 63;
+  const int total = window_prefix(a, dest_counts, n_cwin, base);
+  for (int gr = blockIdx.x * 4 + (threadIdx.x >> 6); gr < total; gr += gridDim.x * 4) {
+    int dl = 0;
+    while (base[dl + 1] <= gr) ++dl;
+    const int r = gr - base[dl];
+    const u32x4* src = reinterpret_cast<const u32x4*>(a.dwin.base[dl] + static_cast<int64_t>(r) * a.dwin.stride[dl]);
+    u32x4* dst = reinterpret_cast<u32x4*>(to_combine ? combine_row(a, dl, r)
+                                                     : reinterpret_cast<char*>(a.y + static_cast<int64_t>(gr) * a.H));
+    if (!dst) continue;
+    for (int pc = lane; pc < a.H / 8; pc += 64) dst[pc] = src[pc];
+  }
+}
+
+// Unfused combine-send: computed row -> combine window of its source.
+__global__ __launch_bounds__(256) void ep_combine_send_kernel(EpArgs a, const int* __restrict__ dest_counts,
+                                                              int n_cwin) {
+  __shared__ int base[XS_MAX_WINDOWS + 1];
+  const int lane = threadIdx.x & 63;
+  const int total = window_prefix(a, dest_counts, n_cwin, base);
+  for (int gr = blockIdx.x * 4 + (threadIdx.x >> 6); gr < total; gr += gridDim.x * 4) {
+    int dl = 0;
+    while (base[dl + 1] <= gr) ++dl;
+    const int r = gr - base[dl];
+    u32x4* dst = reinterpret_cast<u32x4*>(combine_row(a, dl, r));
+    if (!dst) continue;
+    const u32x4* src = reinterpret_cast<const u32x4*>(a.y + static_cast<int64_t>(gr) * a.H);
+    for (int pc = lane; pc < a.H / 8; pc += 64) dst[pc] = src[pc];
+  }
+}
+
+}  // namespace xs
+
+using namespace xs;
+
+namespace xs_host {
+int dispatch_layout(const int32_t*, int32_t, int32_t, int32_t, int32_t, int32_t, int32_t, int32_t*,
+                    int32_t*, int32_t*, int32_t*, int32_t*, int32_t*, void*, int64_t, int32_t*,
+                    hipStream_t);
+int dispatch(const void*, int32_t, int32_t, const int32_t*, const int32_t*, int32_t, int32_t,
+             const WinSet&, int32_t*, hipStream_t);
+int combine_reduce(const void*, int64_t, const float*, int32_t, int32_t, int32_t, void*,
+                   hipStream_t);
+int signal_windows(const WinSet&, hipStream_t);
+int persistent_grid(int max_producers);
+}  // namespace xs_host
+
+namespace {
+
+constexpr int64_t kAlign = 256;
+int64_t align_up(int64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct EpWorkspace {
+  int64_t layout_off, layout_bytes;
+  int64_t meta_off, exp_off, rowexp_off, wave_pos_off, wave_row_off, l1_off;
+  int64_t total;
+  int64_t max_rows;
+};
+
+int n_cwin_of(const xs_ep_layer* L) { return L->n_experts / (L->E / L->W); }
+
+EpWorkspace ep_workspace(const xs_ep_layer* L) {
+  EpWorkspace w{};
+  const int64_t n_chunks = (static_cast<int64_t>(L->T) + 255) / 256;
+  w.layout_off = 0;
+  w.layout_bytes = align_up(static_cast<int64_t>(L->n_src) * n_chunks * L->E * 4);
+  const int64_t max_rows = static_cast<int64_t>(n_cwin_of(L)) * L->cap / kBM + L->n_experts + 1;
+  w.max_rows = max_rows;
+  int64_t o = w.layout_bytes;
+  w.meta_off = o;
+  o += align_up(16 * 4);
+  w.exp_off = o;
+  o += align_up(4LL * L->n_experts * 4);
+  w.rowexp_off = o;
+  o += align_up(max_rows * 4);
+  w.wave_pos_off = o;
+  o += align_up((max_rows + 2) * 4);
+  w.wave_row_off = o;
+  o += align_up((max_rows + 2) * 4);
+  w.l1_off = o;
+  o += align_up(max_rows * 4);
+  w.total = o;
+  return w;
+}
+
+int validate(const xs_ep_layer* L, bool need_out) {
+  if (!L) return XS_EINVAL;
+  if (L->n_src < 1 || L->n_src > 127 || L->T < 0 || L->H < 8 || L->E < 1 || L->E > 1024 ||
+      L->k < 1 || L->k > L->E || L->k > 32 || L->W < 1 || L->W > XS_MAX_WINDOWS || L->E % L->W ||
+      L->src < 0 || L->src >= L->n_src || L->cap < 0)
+    return XS_EINVAL;
+  const int epw = L->E / L->W;
+  if (L->n_experts < 1 || L->e_begin < 0 || L->e_begin % epw || L->n_experts % epw ||
+      L->e_begin + L->n_experts > L->E || L->n_experts > 1024)
+    return XS_EINVAL;
+  if (static_cast<int64_t>(L->T) * L->k >= (1 << 24)) return XS_EINVAL;
+  if (!L->topk_idx || !L->topk_w || !L->expert_counts || !L->src_base || !L->expert_offsets ||
+      !L->dest_counts || !L->slot_row || !L->row_src || !L->dispatch_win || !L->combine_win)
+    return XS_EINVAL;
+  if (need_out && (!L->x || !L->logits || !L->out)) return XS_EINVAL;
+  if (L->expert_mode != XS_EXPERT_SWIGLU && L->expert_mode != XS_EXPERT_IDENTITY) return XS_EINVAL;
+  if (L->H % 8) return XS_EUNSUPPORTED;
+  if (L->expert_mode == XS_EXPERT_SWIGLU) {
+    if (!L->w1 || !L->w2 || !L->h_ws || L->I < 1) return XS_EINVAL;
+    if (L->H % kBN || L->I % (kBN / 2) || L->I % kBK) return XS_EUNSUPPORTED;
+    if (L->h_rows < static_cast<int64_t>(n_cwin_of(L)) * L->cap) return XS_EINVAL;
+  }
+  return XS_OK;
+}
+
+int fill_args(const xs_ep_layer* L, void* workspace, EpArgs* a, WinSet* dws, WinSet* cws) {
+  int rc = xs_host::make_winset(L->dispatch_win, L->W, static_cast<int64_t>(L->H) * 2, dws);
+  if (rc) return rc;
+  for (int d = 0; d < L->W; ++d)
+    if (dws->cap[d] < L->cap) return XS_EINVAL;
+  rc = xs_host::make_winset(L->combine_win, L->n_src, static_cast<int64_t>(L->H) * 2, cws);
+  if (rc) return rc;
+  for (int s = 0; s < L->n_src; ++s)
+    if (cws->cap[s] < static_cast<int64_t>(L->T) * L->k) return XS_EINVAL;
+  const EpWorkspace w = ep_workspace(L);
+  char* ws = static_cast<char*>(workspace);
+  *a = EpArgs{};
+  a->E = L->E;
+  a->epw = L->E / L->W;
+  a->H = L->H;
+  a->I = L->I;
+  a->e_begin = L->e_begin;
+  a->n_experts = L->n_experts;
+  a->cap = L->cap;
+  a->n_src = L->n_src;
+  a->tk = L->T * L->k;
+  a->d_first = L->e_begin / a->epw;
+  a->P1 = L->I / (kBN / 2);
+  a->P2 = L->H / kBN;
+  for (int d = 0; d < n_cwin_of(L); ++d) {
+    a->dwin.base[d] = dws->base[a->d_first + d];
+    a->dwin.stride[d] = dws->stride[a->d_first + d];
+  }
+  for (int s = 0; s < L->n_src; ++s) {
+    a->cwin.base[s] = cws->base[s];
+    a->cwin.stride[s] = cws->stride[s];
+  }
+  a->expert_offsets = L->expert_offsets;
+  a->row_src = L->row_src;
+  a->w1 = static_cast<const uint16_t*>(L->w1);
+  a->w2 = static_cast<const uint16_t*>(L->w2);
+  a->h = static_cast<uint16_t*>(L->h_ws);
+  a->y = static_cast<uint16_t*>(L->y_ws);
+  int* meta = reinterpret_cast<int*>(ws + w.meta_off);
+  int* exp = reinterpret_cast<int*>(ws + w.exp_off);
+  a->meta = meta;
+  a->exp_m = exp;
+  a->exp_rowfirst = exp + L->n_experts;
+  a->exp_hrow = exp + 2 * L->n_experts;
+  a->row_expert = reinterpret_cast<int*>(ws + w.rowexp_off);
+  a->wave_pos = reinterpret_cast<int*>(ws + w.wave_pos_off);
+  a->wave_row = reinterpret_cast<int*>(ws + w.wave_row_off);
+  a->l1_done = reinterpret_cast<int*>(ws + w.l1_off);
+  a->withhold_row = -1;
+  a->lead = 1;
+  return XS_OK;
+}
+
+int launch_plan(const xs_ep_layer* L, const EpArgs& a, int wave_tiles, hipStream_t st) {
+  hipLaunchKernelGGL(ep_plan_kernel, dim3(1), dim3(1024), 0, st, L->expert_counts, L->n_src, L->E,
+                     L->e_begin, L->n_experts, L->expert_offsets, L->cap, a.P1, a.P2, wave_tiles,
+                     const_cast<int*>(a.meta), const_cast<int*>(a.row_expert),
+                     const_cast<int*>(a.exp_m), const_cast<int*>(a.exp_rowfirst),
+                     const_cast<int*>(a.exp_hrow), const_cast<int*>(a.wave_pos),
+                     const_cast<int*>(a.wave_row), a.l1_done);
+  return xs_host::launch_status();
+}
+
+// Chunk length for AUTO from the average-rate bound (Eq. 9) with n1 = 1 Linear-1 tile per
+// cycle and n2 = c aligned Linear-2 bursts of V = K * tile bytes each:
+//   c V / (c (T0 + T_L2) + T_L1) <= R  <=>  c (V/R - T0 - T_L2) <= T_L1.
+int auto_chunk(const xs_pacing* pc, const xs_ep_layer* L, int K) {
+  if (!pc->model) return 0;
+  const xs_model* m = pc->model;
+  const double V = static_cast<double>(K) * kBM * kBN * 2;
+  const double T0 = m->t0_a_us + m->t0_b_us_per_byte * V;
+  // fallback mainloop estimates: tile FLOPs at 40 % of one CU's share of 2.5 PFLOP/s
+  const double cu_flops_us = 2.5e15 / 256.0 * 0.4 * 1e-6;
+  const double tl1 = pc->t_l1_us > 0 ? pc->t_l1_us : 2.0 * kBM * kBN * L->H / cu_flops_us;
+  const double tl2 = pc->t_l2_us > 0 ? pc->t_l2_us : 2.0 * kBM * kBN * L->I / cu_flops_us;
+  const double excess = V / m->R_bytes_per_us - T0 - tl2;
+  if (!(m->R_bytes_per_us > 0) || excess <= 0) return 0;   // drain keeps up: plain interleave
+  return std::max(1, static_cast<int>(std::floor(tl1 / excess)));
+}
+
+}  // namespace
+
+extern "C" int xs_ep_layer_workspace_bytes(const xs_ep_layer* L, int64_t* bytes) {
+  if (!L || !bytes || L->n_src < 1 || L->T < 0 || L->E < 1 || L->W < 1 || L->E % L->W ||
+      L->n_experts < 1 || L->cap < 0)
+    return XS_EINVAL;
+  *bytes = ep_workspace(L).total;
+  return XS_OK;
+}
+
+static int run_ffn(const xs_ep_layer* L, const EpArgs& base, int mode, int l2_combine,
+                   const xs_pacing* pc, const xs_trace* trace, int32_t* dev_status, hipStream_t st) {
+  EpArgs a = base;
+  a.mode = mode;
+  a.l2_combine = l2_combine;
+  a.status = dev_status;
+  a.tr = xs_trace{nullptr, 0, nullptr};
+  if (trace && trace->buf && trace->count) a.tr = *trace;
+  int grid = xs_host::persistent_grid(pc ? pc->max_producers : 0);
+  a.policy = pc ? pc->policy : XS_POLICY_INTERLEAVE;
+  a.lead = pc && pc->lead_rows > 0 ? pc->lead_rows : 1;
+  a.chunk = pc ? pc->chunk_tiles : 0;
+  if (a.policy == XS_POLICY_INTERLEAVE) a.chunk = 0;
+  if (a.policy == XS_POLICY_AUTO) {
+    a.chunk = auto_chunk(pc, L, grid);
+    a.policy = a.chunk > 0 ? XS_POLICY_CHUNK : XS_POLICY_INTERLEAVE;
+  }
+  a.withhold_row = pc ? pc->withhold_row : -1;
+  a.gap_ticks = pc ? xs_host::ns_to_ticks(pc->gap_ns) : 0;
+  const int64_t tmo_us = pc && pc->spin_timeout_us > 0 ? pc->spin_timeout_us : 2000000;
+  a.timeout_ticks = xs_host::ns_to_ticks(tmo_us * 1000);
+  hipLaunchKernelGGL(ep_ffn_kernel, dim3(grid), dim3(kThreads), 0, st, a);
+  return xs_host::launch_status();
+}
+
+extern "C" int xs_expert_ffn(const xs_ep_layer* L, void* workspace, int64_t workspace_bytes,
+                             int32_t* dev_status, void* stream) {
+  int rc = validate(L, false);
+  if (rc) return rc;
+  if (!L->y_ws) return XS_EINVAL;
+  if (!workspace || workspace_bytes < ep_workspace(L).total) return XS_EWORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  EpArgs a;
+  WinSet dws, cws;
+  rc = fill_args(L, workspace, &a, &dws, &cws);
+  if (rc) return rc;
+  a.status = dev_status;
+  if (L->expert_mode == XS_EXPERT_IDENTITY) {
+    hipLaunchKernelGGL(ep_identity_kernel, dim3(2048), dim3(256), 0, st, a, L->dest_counts,
+                       n_cwin_of(L), 0);
+    return xs_host::launch_status();
+  }
+  rc = launch_plan(L, a, 0, st);
+  if (rc) return rc;
+  rc = run_ffn(L, a, 1, 0, nullptr, nullptr, dev_status, st);
+  if (rc) return rc;
+  return run_ffn(L, a, 2, 0, nullptr, nullptr, dev_status, st);
+}
+
+extern "C" int xs_combine_send(const xs_ep_layer* L, int32_t* dev_status, void* stream) {
+  int rc = validate(L, false);
+  if (rc) return rc;
+  if (!L->y_ws) return XS_EINVAL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  EpArgs a;
+  WinSet dws, cws;
+  char dummy[256];
+  rc = fill_args(L, dummy, &a, &dws, &cws);
+  if (rc) return rc;
+  a.status = dev_status;
+  hipLaunchKernelGGL(ep_combine_send_kernel, dim3(2048), dim3(256), 0, st, a, L->dest_counts,
+                     n_cwin_of(L));
+  if (xs_host::launch_status()) return XS_EHIP;
+  return xs_host::signal_windows(cws, st);
+}
+
+extern "C" int xs_fused_ep_layer(const xs_ep_layer* L, const xs_pacing* pacing,
+                                 const xs_trace* trace, void* workspace, int64_t workspace_bytes,
+                                 int32_t* dev_status, void* stream) {
+  int rc = validate(L, true);
+  if (rc) return rc;
+  if (pacing && (pacing->policy < XS_POLICY_BURST || pacing->policy > XS_POLICY_AUTO ||
+                 pacing->lead_rows < 0 || pacing->chunk_tiles < 0 || pacing->max_producers < 0 ||
+                 pacing->gap_ns < 0 || pacing->spin_timeout_us < 0))
+    return XS_EINVAL;
+  const EpWorkspace w = ep_workspace(L);
+  if (!workspace || workspace_bytes < w.total) return XS_EWORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  EpArgs a;
+  WinSet dws, cws;
+  rc = fill_args(L, workspace, &a, &dws, &cws);
+  if (rc) return rc;
+  const int64_t n_all = static_cast<int64_t>(L->n_src) * L->T;
+  if (n_all > 0x7fffffff) return XS_EINVAL;
+  rc = xs_route_topk_softmax(L->logits, static_cast<int32_t>(n_all), L->E, L->k, L->renormalize,
+                             L->topk_idx, L->topk_w, stream);
+  if (rc) return rc;
+  rc = xs_host::dispatch_layout(L->topk_idx, L->n_src, L->T, L->k, L->E, L->W, L->cap,
+                                L->expert_counts, L->src_base, L->expert_offsets, L->dest_counts,
+                                L->slot_row, L->row_src, static_cast<char*>(workspace) + w.layout_off,
+                                w.layout_bytes, dev_status, st);
+  if (rc) return rc;
+  const int64_t so = static_cast<int64_t>(L->src) * L->T * L->k;
+  rc = xs_host::dispatch(L->x, L->T, L->H, L->topk_idx + so, L->slot_row + so, L->k, L->E, dws,
+                         dev_status, st);
+  if (rc) return rc;
+  a.status = dev_status;
+  if (L->expert_mode == XS_EXPERT_IDENTITY) {
+    hipLaunchKernelGGL(ep_identity_kernel, dim3(2048), dim3(256), 0, st, a, L->dest_counts,
+                       n_cwin_of(L), 1);
+    if (xs_host::launch_status()) return XS_EHIP;
+  } else {
+    const int grid = xs_host::persistent_grid(pacing ? pacing->max_producers : 0);
+    const int wave_tiles = pacing && pacing->wave_tiles > 0 ? pacing->wave_tiles : grid;
+    rc = launch_plan(L, a, wave_tiles, st);
+    if (rc) return rc;
+    rc = run_ffn(L, a, 3, 1, pacing, trace, dev_status, st);
+    if (rc) return rc;
+  }
+  rc = xs_host::signal_windows(cws, st);
+  if (rc) return rc;
+  const xs_window& cw = L->combine_win[L->src];
+  return xs_host::combine_reduce(cw.base, cw.row_stride_bytes, L->topk_w + so, L->T, L->k, L->H,
+                                 L->out, st);
+}

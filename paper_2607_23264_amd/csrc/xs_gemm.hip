@@ -1,0 +1,248 @@
+// Plain GEMM and GEMM with scatter epilogues (tensor-parallel row blocks, Ulysses head
+// groups), persistent over 256 x 256 output tiles. The epilogue stores every finished tile
+// straight into its destination windows with 128-bit stores; there is no separate
+// permutation pass (the serial counterpart, xs_scatter_copy, exists for comparison).
+#include <algorithm>
+
+#include "xs_gemm.hpp"
+
+namespace xs {
+
+enum { KIND_PLAIN = 0, KIND_ROW_BLOCK = 1, KIND_HEAD_GROUP = 2 };
+
+struct ScatterArgs {
+  int rpd;
+  int n_proj, n_heads, head_dim, hpg;
+};
+
+// Instance id with consecutive ids on one XCD: workgroups are dealt to the 8 XCDs round
+// robin, so block b runs on XCD b % 8.
+__device__ __forceinline__ int xcd_instance(int b, int G) {
+  return (G % 8) ? b : (b % 8) * (G / 8) + b / 8;
+}
+
+__device__ __forceinline__ void trace_tile(const xs_trace& tr, int kind, int tile, uint64_t t0,
+                                           uint64_t t1, uint64_t t2) {
+  uint32_t i = atomicAdd(tr.count, 1u);
+  if (static_cast<int64_t>(i) < tr.capacity) {
+    uint64_t* r = tr.buf + static_cast<int64_t>(i) * 4;
+    r[0] = (static_cast<uint64_t>(kind) << 56) | (static_cast<uint64_t>(blockIdx.x) << 32) |
+           static_cast<uint32_t>(tile);
+    r[1] = t0;
+    r[2] = t1;
+    r[3] = t2;
+  }
+}
+
+// Head-group destination of output element (m, col); col is a multiple of 8.
+__device__ __forceinline__ char* head_group_dst(const WinSet& win, const ScatterArgs& sa, int M,
+                                                int m, int col) {
+  const int per_proj = sa.n_heads * sa.head_dim;
+  const int p = col / per_proj;
+  const int rem = col - p * per_proj;
+  const int head = rem / sa.head_dim;
+  const int dd = rem - head * sa.head_dim;
+  const int g = head / sa.hpg, lh = head - g * sa.hpg;
+  const int64_t row = (static_cast<int64_t>(p) * sa.hpg + lh) * M + m;
+  return win.base[g] + row * win.stride[g] + dd * 2;
+}
+
+template <int KIND>
+__global__ __launch_bounds__(kThreads, 1) void gemm_tiles_kernel(
+    const uint16_t* __restrict__ A, int64_t lda, const uint16_t* __restrict__ B, int64_t ldb,
+    char* __restrict__ C, int64_t ldc_bytes, int M, int N, int K, ScatterArgs sa, WinSet win,
+    xs_trace tr) {
+  __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
+  uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
+  char** rowptr = reinterpret_cast<char**>(smem + kLdsRowPtrOff);
+  const int tid = threadIdx.x;
+  const int tm = (M + kBM - 1) / kBM, tn = N / kBN, ntiles = tm * tn;
+  const int G = gridDim.x;
+  for (int t = xcd_instance(blockIdx.x, G); t < ntiles; t += G) {
+    const int mb = t / tn, nb = t - mb * tn;
+    const int m0 = mb * kBM, n0 = nb * kBN;
+    const int rows = min(kBM, M - m0);
+    const uint64_t t0 = tr.buf ? wall_ticks() : 0;
+    f32x16 acc[4][2];
+    gemm_mainloop(A + static_cast<int64_t>(m0) * lda, lda, rows, B, ldb, n0, 0, false, K, acc, lds);
+    const uint64_t t1 = tr.buf ? wall_ticks() : 0;
+    if (KIND != KIND_HEAD_GROUP && tid < rows) {
+      const int m = m0 + tid;
+      char* p;
+      if (KIND == KIND_PLAIN) {
+        p = C + static_cast<int64_t>(m) * ldc_bytes + static_cast<int64_t>(n0) * 2;
+      } else {
+        const int d = m / sa.rpd;
+        p = win.base[d] + static_cast<int64_t>(m - d * sa.rpd) * win.stride[d] +
+            static_cast<int64_t>(n0) * 2;
+      }
+      rowptr[tid] = p;
+    }
+    stage_tile(acc, lds);
+    __syncthreads();
+    if (KIND == KIND_HEAD_GROUP) {
+      const int pc = tid & 31;
+      for (int r = tid >> 5; r < rows; r += kThreads / 32) {
+        u32x4 v = *reinterpret_cast<const u32x4*>(lds + r * kEpiPitch + pc * 8);
+        *reinterpret_cast<u32x4*>(head_group_dst(win, sa, M, m0 + r, n0 + pc * 8)) = v;
+      }
+    } else {
+      store_rows(lds, kEpiPitch, kBN, rows, rowptr);
+    }
+    __syncthreads();
+    if (tr.buf && tid == 0) trace_tile(tr, 3, t, t0, t1, wall_ticks());
+  }
+}
+
+// Serial permutation pass: plain output c -> windows (one wave per row).
+template <int KIND>
+__global__ __launch_bounds__(256) void scatter_copy_kernel(const char* __restrict__ c,
+                                                           int64_t ldc_bytes, int M, int N,
+                                                           ScatterArgs sa, WinSet win) {
+  const int lane = threadIdx.x & 63;
+  for (int m = blockIdx.x * 4 + (threadIdx.x >> 6); m < M; m += gridDim.x * 4) {
+    const u32x4* src = reinterpret_cast<const u32x4*>(c + static_cast<int64_t>(m) * ldc_bytes);
+    for (int pc = lane; pc < N / 8; pc += 64) {
+      u32x4 v = src[pc];
+      char* dst;
+      if (KIND == KIND_ROW_BLOCK) {
+        const int d = m / sa.rpd;
+        dst = win.base[d] + static_cast<int64_t>(m - d * sa.rpd) * win.stride[d] + pc * 16;
+      } else {
+        dst = head_group_dst(win, sa, M, m, pc * 8);
+      }
+      *reinterpret_cast<u32x4*>(dst) = v;
+    }
+  }
+}
+
+}  // namespace xs
+
+using namespace xs;
+
+namespace xs_host {
+int signal_windows(const WinSet& ws, hipStream_t st);
+
+int persistent_grid(int max_producers) {
+  int cus = num_cus();
+  if (cus <= 0) cus = 256;
+  if (max_producers > 0 && max_producers < cus) return max_producers;
+  return cus;
+}
+}  // namespace xs_host
+
+static bool gemm_shape_ok(int64_t lda, int64_t ldb, int32_t M, int32_t N, int32_t K) {
+  return M >= 0 && N > 0 && K > 0 && N % kBN == 0 && K % kBK == 0 && lda >= K && ldb >= K &&
+         lda % 8 == 0 && ldb % 8 == 0;
+}
+
+static xs_trace trace_or_empty(const xs_trace* t) {
+  xs_trace e{nullptr, 0, nullptr};
+  if (!t || !t->buf || !t->count) return e;
+  return *t;
+}
+
+extern "C" int xs_gemm(const void* a, int64_t lda, const void* b, int64_t ldb, void* c,
+                       int64_t ldc, int32_t M, int32_t N, int32_t K, const xs_trace* trace,
+                       void* stream) {
+  if (!a || !b || !c) return XS_EINVAL;
+  if (!gemm_shape_ok(lda, ldb, M, N, K) || ldc < N || ldc % 8) return XS_EUNSUPPORTED;
+  if (M == 0) return XS_OK;
+  WinSet none{};
+  none.n = 0;
+  ScatterArgs sa{};
+  const int tiles = ((M + kBM - 1) / kBM) * (N / kBN);
+  const int grid = std::min(tiles, xs_host::persistent_grid(0));
+  hipLaunchKernelGGL(gemm_tiles_kernel<KIND_PLAIN>, dim3(grid), dim3(kThreads), 0,
+                     static_cast<hipStream_t>(stream), static_cast<const uint16_t*>(a), lda,
+                     static_cast<const uint16_t*>(b), ldb, static_cast<char*>(c), ldc * 2, M, N,
+                     K, sa, none, trace_or_empty(trace));
+  return xs_host::launch_status();
+}
+
+static int scatter_setup(const xs_scatter_desc* desc, int32_t M, int32_t N, const xs_window* win,
+                         int32_t W, ScatterArgs* sa, WinSet* ws, int* kind) {
+  if (!desc || !win) return XS_EINVAL;
+  *sa = ScatterArgs{};
+  if (desc->kind == XS_SCATTER_ROW_BLOCK) {
+    const int rpd = desc->rows_per_dest;
+    if (rpd <= 0 || M % rpd || M / rpd != W) return XS_EINVAL;
+    if (rpd % kBM) return XS_EUNSUPPORTED;
+    sa->rpd = rpd;
+    int rc = xs_host::make_winset(win, W, static_cast<int64_t>(N) * 2, ws);
+    if (rc) return rc;
+    for (int d = 0; d < W; ++d)
+      if (ws->cap[d] < rpd) return XS_EINVAL;
+    *kind = KIND_ROW_BLOCK;
+    return XS_OK;
+  }
+  if (desc->kind == XS_SCATTER_HEAD_GROUP) {
+    const int np = desc->n_proj, nh = desc->n_heads, hd = desc->head_dim, hpg = desc->heads_per_group;
+    if (np <= 0 || nh <= 0 || hd <= 0 || hpg <= 0 || nh % hpg || N != np * nh * hd ||
+        nh / hpg != W)
+      return XS_EINVAL;
+    if (hd % 8) return XS_EUNSUPPORTED;
+    sa->n_proj = np;
+    sa->n_heads = nh;
+    sa->head_dim = hd;
+    sa->hpg = hpg;
+    int rc = xs_host::make_winset(win, W, static_cast<int64_t>(hd) * 2, ws);
+    if (rc) return rc;
+    for (int d = 0; d < W; ++d)
+      if (ws->cap[d] < static_cast<int64_t>(np) * hpg * M) return XS_EINVAL;
+    *kind = KIND_HEAD_GROUP;
+    return XS_OK;
+  }
+  return XS_EINVAL;
+}
+
+extern "C" int xs_gemm_scatter(const void* a, int64_t lda, const void* b, int64_t ldb, int32_t M,
+                               int32_t N, int32_t K, const xs_scatter_desc* desc,
+                               const xs_window* win, int32_t W, const xs_trace* trace,
+                               void* stream) {
+  if (!a || !b) return XS_EINVAL;
+  if (!gemm_shape_ok(lda, ldb, M, N, K)) return XS_EUNSUPPORTED;
+  ScatterArgs sa;
+  WinSet ws;
+  int kind = 0;
+  int rc = scatter_setup(desc, M, N, win, W, &sa, &ws, &kind);
+  if (rc) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (M > 0) {
+    const int tiles = ((M + kBM - 1) / kBM) * (N / kBN);
+    const int grid = std::min(tiles, xs_host::persistent_grid(0));
+    if (kind == KIND_ROW_BLOCK)
+      hipLaunchKernelGGL(gemm_tiles_kernel<KIND_ROW_BLOCK>, dim3(grid), dim3(kThreads), 0, st,
+                         static_cast<const uint16_t*>(a), lda, static_cast<const uint16_t*>(b), ldb,
+                         nullptr, 0, M, N, K, sa, ws, trace_or_empty(trace));
+    else
+      hipLaunchKernelGGL(gemm_tiles_kernel<KIND_HEAD_GROUP>, dim3(grid), dim3(kThreads), 0, st,
+                         static_cast<const uint16_t*>(a), lda, static_cast<const uint16_t*>(b), ldb,
+                         nullptr, 0, M, N, K, sa, ws, trace_or_empty(trace));
+    if (xs_host::launch_status()) return XS_EHIP;
+  }
+  return xs_host::signal_windows(ws, st);
+}
+
+extern "C" int xs_scatter_copy(const void* c, int64_t ldc, int32_t M, int32_t N,
+                               const xs_scatter_desc* desc, const xs_window* win, int32_t W,
+                               void* stream) {
+  if (!c || M < 0 || N <= 0 || N % 8 || ldc < N || ldc % 8) return XS_EINVAL;
+  ScatterArgs sa;
+  WinSet ws;
+  int kind = 0;
+  int rc = scatter_setup(desc, M, N, win, W, &sa, &ws, &kind);
+  if (rc) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (M > 0) {
+    const int grid = std::min((M + 3) / 4, 8192);
+    if (kind == KIND_ROW_BLOCK)
+      hipLaunchKernelGGL(scatter_copy_kernel<KIND_ROW_BLOCK>, dim3(grid), dim3(256), 0, st,
+                         static_cast<const char*>(c), ldc * 2, M, N, sa, ws);
+    else
+      hipLaunchKernelGGL(scatter_copy_kernel<KIND_HEAD_GROUP>, dim3(grid), dim3(256), 0, st,
+                         static_cast<const char*>(c), ldc * 2, M, N, sa, ws);
+    if (xs_host::launch_status()) return XS_EHIP;
+  }
+  return xs_host::signal_windows(ws, st);
+}

@@ -1,0 +1,238 @@
+"""Buffers and calls of one rank's expert-parallel layer share, through the C ABI.
+
+This module only allocates torch device memory, uploads inputs and marshals arguments to
+libxstage.so; all arithmetic and data movement of the layer happen in the HIP kernels.
+bf16 tensors are held as int16 storage of the bf16 bit patterns.
+"""
+from __future__ import annotations
+
+import ctypes as C
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+from . import xstage as X
+
+
+def _dev_bits(a: np.ndarray, device) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(device)
+
+
+@dataclass
+class Shape:
+    n_src: int
+    T: int
+    H: int
+    E: int
+    k: int
+    I: int
+    W: int
+    e_begin: int
+    n_experts: int
+    src: int = 0
+    renormalize: int = 0
+    expert_mode: int = X.XS_EXPERT_SWIGLU
+    cap: int | None = None
+
+    @property
+    def epw(self) -> int:
+        return self.E // self.W
+
+    @property
+    def n_cwin(self) -> int:
+        return self.n_experts // self.epw
+
+
+class EPLayer:
+    """Owns every device buffer of one EP layer call (inputs, layout, windows, outputs)."""
+
+    def __init__(self, s: Shape, device="cuda", combine_host: bool = False, sentinel: bool = True):
+        self.s = s
+        self.dev = torch.device(device)
+        cap = s.cap if s.cap is not None else s.n_src * s.T * min(s.k, s.epw)
+        self.cap = cap
+        d = self.dev
+        i32 = torch.int32
+        self.logits = torch.zeros((s.n_src, s.T, s.E), dtype=torch.float32, device=d)
+        self.x_all = torch.zeros((s.n_src, s.T, s.H), dtype=torch.int16, device=d)
+        self.w1 = torch.zeros((s.n_experts, 2 * s.I, s.H), dtype=torch.int16, device=d) \
+            if s.expert_mode == X.XS_EXPERT_SWIGLU else None
+        self.w2 = torch.zeros((s.n_experts, s.H, s.I), dtype=torch.int16, device=d) \
+            if s.expert_mode == X.XS_EXPERT_SWIGLU else None
+        self.topk_idx = torch.zeros((s.n_src, s.T, s.k), dtype=i32, device=d)
+        self.topk_w = torch.zeros((s.n_src, s.T, s.k), dtype=torch.float32, device=d)
+        self.expert_counts = torch.zeros((s.n_src, s.E), dtype=i32, device=d)
+        self.src_base = torch.zeros((s.n_src, s.E), dtype=i32, device=d)
+        self.expert_offsets = torch.zeros((s.E,), dtype=i32, device=d)
+        self.dest_counts = torch.zeros((s.W,), dtype=i32, device=d)
+        self.slot_row = torch.zeros((s.n_src, s.T, s.k), dtype=i32, device=d)
+        self.row_src = torch.full((s.W, cap), -1, dtype=i32, device=d)
+        fill = -1 if sentinel else 0
+        self.dwin = torch.full((s.W, cap, s.H), fill, dtype=torch.int16, device=d) if sentinel \
+            else torch.empty((s.W, cap, s.H), dtype=torch.int16, device=d)
+        self.combine_host = combine_host
+        if combine_host:
+            self._host = HostCoherent(s.n_src * s.T * s.k * s.H * 2)
+            self.cwin = self._host.view.view(s.n_src, s.T * s.k, s.H)
+            self.cwin.fill_(fill)
+        else:
+            self.cwin = torch.full((s.n_src, s.T * s.k, s.H), fill, dtype=torch.int16, device=d) if sentinel \
+                else torch.empty((s.n_src, s.T * s.k, s.H), dtype=torch.int16, device=d)
+        h_rows = s.n_cwin * cap
+        self.h_ws = torch.zeros((h_rows, s.I if s.I else 1), dtype=torch.int16, device=d)
+        self.y_ws = torch.zeros((h_rows, s.H), dtype=torch.int16, device=d)
+        self.out = torch.zeros((s.T, s.H), dtype=torch.int16, device=d)
+        self.status = torch.zeros((1,), dtype=i32, device=d)
+        self._dwins = X.windows([X.window(self.dwin[w]) for w in range(s.W)])
+        self._cwins = X.windows([self._cwin_desc(i) for i in range(s.n_src)])
+        self.L = self._layer_struct()
+        nb = C.c_int64()
+        X.check(X.xs_ep_layer_workspace_bytes(C.byref(self.L), C.byref(nb)), "workspace")
+        self.workspace = torch.zeros((max(1, nb.value),), dtype=torch.uint8, device=d)
+
+    def _cwin_desc(self, i):
+        t = self.cwin[i]
+        return X.xs_window(t.data_ptr(), t.shape[0], t.stride(0) * 2, None)
+
+    def _layer_struct(self) -> X.xs_ep_layer:
+        s = self.s
+        L = X.xs_ep_layer()
+        for f in ("n_src", "T", "H", "E", "k", "I", "W", "e_begin", "n_experts", "src", "renormalize",
+                  "expert_mode"):
+            setattr(L, f, getattr(s, f))
+        L.cap = self.cap
+        L.logits = self.logits.data_ptr()
+        L.x = self.x_all[s.src].data_ptr()
+        L.w1 = X.ptr(self.w1)
+        L.w2 = X.ptr(self.w2)
+        L.topk_idx = self.topk_idx.data_ptr()
+        L.topk_w = self.topk_w.data_ptr()
+        L.expert_counts = self.expert_counts.data_ptr()
+        L.src_base = self.src_base.data_ptr()
+        L.expert_offsets = self.expert_offsets.data_ptr()
+        L.dest_counts = self.dest_counts.data_ptr()
+        L.slot_row = self.slot_row.data_ptr()
+        L.row_src = self.row_src.data_ptr()
+        L.dispatch_win = C.cast(self._dwins, C.POINTER(X.xs_window))
+        L.combine_win = C.cast(self._cwins, C.POINTER(X.xs_window))
+        L.h_ws = self.h_ws.data_ptr()
+        L.h_rows = self.h_ws.shape[0]
+        L.y_ws = self.y_ws.data_ptr()
+        L.out = self.out.data_ptr()
+        return L
+
+    # -------------------------------------------------------------------------- inputs
+    def upload(self, logits: np.ndarray, x_bits: np.ndarray, w1_bits=None, w2_bits=None):
+        self.logits.copy_(torch.from_numpy(np.ascontiguousarray(logits, dtype=np.float32)))
+        self.x_all.copy_(_dev_bits(x_bits, "cpu"))
+        if w1_bits is not None:
+            for i in range(w1_bits.shape[0]):   # expert by expert to bound host staging
+                self.w1[i].copy_(_dev_bits(w1_bits[i], "cpu"))
+                self.w2[i].copy_(_dev_bits(w2_bits[i], "cpu"))
+        torch.cuda.synchronize(self.dev)
+
+    @property
+    def stream(self):
+        return torch.cuda.current_stream(self.dev).cuda_stream
+
+    # -------------------------------------------------------------------------- steps
+    def route(self):
+        s = self.s
+        X.check(X.xs_route_topk_softmax(self.logits.data_ptr(), s.n_src * s.T, s.E, s.k, s.renormalize,
+                                        self.topk_idx.data_ptr(), self.topk_w.data_ptr(), self.stream),
+                "route")
+
+    def layout(self):
+        s = self.s
+        ws = self.workspace
+        X.check(X.xs_dispatch_layout(self.topk_idx.data_ptr(), s.n_src, s.T, s.k, s.E, s.W, self.cap,
+                                     self.expert_counts.data_ptr(), self.src_base.data_ptr(),
+                                     self.expert_offsets.data_ptr(), self.dest_counts.data_ptr(),
+                                     self.slot_row.data_ptr(), self.row_src.data_ptr(), ws.data_ptr(),
+                                     ws.numel(), self.status.data_ptr(), self.stream), "layout")
+
+    def dispatch(self, src: int):
+        s = self.s
+        X.check(X.xs_dispatch(self.x_all[src].data_ptr(), s.T, s.H, self.topk_idx[src].data_ptr(),
+                              self.slot_row[src].data_ptr(), s.k, s.E, self._dwins, s.W,
+                              self.status.data_ptr(), self.stream), "dispatch")
+
+    def expert_ffn(self):
+        ws = self.workspace
+        X.check(X.xs_expert_ffn(C.byref(self.L), ws.data_ptr(), ws.numel(), self.status.data_ptr(),
+                                self.stream), "expert_ffn")
+
+    def combine_send(self):
+        X.check(X.xs_combine_send(C.byref(self.L), self.status.data_ptr(), self.stream), "combine_send")
+
+    def combine_reduce(self):
+        s = self.s
+        c = self.cwin[s.src]
+        X.check(X.xs_combine_reduce(c.data_ptr(), c.stride(0) * 2, self.topk_w[s.src].data_ptr(), s.T, s.k,
+                                    s.H, self.out.data_ptr(), self.stream), "combine_reduce")
+
+    def prefill_other_sources(self, remote_combine_bits: np.ndarray | None = None):
+        """Untimed set-up standing in for the other ranks: route + layout of every source,
+        dispatch of every source other than ``src`` and, optionally, the rows of this rank's
+        combine buffer that other ranks' experts would write."""
+        self.route()
+        self.layout()
+        for s in range(self.s.n_src):
+            if s != self.s.src:
+                self.dispatch(s)
+        if remote_combine_bits is not None:
+            self.cwin[self.s.src].copy_(_dev_bits(remote_combine_bits, "cpu"))
+        torch.cuda.synchronize(self.dev)
+
+    def fused(self, pacing: X.xs_pacing | None = None, trace: X.xs_trace | None = None):
+        ws = self.workspace
+        X.check(X.xs_fused_ep_layer(C.byref(self.L), C.byref(pacing) if pacing is not None else None,
+                                    C.byref(trace) if trace is not None else None, ws.data_ptr(),
+                                    ws.numel(), self.status.data_ptr(), self.stream), "fused_ep_layer")
+
+    def unfused(self):
+        self.route()
+        self.layout()
+        self.dispatch(self.s.src)
+        self.expert_ffn()
+        self.combine_send()
+        self.combine_reduce()
+
+
+def pacing(policy=X.XS_POLICY_INTERLEAVE, lead=1, chunk=0, max_producers=0, wave_tiles=0, gap_ns=0,
+           spin_timeout_us=0, withhold_row=-1, t_l1_us=0.0, t_l2_us=0.0, model=None) -> X.xs_pacing:
+    p = X.xs_pacing(policy, lead, chunk, max_producers, wave_tiles, gap_ns, spin_timeout_us, withhold_row,
+                    t_l1_us, t_l2_us, None)
+    if model is not None:
+        p._model_ref = model
+        p.model = C.pointer(model)
+    return p
+
+
+class HostCoherent:
+    """Fine-grained host-coherent memory (hipHostMalloc with hipHostMallocCoherent): a slow
+    store sink whose writes cross the fabric to host memory. ``view`` is a CPU tensor over it;
+    ``ptr`` is the address kernels store to."""
+
+    _hip = None
+    COHERENT = 0x40000000
+
+    def __init__(self, nbytes: int):
+        if HostCoherent._hip is None:
+            HostCoherent._hip = C.CDLL("libamdhip64.so")
+            HostCoherent._hip.hipHostMalloc.argtypes = [C.POINTER(C.c_void_p), C.c_size_t, C.c_uint]
+            HostCoherent._hip.hipHostFree.argtypes = [C.c_void_p]
+        p = C.c_void_p()
+        rc = HostCoherent._hip.hipHostMalloc(C.byref(p), C.c_size_t(nbytes), C.c_uint(self.COHERENT))
+        if rc != 0 or not p.value:
+            raise RuntimeError(f"hipHostMalloc({nbytes}) failed: {rc}")
+        self.ptr = p.value
+        self.nbytes = nbytes
+        arr = np.ctypeslib.as_array(C.cast(p, C.POINTER(C.c_int16)), shape=(nbytes // 2,))
+        self.view = torch.from_numpy(arr)
+
+    def free(self):
+        if self.ptr:
+            HostCoherent._hip.hipHostFree(C.c_void_p(self.ptr))
+            self.ptr = 0

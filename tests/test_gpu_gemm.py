@@ -1,0 +1,151 @@
+"""GPU parity of the MFMA GEMM and its scatter epilogues (TP row blocks, Ulysses head
+groups) against the CPU oracle, through the C ABI."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import scatter as osc
+from oracle.ep import f64_to_bf16_bits
+from gpu_helpers import assert_close, dev_bits, host_bits, require_gpu, xs
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _gemm(a_bits, bt_bits):
+    X = xs()
+    M, K = a_bits.shape
+    N = bt_bits.shape[0]
+    a, b = dev_bits(a_bits), dev_bits(bt_bits)
+    c = torch.full((M, N), -1, dtype=torch.int16, device="cuda")
+    X.check(X.xs_gemm(a.data_ptr(), K, b.data_ptr(), K, c.data_ptr(), N, M, N, K, None, _stream()))
+    torch.cuda.synchronize()
+    return host_bits(c)
+
+
+@pytest.mark.parametrize("M,N,K", [(300, 512, 192), (1, 256, 64), (256, 256, 64), (513, 768, 1024)])
+def test_gemm_ragged_matches_oracle(M, N, K):
+    a = synth.normal_bf16(0, 5, (M, K))
+    b = synth.normal_bf16(0, 6, (K, N), std=0.05)
+    c = _gemm(a, np.ascontiguousarray(b.T))
+    assert_close(c, osc.gemm(a, b), f"gemm {M}x{N}x{K}")
+
+
+def test_gemm_integer_operands_bitexact():
+    # |sums| < 2^24: fp32 accumulation is exact in any order, so the rounded bits are unique
+    a = synth.int_valued_bf16(0, 1, (384, 320))
+    b = synth.int_valued_bf16(0, 2, (320, 512))
+    c = _gemm(a, np.ascontiguousarray(b.T))
+    assert np.array_equal(c, f64_to_bf16_bits(osc.gemm(a, b)))
+
+
+def _windows_rowblock(W, rpd, N):
+    X = xs()
+    win = torch.full((W, rpd, N), -1, dtype=torch.int16, device="cuda")
+    return win, X.windows([X.window(win[d]) for d in range(W)])
+
+
+def _tp(a_bits, b_bits, rpd, serial=False):
+    X = xs()
+    M, K = a_bits.shape
+    N = b_bits.shape[1]
+    W = M // rpd
+    a, bt = dev_bits(a_bits), dev_bits(np.ascontiguousarray(b_bits.T))
+    win, wins = _windows_rowblock(W, rpd, N)
+    desc = X.xs_scatter_desc(X.XS_SCATTER_ROW_BLOCK, rpd, 0, 0, 0, 0)
+    if serial:
+        c = torch.empty((M, N), dtype=torch.int16, device="cuda")
+        X.check(X.xs_gemm(a.data_ptr(), K, bt.data_ptr(), K, c.data_ptr(), N, M, N, K, None, _stream()))
+        X.check(X.xs_scatter_copy(c.data_ptr(), N, M, N, desc, wins, W, _stream()))
+    else:
+        X.check(X.xs_gemm_scatter(a.data_ptr(), K, bt.data_ptr(), K, M, N, K, desc, wins, W, None, _stream()))
+    torch.cuda.synchronize()
+    return host_bits(win)
+
+
+def test_tp_identity_b_copies_row_blocks_bitexact():
+    a = synth.normal_bf16(0, 5, (1024, 256))
+    b = synth.to_bf16_bits(np.eye(256, dtype=np.float32))
+    win = _tp(a, b, 256)
+    assert np.array_equal(win, a.reshape(4, 256, 256))
+
+
+def test_tp_full_size_sampled_and_fused_equals_serial():
+    cfg = synth.TP_ROWBLOCK
+    inp = synth.tp_inputs(cfg, 0)
+    rpd = cfg.M // cfg.W
+    fused = _tp(inp["a"], inp["b"], rpd)
+    serial = _tp(inp["a"], inp["b"], rpd, serial=True)
+    assert np.array_equal(fused, serial)
+    g = np.random.default_rng(0)
+    rows = np.concatenate([[0, cfg.M - 1, rpd - 1, rpd], g.choice(cfg.M, 28, replace=False)])
+    ref = osc.gemm(inp["a"][rows], inp["b"])
+    got = np.stack([fused[m // rpd, m % rpd] for m in rows])
+    assert_close(got, ref, "tp sampled rows")
+
+
+def _sp(x_bits, w_bits, nh, hd, hpg, serial=False):
+    X = xs()
+    S, Dm = x_bits.shape
+    N = w_bits.shape[1]
+    G = nh // hpg
+    x, wt = dev_bits(x_bits), dev_bits(np.ascontiguousarray(w_bits.T))
+    win = torch.full((G, 3, hpg, S, hd), -1, dtype=torch.int16, device="cuda")
+    wins = X.windows([X.xs_window(win[g].data_ptr(), 3 * hpg * S, hd * 2, None) for g in range(G)])
+    desc = X.xs_scatter_desc(X.XS_SCATTER_HEAD_GROUP, 0, 3, nh, hd, hpg)
+    if serial:
+        c = torch.empty((S, N), dtype=torch.int16, device="cuda")
+        X.check(X.xs_gemm(x.data_ptr(), Dm, wt.data_ptr(), Dm, c.data_ptr(), N, S, N, Dm, None, _stream()))
+        X.check(X.xs_scatter_copy(c.data_ptr(), N, S, N, desc, wins, G, _stream()))
+    else:
+        X.check(X.xs_gemm_scatter(x.data_ptr(), Dm, wt.data_ptr(), Dm, S, N, Dm, desc, wins, G, None, _stream()))
+    torch.cuda.synchronize()
+    return host_bits(win)
+
+
+def test_sp_small_matches_oracle_bitexact_on_identity():
+    S, nh, hd, hpg = 300, 8, 32, 2
+    N = 3 * nh * hd
+    x = synth.normal_bf16(0, 7, (S, N))
+    w = synth.to_bf16_bits(np.eye(N, dtype=np.float32))
+    win = _sp(x, w, nh, hd, hpg)
+    _, ref = osc.sp_head_group_scatter(x, w, nh, hd, hpg)
+    assert np.array_equal(win, ref)
+
+
+def test_sp_full_size_sampled_and_fused_equals_serial():
+    cfg = synth.SP_QKV
+    inp = synth.sp_inputs(cfg, 0)
+    fused = _sp(inp["x"], inp["w"], cfg.n_heads, cfg.head_dim, cfg.heads_per_group)
+    serial = _sp(inp["x"], inp["w"], cfg.n_heads, cfg.head_dim, cfg.heads_per_group, serial=True)
+    assert np.array_equal(fused, serial)
+    g = np.random.default_rng(2)
+    rows = np.concatenate([[0, cfg.S - 1], g.choice(cfg.S, 14, replace=False)])
+    ref = osc.gemm(inp["x"][rows], inp["w"])      # [rows, 3*Dm]
+    got = np.empty_like(ref)
+    for c in range(ref.shape[1]):
+        gg, which, lh, dd = osc.sp_window_index(c, cfg.n_heads, cfg.head_dim, cfg.heads_per_group)
+        got_c = fused[gg, which, lh, rows, dd]
+        got[:, c] = got_c
+    assert_close(got.astype(np.uint16), ref, "sp sampled rows")
+
+
+def test_scatter_rejects_bad_descriptors():
+    X = xs()
+    a = torch.zeros((512, 64), dtype=torch.int16, device="cuda")
+    b = torch.zeros((256, 64), dtype=torch.int16, device="cuda")
+    win, wins = _windows_rowblock(2, 256, 256)
+    bad = X.xs_scatter_desc(X.XS_SCATTER_ROW_BLOCK, 200, 0, 0, 0, 0)
+    assert X.xs_gemm_scatter(a.data_ptr(), 64, b.data_ptr(), 64, 512, 256, 64, bad, wins, 2, None,
+                             None) != X.XS_OK
+    assert X.xs_gemm(a.data_ptr(), 64, b.data_ptr(), 64, a.data_ptr(), 64, 512, 100, 64, None,
+                     None) == X.XS_EUNSUPPORTED
