@@ -1,0 +1,228 @@
+"""Benchmark of the fused expert-parallel layer share on one MI355X.
+
+One step = one pass of the whole hot path over one batch: route (all sources) -> dispatch
+layout -> dispatch stores of this rank's tokens -> persistent Linear-1 / Linear-2 kernel with
+the combine-send epilogue -> combine-reduce. Workload: one rank's share of a
+DeepSeek-V3-like layer (8 ranks x 4096 tokens, H=7168, 256 experts / 32 local, top-8,
+SwiGLU I=2048, 8 destination windows in HBM), synthetic seeded inputs, bf16 with fp32
+accumulation. Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+METRIC = "fused EP layer µs + GEMM MFMA util % + dispatch/combine store GB/s, 1 MI355X"
+MFMA_PEAK_BF16 = 2.5e15      # dense bf16 FLOP/s
+HBM_PEAK = 8.0e12            # B/s
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--routing", choices=["uniform", "zipf"], default="uniform")
+    p.add_argument("--policy", choices=["burst", "interleave", "chunk"], default="interleave")
+    p.add_argument("--lead", type=int, default=0, help="0 = the anti-starvation knee")
+    p.add_argument("--chunk", type=int, default=2)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-phases", action="store_true")
+    p.add_argument("--seed", type=int, default=0)
+    return p.parse_args()
+
+
+def cpu_baseline(cfg, inp, rank, seed):
+    """The oracle, untuned, on a bounded sample of the same workload, scaled to one layer."""
+    from oracle import ep as oep
+    threads = len(os.sched_getaffinity(0))
+    t0 = time.perf_counter()
+    idx = np.empty((cfg.n_src, cfg.T, cfg.k), np.int32)
+    w = np.empty((cfg.n_src, cfg.T, cfg.k), np.float32)
+    for s in range(cfg.n_src):
+        idx[s], w[s] = oep.route_topk_softmax(inp["logits"][s], cfg.k)
+    lay = oep.dispatch_layout(idx, cfg.E, cfg.W)
+    t_route_layout = time.perf_counter() - t0
+    # dispatch: the first n_tok tokens of this rank into windows sized for them
+    n_tok = 512
+    t1 = time.perf_counter()
+    cap_s = int(lay["dest_counts"].max())
+    sub = idx[rank:rank + 1, :n_tok]
+    lay_s = oep.dispatch_layout(sub, cfg.E, cfg.W)
+    oep.dispatch(inp["x"][rank:rank + 1, :n_tok], sub, lay_s["slot_row"], cfg.E, cfg.W,
+                 int(lay_s["dest_counts"].max()))
+    t_disp = (time.perf_counter() - t1) * cfg.T / n_tok
+    # expert FFN: two local experts on all their rows, scaled by total rows / sampled rows
+    experts = list(range(rank * cfg.E_local, (rank + 1) * cfg.E_local))
+    total = lay["expert_counts"].sum(0)
+    rows_all = int(sum(total[e] for e in experts))
+    t2 = time.perf_counter()
+    rows_s = 0
+    g = np.random.default_rng(seed)
+    for i in (0, 1):
+        m = int(total[experts[i]])
+        xr = synth_rows(g, m, cfg.H)
+        oep.expert_ffn(xr, inp["w1"][i], inp["w2"][i])
+        rows_s += m
+    t_ffn = (time.perf_counter() - t2) * rows_all / max(1, rows_s)
+    # combine-reduce of n_tok tokens
+    t3 = time.perf_counter()
+    cb = inp["fill"][: n_tok * cfg.k]
+    oep.combine_reduce(cb, w[rank, :n_tok])
+    t_comb = (time.perf_counter() - t3) * cfg.T / n_tok
+    wall = time.perf_counter() - t0
+    total_s = t_route_layout + t_disp + t_ffn + t_comb
+    return {"value": total_s * 1e6, "unit": "us", "cores": threads, "kind": "oracle",
+            "sample": (f"route+layout of all {cfg.n_src}x{cfg.T} tokens; dispatch and combine-reduce of "
+                       f"{n_tok} tokens scaled x{cfg.T // n_tok}; expert FFN of 2 of {cfg.E_local} local "
+                       f"experts ({rows_s} of {rows_all} rows) scaled by rows; {wall:.1f} s of CPU time"),
+            "cpu": platform.processor() or platform.machine(),
+            "phases_us": {"route_layout": t_route_layout * 1e6, "dispatch": t_disp * 1e6,
+                          "expert_ffn": t_ffn * 1e6, "combine_reduce": t_comb * 1e6}}
+
+
+def synth_rows(g, m, H):
+    import synth
+    return synth.to_bf16_bits(g.standard_normal((m, H), dtype=np.float32))
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {a.gpus}); this build has no multi-GPU path",
+              file=sys.stderr)
+        sys.exit(2)
+    import dataclasses
+    import torch
+    import synth
+    from paper_2607_23264_amd import xstage as X
+    from paper_2607_23264_amd.layer import EPLayer, Shape, pacing
+
+    torch.cuda.set_device(0)
+    cfg = dataclasses.replace(synth.EP_DSV3_SHARE, routing=a.routing)
+    t0 = time.time()
+    log(f"[bench] generating inputs for {cfg.name} ({a.routing})")
+    inp = {"logits": synth.ep_logits(cfg, a.seed), "x": synth.ep_x(cfg, a.seed)}
+    rank = 0
+    if a.routing == "zipf":
+        from oracle.ep import route_topk_softmax  # only to pick the most-loaded rank for the sample
+        loads = np.zeros(cfg.W, np.int64)
+        for s in range(cfg.n_src):
+            loads += np.bincount(route_topk_softmax(inp["logits"][s], cfg.k)[0].ravel() // cfg.E_local,
+                                 minlength=cfg.W)
+        rank = int(loads.argmax())
+    cfg = dataclasses.replace(cfg, rank=rank)
+    experts = synth.computed_experts(cfg)
+    inp["w1"], inp["w2"] = synth.ep_weights(cfg, experts, a.seed)
+    inp["fill"] = synth.ep_remote_combine_fill(cfg, a.seed)
+    log(f"[bench] inputs ready in {time.time() - t0:.1f} s; uploading")
+    s = Shape(cfg.n_src, cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.W, experts[0], len(experts), src=rank)
+    lay = EPLayer(s, sentinel=False)
+    lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
+    lay.prefill_other_sources(inp["fill"])
+    pol = {"burst": pacing(X.XS_POLICY_BURST),
+           "interleave": pacing(X.XS_POLICY_INTERLEAVE, lead=a.lead),
+           "chunk": pacing(X.XS_POLICY_CHUNK, lead=a.lead, chunk=a.chunk)}
+    ev = X.HipEvents(2 * a.steps + 2)
+    lay.L.ffn_event_begin = None
+    lay.L.ffn_event_end = None
+    for _ in range(a.warmup):
+        lay.fused(pol[a.policy])
+    torch.cuda.synchronize()
+    log(f"[bench] warmup done; timing {a.steps} steps ({a.policy})")
+    stream = torch.cuda.current_stream().cuda_stream
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(a.steps):
+        lay.L.ffn_event_begin = ev.ev[2 * i]
+        lay.L.ffn_event_end = ev.ev[2 * i + 1]
+        lay.fused(pol[a.policy])
+    stop.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    ffn_ms = [ev.elapsed_ms(2 * i, 2 * i + 1) for i in range(a.steps)]
+    lay.L.ffn_event_begin = None
+    lay.L.ffn_event_end = None
+    status = int(lay.status.item())
+    if status:
+        log(f"[bench] device status {status}: {X.xs_strerror(status).decode()}")
+        sys.exit(1)
+    ms_per_step = total_ms / a.steps
+    rows = int(lay.dest_counts[rank].item())
+    flops = 6.0 * cfg.H * cfg.I * rows
+    ffn_avg = float(np.mean(ffn_ms))
+    achieved_tflops = flops / (ffn_avg * 1e-3) / 1e12
+    log(f"[bench] {ms_per_step * 1e3:.1f} us/step, FFN kernel {ffn_avg * 1e3:.1f} us "
+        f"({achieved_tflops:.1f} TFLOP/s, {rows} rows)")
+
+    res = {"metric": METRIC, "value": ms_per_step * 1e3, "unit": "us", "n_gpus": 1, "steps": a.steps,
+           "warmup": a.warmup, "ms_per_step": ms_per_step, "higher_is_better": False, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": f"{cfg.name} ({a.routing} routing, rank {rank}; one rank's EP share)",
+                      "policy": a.policy, "lead_rows": a.lead, "rows_computed": rows,
+                      "global_tokens": cfg.n_src * cfg.T, "seq_len": cfg.T}}
+    res["mfma_util_pct"] = 100.0 * achieved_tflops * 1e12 / MFMA_PEAK_BF16
+    res["roofline"] = {"bound": "mfma", "kernel": "ep_ffn_kernel (persistent Linear-1 + Linear-2)",
+                       "achieved": achieved_tflops, "peak": MFMA_PEAK_BF16 / 1e12, "unit": "TFLOP/s",
+                       "frac": achieved_tflops * 1e12 / MFMA_PEAK_BF16, "traffic": None,
+                       "flops_per_launch": flops, "avg_launch_us": ffn_avg * 1e3}
+
+    if not a.no_phases:
+        log("[bench] phase breakdown (unfused calls)")
+        ph = {}
+        reps = 5
+
+        def timed(fn):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            fn()
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / reps * 1e3
+
+        ph["route_us"] = timed(lay.route)
+        ph["layout_us"] = timed(lay.layout)
+        ph["dispatch_us"] = timed(lambda: lay.dispatch(rank))
+        ph["expert_ffn_unfused_us"] = timed(lay.expert_ffn)
+        ph["combine_send_us"] = timed(lay.combine_send)
+        ph["combine_reduce_us"] = timed(lay.combine_reduce)
+        disp_bytes = cfg.T * cfg.k * cfg.H * 2
+        comb_bytes = rows * cfg.H * 2
+        ph["dispatch_store_GBps"] = disp_bytes / (ph["dispatch_us"] * 1e-6) / 1e9
+        ph["combine_send_store_GBps"] = comb_bytes / (ph["combine_send_us"] * 1e-6) / 1e9
+        ph["combine_reduce_GBps"] = (cfg.T * cfg.k * cfg.H * 2 + cfg.T * cfg.H * 2) / (ph["combine_reduce_us"] * 1e-6) / 1e9
+        for name, p in pol.items():
+            ph[f"fused_{name}_us"] = timed(lambda p=p: lay.fused(p))
+        res["phases"] = ph
+        res["store_GBps"] = {"dispatch": ph["dispatch_store_GBps"], "combine_send": ph["combine_send_store_GBps"],
+                             "frac_of_hbm_peak_dispatch": ph["dispatch_store_GBps"] * 1e9 / HBM_PEAK,
+                             "frac_of_hbm_peak_combine_send": ph["combine_send_store_GBps"] * 1e9 / HBM_PEAK}
+        log("[bench] " + ", ".join(f"{k}={v:.1f}" for k, v in ph.items()))
+    if int(lay.status.item()):
+        log("[bench] device status set during phases")
+        sys.exit(1)
+    del lay
+    torch.cuda.empty_cache()
+    if not a.no_cpu_baseline:
+        log("[bench] oracle on the host (bounded sample)")
+        res["cpu_baseline"] = cpu_baseline(cfg, inp, rank, a.seed)
+        log(f"[bench] oracle sample: {res['cpu_baseline']['value']:.0f} us/layer equivalent")
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -152,6 +152,8 @@ typedef struct xs_ep_layer {
   int64_t h_rows;             /* >= (n_experts / (E / W)) * cap */
   void* y_ws;                 /* device bf16 [h_rows][H]; only used by the unfused path */
   void* out;                  /* device bf16 [T][H], combined output of source `src` */
+  void* ffn_event_begin;      /* optional hipEvent_t pair recorded on `stream` right before */
+  void* ffn_event_end;        /* and after the expert-FFN kernel launch(es); may be NULL */
 } xs_ep_layer;
 
 enum { XS_EXPERT_SWIGLU = 0, XS_EXPERT_IDENTITY = 1 };
@@ -160,7 +162,9 @@ enum { XS_EXPERT_SWIGLU = 0, XS_EXPERT_IDENTITY = 1 };
  *   XS_POLICY_BURST      Expert-Wave (Sec. 4.3): per wave of experts, all Linear-1 tiles
  *                        then all Linear-2 tiles (whose epilogues are the store bursts).
  *   XS_POLICY_INTERLEAVE cross-wave interleaving (App. A.2, Alg. 1) with lead D =
- *                        lead_rows >= 1 rows of Linear-1 over Linear-2.
+ *                        lead_rows rows of Linear-1 over Linear-2; lead_rows = 0 takes the
+ *                        anti-starvation knee of App. A.2, ceil(grid / P1) with P1 = I / 128
+ *                        Linear-1 tiles per row.
  *   XS_POLICY_CHUNK      Alg. 1 with at most chunk_tiles consecutive Linear-2 tiles before
  *                        a ready Linear-1 tile is forced.
  *   XS_POLICY_AUTO       CHUNK with chunk_tiles chosen from `model`: the largest run of

@@ -118,7 +118,7 @@ __global__ __launch_bounds__(1024) void ep_plan_kernel(const int* __restrict__ e
 }
 
 __device__ __forceinline__ void ep_l1_tile(const EpArgs& a, int p, int nt, bool fused,
-                                           uint16_t* lds, char** rowptr) {
+                                           char* lds, char** rowptr) {
   const int tid = threadIdx.x;
   const int x = a.row_expert[p];
   const int e = a.e_begin + x;
@@ -130,7 +130,7 @@ __device__ __forceinline__ void ep_l1_tile(const EpArgs& a, int p, int nt, bool 
   const uint16_t* A = reinterpret_cast<const uint16_t*>(
       a.dwin.base[dl] + static_cast<int64_t>(a.expert_offsets[e] + m0) * a.dwin.stride[dl]);
   const uint16_t* B = a.w1 + static_cast<int64_t>(x) * 2 * a.I * a.H;
-  f32x16 acc[4][2];
+  Acc acc;
   gemm_mainloop(A, lda, rows, B, a.H, nt * (kBN / 2), a.I, true, a.H, acc, lds);
   const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
   if (tid < rows)
@@ -140,7 +140,8 @@ __device__ __forceinline__ void ep_l1_tile(const EpArgs& a, int p, int nt, bool 
   __syncthreads();
   store_rows(lds, kEpiPitchH, kBN / 2, rows, rowptr);
   if (fused) {
-    __threadfence();   // each wave: its h stores complete and visible at agent scope
+    // The workgroup barrier orders every wave's h stores before thread 0's agent-scope
+    // release (one L2 writeback per tile instead of one per wave).
     __syncthreads();
     if (tid == 0 && p != a.withhold_row)
       __hip_atomic_fetch_add(&a.l1_done[p], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
@@ -161,12 +162,14 @@ __device__ __forceinline__ void ep_l1_tile(const EpArgs& a, int p, int nt, bool 
 }
 
 // Returns false if the wait for row p's Linear-1 tiles expired (the tile is then skipped).
+// Polls with relaxed agent-scope loads; one acquire fence once the row is complete (an
+// acquire load per poll would invalidate the caches on every iteration).
 __device__ __forceinline__ bool ep_wait_row(const EpArgs& a, int p, int* flag) {
   if (threadIdx.x == 0) {
     int ok = 1;
-    if (__hip_atomic_load(&a.l1_done[p], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < a.P1) {
+    if (__hip_atomic_load(&a.l1_done[p], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < a.P1) {
       const uint64_t t0 = wall_ticks();
-      while (__hip_atomic_load(&a.l1_done[p], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) <
+      while (__hip_atomic_load(&a.l1_done[p], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <
              a.P1) {
         if (wall_ticks() - t0 > static_cast<uint64_t>(a.timeout_ticks)) {
           ok = 0;
@@ -176,6 +179,7 @@ __device__ __forceinline__ bool ep_wait_row(const EpArgs& a, int p, int* flag) {
         __builtin_amdgcn_s_sleep(2);
       }
     }
+    if (ok) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     *flag = ok;
   }
   __syncthreads();
@@ -185,7 +189,7 @@ __device__ __forceinline__ bool ep_wait_row(const EpArgs& a, int p, int* flag) {
 }
 
 __device__ __forceinline__ void ep_l2_tile(const EpArgs& a, int p, int nt, bool fused,
-                                           uint16_t* lds, char** rowptr, int* flag) {
+                                           char* lds, char** rowptr, int* flag) {
   const int tid = threadIdx.x;
   const uint64_t t0 = a.tr.buf ? wall_ticks() : 0;
   if (fused && !ep_wait_row(a, p, flag)) return;
@@ -196,7 +200,7 @@ __device__ __forceinline__ void ep_l2_tile(const EpArgs& a, int p, int nt, bool 
   const uint16_t* A = a.h + static_cast<int64_t>(a.exp_hrow[x] + m0) * a.I;
   const uint16_t* B = a.w2 + static_cast<int64_t>(x) * a.H * a.I;
   const int n0 = nt * kBN;
-  f32x16 acc[4][2];
+  Acc acc;
   gemm_mainloop(A, a.I, rows, B, a.I, n0, 0, false, a.I, acc, lds);
   const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
   if (tid < rows) {
@@ -245,7 +249,7 @@ __device__ __forceinline__ int xcd_instance_ep(int b, int G) {
 
 __global__ __launch_bounds__(kThreads, 1) void ep_ffn_kernel(EpArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
-  uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
+  char* lds = smem;
   char** rowptr = reinterpret_cast<char**>(smem + kLdsRowPtrOff);
   int* flag = reinterpret_cast<int*>(smem + kLdsMiscOff);
   const int P = a.meta[0];
@@ -526,7 +530,9 @@ static int run_ffn(const xs_ep_layer* L, const EpArgs& base, int mode, int l2_co
   if (trace && trace->buf && trace->count) a.tr = *trace;
   int grid = xs_host::persistent_grid(pc ? pc->max_producers : 0);
   a.policy = pc ? pc->policy : XS_POLICY_INTERLEAVE;
-  a.lead = pc && pc->lead_rows > 0 ? pc->lead_rows : 1;
+  // lead 0 = the anti-starvation knee of App. A.2, ceil(b_n K / (2 I)) = ceil(G / P1) rows:
+  // one round of Linear-1 tiles over all producers
+  a.lead = pc && pc->lead_rows > 0 ? pc->lead_rows : (grid + a.P1 - 1) / a.P1;
   a.chunk = pc ? pc->chunk_tiles : 0;
   if (a.policy == XS_POLICY_INTERLEAVE) a.chunk = 0;
   if (a.policy == XS_POLICY_AUTO) {
@@ -560,9 +566,15 @@ extern "C" int xs_expert_ffn(const xs_ep_layer* L, void* workspace, int64_t work
   }
   rc = launch_plan(L, a, 0, st);
   if (rc) return rc;
+  if (L->ffn_event_begin && hipEventRecord(static_cast<hipEvent_t>(L->ffn_event_begin), st) != hipSuccess)
+    return XS_EHIP;
   rc = run_ffn(L, a, 1, 0, nullptr, nullptr, dev_status, st);
   if (rc) return rc;
-  return run_ffn(L, a, 2, 0, nullptr, nullptr, dev_status, st);
+  rc = run_ffn(L, a, 2, 0, nullptr, nullptr, dev_status, st);
+  if (rc) return rc;
+  if (L->ffn_event_end && hipEventRecord(static_cast<hipEvent_t>(L->ffn_event_end), st) != hipSuccess)
+    return XS_EHIP;
+  return XS_OK;
 }
 
 extern "C" int xs_combine_send(const xs_ep_layer* L, int32_t* dev_status, void* stream) {
@@ -622,8 +634,13 @@ extern "C" int xs_fused_ep_layer(const xs_ep_layer* L, const xs_pacing* pacing,
     const int wave_tiles = pacing && pacing->wave_tiles > 0 ? pacing->wave_tiles : grid;
     rc = launch_plan(L, a, wave_tiles, st);
     if (rc) return rc;
+    if (L->ffn_event_begin &&
+        hipEventRecord(static_cast<hipEvent_t>(L->ffn_event_begin), st) != hipSuccess)
+      return XS_EHIP;
     rc = run_ffn(L, a, 3, 1, pacing, trace, dev_status, st);
     if (rc) return rc;
+    if (L->ffn_event_end && hipEventRecord(static_cast<hipEvent_t>(L->ffn_event_end), st) != hipSuccess)
+      return XS_EHIP;
   }
   rc = xs_host::signal_windows(cws, st);
   if (rc) return rc;

@@ -21,6 +21,21 @@ __device__ __forceinline__ int xcd_instance(int b, int G) {
   return (G % 8) ? b : (b % 8) * (G / 8) + b / 8;
 }
 
+// Work index -> output tile, grouped by kGroupM M-tiles: consecutive work indices walk down
+// kGroupM tile rows, then across. With 32 instances per XCD taking 32 consecutive work
+// indices per round, each XCD's L2 serves a 4 x 8 block of tiles: 4 A row-blocks and 8 B
+// column-blocks instead of 1 and 32.
+constexpr int kGroupM = 4;
+__device__ __forceinline__ void grouped_tile(int w, int tm, int tn, int* mb, int* nb) {
+  const int per_group = kGroupM * tn;
+  const int g = w / per_group;
+  const int first = g * kGroupM;
+  const int gm = min(kGroupM, tm - first);
+  const int local = w - g * per_group;
+  *mb = first + local % gm;
+  *nb = local / gm;
+}
+
 __device__ __forceinline__ void trace_tile(const xs_trace& tr, int kind, int tile, uint64_t t0,
                                            uint64_t t1, uint64_t t2) {
   uint32_t i = atomicAdd(tr.count, 1u);
@@ -53,17 +68,18 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tiles_kernel(
     char* __restrict__ C, int64_t ldc_bytes, int M, int N, int K, ScatterArgs sa, WinSet win,
     xs_trace tr) {
   __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
-  uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
+  char* lds = smem;
   char** rowptr = reinterpret_cast<char**>(smem + kLdsRowPtrOff);
   const int tid = threadIdx.x;
   const int tm = (M + kBM - 1) / kBM, tn = N / kBN, ntiles = tm * tn;
   const int G = gridDim.x;
   for (int t = xcd_instance(blockIdx.x, G); t < ntiles; t += G) {
-    const int mb = t / tn, nb = t - mb * tn;
+    int mb, nb;
+    grouped_tile(t, tm, tn, &mb, &nb);
     const int m0 = mb * kBM, n0 = nb * kBN;
     const int rows = min(kBM, M - m0);
     const uint64_t t0 = tr.buf ? wall_ticks() : 0;
-    f32x16 acc[4][2];
+    Acc acc;
     gemm_mainloop(A + static_cast<int64_t>(m0) * lda, lda, rows, B, ldb, n0, 0, false, K, acc, lds);
     const uint64_t t1 = tr.buf ? wall_ticks() : 0;
     if (KIND != KIND_HEAD_GROUP && tid < rows) {
@@ -83,7 +99,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tiles_kernel(
     if (KIND == KIND_HEAD_GROUP) {
       const int pc = tid & 31;
       for (int r = tid >> 5; r < rows; r += kThreads / 32) {
-        u32x4 v = *reinterpret_cast<const u32x4*>(lds + r * kEpiPitch + pc * 8);
+        u32x4 v = *reinterpret_cast<const u32x4*>(lds + (r * kEpiPitch + pc * 8) * 2);
         *reinterpret_cast<u32x4*>(head_group_dst(win, sa, M, m0 + r, n0 + pc * 8)) = v;
       }
     } else {

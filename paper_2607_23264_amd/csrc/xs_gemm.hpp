@@ -1,159 +1,200 @@
-// MFMA bf16 GEMM core for gfx950: 256x256 output tile, K step 64, 512 threads (8 waves as
-// 2 (M) x 4 (N), each wave 128 x 64 = 4 x 2 blocks of v_mfma_f32_32x32x16_bf16), operands
-// double-buffered in LDS (2 x 64 KiB) and staged through registers one K step ahead.
+// MFMA bf16 GEMM core for gfx950: 256x256 output tile, K step 64, 256 threads = 4 waves, one
+// per SIMD, as 2 (M) x 2 (N) waves of 128 x 128 each = 4 x 4 blocks of
+// v_mfma_f32_32x32x16_bf16 (256 fp32 accumulators per lane).
 //
-// LDS operand layout: row-major [256][64] bf16 per operand, 128 B per row split into eight
-// 16-byte pieces; piece c of row r sits at position c ^ ((r >> 1) & 7), so the 16 lanes of a
-// ds_read_b128 / ds_write_b128 phase touch 16 distinct 16-byte bank groups.
+// Operands move global -> LDS with gfx950's direct 128-bit loads (global_load_lds_dwordx4):
+// no staging registers and no LDS store instructions. Two LDS stages of [256][64] bf16 per
+// operand (2 x 64 KiB); the loads of stage k+1 are issued right after the barrier that
+// opens stage k and land while stage k is multiplied.
 //
-// C = A B^T: A rows are K-contiguous, B is output-major ([N][K], K-contiguous), so both MFMA
-// operands are 16-byte contiguous loads from LDS.
+// LDS operand layout: 128 B per row in eight 16-byte pieces; logical piece c of row r sits at
+// physical position c ^ ((r >> 1) & 7). A direct load writes 64 consecutive pieces (8 rows)
+// per wave instruction, so the swizzle is applied on the global side: the lane that fills
+// physical piece p of row r fetches logical piece p ^ ((r >> 1) & 7). The 16 lanes of each
+// ds_read_b128 phase then hit 16 distinct 16-byte bank groups.
+//
+// C = A B^T: A rows are K-contiguous and B is output-major ([N][K], K-contiguous), so both
+// MFMA operands are 16-byte contiguous reads from LDS.
 #pragma once
 #include "xs_common.hpp"
 
 namespace xs {
 
-constexpr int kBM = 256, kBN = 256, kBK = 64, kThreads = 512;
-constexpr int kOpElems = (kBM + kBN) * kBK;                 // one LDS stage, elements
-constexpr int kLdsOperandBytes = 2 * kOpElems * 2;           // 131072
+constexpr int kBM = 256, kBN = 256, kBK = 64, kThreads = 256;
+constexpr int kOpBytes = kBM * kBK * 2;                      // one operand stage: 32 KiB
+constexpr int kStageBytes = 2 * kOpBytes;                    // A + B: 64 KiB
 constexpr int kEpiPitch = kBN + 8;                           // bf16 per staged output row
 constexpr int kEpiPitchH = kBN / 2 + 8;                      // SwiGLU output rows (128 wide)
 constexpr int kLdsEpiBytes = kBM * kEpiPitch * 2;            // 135168
 constexpr int kLdsRowPtrOff = kLdsEpiBytes;                  // 256 row pointers
 constexpr int kLdsMiscOff = kLdsRowPtrOff + kBM * 8;         // small scheduler scratch
 constexpr int kLdsBytes = kLdsMiscOff + 64;
+static_assert(2 * kStageBytes <= kLdsEpiBytes, "operand stages must fit under the epilogue tile");
+
+// address-space-qualified pointees for the direct-load builtin (C-style casts convert)
+typedef __attribute__((address_space(3))) void lds_void;
+typedef const __attribute__((address_space(1))) void glob_void;
 
 // B tile row r -> weight row. SwiGLU tiles interleave gate and up rows in blocks of 32 so
-// that each wave's 64 columns hold 32 gate columns and the 32 matching up columns.
+// that each wave's 128 columns hold gate/up pairs for 64 output columns.
 __device__ __forceinline__ int b_row_map(int r, int n0, int half, bool swiglu) {
   return swiglu ? n0 + ((r >> 5) & 1) * half + (r >> 6) * 32 + (r & 31) : n0 + r;
 }
 
-__device__ __forceinline__ void zero_acc(f32x16 (&acc)[4][2]) {
+typedef f32x16 Acc[4][4];
+
+__device__ __forceinline__ void zero_acc(Acc& acc) {
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
 }
 
-// acc += A[0:256, 0:K] * B[rows(0:256), 0:K]^T. Rows of A at or beyond a_rows read row
-// a_rows - 1 (their results are never stored). Ends with a block barrier.
+// s_waitcnt vmcnt(0) only (expcnt and lgkmcnt left at their maxima).
+__device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// acc = A[0:256, 0:K] * B[rows(0:256), 0:K]^T. Rows of A at or beyond a_rows read row
+// a_rows - 1 (their results are never stored). Ends with a block barrier, after which the
+// LDS may be reused.
 __device__ __forceinline__ void gemm_mainloop(const uint16_t* __restrict__ A, int64_t lda,
                                               int a_rows, const uint16_t* __restrict__ B,
                                               int64_t ldb, int b_n0, int b_half, bool swiglu,
-                                              int K, f32x16 (&acc)[4][2], uint16_t* lds) {
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wm = w >> 2, wn = w & 3;
-  const int pc = tid & 7, pr = tid >> 3;        // load piece / row of this thread
-  const uint16_t* ga[4];
-  const uint16_t* gb[4];
-  int soff[4];
+                                              int K, Acc& acc, char* lds) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  // direct-load sources: instruction i of wave w fills rows [32 i + 8 w, +8) of a stage; the
+  // swizzle term of those rows does not depend on i. 32-bit element offsets from the
+  // wave-uniform bases keep the per-lane state small (the bases stay in scalar registers).
+  const int lr = lane >> 3, lp = lane & 7;
+  const int c8 = (lp ^ ((4 * w + (lr >> 1)) & 7)) * 8;
+  uint32_t oa[8], ob[8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    int r = pr + 64 * i;
-    int ar = r < a_rows ? r : a_rows - 1;
-    ga[i] = A + static_cast<int64_t>(ar) * lda + pc * 8;
-    gb[i] = B + static_cast<int64_t>(b_row_map(r, b_n0, b_half, swiglu)) * ldb + pc * 8;
-    soff[i] = r * kBK + ((pc ^ ((r >> 1) & 7)) << 3);
+  for (int i = 0; i < 8; ++i) {
+    const int r = 32 * i + 8 * w + lr;
+    const int ar = r < a_rows ? r : a_rows - 1;
+    oa[i] = static_cast<uint32_t>(ar * lda + c8);
+    ob[i] = static_cast<uint32_t>(b_row_map(r, b_n0, b_half, swiglu) * ldb + c8);
   }
-  // fragment read offsets (elements) inside one operand stage
+  // fragment reads: row (wm*128 + i*32 + lane%32) of A, (wn*128 + j*32 + lane%32) of B
   const int swz = (lane >> 1) & 7;
   const int khalf = lane >> 5;
-  int aoff[4], boff[2];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) aoff[i] = (wm * 128 + i * 32 + (lane & 31)) * kBK;
-#pragma unroll
-  for (int j = 0; j < 2; ++j) boff[j] = kBM * kBK + (wn * 64 + j * 32 + (lane & 31)) * kBK;
+  const int arow = (wm * 128 + (lane & 31)) * kBK * 2;
+  const int brow = kOpBytes + (wn * 128 + (lane & 31)) * kBK * 2;
 
   zero_acc(acc);
   const int nk = K / kBK;
-  u32x4 ra[4], rb[4];
+  auto issue = [&](int kt) {
+    char* st = lds + (kt & 1) * kStageBytes;
+    const uint16_t* a0 = A + kt * kBK;
+    const uint16_t* b0 = B + kt * kBK;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    ra[i] = *reinterpret_cast<const u32x4*>(ga[i]);
-    rb[i] = *reinterpret_cast<const u32x4*>(gb[i]);
-  }
+    for (int i = 0; i < 8; ++i) {
+      const int off = (4 * i + w) * 1024;   // 64 pieces of 16 B
+      __builtin_amdgcn_global_load_lds((glob_void*)(a0 + oa[i]), (lds_void*)(st + off), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((glob_void*)(b0 + ob[i]), (lds_void*)(st + kOpBytes + off), 16,
+                                       0, 0);
+    }
+  };
+  // Software pipeline. Fragments are double-buffered in registers: the reads of k sub-step
+  // kk + 1 are in flight while the 16 MFMAs of sub-step kk issue (sched_group_barrier pins the
+  // MFMA / ds_read alternation; left alone the scheduler reuses one fragment register set and
+  // waits out every LDS read). At a stage boundary the first 8 MFMAs of the last sub-step are
+  // issued before the vmcnt wait and the barrier, so the matrix pipe keeps working while the
+  // workgroup synchronises; the reads of the next stage's first sub-step then overlap the
+  // remaining 8 MFMAs.
+  bf16x8 af[2][4], bfr[2][4];
+  auto frags = [&](const char* cur, int kk, int buf) {
+    const int piece = (((kk * 2 + khalf) ^ swz) << 4);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    *reinterpret_cast<u32x4*>(lds + soff[i]) = ra[i];
-    *reinterpret_cast<u32x4*>(lds + kBM * kBK + soff[i]) = rb[i];
+    for (int i = 0; i < 4; ++i)
+      af[buf][i] = *reinterpret_cast<const bf16x8*>(cur + arow + i * 32 * kBK * 2 + piece);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      bfr[buf][j] = *reinterpret_cast<const bf16x8*>(cur + brow + j * 32 * kBK * 2 + piece);
+  };
+  auto mma = [&](int buf, int i0, int i1) {
+#pragma unroll
+    for (int i = i0; i < i1; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[buf][i], bfr[buf][j], acc[i][j], 0, 0, 0);
+  };
+  issue(0);
+  wait_vm0();
+  __syncthreads();
+  if (nk > 1) issue(1);
+  frags(lds, 0, 0);
+  for (int kt = 0; kt < nk; ++kt) {
+    const char* cur = lds + (kt & 1) * kStageBytes;
+#pragma unroll
+    for (int kk = 0; kk < 3; ++kk) {
+      frags(cur, kk + 1, (kk + 1) & 1);
+      mma(kk & 1, 0, 4);
+#pragma unroll
+      for (int g = 0; g < 8; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one ds_read
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    }
+    // sub-step 3 (fragments in buffer 1): half the MFMAs, then the stage boundary
+    mma(1, 0, 2);
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    if (kt + 1 < nk) {
+      wait_vm0();          // this wave's loads of stage kt + 1 have landed
+      __syncthreads();     // every wave's have, and stage kt is no longer read
+      if (kt + 2 < nk) issue(kt + 2);
+      frags(lds + ((kt + 1) & 1) * kStageBytes, 0, 0);
+    }
+    mma(1, 2, 4);
   }
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    uint16_t* cur = lds + (kt & 1) * kOpElems;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      const int k0 = (kt + 1) * kBK;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        ra[i] = *reinterpret_cast<const u32x4*>(ga[i] + k0);
-        rb[i] = *reinterpret_cast<const u32x4*>(gb[i] + k0);
-      }
-    }
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int piece = ((kk * 2 + khalf) ^ swz) << 3;
-      bf16x8 af[4], bfr[2];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8*>(cur + aoff[i] + piece);
-#pragma unroll
-      for (int j = 0; j < 2; ++j) bfr[j] = *reinterpret_cast<const bf16x8*>(cur + boff[j] + piece);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-    if (more) {
-      uint16_t* nxt = lds + ((kt + 1) & 1) * kOpElems;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        *reinterpret_cast<u32x4*>(nxt + soff[i]) = ra[i];
-        *reinterpret_cast<u32x4*>(nxt + kBM * kBK + soff[i]) = rb[i];
-      }
-    }
-    __syncthreads();
-  }
 }
 
 // Accumulators -> bf16 tile in LDS, row-major [256][kEpiPitch].
-__device__ __forceinline__ void stage_tile(const f32x16 (&acc)[4][2], uint16_t* lds) {
+__device__ __forceinline__ void stage_tile(const Acc& acc, char* lds_bytes) {
+  uint16_t* lds = reinterpret_cast<uint16_t*>(lds_bytes);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int wm = w >> 2, wn = w & 3;
+  const int wm = w >> 1, wn = w & 1;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
-        int row = wm * 128 + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
-        int col = wn * 64 + j * 32 + (lane & 31);
+        const int row = wm * 128 + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
+        const int col = wn * 128 + j * 32 + (lane & 31);
         lds[row * kEpiPitch + col] = static_cast<uint16_t>(f2bf(acc[i][j][q]));
       }
 }
 
-// SwiGLU of a gate/up tile -> bf16 h tile [256][kEpiPitchH] in LDS (128 columns).
-__device__ __forceinline__ void stage_swiglu(const f32x16 (&acc)[4][2], uint16_t* lds) {
+// SwiGLU of a gate/up tile -> bf16 h tile [256][kEpiPitchH] in LDS (128 columns): blocks j
+// and j + 1 of a wave hold the gate and up values of the same 32 output columns.
+__device__ __forceinline__ void stage_swiglu(const Acc& acc, char* lds_bytes) {
+  uint16_t* lds = reinterpret_cast<uint16_t*>(lds_bytes);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int wm = w >> 2, wn = w & 3;
+  const int wm = w >> 1, wn = w & 1;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      float g = acc[i][0][q], u = acc[i][1][q];
-      float h = g / (1.f + __expf(-g)) * u;
-      int row = wm * 128 + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
-      int col = wn * 32 + (lane & 31);
-      lds[row * kEpiPitchH + col] = static_cast<uint16_t>(f2bf(h));
-    }
+    for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const float g = acc[i][2 * jj][q], u = acc[i][2 * jj + 1][q];
+        const float h = g / (1.f + __expf(-g)) * u;
+        const int row = wm * 128 + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
+        const int col = wn * 64 + jj * 32 + (lane & 31);
+        lds[row * kEpiPitchH + col] = static_cast<uint16_t>(f2bf(h));
+      }
 }
 
-// Stores staged rows [0, rows) through the per-row destination pointers in LDS.
-// cols = 256 (plain) or 128 (SwiGLU). Every piece is one 128-bit store.
-__device__ __forceinline__ void store_rows(const uint16_t* lds, int pitch, int cols, int rows,
+// Stores staged rows [0, rows) through the per-row destination pointers in LDS (null rows are
+// skipped). cols = 256 (plain) or 128 (SwiGLU). Every piece is one 128-bit store.
+__device__ __forceinline__ void store_rows(const char* lds_bytes, int pitch, int cols, int rows,
                                            char* const* rowptr) {
+  const uint16_t* lds = reinterpret_cast<const uint16_t*>(lds_bytes);
   const int tid = threadIdx.x;
   const int per_row = cols / 8;                // 16-byte pieces per row
   const int rows_per_pass = kThreads / per_row;

@@ -59,7 +59,7 @@ class xs_ep_layer(C.Structure):
                 ("expert_counts", vp), ("src_base", vp), ("expert_offsets", vp), ("dest_counts", vp),
                 ("slot_row", vp), ("row_src", vp), ("dispatch_win", C.POINTER(xs_window)),
                 ("combine_win", C.POINTER(xs_window)), ("h_ws", vp), ("h_rows", i64), ("y_ws", vp),
-                ("out", vp)]
+                ("out", vp), ("ffn_event_begin", vp), ("ffn_event_end", vp)]
 
 
 class xs_scatter_desc(C.Structure):
@@ -168,3 +168,42 @@ def windows(ws) -> C.Array:
 
 def trace(buf, count) -> xs_trace:
     return xs_trace(buf.data_ptr(), buf.numel() // 4, count.data_ptr())
+
+
+class HipEvents:
+    """Raw hipEvent_t handles (created with timing enabled) for the library to record
+    around a kernel on the caller's stream."""
+
+    _hip = None
+
+    def __init__(self, n: int):
+        if HipEvents._hip is None:
+            h = C.CDLL("libamdhip64.so")
+            h.hipEventCreate.argtypes = [C.POINTER(vp)]
+            h.hipEventDestroy.argtypes = [vp]
+            h.hipEventSynchronize.argtypes = [vp]
+            h.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), vp, vp]
+            h.hipEventRecord.argtypes = [vp, vp]
+            HipEvents._hip = h
+        self.ev = []
+        for _ in range(n):
+            e = vp()
+            if HipEvents._hip.hipEventCreate(C.byref(e)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            self.ev.append(e.value)
+
+    def record(self, i: int, stream) -> None:
+        if HipEvents._hip.hipEventRecord(self.ev[i], stream) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def elapsed_ms(self, i: int, j: int) -> float:
+        HipEvents._hip.hipEventSynchronize(self.ev[j])
+        ms = C.c_float()
+        if HipEvents._hip.hipEventElapsedTime(C.byref(ms), self.ev[i], self.ev[j]) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(ms.value)
+
+    def destroy(self):
+        for e in self.ev:
+            HipEvents._hip.hipEventDestroy(e)
+        self.ev = []
