@@ -325,7 +325,8 @@ int xs_model_fit(const xs_calib* c, xs_model* out);
 
 /* Remote-store microbenchmark (Sec. 3.1): K producer workgroups each store B bytes per
  * burst into `target` (HBM window or host-coherent sink), separated by a non-injecting
- * gap of gap_ns nanoseconds; n_bursts bursts per producer.
+ * gap of gap_ns nanoseconds; n_bursts (1..256) bursts per producer. Timestamps are kept
+ * on chip while the bursts run and written after the last one.
  *   mode XS_MB_PERIODIC   bursts back to back with the gap in between
  *   mode XS_MB_COMPLETION after each burst the producer waits for its stores to complete
  *                         (the completion-coupled counterfactual) before the gap
@@ -342,7 +343,7 @@ typedef struct xs_microbench_args {
   int32_t n_bursts;
   int32_t gap_ns;
   int32_t mode;
-  int32_t store_waves;    /* waves per producer issuing the stores (1..4) */
+  int32_t store_waves;    /* waves per producer issuing the stores (1..8) */
 } xs_microbench_args;
 
 int xs_xstage_microbench(const xs_microbench_args* args, const xs_trace* trace, void* stream);

@@ -8,14 +8,18 @@
 
 namespace xs {
 
+constexpr int kMaxBursts = 256;
+
+// Timestamps stay in LDS while the bursts run; one slot reservation per producer after the
+// last burst, so recording never sits between two bursts.
 __global__ void xstage_mb_kernel(char* __restrict__ target, int64_t target_bytes, int B,
                                  int n_bursts, int64_t gap_ticks, int mode, xs_trace tr) {
-  __shared__ uint64_t t_start;
+  __shared__ uint64_t ts[3][kMaxBursts];
   const int p = blockIdx.x, tid = threadIdx.x;
   const int pieces = B / 16;
   for (int b = 0; b < n_bursts; ++b) {
     __syncthreads();
-    if (tid == 0) t_start = wall_ticks();
+    if (tid == 0) ts[0][b] = wall_ticks();
     const int64_t off = ((static_cast<int64_t>(p) * n_bursts + b) * B) % target_bytes;
     u32x4* dst = reinterpret_cast<u32x4*>(target + off);
     u32x4 v;
@@ -28,17 +32,23 @@ __global__ void xstage_mb_kernel(char* __restrict__ target, int64_t target_bytes
     }
     if (mode == XS_MB_COMPLETION) __threadfence_system();
     __syncthreads();
-    const uint64_t t1 = wall_ticks();
     if (tid == 0) {
+      ts[1][b] = wall_ticks();
       spin_ticks(static_cast<uint64_t>(gap_ticks));
-      const uint64_t t2 = wall_ticks();
-      uint32_t i = atomicAdd(tr.count, 1u);
-      if (static_cast<int64_t>(i) < tr.capacity) {
-        uint64_t* r = tr.buf + static_cast<int64_t>(i) * 4;
+      ts[2][b] = wall_ticks();
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const uint32_t base = atomicAdd(tr.count, static_cast<uint32_t>(n_bursts));
+    for (int b = 0; b < n_bursts; ++b) {
+      const int64_t i = static_cast<int64_t>(base) + b;
+      if (i < tr.capacity) {
+        uint64_t* r = tr.buf + i * 4;
         r[0] = (static_cast<uint64_t>(p) << 32) | static_cast<uint32_t>(b);
-        r[1] = t_start;
-        r[2] = t1;
-        r[3] = t2;
+        r[1] = ts[0][b];
+        r[2] = ts[1][b];
+        r[3] = ts[2][b];
       }
     }
   }
@@ -49,9 +59,9 @@ __global__ void xstage_mb_kernel(char* __restrict__ target, int64_t target_bytes
 extern "C" int xs_xstage_microbench(const xs_microbench_args* a, const xs_trace* trace,
                                     void* stream) {
   if (!a || !trace || !trace->buf || !trace->count || !a->target) return XS_EINVAL;
-  if (a->K < 1 || a->K > 65535 || a->B_bytes < 1024 || a->B_bytes % 1024 || a->n_bursts < 1 ||
+  if (a->K < 1 || a->K > 65535 || a->B_bytes < 1024 || a->B_bytes % 1024 || a->n_bursts < 1 || a->n_bursts > xs::kMaxBursts ||
       a->gap_ns < 0 || (a->mode != XS_MB_PERIODIC && a->mode != XS_MB_COMPLETION) ||
-      a->store_waves < 1 || a->store_waves > 4)
+      a->store_waves < 1 || a->store_waves > 8)
     return XS_EINVAL;
   if (a->target_bytes < a->B_bytes || a->target_bytes % a->B_bytes ||
       (reinterpret_cast<uintptr_t>(a->target) & 15))

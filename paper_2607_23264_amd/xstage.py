@@ -203,6 +203,14 @@ class HipEvents:
             raise RuntimeError("hipEventElapsedTime failed")
         return float(ms.value)
 
+    @staticmethod
+    def elapsed_ms_pair(a, b) -> float:
+        HipEvents._hip.hipEventSynchronize(b)
+        ms = C.c_float()
+        if HipEvents._hip.hipEventElapsedTime(C.byref(ms), a, b) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(ms.value)
+
     def destroy(self):
         for e in self.ev:
             HipEvents._hip.hipEventDestroy(e)
