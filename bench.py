@@ -18,6 +18,7 @@ import time
 
 import numpy as np
 
+HERE = os.path.dirname(os.path.abspath(__file__))
 METRIC = "fused EP layer µs + GEMM MFMA util % + dispatch/combine store GB/s, 1 MI355X"
 MFMA_PEAK_BF16 = 2.5e15      # dense bf16 FLOP/s
 HBM_PEAK = 8.0e12            # B/s
@@ -38,12 +39,17 @@ def parse():
     p.add_argument("--chunk", type=int, default=2)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-phases", action="store_true")
+    p.add_argument("--policies", action="store_true",
+                   help="also time the fused layer under every pacing policy (phases)")
     p.add_argument("--seed", type=int, default=0)
     return p.parse_args()
 
 
-def cpu_baseline(cfg, inp, rank, seed):
-    """The oracle, untuned, on a bounded sample of the same workload, scaled to one layer."""
+def cpu_baseline(cfg, inp, rank, seed, ffn_budget_s=12.0, comb_budget_s=3.0):
+    """The oracle, untuned, on a bounded sample of the same layer share: route and layout of
+    every source's tokens, dispatch of this rank's tokens, the SwiGLU FFN of local experts on
+    as many rows as the layout gives each (synthetic rows of the dispatched distribution) and
+    the combine-reduce of this rank's tokens. BLAS threads = the host cores it may use."""
     from oracle import ep as oep
     threads = len(os.sched_getaffinity(0))
     t0 = time.perf_counter()
@@ -53,39 +59,43 @@ def cpu_baseline(cfg, inp, rank, seed):
         idx[s], w[s] = oep.route_topk_softmax(inp["logits"][s], cfg.k)
     lay = oep.dispatch_layout(idx, cfg.E, cfg.W)
     t_route_layout = time.perf_counter() - t0
-    # dispatch: the first n_tok tokens of this rank into windows sized for them
-    n_tok = 512
     t1 = time.perf_counter()
-    cap_s = int(lay["dest_counts"].max())
-    sub = idx[rank:rank + 1, :n_tok]
+    sub = idx[rank:rank + 1]
     lay_s = oep.dispatch_layout(sub, cfg.E, cfg.W)
-    oep.dispatch(inp["x"][rank:rank + 1, :n_tok], sub, lay_s["slot_row"], cfg.E, cfg.W,
+    oep.dispatch(inp["x"][rank:rank + 1], sub, lay_s["slot_row"], cfg.E, cfg.W,
                  int(lay_s["dest_counts"].max()))
-    t_disp = (time.perf_counter() - t1) * cfg.T / n_tok
-    # expert FFN: two local experts on all their rows, scaled by total rows / sampled rows
+    t_disp = time.perf_counter() - t1
     experts = list(range(rank * cfg.E_local, (rank + 1) * cfg.E_local))
     total = lay["expert_counts"].sum(0)
+    # the FFN and the combine-reduce run until a time budget is spent; their times are then
+    # scaled by the share of the work done (rows, tokens)
     rows_all = int(sum(total[e] for e in experts))
     t2 = time.perf_counter()
-    rows_s = 0
     g = np.random.default_rng(seed)
-    for i in (0, 1):
-        m = int(total[experts[i]])
-        xr = synth_rows(g, m, cfg.H)
-        oep.expert_ffn(xr, inp["w1"][i], inp["w2"][i])
-        rows_s += m
-    t_ffn = (time.perf_counter() - t2) * rows_all / max(1, rows_s)
-    # combine-reduce of n_tok tokens
+    rows_done, n_exp = 0, 0
+    for i, e in enumerate(experts):
+        m = int(total[e])
+        oep.expert_ffn(synth_rows(g, m, cfg.H), inp["w1"][i], inp["w2"][i])
+        rows_done += m
+        n_exp += 1
+        if time.perf_counter() - t2 > ffn_budget_s:
+            break
+    t_ffn = (time.perf_counter() - t2) * rows_all / max(1, rows_done)
     t3 = time.perf_counter()
-    cb = inp["fill"][: n_tok * cfg.k]
-    oep.combine_reduce(cb, w[rank, :n_tok])
-    t_comb = (time.perf_counter() - t3) * cfg.T / n_tok
+    tok, chunk = 0, 256
+    while tok < cfg.T:
+        oep.combine_reduce(inp["fill"][tok * cfg.k:(tok + chunk) * cfg.k], w[rank, tok:tok + chunk])
+        tok += chunk
+        if time.perf_counter() - t3 > comb_budget_s:
+            break
+    t_comb = (time.perf_counter() - t3) * cfg.T / tok
     wall = time.perf_counter() - t0
     total_s = t_route_layout + t_disp + t_ffn + t_comb
     return {"value": total_s * 1e6, "unit": "us", "cores": threads, "kind": "oracle",
-            "sample": (f"route+layout of all {cfg.n_src}x{cfg.T} tokens; dispatch and combine-reduce of "
-                       f"{n_tok} tokens scaled x{cfg.T // n_tok}; expert FFN of 2 of {cfg.E_local} local "
-                       f"experts ({rows_s} of {rows_all} rows) scaled by rows; {wall:.1f} s of CPU time"),
+            "sample": (f"route+layout of all {cfg.n_src}x{cfg.T} tokens and dispatch of rank {rank}'s "
+                       f"{cfg.T} tokens in full; SwiGLU FFN of {n_exp} of {cfg.E_local} local experts "
+                       f"({rows_done} of {rows_all} rows, synthetic rows) scaled by rows; combine-reduce "
+                       f"of {tok} of {cfg.T} tokens scaled by tokens; {wall:.1f} s of CPU time"),
             "cpu": platform.processor() or platform.machine(),
             "phases_us": {"route_layout": t_route_layout * 1e6, "dispatch": t_disp * 1e6,
                           "expert_ffn": t_ffn * 1e6, "combine_reduce": t_comb * 1e6}}
@@ -172,11 +182,19 @@ def main():
            "config": {"workload": f"{cfg.name} ({a.routing} routing, rank {rank}; one rank's EP share)",
                       "policy": a.policy, "lead_rows": a.lead, "rows_computed": rows,
                       "global_tokens": cfg.n_src * cfg.T, "seq_len": cfg.T}}
+    # algorithmic HBM bytes of one launch: dispatched rows read once, both weight matrices of
+    # every local expert read once, h written and read back once, output rows stored once
+    alg_bytes = 2.0 * (rows * cfg.H + len(experts) * 3 * cfg.H * cfg.I + 2 * rows * cfg.I + rows * cfg.H)
+    from paper_2607_23264_amd.profiling import read_traffic
+    tr = read_traffic(os.path.join(HERE, "profiles", "ep_ffn_kernel_dsv3_share_traffic.md"))
     res["mfma_util_pct"] = 100.0 * achieved_tflops * 1e12 / MFMA_PEAK_BF16
-    res["roofline"] = {"bound": "mfma", "kernel": "ep_ffn_kernel (persistent Linear-1 + Linear-2)",
+    res["roofline"] = {"bound": "mfma", "kernel": "ep_ffn_kernel<3> (persistent fused Linear-1 + Linear-2)",
                        "achieved": achieved_tflops, "peak": MFMA_PEAK_BF16 / 1e12, "unit": "TFLOP/s",
-                       "frac": achieved_tflops * 1e12 / MFMA_PEAK_BF16, "traffic": None,
-                       "flops_per_launch": flops, "avg_launch_us": ffn_avg * 1e3}
+                       "frac": achieved_tflops * 1e12 / MFMA_PEAK_BF16,
+                       "traffic": tr["traffic_bytes"] if tr else None,
+                       "flops_per_launch": flops, "algorithmic_bytes_per_launch": alg_bytes,
+                       "avg_launch_us": ffn_avg * 1e3,
+                       "hbm_GBps_algorithmic": alg_bytes / (ffn_avg * 1e-3) / 1e9}
 
     if not a.no_phases:
         log("[bench] phase breakdown (unfused calls)")
@@ -206,7 +224,8 @@ def main():
         ph["combine_send_store_GBps"] = comb_bytes / (ph["combine_send_us"] * 1e-6) / 1e9
         ph["combine_reduce_GBps"] = (cfg.T * cfg.k * cfg.H * 2 + cfg.T * cfg.H * 2) / (ph["combine_reduce_us"] * 1e-6) / 1e9
         for name, p in pol.items():
-            ph[f"fused_{name}_us"] = timed(lambda p=p: lay.fused(p))
+            if a.policies or name == a.policy:
+                ph[f"fused_{name}_us"] = timed(lambda p=p: lay.fused(p))
         res["phases"] = ph
         res["store_GBps"] = {"dispatch": ph["dispatch_store_GBps"], "combine_send": ph["combine_send_store_GBps"],
                              "frac_of_hbm_peak_dispatch": ph["dispatch_store_GBps"] * 1e9 / HBM_PEAK,

@@ -50,7 +50,6 @@ struct EpArgs {
   const int* wave_pos;
   const int* wave_row;
   int* l1_done;
-  int mode;                    // bit 0: Linear-1 tiles, bit 1: Linear-2 tiles
   int l2_combine;              // Linear-2 epilogue: 1 = combine windows, 0 = y rows
   int policy, lead, chunk, withhold_row;
   int64_t gap_ticks, timeout_ticks;
@@ -247,6 +246,9 @@ __device__ __forceinline__ int xcd_instance_ep(int b, int G) {
   return (G % 8) ? b : (b % 8) * (G / 8) + b / 8;
 }
 
+// MODE 3: fused Linear-1 + Linear-2 (the EP layer); 1 / 2: one GEMM stream only (unfused
+// expert FFN). A template parameter so each variant is its own kernel in a trace.
+template <int MODE>
 __global__ __launch_bounds__(kThreads, 1) void ep_ffn_kernel(EpArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
   char* lds = smem;
@@ -255,9 +257,9 @@ __global__ __launch_bounds__(kThreads, 1) void ep_ffn_kernel(EpArgs a) {
   const int P = a.meta[0];
   const int G = gridDim.x;
   const int g = xcd_instance_ep(blockIdx.x, G);
-  const bool fused = a.mode == 3;
-  const int n1 = (a.mode & 1) ? P * a.P1 : 0;
-  const int n2 = (a.mode & 2) ? P * a.P2 : 0;
+  constexpr bool fused = MODE == 3;
+  const int n1 = (MODE & 1) ? P * a.P1 : 0;
+  const int n2 = (MODE & 2) ? P * a.P2 : 0;
   if (fused && a.policy == XS_POLICY_BURST) {
     const int nw = a.meta[1], total = a.meta[2];
     int w = 0;
@@ -523,7 +525,6 @@ extern "C" int xs_ep_layer_workspace_bytes(const xs_ep_layer* L, int64_t* bytes)
 static int run_ffn(const xs_ep_layer* L, const EpArgs& base, int mode, int l2_combine,
                    const xs_pacing* pc, const xs_trace* trace, int32_t* dev_status, hipStream_t st) {
   EpArgs a = base;
-  a.mode = mode;
   a.l2_combine = l2_combine;
   a.status = dev_status;
   a.tr = xs_trace{nullptr, 0, nullptr};
@@ -543,7 +544,12 @@ static int run_ffn(const xs_ep_layer* L, const EpArgs& base, int mode, int l2_co
   a.gap_ticks = pc ? xs_host::ns_to_ticks(pc->gap_ns) : 0;
   const int64_t tmo_us = pc && pc->spin_timeout_us > 0 ? pc->spin_timeout_us : 2000000;
   a.timeout_ticks = xs_host::ns_to_ticks(tmo_us * 1000);
-  hipLaunchKernelGGL(ep_ffn_kernel, dim3(grid), dim3(kThreads), 0, st, a);
+  if (mode == 1)
+    hipLaunchKernelGGL(ep_ffn_kernel<1>, dim3(grid), dim3(kThreads), 0, st, a);
+  else if (mode == 2)
+    hipLaunchKernelGGL(ep_ffn_kernel<2>, dim3(grid), dim3(kThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL(ep_ffn_kernel<3>, dim3(grid), dim3(kThreads), 0, st, a);
   return xs_host::launch_status();
 }
 

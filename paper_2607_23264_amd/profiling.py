@@ -1,0 +1,168 @@
+"""rocprofv3 helpers: a plain copy of known size (the counter calibration) and summaries.
+
+  python -m paper_2607_23264_amd.profiling copy [--mib N] [--reps R]
+      R device-to-device copies of N MiB (torch's copy kernel). Under
+      `rocprofv3 --pmc FETCH_SIZE` / `--pmc WRITE_SIZE` the counters of these dispatches
+      against their known bytes give the scale factor of each counter.
+  python -m paper_2607_23264_amd.profiling stats --csv K.csv --command CMD --out F.md
+      Markdown summary of a `--kernel-trace --stats` kernel_stats.csv.
+  python -m paper_2607_23264_amd.profiling traffic --kernel NAME --fetch F.csv --write W.csv
+      --copy-fetch CF.csv --copy-write CW.csv --copy-bytes B --commands CMDS --out F.md
+      Per-dispatch HBM bytes of one kernel from two counter passes, each scaled by what the
+      same counter reads for the copy; writes a markdown summary whose `traffic-json:` line
+      the benchmark reads, keyed by the hash of the kernel's sources.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import json
+import os
+import re
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+# sources that define the fused expert-FFN kernel's code (a change to any of them makes a
+# stored traffic measurement stale)
+FFN_KERNEL_SOURCES = ("csrc/xs_ep_ffn.hip", "csrc/xs_gemm.hpp", "csrc/xs_common.hpp", "build.py")
+
+
+def sources_hash(paths=FFN_KERNEL_SOURCES) -> str:
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(HERE, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(md_path: str, kernel_hash: str | None = None):
+    """The `traffic-json:` record of a traffic summary, or None if absent or stale."""
+    try:
+        with open(md_path) as f:
+            for line in f:
+                if line.startswith("traffic-json:"):
+                    rec = json.loads(line[len("traffic-json:"):])
+                    if rec.get("sources_sha") != (kernel_hash or sources_hash()):
+                        return None
+                    return rec
+    except OSError:
+        return None
+    return None
+
+
+def _rows(path):
+    with open(path, newline="") as f:
+        return list(csv.DictReader(f))
+
+
+def _short(name: str) -> str:
+    m = re.match(r"(?:void )?([^(]*)", name)
+    return (m.group(1) if m else name).strip()
+
+
+def cmd_copy(a):
+    import torch
+    torch.cuda.set_device(0)
+    n = a.mib << 20
+    src = torch.ones(n // 2, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(a.reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(f"copy: {a.reps} x {n} bytes", flush=True)
+
+
+def cmd_stats(a):
+    rows = _rows(a.csv)
+    key = lambda r, *ks: next((r[k] for k in ks if k in r), None)
+    out = ["# rocprofv3 kernel statistics", "", "Command (run from the repository root):", "",
+           "```", a.command, "```", "", "| kernel | calls | average µs | min µs | max µs | total % |",
+           "|---|---:|---:|---:|---:|---:|"]
+    for r in rows:
+        name = _short(key(r, "Name", "KernelName", "Kernel_Name") or "?")
+        calls = key(r, "Calls")
+        avg = float(key(r, "AverageNs") or 0) / 1e3
+        mn = float(key(r, "MinNs") or 0) / 1e3
+        mx = float(key(r, "MaxNs") or 0) / 1e3
+        pct = float(key(r, "Percentage") or 0)
+        out.append(f"| `{name}` | {calls} | {avg:.1f} | {mn:.1f} | {mx:.1f} | {pct:.2f} |")
+    if a.note:
+        out += ["", a.note]
+    with open(a.out, "w") as f:
+        f.write("\n".join(out) + "\n")
+    print("\n".join(out))
+
+
+def _per_dispatch(path, kernel, counter):
+    vals = [float(r["Counter_Value"]) for r in _rows(path)
+            if r["Counter_Name"] == counter and _short(r["Kernel_Name"]).startswith(kernel)]
+    return vals
+
+
+def cmd_traffic(a):
+    fetch = _per_dispatch(a.fetch, a.kernel, "FETCH_SIZE")
+    write = _per_dispatch(a.write, a.kernel, "WRITE_SIZE")
+    cf = max(_per_dispatch(a.copy_fetch, a.copy_kernel, "FETCH_SIZE"))
+    cw = max(_per_dispatch(a.copy_write, a.copy_kernel, "WRITE_SIZE"))
+    kf = a.copy_bytes / (cf * 1024.0)      # true bytes per counted byte
+    kw = a.copy_bytes / (cw * 1024.0)
+    if not fetch or not write:
+        sys.exit(f"no {a.kernel} dispatches in the counter files")
+    mean = lambda v: sum(v) / len(v)
+    fb, wb = mean(fetch) * 1024.0 * kf, mean(write) * 1024.0 * kw
+    rec = {"kernel": a.kernel, "sources_sha": sources_hash(), "fetch_bytes": fb, "write_bytes": wb,
+           "traffic_bytes": fb + wb, "fetch_scale": kf, "write_scale": kw,
+           "dispatches": [len(fetch), len(write)], "algorithmic_bytes": a.algorithmic_bytes}
+    out = ["# HBM traffic per dispatch (rocprofv3 counters)", "",
+           f"Kernel: `{a.kernel}`", "", "Commands (run from the repository root, one counter pass each):", "",
+           "```", *a.commands.split(";;"), "```", "",
+           "FETCH_SIZE and WRITE_SIZE are read in KiB per dispatch and scaled by what the same counter",
+           f"reads for a plain copy of {a.copy_bytes} bytes (`{a.copy_kernel}`): "
+           f"FETCH_SIZE x {kf:.3f}, WRITE_SIZE x {kw:.3f}.", "",
+           "| quantity | value |", "|---|---:|",
+           f"| dispatches (fetch pass, write pass) | {len(fetch)}, {len(write)} |",
+           f"| FETCH_SIZE raw, KiB/dispatch (mean) | {mean(fetch):.0f} |",
+           f"| WRITE_SIZE raw, KiB/dispatch (mean) | {mean(write):.0f} |",
+           f"| copy FETCH_SIZE / WRITE_SIZE, KiB | {cf:.0f} / {cw:.0f} |",
+           f"| fetched bytes per dispatch (scaled) | {fb / 1e9:.3f} GB |",
+           f"| written bytes per dispatch (scaled) | {wb / 1e9:.3f} GB |",
+           f"| total HBM bytes per dispatch | {(fb + wb) / 1e9:.3f} GB |"]
+    if a.algorithmic_bytes:
+        out.append(f"| algorithmic bytes per dispatch | {a.algorithmic_bytes / 1e9:.3f} GB |")
+        out.append(f"| traffic / algorithmic | {(fb + wb) / a.algorithmic_bytes:.2f} |")
+    out += ["", "traffic-json: " + json.dumps(rec)]
+    with open(a.out, "w") as f:
+        f.write("\n".join(out) + "\n")
+    print("\n".join(out))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    c = sub.add_parser("copy")
+    c.add_argument("--mib", type=int, default=1024)
+    c.add_argument("--reps", type=int, default=3)
+    s = sub.add_parser("stats")
+    s.add_argument("--csv", required=True)
+    s.add_argument("--command", required=True)
+    s.add_argument("--out", required=True)
+    s.add_argument("--note", default="")
+    t = sub.add_parser("traffic")
+    t.add_argument("--kernel", required=True)
+    t.add_argument("--fetch", required=True)
+    t.add_argument("--write", required=True)
+    t.add_argument("--copy-fetch", required=True)
+    t.add_argument("--copy-write", required=True)
+    t.add_argument("--copy-bytes", type=float, required=True)
+    t.add_argument("--copy-kernel", default="__amd_rocclr_copyBuffer")
+    t.add_argument("--algorithmic-bytes", type=float, default=0.0)
+    t.add_argument("--commands", required=True, help="the counter commands, separated by ';;'")
+    t.add_argument("--out", required=True)
+    a = ap.parse_args()
+    {"copy": cmd_copy, "stats": cmd_stats, "traffic": cmd_traffic}[a.cmd](a)
+
+
+if __name__ == "__main__":
+    main()
