@@ -8,7 +8,9 @@
 // Operands move global -> LDS with gfx950's direct 128-bit loads (global_load_lds_dwordx4):
 // no staging registers and no LDS store instructions. Two LDS stages of [256][64] bf16 per
 // operand (2 x 64 KiB); the loads of stage k+1 are issued right after the barrier that
-// opens stage k and land while stage k is multiplied.
+// opens stage k and land while stage k is multiplied. (Measured alternatives that lost:
+// four or five stages of K step 32, whose extra barriers cost more than the deeper prefetch
+// gains, and loads through registers with LDS stores.)
 //
 // LDS operand layout: 128 B per row in eight 16-byte pieces; logical piece c of row r sits at
 // physical position c ^ ((r >> 1) & 7). A direct load writes 64 consecutive pieces (8 rows)
@@ -17,7 +19,14 @@
 // ds_read_b128 phase then hit 16 distinct 16-byte bank groups (no bank conflicts measured).
 //
 // C = A B^T: A rows are K-contiguous and B is output-major ([N][K], K-contiguous), so both
-// MFMA operands are 16-byte contiguous reads from LDS.
+// MFMA operands are 16-byte contiguous reads from LDS. The MFMA is issued with the B
+// fragment as its first operand, so each lane's accumulators hold four consecutive output
+// columns of one row per group (8-byte epilogue writes instead of 2-byte ones).
+//
+// Partial tiles (an expert's last 256-row block) skip the MFMAs and fragment reads of the
+// 32-row blocks that hold no valid row: each wave runs the pipeline instantiated for its
+// number of valid 32-row blocks (0 to 4); every instantiation issues the same loads and
+// barriers, so the workgroup stays in step.
 #pragma once
 #include "xs_common.hpp"
 
@@ -58,75 +67,65 @@ __device__ __forceinline__ void zero_acc(Acc& acc) {
 // s_waitcnt vmcnt(0) only (expcnt and lgkmcnt left at their maxima).
 __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
-// acc = A[0:256, 0:K] * B[rows(0:256), 0:K]^T. Rows of A at or beyond a_rows read row
-// a_rows - 1 (their results are never stored). Ends with a block barrier, after which the
-// LDS may be reused.
-__device__ __forceinline__ void gemm_mainloop(const uint16_t* __restrict__ A, int64_t lda,
-                                              int a_rows, const uint16_t* __restrict__ B,
-                                              int64_t ldb, int b_n0, int b_half, bool swiglu,
-                                              int K, Acc& acc, char* lds) {
+// Per-wave operand addressing, computed once per tile.
+struct TileAddr {
+  const char* a;          // A tile base (row 0, k 0)
+  const char* b;          // B base
+  uint32_t oa[4], ob[4];  // per-lane byte offsets of the four direct loads of each operand
+  int arow, brow;         // LDS byte offsets of this lane's fragment rows (A, B)
+  int w;                  // wave index (uniform)
+};
+
+// The software pipeline for a wave that multiplies NI of its four 32-row blocks.
+//
+// Fragments are double-buffered in registers: the reads of k sub-step kk + 1 are in flight
+// while the MFMAs of sub-step kk issue. sched_group_barrier pins the order (one MFMA, then
+// two fragment reads, three times, then the remaining MFMAs): left alone the scheduler reuses
+// one fragment register set and waits out every LDS read. At a stage boundary three quarters
+// of the last sub-step's MFMAs are issued before the vmcnt wait and the barrier, so the
+// matrix pipe keeps working while the workgroup synchronises; the next stage's first
+// fragments are read before the next loads are issued.
+template <int NI>
+__device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc, char* lds) {
   const int lane = threadIdx.x & 63;
-  // the wave index is uniform: keep it scalar so the LDS destinations (M0) are scalar math
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wm = w >> 2, wn = w & 3;
-  // direct-load sources: instruction i of wave w fills rows [64 i + 8 w, +8) of a stage; the
-  // swizzle term of those rows does not depend on i. 32-bit byte offsets from the
-  // wave-uniform bases keep the per-lane state small and let the loads use the
-  // scalar-base + vector-offset addressing form.
-  const int lr = lane >> 3, lp = lane & 7;
-  const int c16 = (lp ^ ((4 * w + (lr >> 1)) & 7)) * 16;
-  uint32_t oa[4], ob[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = 64 * i + 8 * w + lr;
-    const int ar = r < a_rows ? r : a_rows - 1;
-    oa[i] = static_cast<uint32_t>(ar * lda * 2 + c16);
-    ob[i] = static_cast<uint32_t>(b_row_map(r, b_n0, b_half, swiglu) * ldb * 2 + c16);
-  }
-  // fragment reads: row (wm*128 + i*32 + lane%32) of A, (wn*64 + j*32 + lane%32) of B
+  const int w = ta.w;
   const int swz = (lane >> 1) & 7;
   const int khalf = lane >> 5;
-  const int arow = (wm * 128 + (lane & 31)) * kBK * 2;
-  const int brow = kOpBytes + (wn * 64 + (lane & 31)) * kBK * 2;
-
-  zero_acc(acc);
-  const int nk = K / kBK;
   auto issue = [&](int kt) {
     char* st = lds + (kt & 1) * kStageBytes;
-    const char* a0 = reinterpret_cast<const char*>(A + kt * kBK);
-    const char* b0 = reinterpret_cast<const char*>(B + kt * kBK);
+    const char* a0 = ta.a + kt * kBK * 2;
+    const char* b0 = ta.b + kt * kBK * 2;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int off = (8 * i + w) * 1024;   // 64 pieces of 16 B
-      __builtin_amdgcn_global_load_lds((glob_void*)(a0 + oa[i]), (lds_void*)(st + off), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds((glob_void*)(b0 + ob[i]), (lds_void*)(st + kOpBytes + off), 16,
-                                       0, 0);
+      __builtin_amdgcn_global_load_lds((glob_void*)(a0 + ta.oa[i]), (lds_void*)(st + off), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((glob_void*)(b0 + ta.ob[i]), (lds_void*)(st + kOpBytes + off),
+                                       16, 0, 0);
     }
   };
-  // Software pipeline. Fragments are double-buffered in registers: the reads of k sub-step
-  // kk + 1 are in flight while the 8 MFMAs of sub-step kk issue (sched_group_barrier pins the
-  // MFMA / ds_read alternation; left alone the scheduler reuses one fragment register set and
-  // waits out every LDS read). At a stage boundary half the MFMAs of the last sub-step are
-  // issued before the vmcnt wait and the barrier, so the matrix pipe keeps working while the
-  // workgroup synchronises; the reads of the next stage's first sub-step then overlap the
-  // remaining MFMAs.
   bf16x8 af[2][4], bfr[2][2];
   auto frags = [&](const char* cur, int kk, int buf) {
+    if (NI == 0) return;
     const int piece = (((kk * 2 + khalf) ^ swz) << 4);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      af[buf][i] = *reinterpret_cast<const bf16x8*>(cur + arow + i * 32 * kBK * 2 + piece);
+    for (int i = 0; i < NI; ++i)
+      af[buf][i] = *reinterpret_cast<const bf16x8*>(cur + ta.arow + i * 32 * kBK * 2 + piece);
 #pragma unroll
     for (int j = 0; j < 2; ++j)
-      bfr[buf][j] = *reinterpret_cast<const bf16x8*>(cur + brow + j * 32 * kBK * 2 + piece);
+      bfr[buf][j] = *reinterpret_cast<const bf16x8*>(cur + ta.brow + j * 32 * kBK * 2 + piece);
   };
   auto mma = [&](int buf, int i0, int i1) {
 #pragma unroll
     for (int i = i0; i < i1; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[buf][i], bfr[buf][j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[buf][j], af[buf][i], acc[i][j], 0, 0, 0);
   };
+  // per sub-step: 2 NI MFMAs and NI + 2 fragment reads
+  constexpr int kReads = NI + 2, kMfma = 2 * NI;
+  constexpr int kPairs = kReads / 2, kOdd = kReads % 2;
+  constexpr int kRest = kMfma - kPairs - kOdd;
+  constexpr int kPre = NI < 3 ? NI : 3;
   issue(0);
   wait_vm0();
   __syncthreads();
@@ -137,60 +136,123 @@ __device__ __forceinline__ void gemm_mainloop(const uint16_t* __restrict__ A, in
 #pragma unroll
     for (int kk = 0; kk < 3; ++kk) {
       frags(cur, kk + 1, (kk + 1) & 1);
-      mma(kk & 1, 0, 4);
+      mma(kk & 1, 0, NI);
+      if (NI > 0) {
 #pragma unroll
-      for (int g = 0; g < 6; ++g) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one ds_read
+        for (int g = 0; g < kPairs; ++g) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // two ds_reads
+        }
+        if (kOdd) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        if (kRest > 0) __builtin_amdgcn_sched_group_barrier(0x008, kRest, 0);
       }
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     }
-    // sub-step 3 (fragments in buffer 1): half the MFMAs, then the stage boundary
-    mma(1, 0, 2);
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    // sub-step 3 (fragments in buffer 1): most MFMAs, then the stage boundary
+    mma(1, 0, kPre);
+    if (NI > 0) __builtin_amdgcn_sched_group_barrier(0x008, 2 * kPre, 0);
     if (kt + 1 < nk) {
       wait_vm0();          // this wave's loads of stage kt + 1 have landed
       __syncthreads();     // every wave's have, and stage kt is no longer read
-      if (kt + 2 < nk) issue(kt + 2);
       frags(lds + ((kt + 1) & 1) * kStageBytes, 0, 0);
+      if (kt + 2 < nk) issue(kt + 2);
     }
-    mma(1, 2, 4);
+    mma(1, kPre, NI);
+  }
+}
+
+// acc = A[0:256, 0:K] * B[rows(0:256), 0:K]^T. Rows of A at or beyond a_rows read row
+// a_rows - 1 and their 32-row blocks are skipped where a whole block is past a_rows (their
+// results are zero or stale and are never stored). Ends with a block barrier, after which the
+// LDS may be reused. Accumulator layout: acc[i][j][q] is output
+//   row wm*128 + 32 i + lane % 32, column wn*64 + 32 j + 8 (q / 4) + 4 (lane / 32) + q % 4.
+__device__ __forceinline__ void gemm_mainloop(const uint16_t* __restrict__ A, int64_t lda,
+                                              int a_rows, const uint16_t* __restrict__ B,
+                                              int64_t ldb, int b_n0, int b_half, bool swiglu,
+                                              int K, Acc& acc, char* lds) {
+  const int lane = threadIdx.x & 63;
+  // the wave index is uniform: keep it scalar so the LDS destinations (M0) are scalar math
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = w >> 2, wn = w & 3;
+  TileAddr ta;
+  ta.a = reinterpret_cast<const char*>(A);
+  ta.b = reinterpret_cast<const char*>(B);
+  ta.w = w;
+  // direct-load sources: instruction i of wave w fills rows [64 i + 8 w, +8) of a stage; the
+  // swizzle term of those rows does not depend on i. 32-bit byte offsets from the
+  // wave-uniform bases keep the per-lane state small and let the loads use the
+  // scalar-base + vector-offset addressing form.
+  const int lr = lane >> 3, lp = lane & 7;
+  const int c16 = (lp ^ ((4 * w + (lr >> 1)) & 7)) * 16;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = 64 * i + 8 * w + lr;
+    const int ar = r < a_rows ? r : a_rows - 1;
+    ta.oa[i] = static_cast<uint32_t>(ar * lda * 2 + c16);
+    ta.ob[i] = static_cast<uint32_t>(b_row_map(r, b_n0, b_half, swiglu) * ldb * 2 + c16);
+  }
+  // fragment reads: row (wm*128 + i*32 + lane%32) of A, (wn*64 + j*32 + lane%32) of B
+  ta.arow = (wm * 128 + (lane & 31)) * kBK * 2;
+  ta.brow = kOpBytes + (wn * 64 + (lane & 31)) * kBK * 2;
+  zero_acc(acc);
+  const int nk = K / kBK;
+  const int valid = a_rows - wm * 128;
+  const int ni = valid >= 128 ? 4 : (valid <= 0 ? 0 : (valid + 31) >> 5);
+  switch (__builtin_amdgcn_readfirstlane(ni)) {
+    case 4: mainloop_ni<4>(ta, nk, acc, lds); break;
+    case 3: mainloop_ni<3>(ta, nk, acc, lds); break;
+    case 2: mainloop_ni<2>(ta, nk, acc, lds); break;
+    case 1: mainloop_ni<1>(ta, nk, acc, lds); break;
+    default: mainloop_ni<0>(ta, nk, acc, lds); break;
   }
   __syncthreads();
 }
 
-// Accumulators -> bf16 tile in LDS, row-major [256][kEpiPitch].
-__device__ __forceinline__ void stage_tile(const Acc& acc, char* lds_bytes) {
-  uint16_t* lds = reinterpret_cast<uint16_t*>(lds_bytes);
+// Accumulators -> bf16 tile in LDS, row-major [256][kEpiPitch]; four columns per 8-byte write.
+__device__ __forceinline__ void stage_tile(const Acc& acc, char* lds) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w >> 2, wn = w & 3;
+  const int row0 = wm * 128 + (lane & 31);
+  const int col0 = wn * 64 + 4 * (lane >> 5);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int row = wm * 128 + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
-        const int col = wn * 64 + j * 32 + (lane & 31);
-        lds[row * kEpiPitch + col] = static_cast<uint16_t>(f2bf(acc[i][j][q]));
+      for (int g = 0; g < 4; ++g) {
+        uint2 v;
+        v.x = pack_bf16x2(acc[i][j][4 * g], acc[i][j][4 * g + 1]);
+        v.y = pack_bf16x2(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+        const int row = row0 + 32 * i, col = col0 + 32 * j + 8 * g;
+        *reinterpret_cast<uint2*>(lds + (row * kEpiPitch + col) * 2) = v;
       }
 }
 
-// SwiGLU of a gate/up tile -> bf16 h tile [256][kEpiPitchH] in LDS (128 columns): block 0 of
-// a wave holds the gate values and block 1 the up values of the same 32 output columns.
-__device__ __forceinline__ void stage_swiglu(const Acc& acc, char* lds_bytes) {
-  uint16_t* lds = reinterpret_cast<uint16_t*>(lds_bytes);
+// SwiGLU of a gate/up tile -> bf16 h tile [256][kEpiPitchH] in LDS (128 columns): B block 0
+// of a wave holds the gate rows and block 1 the up rows of the same 32 output columns, so
+// gate and up of one output sit in the same lane and register index.
+__device__ __forceinline__ void stage_swiglu(const Acc& acc, char* lds) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w >> 2, wn = w & 3;
+  const int row0 = wm * 128 + (lane & 31);
+  const int col0 = wn * 32 + 4 * (lane >> 5);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const float g = acc[i][0][q], u = acc[i][1][q];
-      const float h = g / (1.f + __expf(-g)) * u;
-      const int row = wm * 128 + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
-      const int col = wn * 32 + (lane & 31);
-      lds[row * kEpiPitchH + col] = static_cast<uint16_t>(f2bf(h));
+    for (int g = 0; g < 4; ++g) {
+      float h[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float gt = acc[i][0][4 * g + q], up = acc[i][1][4 * g + q];
+        h[q] = gt / (1.f + __expf(-gt)) * up;
+      }
+      uint2 v;
+      v.x = pack_bf16x2(h[0], h[1]);
+      v.y = pack_bf16x2(h[2], h[3]);
+      const int row = row0 + 32 * i, col = col0 + 8 * g;
+      *reinterpret_cast<uint2*>(lds + (row * kEpiPitchH + col) * 2) = v;
     }
 }
 
