@@ -37,6 +37,8 @@ def parse():
     p.add_argument("--policy", choices=["burst", "interleave", "chunk"], default="interleave")
     p.add_argument("--lead", type=int, default=0, help="0 = the anti-starvation knee")
     p.add_argument("--chunk", type=int, default=2)
+    p.add_argument("--claim", choices=["static", "dynamic"], default="dynamic",
+                   help="how producers take tiles (dynamic: shared counters, same tile rule)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-phases", action="store_true")
     p.add_argument("--policies", action="store_true",
@@ -140,9 +142,10 @@ def main():
     lay = EPLayer(s, sentinel=False)
     lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
     lay.prefill_other_sources(inp["fill"])
-    pol = {"burst": pacing(X.XS_POLICY_BURST),
-           "interleave": pacing(X.XS_POLICY_INTERLEAVE, lead=a.lead),
-           "chunk": pacing(X.XS_POLICY_CHUNK, lead=a.lead, chunk=a.chunk)}
+    claim = X.XS_CLAIM_DYNAMIC if a.claim == "dynamic" else X.XS_CLAIM_STATIC
+    pol = {"burst": pacing(X.XS_POLICY_BURST, claim=claim),
+           "interleave": pacing(X.XS_POLICY_INTERLEAVE, lead=a.lead, claim=claim),
+           "chunk": pacing(X.XS_POLICY_CHUNK, lead=a.lead, chunk=a.chunk, claim=claim)}
     ev = X.HipEvents(2 * a.steps + 2)
     lay.L.ffn_event_begin = None
     lay.L.ffn_event_end = None
@@ -180,7 +183,7 @@ def main():
            "warmup": a.warmup, "ms_per_step": ms_per_step, "higher_is_better": False, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
            "config": {"workload": f"{cfg.name} ({a.routing} routing, rank {rank}; one rank's EP share)",
-                      "policy": a.policy, "lead_rows": a.lead, "rows_computed": rows,
+                      "policy": a.policy, "claim": a.claim, "lead_rows": a.lead, "rows_computed": rows,
                       "global_tokens": cfg.n_src * cfg.T, "seq_len": cfg.T}}
     # algorithmic HBM bytes of one launch: dispatched rows read once, both weight matrices of
     # every local expert read once, h written and read back once, output rows stored once

@@ -175,9 +175,18 @@ enum { XS_EXPERT_SWIGLU = 0, XS_EXPERT_IDENTITY = 1 };
  * max_producers caps the persistent grid (0 = one workgroup per CU); wave_tiles is the
  * minimum Linear-1 tile count of an expert wave (0 = the grid size); gap_ns inserts a
  * non-injecting wait of that many nanoseconds after every Linear-2 store burst.
+ * claim selects how producers take tiles:
+ *   XS_CLAIM_STATIC   producer g of G takes the entries g, g + G, ... of each tile stream
+ *                     (the per-instance cursors of Alg. 1);
+ *   XS_CLAIM_DYNAMIC  producers take the next entry of a stream from a shared counter when
+ *                     they finish a tile, under the same rule (a Linear-2 tile of row p is
+ *                     taken only when every Linear-1 tile of rows <= p + D - 1 has been
+ *                     taken; BURST: the next entry of the Expert-Wave list). Same tiles and
+ *                     bytes; balances producers whose tiles differ in length.
  * Every policy computes the same tiles and stores the same bytes; outputs are
  * bit-identical across policies. */
 enum { XS_POLICY_BURST = 0, XS_POLICY_INTERLEAVE = 1, XS_POLICY_CHUNK = 2, XS_POLICY_AUTO = 3 };
+enum { XS_CLAIM_STATIC = 0, XS_CLAIM_DYNAMIC = 1 };
 
 struct xs_model;
 typedef struct xs_pacing {
@@ -190,6 +199,8 @@ typedef struct xs_pacing {
   int32_t spin_timeout_us;        /* bound of each dependency wait; 0 = 2 s */
   int32_t withhold_row;           /* failure-path hook: this row never signals Linear-1
                                      completion, so its Linear-2 waits expire (-1 = none) */
+  int32_t claim;                  /* XS_CLAIM_STATIC or XS_CLAIM_DYNAMIC */
+  int32_t reserved;               /* must be 0 */
   double t_l1_us, t_l2_us;        /* AUTO: mainloop time of one Linear-1 / Linear-2 tile;
                                      0 = estimate from the tile FLOPs */
   const struct xs_model* model;   /* host, for XS_POLICY_AUTO; may be NULL */

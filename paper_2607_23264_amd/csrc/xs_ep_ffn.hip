@@ -15,6 +15,9 @@
 //               next Linear-2 tile is taken when its row trails the Linear-1 cursor's row by
 //               at least D rows, otherwise the next Linear-1 tile.
 //   CHUNK       Alg. 1 with at most c consecutive Linear-2 tiles before a Linear-1 tile.
+// With dynamic claiming the per-instance cursors become two shared counters: a workgroup
+// that finishes a tile takes the next Linear-2 entry if its row trails the first untaken
+// Linear-1 row by at least D rows (and the chunk cap allows), else the next Linear-1 entry.
 // Deadlock freedom needs every workgroup resident (grid <= CUs, one workgroup per CU by
 // LDS) and D >= 1: an instance only waits on a row strictly behind its own Linear-1 cursor,
 // so the lowest row anyone waits on always has its Linear-1 owners running.
@@ -50,6 +53,8 @@ struct EpArgs {
   const int* wave_pos;
   const int* wave_row;
   int* l1_done;
+  int* claim_ctr;              // [0] Linear-1 / wave-list entries taken, [1] Linear-2 entries taken
+  int claim;                   // XS_CLAIM_STATIC / XS_CLAIM_DYNAMIC
   int l2_combine;              // Linear-2 epilogue: 1 = combine windows, 0 = y rows
   int policy, lead, chunk, withhold_row;
   int64_t gap_ticks, timeout_ticks;
@@ -106,6 +111,8 @@ __global__ __launch_bounds__(1024) void ep_plan_kernel(const int* __restrict__ e
     meta[1] = nw;
     meta[2] = rows * (P1 + P2);
     meta[3] = hrow;
+    meta[8] = 0;   // claim counters (dynamic claiming)
+    meta[9] = 0;
     s_rows = rows;
   }
   __syncthreads();
@@ -246,6 +253,93 @@ __device__ __forceinline__ int xcd_instance_ep(int b, int G) {
   return (G % 8) ? b : (b % 8) * (G / 8) + b / 8;
 }
 
+// Dynamic claiming. Thread 0 takes the next tile and broadcasts it through LDS:
+//   > 0: Linear-1 entry (value - 1), < -1: Linear-2 entry (-value - 2), -1: no work left.
+// Linear-2 entries are taken as tickets (one fetch_add, no retry loop): a producer holds at
+// most one ticket and runs it only once its row p satisfies p + D <= (first untaken
+// Linear-1 row); until then it keeps taking Linear-1 tiles itself. So every Linear-1 tile a
+// Linear-2 tile waits on has an owner that runs it without waiting, and the holder of an
+// early ticket advances the Linear-1 frontier it waits for. The ticket is taken when the
+// shared Linear-2 counter's next entry is already eligible, so tickets are rarely held long.
+__device__ __forceinline__ int ep_claim(const EpArgs& a, int n1, int n2, int& run, int& ticket) {
+  int* c1p = a.claim_ctr;
+  int* c2p = a.claim_ctr + 1;
+  for (;;) {
+    const int c1 = __hip_atomic_load(c1p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const bool l1_left = c1 < n1;
+    const int p1 = l1_left ? c1 / a.P1 : 0x3fffffff;
+    const bool chunk_ok = !(a.chunk > 0 && run >= a.chunk && l1_left);
+    if (ticket == -1 && chunk_ok) {
+      const int c2 = __hip_atomic_load(c2p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (c2 >= n2) {
+        ticket = -2;   // Linear-2 entries exhausted
+      } else if (c2 / a.P2 + a.lead <= p1) {
+        const int k = __hip_atomic_fetch_add(c2p, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ticket = k < n2 ? k : -2;
+      }
+    }
+    if (ticket >= 0 && chunk_ok && ticket / a.P2 + a.lead <= p1) {
+      const int k = ticket;
+      ticket = -1;
+      ++run;
+      return -k - 2;
+    }
+    if (l1_left) {
+      const int k = __hip_atomic_fetch_add(c1p, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (k < n1) {
+        run = 0;
+        return k + 1;
+      }
+      continue;   // Linear-1 exhausted meanwhile: every held ticket is now eligible
+    }
+    if (ticket == -2) return -1;
+    // Linear-1 exhausted, no ticket yet (chunk_ok holds): the loop takes one above
+  }
+}
+
+template <int MODE>
+__device__ __forceinline__ void ep_dynamic(const EpArgs& a, int n1, int n2, char* lds, char** rowptr,
+                                           int* flag) {
+  constexpr bool fused = MODE == 3;
+  int run = 0, ticket = n2 > 0 ? -1 : -2;   // thread 0 only
+  if (fused && a.policy == XS_POLICY_BURST) {
+    const int nw = a.meta[1], total = a.meta[2];
+    for (;;) {
+      if (threadIdx.x == 0)
+        flag[1] = __hip_atomic_fetch_add(a.claim_ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __syncthreads();
+      const int pos = flag[1];
+      __syncthreads();
+      if (pos >= total) return;
+      int w = 0;
+      while (w + 1 < nw && a.wave_pos[w + 1] <= pos) ++w;
+      const int off = pos - a.wave_pos[w];
+      const int r0 = a.wave_row[w], nl1 = (a.wave_row[w + 1] - r0) * a.P1;
+      if (off < nl1) {
+        const int k1 = r0 * a.P1 + off;
+        ep_l1_tile(a, k1 / a.P1, k1 % a.P1, true, lds, rowptr);
+      } else {
+        const int k2 = r0 * a.P2 + (off - nl1);
+        ep_l2_tile(a, k2 / a.P2, k2 % a.P2, true, lds, rowptr, flag);
+      }
+    }
+  }
+  for (;;) {
+    if (threadIdx.x == 0) flag[1] = ep_claim(a, n1, n2, run, ticket);
+    __syncthreads();
+    const int t = flag[1];
+    __syncthreads();
+    if (t == -1) return;
+    if (t > 0) {
+      const int k1 = t - 1;
+      ep_l1_tile(a, k1 / a.P1, k1 % a.P1, fused, lds, rowptr);
+    } else {
+      const int k2 = -t - 2;
+      ep_l2_tile(a, k2 / a.P2, k2 % a.P2, fused, lds, rowptr, flag);
+    }
+  }
+}
+
 // MODE 3: fused Linear-1 + Linear-2 (the EP layer); 1 / 2: one GEMM stream only (unfused
 // expert FFN). A template parameter so each variant is its own kernel in a trace.
 template <int MODE>
@@ -275,6 +369,10 @@ __global__ __launch_bounds__(kThreads, 1) void ep_ffn_kernel(EpArgs a) {
         ep_l2_tile(a, k2 / a.P2, k2 % a.P2, true, lds, rowptr, flag);
       }
     }
+    return;
+  }
+  if (a.claim == XS_CLAIM_DYNAMIC) {
+    ep_dynamic<MODE>(a, n1, n2, lds, rowptr, flag);
     return;
   }
   const int D = a.lead, c = a.chunk;
@@ -480,6 +578,7 @@ int fill_args(const xs_ep_layer* L, void* workspace, EpArgs* a, WinSet* dws, Win
   a->wave_pos = reinterpret_cast<int*>(ws + w.wave_pos_off);
   a->wave_row = reinterpret_cast<int*>(ws + w.wave_row_off);
   a->l1_done = reinterpret_cast<int*>(ws + w.l1_off);
+  a->claim_ctr = meta + 8;
   a->withhold_row = -1;
   a->lead = 1;
   return XS_OK;
@@ -541,6 +640,7 @@ static int run_ffn(const xs_ep_layer* L, const EpArgs& base, int mode, int l2_co
     a.policy = a.chunk > 0 ? XS_POLICY_CHUNK : XS_POLICY_INTERLEAVE;
   }
   a.withhold_row = pc ? pc->withhold_row : -1;
+  a.claim = pc ? pc->claim : XS_CLAIM_STATIC;
   a.gap_ticks = pc ? xs_host::ns_to_ticks(pc->gap_ns) : 0;
   const int64_t tmo_us = pc && pc->spin_timeout_us > 0 ? pc->spin_timeout_us : 2000000;
   a.timeout_ticks = xs_host::ns_to_ticks(tmo_us * 1000);
@@ -607,7 +707,9 @@ extern "C" int xs_fused_ep_layer(const xs_ep_layer* L, const xs_pacing* pacing,
   if (rc) return rc;
   if (pacing && (pacing->policy < XS_POLICY_BURST || pacing->policy > XS_POLICY_AUTO ||
                  pacing->lead_rows < 0 || pacing->chunk_tiles < 0 || pacing->max_producers < 0 ||
-                 pacing->gap_ns < 0 || pacing->spin_timeout_us < 0))
+                 pacing->gap_ns < 0 || pacing->spin_timeout_us < 0 ||
+                 (pacing->claim != XS_CLAIM_STATIC && pacing->claim != XS_CLAIM_DYNAMIC) ||
+                 pacing->reserved != 0))
     return XS_EINVAL;
   const EpWorkspace w = ep_workspace(L);
   if (!workspace || workspace_bytes < w.total) return XS_EWORKSPACE;

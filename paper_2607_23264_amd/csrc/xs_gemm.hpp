@@ -6,11 +6,13 @@
 // matrix pipe) by about 20 %.
 //
 // Operands move global -> LDS with gfx950's direct 128-bit loads (global_load_lds_dwordx4):
-// no staging registers and no LDS store instructions. Two LDS stages of [256][64] bf16 per
-// operand (2 x 64 KiB); the loads of stage k+1 are issued right after the barrier that
-// opens stage k and land while stage k is multiplied. (Measured alternatives that lost:
-// four or five stages of K step 32, whose extra barriers cost more than the deeper prefetch
-// gains, and loads through registers with LDS stores.)
+// no staging registers and no LDS store instructions. LDS holds two stages of the A tile
+// ([256][64] bf16 each) and three of the B tile, 160 KiB in all: A (activations, shared by
+// every tile of a row block and mostly L2-resident) is loaded one K step ahead, B (weights,
+// streamed from HBM) two K steps ahead, so a weight load has two K steps of MFMA work to
+// land in. (Measured alternatives that lost: four or five stages of K step 32, whose extra
+// barriers cost more than the deeper prefetch gains, and loads through registers with LDS
+// stores.)
 //
 // LDS operand layout: 128 B per row in eight 16-byte pieces; logical piece c of row r sits at
 // physical position c ^ ((r >> 1) & 7). A direct load writes 64 consecutive pieces (8 rows)
@@ -34,14 +36,20 @@ namespace xs {
 
 constexpr int kBM = 256, kBN = 256, kBK = 64, kThreads = 512;
 constexpr int kOpBytes = kBM * kBK * 2;                      // one operand stage: 32 KiB
-constexpr int kStageBytes = 2 * kOpBytes;                    // A + B: 64 KiB
+// LDS operand stages: A in two buffers [0, 64 KiB), B in three [64 KiB, 160 KiB)
+constexpr int kAStages = 2, kBStages = 3;
+constexpr int kBBase = kAStages * kOpBytes;
+constexpr int kLdsOpBytes = (kAStages + kBStages) * kOpBytes;   // 160 KiB
 constexpr int kEpiPitch = kBN + 8;                           // bf16 per staged output row
 constexpr int kEpiPitchH = kBN / 2 + 8;                      // SwiGLU output rows (128 wide)
 constexpr int kLdsEpiBytes = kBM * kEpiPitch * 2;            // 135168
 constexpr int kLdsRowPtrOff = kLdsEpiBytes;                  // 256 row pointers
 constexpr int kLdsMiscOff = kLdsRowPtrOff + kBM * 8;         // small scheduler scratch
-constexpr int kLdsBytes = kLdsMiscOff + 64;
-static_assert(2 * kStageBytes <= kLdsEpiBytes, "operand stages must fit under the epilogue tile");
+constexpr int kLdsBytes = kLdsOpBytes;
+// The epilogue tile, the row pointers and the scheduler scratch reuse the operand stages:
+// they are only touched between a mainloop's final barrier and the next mainloop's loads.
+static_assert(kLdsMiscOff + 64 <= kLdsBytes, "epilogue area must fit in the operand stages");
+static_assert(kLdsBytes <= 160 * 1024, "gfx950 LDS per workgroup");
 
 // address-space-qualified pointees for the direct-load builtin (C-style casts convert)
 typedef __attribute__((address_space(3))) void lds_void;
@@ -91,28 +99,32 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
   const int w = ta.w;
   const int swz = (lane >> 1) & 7;
   const int khalf = lane >> 5;
-  auto issue = [&](int kt) {
-    char* st = lds + (kt & 1) * kStageBytes;
+  auto issue_a = [&](int kt) {
+    char* st = lds + (kt & 1) * kOpBytes;
     const char* a0 = ta.a + kt * kBK * 2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      __builtin_amdgcn_global_load_lds((glob_void*)(a0 + ta.oa[i]), (lds_void*)(st + (8 * i + w) * 1024),
+                                       16, 0, 0);
+  };
+  auto issue_b = [&](int kt, int slot) {
+    char* st = lds + kBBase + slot * kOpBytes;
     const char* b0 = ta.b + kt * kBK * 2;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int off = (8 * i + w) * 1024;   // 64 pieces of 16 B
-      __builtin_amdgcn_global_load_lds((glob_void*)(a0 + ta.oa[i]), (lds_void*)(st + off), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds((glob_void*)(b0 + ta.ob[i]), (lds_void*)(st + kOpBytes + off),
+    for (int i = 0; i < 4; ++i)
+      __builtin_amdgcn_global_load_lds((glob_void*)(b0 + ta.ob[i]), (lds_void*)(st + (8 * i + w) * 1024),
                                        16, 0, 0);
-    }
   };
   bf16x8 af[2][4], bfr[2][2];
-  auto frags = [&](const char* cur, int kk, int buf) {
+  auto frags = [&](const char* ca, const char* cb, int kk, int buf) {
     if (NI == 0) return;
     const int piece = (((kk * 2 + khalf) ^ swz) << 4);
 #pragma unroll
     for (int i = 0; i < NI; ++i)
-      af[buf][i] = *reinterpret_cast<const bf16x8*>(cur + ta.arow + i * 32 * kBK * 2 + piece);
+      af[buf][i] = *reinterpret_cast<const bf16x8*>(ca + ta.arow + i * 32 * kBK * 2 + piece);
 #pragma unroll
     for (int j = 0; j < 2; ++j)
-      bfr[buf][j] = *reinterpret_cast<const bf16x8*>(cur + ta.brow + j * 32 * kBK * 2 + piece);
+      bfr[buf][j] = *reinterpret_cast<const bf16x8*>(cb + ta.brow + j * 32 * kBK * 2 + piece);
   };
   auto mma = [&](int buf, int i0, int i1) {
 #pragma unroll
@@ -126,16 +138,29 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
   constexpr int kPairs = kReads / 2, kOdd = kReads % 2;
   constexpr int kRest = kMfma - kPairs - kOdd;
   constexpr int kPre = NI < 3 ? NI : 3;
-  issue(0);
-  wait_vm0();
-  __syncthreads();
-  if (nk > 1) issue(1);
-  frags(lds, 0, 0);
+  // Issue order: A(0), B(0), B(1) | A(1), B(2) | A(2), B(3) | ... At the boundary into
+  // stage s + 1 the loads newer than A(s + 1) are only B(s + 2) (4 per wave), so waiting for
+  // stage s + 1 is vmcnt(4), or vmcnt(0) when B(s + 2) does not exist.
+  issue_a(0);
+  issue_b(0, 0);
+  if (nk > 1) {
+    issue_b(1, 1);
+    __builtin_amdgcn_s_waitcnt(0x0F74);   // vmcnt(4): A(0) and B(0) have landed
+  } else {
+    wait_vm0();
+  }
+  __builtin_amdgcn_s_barrier();
+  if (nk > 1) issue_a(1);
+  if (nk > 2) issue_b(2, 2);
+  frags(lds, lds + kBBase, 0, 0);
+  int bs = 0;   // B slot of stage kt (kt mod 3)
   for (int kt = 0; kt < nk; ++kt) {
-    const char* cur = lds + (kt & 1) * kStageBytes;
+    const char* ca = lds + (kt & 1) * kOpBytes;
+    const char* cb = lds + kBBase + bs * kOpBytes;
+    const int bs_next = bs == 2 ? 0 : bs + 1;
 #pragma unroll
     for (int kk = 0; kk < 3; ++kk) {
-      frags(cur, kk + 1, (kk + 1) & 1);
+      frags(ca, cb, kk + 1, (kk + 1) & 1);
       mma(kk & 1, 0, NI);
       if (NI > 0) {
 #pragma unroll
@@ -154,12 +179,22 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
     mma(1, 0, kPre);
     if (NI > 0) __builtin_amdgcn_sched_group_barrier(0x008, 2 * kPre, 0);
     if (kt + 1 < nk) {
-      wait_vm0();          // this wave's loads of stage kt + 1 have landed
-      __syncthreads();     // every wave's have, and stage kt is no longer read
-      frags(lds + ((kt + 1) & 1) * kStageBytes, 0, 0);
-      if (kt + 2 < nk) issue(kt + 2);
+      // this wave's loads of stage kt + 1 have landed ...
+      if (kt + 2 < nk)
+        __builtin_amdgcn_s_waitcnt(0x0F74);   // vmcnt(4)
+      else
+        wait_vm0();
+      // ... and every wave's, and stage kt is no longer read. A bare s_barrier: the
+      // workgroup fence of __syncthreads would wait for every outstanding load (vmcnt(0)),
+      // including the weight loads meant to stay in flight. LDS needs no fence: each wave
+      // has waited for its own direct loads above, and LDS has no cache to flush.
+      __builtin_amdgcn_s_barrier();
+      frags(lds + ((kt + 1) & 1) * kOpBytes, lds + kBBase + bs_next * kOpBytes, 0, 0);
+      if (kt + 2 < nk) issue_a(kt + 2);      // into A buffer kt & 1
+      if (kt + 3 < nk) issue_b(kt + 3, bs);  // into B slot (kt + 3) mod 3 = kt mod 3
     }
     mma(1, kPre, NI);
+    bs = bs_next;
   }
 }
 
@@ -193,9 +228,10 @@ __device__ __forceinline__ void gemm_mainloop(const uint16_t* __restrict__ A, in
     ta.oa[i] = static_cast<uint32_t>(ar * lda * 2 + c16);
     ta.ob[i] = static_cast<uint32_t>(b_row_map(r, b_n0, b_half, swiglu) * ldb * 2 + c16);
   }
-  // fragment reads: row (wm*128 + i*32 + lane%32) of A, (wn*64 + j*32 + lane%32) of B
+  // fragment reads: row (wm*128 + i*32 + lane%32) of A, (wn*64 + j*32 + lane%32) of B, as
+  // byte offsets inside a stage buffer
   ta.arow = (wm * 128 + (lane & 31)) * kBK * 2;
-  ta.brow = kOpBytes + (wn * 64 + (lane & 31)) * kBK * 2;
+  ta.brow = (wn * 64 + (lane & 31)) * kBK * 2;
   zero_acc(acc);
   const int nk = K / kBK;
   const int valid = a_rows - wm * 128;

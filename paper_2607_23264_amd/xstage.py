@@ -22,6 +22,7 @@ XS_OK, XS_EINVAL, XS_EUNSUPPORTED, XS_EHIP, XS_EWORKSPACE, XS_ECAPACITY, XS_ETIM
 XS_MAX_WINDOWS = 64
 XS_EXPERT_SWIGLU, XS_EXPERT_IDENTITY = 0, 1
 XS_POLICY_BURST, XS_POLICY_INTERLEAVE, XS_POLICY_CHUNK, XS_POLICY_AUTO = 0, 1, 2, 3
+XS_CLAIM_STATIC, XS_CLAIM_DYNAMIC = 0, 1
 XS_SCATTER_ROW_BLOCK, XS_SCATTER_HEAD_GROUP = 0, 1
 XS_MB_PERIODIC, XS_MB_COMPLETION = 0, 1
 
@@ -44,6 +45,7 @@ class xs_model(C.Structure):
 class xs_pacing(C.Structure):
     _fields_ = [("policy", i32), ("lead_rows", i32), ("chunk_tiles", i32), ("max_producers", i32),
                 ("wave_tiles", i32), ("gap_ns", i32), ("spin_timeout_us", i32), ("withhold_row", i32),
+                ("claim", i32), ("reserved", i32),
                 ("t_l1_us", f64), ("t_l2_us", f64), ("model", C.POINTER(xs_model))]
 
 

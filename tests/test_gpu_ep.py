@@ -196,7 +196,10 @@ def _policies():
             "chunk1": pacing(X.XS_POLICY_CHUNK, lead=1, chunk=1),
             "chunk2_p8": pacing(X.XS_POLICY_CHUNK, lead=2, chunk=2, max_producers=8),
             "auto_nomodel": pacing(X.XS_POLICY_AUTO), "burst_p16_w4": pacing(X.XS_POLICY_BURST, max_producers=16,
-                                                                              wave_tiles=4)}
+                                                                              wave_tiles=4),
+            "interleave_dyn": pacing(X.XS_POLICY_INTERLEAVE, lead=1, claim=X.XS_CLAIM_DYNAMIC),
+            "chunk2_p8_dyn": pacing(X.XS_POLICY_CHUNK, lead=2, chunk=2, max_producers=8, claim=X.XS_CLAIM_DYNAMIC),
+            "burst_w4_dyn": pacing(X.XS_POLICY_BURST, wave_tiles=4, claim=X.XS_CLAIM_DYNAMIC)}
 
 
 def test_tiny_layer_all_policies_match_oracle_and_each_other():
@@ -295,8 +298,8 @@ def _full_share(routing):
     return cfg
 
 
-@pytest.mark.parametrize("routing", ["uniform", "zipf"])
-def test_dsv3_share_full_size_sampled(routing):
+@pytest.mark.parametrize("routing,claim", [("uniform", 0), ("zipf", 1)])
+def test_dsv3_share_full_size_sampled(routing, claim):
     cfg = _full_share(routing)
     inp = synth.ep_inputs(cfg, 0)
     experts = synth.computed_experts(cfg)
@@ -305,7 +308,7 @@ def test_dsv3_share_full_size_sampled(routing):
     lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
     lay.prefill_other_sources(fill)
     from paper_2607_23264_amd.layer import pacing
-    lay.fused(pacing(xs().XS_POLICY_INTERLEAVE, lead=1))
+    lay.fused(pacing(xs().XS_POLICY_INTERLEAVE, lead=0, claim=claim))
     torch.cuda.synchronize()
     assert int(lay.status.item()) == 0
     # layout of all sources is bit-exact
@@ -380,14 +383,55 @@ def test_device_tile_order_matches_schedule_oracle(policy):
         assert got == exp, f"workgroup {b}"
 
 
-def test_withheld_dependency_times_out_and_kernel_exits():
+@pytest.mark.parametrize("policy", ["interleave", "chunk", "burst"])
+def test_dynamic_claim_takes_every_tile_once_after_its_dependencies(policy):
     from paper_2607_23264_amd.layer import pacing
     X = xs()
     cfg = synth.EP_TINY
     inp = synth.ep_inputs(cfg, 0)
     lay = _ep_layer(cfg)
     lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
-    lay.fused(pacing(X.XS_POLICY_INTERLEAVE, lead=1, withhold_row=0, spin_timeout_us=2000))
+    G = 8
+    pol = {"interleave": pacing(X.XS_POLICY_INTERLEAVE, lead=1, max_producers=G, claim=X.XS_CLAIM_DYNAMIC),
+           "chunk": pacing(X.XS_POLICY_CHUNK, lead=1, chunk=1, max_producers=G, claim=X.XS_CLAIM_DYNAMIC),
+           "burst": pacing(X.XS_POLICY_BURST, max_producers=G, wave_tiles=16, claim=X.XS_CLAIM_DYNAMIC)}[policy]
+    buf = torch.zeros((4096, 4), dtype=torch.int64, device="cuda")
+    cnt = torch.zeros((1,), dtype=torch.int32, device="cuda")
+    lay.fused(pol, X.xs_trace(buf.data_ptr(), buf.shape[0], cnt.data_ptr()))
+    torch.cuda.synchronize()
+    assert int(lay.status.item()) == 0
+    kind, wg, tile, r = _records(buf, cnt)
+    idx = oep.route_topk_softmax(inp["logits"][0], cfg.k)[0][None]
+    counts = oep.dispatch_layout(idx, cfg.E, cfg.W)["expert_counts"].sum(0)
+    P = sum((int(c) + 255) // 256 for c in counts)
+    P1, P2 = cfg.I // 128, cfg.H // 256
+    # every tile exactly once, on producers 0..G-1
+    assert sorted(tile[kind == 1].tolist()) == list(range(P * P1))
+    assert sorted(tile[kind == 2].tolist()) == list(range(P * P2))
+    assert set(wg.tolist()) <= set(range(G))
+    # a Linear-2 tile's mainloop ends after every Linear-1 tile of its row has stored h
+    l1_end = {}
+    for t, e in zip(tile[kind == 1], r[kind == 1, 3].astype(np.int64)):
+        l1_end[int(t) // P1] = max(l1_end.get(int(t) // P1, 0), int(e))
+    for t, m in zip(tile[kind == 2], r[kind == 2, 2].astype(np.int64)):
+        assert int(m) >= l1_end[int(t) // P2], f"Linear-2 tile {int(t)} ran before its row"
+    # and the output equals the static order's, bit for bit
+    out_dyn = host_bits(lay.out)
+    lay.out.zero_()
+    lay.fused(pacing(X.XS_POLICY_INTERLEAVE, lead=1))
+    torch.cuda.synchronize()
+    assert np.array_equal(out_dyn, host_bits(lay.out))
+
+
+@pytest.mark.parametrize("claim", [0, 1])
+def test_withheld_dependency_times_out_and_kernel_exits(claim):
+    from paper_2607_23264_amd.layer import pacing
+    X = xs()
+    cfg = synth.EP_TINY
+    inp = synth.ep_inputs(cfg, 0)
+    lay = _ep_layer(cfg)
+    lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
+    lay.fused(pacing(X.XS_POLICY_INTERLEAVE, lead=1, withhold_row=0, spin_timeout_us=2000, claim=claim))
     torch.cuda.synchronize()
     assert int(lay.status.item()) == X.XS_ETIMEOUT
     # the library never clears the status; a clean run after a reset reports ok again
@@ -406,6 +450,11 @@ def test_bad_arguments_rejected_synchronously():
     p.policy = 9
     assert X.xs_fused_ep_layer(C.byref(lay.L), C.byref(p), None, lay.workspace.data_ptr(),
                                lay.workspace.numel(), lay.status.data_ptr(), None) == X.XS_EINVAL
+    for field, value in (("claim", 2), ("reserved", 1), ("lead_rows", -1)):
+        p = pacing(X.XS_POLICY_INTERLEAVE)
+        setattr(p, field, value)
+        assert X.xs_fused_ep_layer(C.byref(lay.L), C.byref(p), None, lay.workspace.data_ptr(),
+                                   lay.workspace.numel(), lay.status.data_ptr(), None) == X.XS_EINVAL, field
     assert X.xs_fused_ep_layer(C.byref(lay.L), None, None, lay.workspace.data_ptr(), 16,
                                lay.status.data_ptr(), None) == X.XS_EWORKSPACE
     assert X.xs_route_topk_softmax(lay.logits.data_ptr(), 4, 8, 9, 0, lay.topk_idx.data_ptr(),
