@@ -152,7 +152,7 @@ __device__ __forceinline__ void ep_l1_tile(const EpArgs& a, int p, int nt, bool 
     if (tid == 0 && p != a.withhold_row)
       __hip_atomic_fetch_add(&a.l1_done[p], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
   } else {
-    __syncthreads();
+    lds_barrier();   // the unfused h rows are read by a later launch
   }
   if (a.tr.buf && tid == 0) {
     uint32_t i = atomicAdd(a.tr.count, 1u);
@@ -206,14 +206,17 @@ __device__ __forceinline__ void ep_l2_tile(const EpArgs& a, int p, int nt, bool 
   const uint16_t* A = a.h + static_cast<int64_t>(a.exp_hrow[x] + m0) * a.I;
   const uint16_t* B = a.w2 + static_cast<int64_t>(x) * a.H * a.I;
   const int n0 = nt * kBN;
+  // the destination of this thread's output row, loaded before the mainloop so that its
+  // latency is hidden behind the MFMAs
+  int code = -1;
+  if (a.l2_combine && tid < rows)
+    code = a.row_src[static_cast<int64_t>(e / a.epw) * a.cap + a.expert_offsets[e] + m0 + tid];
   Acc acc;
   gemm_mainloop(A, a.I, rows, B, a.I, n0, 0, false, a.I, acc, lds);
   const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
   if (tid < rows) {
     char* ptr;
     if (a.l2_combine) {
-      const int d = e / a.epw;
-      const int code = a.row_src[static_cast<int64_t>(d) * a.cap + a.expert_offsets[e] + m0 + tid];
       const int src = code >> 24, slot = code & 0xffffff;
       if (code >= 0 && src < a.n_src && slot < a.tk) {
         ptr = a.cwin.base[src] + static_cast<int64_t>(slot) * a.cwin.stride[src] +
@@ -230,7 +233,9 @@ __device__ __forceinline__ void ep_l2_tile(const EpArgs& a, int p, int nt, bool 
   stage_tile(acc, lds);
   __syncthreads();
   store_rows(lds, kEpiPitch, kBN, rows, rowptr);
-  __syncthreads();
+  // The combine rows are read only after the kernel (window signal, combine-reduce): the
+  // stores drain while the next tile runs.
+  lds_barrier();
   if (tid == 0) {
     const uint64_t t2 = a.tr.buf ? wall_ticks() : 0;
     if (a.tr.buf) {

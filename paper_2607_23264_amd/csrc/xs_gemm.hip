@@ -105,7 +105,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tiles_kernel(
     } else {
       store_rows(lds, kEpiPitch, kBN, rows, rowptr);
     }
-    __syncthreads();
+    lds_barrier();   // output tiles are read only after the kernel
     if (tr.buf && tid == 0) trace_tile(tr, 3, t, t0, t1, wall_ticks());
   }
 }
