@@ -41,6 +41,8 @@ def parse():
                    help="how producers take tiles (dynamic: shared counters, same tile rule)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-phases", action="store_true")
+    p.add_argument("--no-scatter", action="store_true", help="skip the TP / SP scatter GEMM lines")
+    p.add_argument("--no-slow-sink", action="store_true", help="skip the host-coherent sink line")
     p.add_argument("--policies", action="store_true",
                    help="also time the fused layer under every pacing policy (phases)")
     p.add_argument("--seed", type=int, default=0)
@@ -103,6 +105,120 @@ def cpu_baseline(cfg, inp, rank, seed, ffn_budget_s=12.0, comb_budget_s=3.0):
                           "expert_ffn": t_ffn * 1e6, "combine_reduce": t_comb * 1e6}}
 
 
+def scatter_lines(X, torch, synth, reps=20):
+    """TP row-block and Ulysses head-group scatter GEMMs: fused epilogue vs the plain GEMM
+    (residual E_res = fused - plain, Sec. 5.4) vs the serial GEMM + permutation copy."""
+    import ctypes as C
+    st = torch.cuda.current_stream().cuda_stream
+    out = {}
+
+    def dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda()
+
+    def timed(*fns, rounds=5):
+        """Median per call of each function, timed in interleaved rounds (clock drift and
+        the first-run boost then fall on every variant alike)."""
+        for fn in fns:
+            fn()
+        torch.cuda.synchronize()
+        t = [[] for _ in fns]
+        for _ in range(rounds):
+            for i, fn in enumerate(fns):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(reps // rounds):
+                    fn()
+                e1.record()
+                torch.cuda.synchronize()
+                t[i].append(e0.elapsed_time(e1) / (reps // rounds) * 1e3)
+        return [float(np.median(x)) for x in t]
+
+    tp = synth.TP_ROWBLOCK
+    inp = synth.tp_inputs(tp, 0)
+    a, bt = dev(inp["a"]), dev(np.ascontiguousarray(inp["b"].T))
+    rpd = tp.M // tp.W
+    win = torch.empty((tp.W, rpd, tp.N), dtype=torch.int16, device="cuda")
+    wins = X.windows([X.window(win[d]) for d in range(tp.W)])
+    desc = X.xs_scatter_desc(X.XS_SCATTER_ROW_BLOCK, rpd, 0, 0, 0, 0)
+    c = torch.empty((tp.M, tp.N), dtype=torch.int16, device="cuda")
+    M, N, K = tp.M, tp.N, tp.K
+    f = lambda: X.check(X.xs_gemm_scatter(a.data_ptr(), K, bt.data_ptr(), K, M, N, K, desc, wins, tp.W, None, st))
+    g = lambda: X.check(X.xs_gemm(a.data_ptr(), K, bt.data_ptr(), K, c.data_ptr(), N, M, N, K, None, st))
+    sc = lambda: X.check(X.xs_scatter_copy(c.data_ptr(), N, M, N, desc, wins, tp.W, st))
+    out["tp_rowblock"] = _scatter_result(tp.name, 2.0 * M * N * K, 2.0 * M * N,
+                                         *timed(f, g, lambda: (g(), sc())))
+    del a, bt, win, c
+    sp = synth.SP_QKV
+    inp = synth.sp_inputs(sp, 0)
+    x, wt = dev(inp["x"]), dev(np.ascontiguousarray(inp["w"].T))
+    S, Dm = sp.S, sp.Dm
+    N = 3 * sp.n_heads * sp.head_dim
+    G = sp.n_heads // sp.heads_per_group
+    win = torch.empty((G, 3, sp.heads_per_group, S, sp.head_dim), dtype=torch.int16, device="cuda")
+    wins = X.windows([X.xs_window(win[q].data_ptr(), 3 * sp.heads_per_group * S, sp.head_dim * 2, None)
+                      for q in range(G)])
+    desc = X.xs_scatter_desc(X.XS_SCATTER_HEAD_GROUP, 0, 3, sp.n_heads, sp.head_dim, sp.heads_per_group)
+    c = torch.empty((S, N), dtype=torch.int16, device="cuda")
+    f = lambda: X.check(X.xs_gemm_scatter(x.data_ptr(), Dm, wt.data_ptr(), Dm, S, N, Dm, desc, wins, G, None, st))
+    g = lambda: X.check(X.xs_gemm(x.data_ptr(), Dm, wt.data_ptr(), Dm, c.data_ptr(), N, S, N, Dm, None, st))
+    sc = lambda: X.check(X.xs_scatter_copy(c.data_ptr(), N, S, N, desc, wins, G, st))
+    out["sp_qkv"] = _scatter_result(sp.name, 2.0 * S * N * Dm, 2.0 * S * N, *timed(f, g, lambda: (g(), sc())))
+    del x, wt, win, c
+    torch.cuda.empty_cache()
+    return out
+
+
+def _scatter_result(name, flops, store_bytes, t_fused, t_plain, t_serial):
+    return {"workload": name, "fused_us": t_fused, "plain_gemm_us": t_plain, "serial_us": t_serial,
+            "fused_TFLOPs": flops / (t_fused * 1e-6) / 1e12,
+            "mfma_frac": flops / (t_fused * 1e-6) / MFMA_PEAK_BF16,
+            "residual_us": t_fused - t_plain, "speedup_vs_serial": t_serial / t_fused,
+            "stored_bytes": store_bytes}
+
+
+def store_ceiling(X, torch):
+    """Plain store stream into HBM: 256 producers x 8 waves of 128-bit stores, zero gap, 1 GiB
+    at fresh addresses (the remote-store microbenchmark)."""
+    from paper_2607_23264_amd.calibrate import run_bursts
+    nb = 1 << 30
+    buf = torch.empty(nb // 2, dtype=torch.int16, device="cuda")
+    K, B = 256, 256 << 10
+    n = nb // (K * B)
+    run_bursts(buf.data_ptr(), nb, K, B, n, 0, store_waves=8)
+    spans = [run_bursts(buf.data_ptr(), nb, K, B, n, 0, store_waves=8).total_span_us for _ in range(3)]
+    del buf
+    torch.cuda.empty_cache()
+    span = float(np.median(spans))
+    return {"bytes": nb, "span_us": span, "GBps": nb / (span * 1e-6) / 1e9,
+            "frac_of_hbm_peak": nb / (span * 1e-6) / HBM_PEAK}
+
+
+def slow_sink_line(X, torch, synth, reps=7):
+    """Config 5 in brief: the tiny layer with its combine windows in host-coherent memory,
+    BURST vs paced issue at two producer caps, with the calibrated model's stall prediction
+    (the full sweep is paper_2607_23264_amd.slow_sink)."""
+    from paper_2607_23264_amd import slow_sink as ss
+    from paper_2607_23264_amd.calibrate import to_model
+    ch, cd = ss.calibrate_sinks(256, [16384, 65536, 262144], store_waves=8, target_bytes=256 << 20)
+    host_model = to_model(ch, capacity="knee")
+    rows = ss.sweep_layer(synth.EP_TINY, host_model, [16, 0], [8], reps, X.xs_clock_rate_hz())
+    res = {"host_sink": {k: ch.model[k] for k in ("t0_a_us", "t0_b_us_per_byte", "R_bytes_per_us",
+                                                  "Q_knee_bracket_bytes")},
+           "hbm_R_bytes_per_us": cd.model["R_bytes_per_us"], "layers": {}}
+    for cap in (16, 256):
+        host = [r for r in rows if r["sink"] == "host" and r["max_producers"] == cap]
+        burst = next(r for r in host if r["policy"] == "burst")
+        best = min((r for r in host if r["policy"] != "burst"), key=lambda r: r["kernel_us_median"])
+        res["layers"][f"cap{cap}"] = {
+            "burst_us": burst["kernel_us_median"], "best_policy": best["policy"],
+            "best_us": best["kernel_us_median"],
+            "pacing_speedup": burst["kernel_us_median"] / best["kernel_us_median"],
+            "stall_fraction_burst": burst["stall_fraction"], "stall_fraction_best": best["stall_fraction"],
+            "stall_predicted_us_burst": burst["stall_predicted_us"],
+            "stall_measured_us_burst": burst["stall_measured_us"]}
+    return res
+
+
 def synth_rows(g, m, H):
     import synth
     return synth.to_bf16_bits(g.standard_normal((m, H), dtype=np.float32))
@@ -147,8 +263,8 @@ def main():
            "interleave": pacing(X.XS_POLICY_INTERLEAVE, lead=a.lead, claim=claim),
            "chunk": pacing(X.XS_POLICY_CHUNK, lead=a.lead, chunk=a.chunk, claim=claim)}
     ev = X.HipEvents(2 * a.steps + 2)
-    lay.L.ffn_event_begin = None
-    lay.L.ffn_event_end = None
+    for i in range(8):
+        lay.L.events[i] = None
     for _ in range(a.warmup):
         lay.fused(pol[a.policy])
     torch.cuda.synchronize()
@@ -158,15 +274,28 @@ def main():
     torch.cuda.synchronize()
     start.record()
     for i in range(a.steps):
-        lay.L.ffn_event_begin = ev.ev[2 * i]
-        lay.L.ffn_event_end = ev.ev[2 * i + 1]
+        lay.L.events[X.XS_EV_FFN] = ev.ev[2 * i]
+        lay.L.events[X.XS_EV_FFN_END] = ev.ev[2 * i + 1]
         lay.fused(pol[a.policy])
     stop.record()
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(stop)
     ffn_ms = [ev.elapsed_ms(2 * i, 2 * i + 1) for i in range(a.steps)]
-    lay.L.ffn_event_begin = None
-    lay.L.ffn_event_end = None
+    lay.L.events[X.XS_EV_FFN] = None
+    lay.L.events[X.XS_EV_FFN_END] = None
+    # phases inside the step: every phase boundary recorded, after the timed region
+    n_ph = 10
+    pev = X.HipEvents(8 * n_ph)
+    for i in range(n_ph):
+        for e in range(8):
+            lay.L.events[e] = pev.ev[8 * i + e]
+        lay.fused(pol[a.policy])
+    torch.cuda.synchronize()
+    for e in range(8):
+        lay.L.events[e] = None
+    names = ["route", "layout", "dispatch", "plan", "expert_ffn", "signal", "combine_reduce"]
+    in_step = {n: float(np.median([pev.elapsed_ms(8 * i + j, 8 * i + j + 1) * 1e3 for i in range(n_ph)]))
+               for j, n in enumerate(names)}
     status = int(lay.status.item())
     if status:
         log(f"[bench] device status {status}: {X.xs_strerror(status).decode()}")
@@ -190,6 +319,16 @@ def main():
     alg_bytes = 2.0 * (rows * cfg.H + len(experts) * 3 * cfg.H * cfg.I + 2 * rows * cfg.I + rows * cfg.H)
     from paper_2607_23264_amd.profiling import read_traffic
     tr = read_traffic(os.path.join(HERE, "profiles", "ep_ffn_kernel_dsv3_share_traffic.md"))
+    disp_bytes = cfg.T * cfg.k * cfg.H * 2          # stored rows (plus T * H * 2 read)
+    red_bytes = cfg.T * cfg.k * cfg.H * 2 + cfg.T * cfg.H * 2
+    res["phases_in_step_us"] = in_step
+    res["store_GBps"] = {
+        "dispatch_stored": disp_bytes / (in_step["dispatch"] * 1e-6) / 1e9,
+        "dispatch_moved": (disp_bytes + cfg.T * cfg.H * 2) / (in_step["dispatch"] * 1e-6) / 1e9,
+        "combine_reduce_moved": red_bytes / (in_step["combine_reduce"] * 1e-6) / 1e9}
+    res["store_GBps"]["dispatch_frac_of_hbm_peak"] = res["store_GBps"]["dispatch_moved"] * 1e9 / HBM_PEAK
+    res["store_GBps"]["combine_reduce_frac_of_hbm_peak"] = res["store_GBps"]["combine_reduce_moved"] * 1e9 / HBM_PEAK
+    log("[bench] in-step phases (us): " + ", ".join(f"{k}={v:.1f}" for k, v in in_step.items()))
     res["mfma_util_pct"] = 100.0 * achieved_tflops * 1e12 / MFMA_PEAK_BF16
     res["roofline"] = {"bound": "mfma", "kernel": "ep_ffn_kernel<3> (persistent fused Linear-1 + Linear-2)",
                        "achieved": achieved_tflops, "peak": MFMA_PEAK_BF16 / 1e12, "unit": "TFLOP/s",
@@ -200,7 +339,7 @@ def main():
                        "hbm_GBps_algorithmic": alg_bytes / (ffn_avg * 1e-3) / 1e9}
 
     if not a.no_phases:
-        log("[bench] phase breakdown (unfused calls)")
+        log("[bench] phase breakdown (each call timed alone, back to back)")
         ph = {}
         reps = 5
 
@@ -229,16 +368,24 @@ def main():
         for name, p in pol.items():
             if a.policies or name == a.policy:
                 ph[f"fused_{name}_us"] = timed(lambda p=p: lay.fused(p))
-        res["phases"] = ph
-        res["store_GBps"] = {"dispatch": ph["dispatch_store_GBps"], "combine_send": ph["combine_send_store_GBps"],
-                             "frac_of_hbm_peak_dispatch": ph["dispatch_store_GBps"] * 1e9 / HBM_PEAK,
-                             "frac_of_hbm_peak_combine_send": ph["combine_send_store_GBps"] * 1e9 / HBM_PEAK}
+        res["phases_isolated"] = ph
         log("[bench] " + ", ".join(f"{k}={v:.1f}" for k, v in ph.items()))
     if int(lay.status.item()):
         log("[bench] device status set during phases")
         sys.exit(1)
     del lay
     torch.cuda.empty_cache()
+    if not a.no_phases:
+        log("[bench] store ceiling")
+        res["store_ceiling"] = store_ceiling(X, torch)
+    if not a.no_scatter:
+        log("[bench] TP / SP scatter GEMMs")
+        res["scatter"] = scatter_lines(X, torch, synth)
+        log("[bench] " + json.dumps(res["scatter"]))
+    if not a.no_slow_sink:
+        log("[bench] slow sink (host-coherent combine windows)")
+        res["slow_sink"] = slow_sink_line(X, torch, synth)
+        log("[bench] " + json.dumps(res["slow_sink"]["layers"]))
     if not a.no_cpu_baseline:
         log("[bench] oracle on the host (bounded sample)")
         res["cpu_baseline"] = cpu_baseline(cfg, inp, rank, a.seed)

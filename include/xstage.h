@@ -152,9 +152,18 @@ typedef struct xs_ep_layer {
   int64_t h_rows;             /* >= (n_experts / (E / W)) * cap */
   void* y_ws;                 /* device bf16 [h_rows][H]; only used by the unfused path */
   void* out;                  /* device bf16 [T][H], combined output of source `src` */
-  void* ffn_event_begin;      /* optional hipEvent_t pair recorded on `stream` right before */
-  void* ffn_event_end;        /* and after the expert-FFN kernel launch(es); may be NULL */
+  void* events[8];            /* optional hipEvent_t per phase boundary (NULL = not recorded),
+                                 recorded on `stream`; see XS_EV_* */
 } xs_ep_layer;
+
+/* Phase boundaries of the EP entry points: events[XS_EV_x] is recorded right before the
+ * first launch of phase x (XS_EV_FFN_END right after the expert-FFN kernel(s), XS_EV_END
+ * after the last launch). xs_fused_ep_layer records all of them; xs_expert_ffn records
+ * XS_EV_PLAN, XS_EV_FFN and XS_EV_FFN_END. */
+enum {
+  XS_EV_ROUTE = 0, XS_EV_LAYOUT = 1, XS_EV_DISPATCH = 2, XS_EV_PLAN = 3, XS_EV_FFN = 4,
+  XS_EV_FFN_END = 5, XS_EV_REDUCE = 6, XS_EV_END = 7
+};
 
 enum { XS_EXPERT_SWIGLU = 0, XS_EXPERT_IDENTITY = 1 };
 

@@ -618,6 +618,12 @@ int auto_chunk(const xs_pacing* pc, const xs_ep_layer* L, int K) {
 
 }  // namespace
 
+// Records the phase event `i` of the layer descriptor, if the caller set one.
+static int record_event(const xs_ep_layer* L, int i, hipStream_t st) {
+  if (!L->events[i]) return XS_OK;
+  return hipEventRecord(static_cast<hipEvent_t>(L->events[i]), st) == hipSuccess ? XS_OK : XS_EHIP;
+}
+
 extern "C" int xs_ep_layer_workspace_bytes(const xs_ep_layer* L, int64_t* bytes) {
   if (!L || !bytes || L->n_src < 1 || L->T < 0 || L->E < 1 || L->W < 1 || L->E % L->W ||
       L->n_experts < 1 || L->cap < 0)
@@ -675,17 +681,15 @@ extern "C" int xs_expert_ffn(const xs_ep_layer* L, void* workspace, int64_t work
                        n_cwin_of(L), 0);
     return xs_host::launch_status();
   }
+  if ((rc = record_event(L, XS_EV_PLAN, st))) return rc;
   rc = launch_plan(L, a, 0, st);
   if (rc) return rc;
-  if (L->ffn_event_begin && hipEventRecord(static_cast<hipEvent_t>(L->ffn_event_begin), st) != hipSuccess)
-    return XS_EHIP;
+  if ((rc = record_event(L, XS_EV_FFN, st))) return rc;
   rc = run_ffn(L, a, 1, 0, nullptr, nullptr, dev_status, st);
   if (rc) return rc;
   rc = run_ffn(L, a, 2, 0, nullptr, nullptr, dev_status, st);
   if (rc) return rc;
-  if (L->ffn_event_end && hipEventRecord(static_cast<hipEvent_t>(L->ffn_event_end), st) != hipSuccess)
-    return XS_EHIP;
-  return XS_OK;
+  return record_event(L, XS_EV_FFN_END, st);
 }
 
 extern "C" int xs_combine_send(const xs_ep_layer* L, int32_t* dev_status, void* stream) {
@@ -725,20 +729,25 @@ extern "C" int xs_fused_ep_layer(const xs_ep_layer* L, const xs_pacing* pacing,
   if (rc) return rc;
   const int64_t n_all = static_cast<int64_t>(L->n_src) * L->T;
   if (n_all > 0x7fffffff) return XS_EINVAL;
+  if ((rc = record_event(L, XS_EV_ROUTE, st))) return rc;
   rc = xs_route_topk_softmax(L->logits, static_cast<int32_t>(n_all), L->E, L->k, L->renormalize,
                              L->topk_idx, L->topk_w, stream);
   if (rc) return rc;
+  if ((rc = record_event(L, XS_EV_LAYOUT, st))) return rc;
   rc = xs_host::dispatch_layout(L->topk_idx, L->n_src, L->T, L->k, L->E, L->W, L->cap,
                                 L->expert_counts, L->src_base, L->expert_offsets, L->dest_counts,
                                 L->slot_row, L->row_src, static_cast<char*>(workspace) + w.layout_off,
                                 w.layout_bytes, dev_status, st);
   if (rc) return rc;
   const int64_t so = static_cast<int64_t>(L->src) * L->T * L->k;
+  if ((rc = record_event(L, XS_EV_DISPATCH, st))) return rc;
   rc = xs_host::dispatch(L->x, L->T, L->H, L->topk_idx + so, L->slot_row + so, L->k, L->E, dws,
                          dev_status, st);
   if (rc) return rc;
   a.status = dev_status;
+  if ((rc = record_event(L, XS_EV_PLAN, st))) return rc;
   if (L->expert_mode == XS_EXPERT_IDENTITY) {
+    if ((rc = record_event(L, XS_EV_FFN, st))) return rc;
     hipLaunchKernelGGL(ep_identity_kernel, dim3(2048), dim3(256), 0, st, a, L->dest_counts,
                        n_cwin_of(L), 1);
     if (xs_host::launch_status()) return XS_EHIP;
@@ -747,17 +756,17 @@ extern "C" int xs_fused_ep_layer(const xs_ep_layer* L, const xs_pacing* pacing,
     const int wave_tiles = pacing && pacing->wave_tiles > 0 ? pacing->wave_tiles : grid;
     rc = launch_plan(L, a, wave_tiles, st);
     if (rc) return rc;
-    if (L->ffn_event_begin &&
-        hipEventRecord(static_cast<hipEvent_t>(L->ffn_event_begin), st) != hipSuccess)
-      return XS_EHIP;
+    if ((rc = record_event(L, XS_EV_FFN, st))) return rc;
     rc = run_ffn(L, a, 3, 1, pacing, trace, dev_status, st);
     if (rc) return rc;
-    if (L->ffn_event_end && hipEventRecord(static_cast<hipEvent_t>(L->ffn_event_end), st) != hipSuccess)
-      return XS_EHIP;
   }
+  if ((rc = record_event(L, XS_EV_FFN_END, st))) return rc;
   rc = xs_host::signal_windows(cws, st);
   if (rc) return rc;
+  if ((rc = record_event(L, XS_EV_REDUCE, st))) return rc;
   const xs_window& cw = L->combine_win[L->src];
-  return xs_host::combine_reduce(cw.base, cw.row_stride_bytes, L->topk_w + so, L->T, L->k, L->H,
-                                 L->out, st);
+  rc = xs_host::combine_reduce(cw.base, cw.row_stride_bytes, L->topk_w + so, L->T, L->k, L->H,
+                               L->out, st);
+  if (rc) return rc;
+  return record_event(L, XS_EV_END, st);
 }

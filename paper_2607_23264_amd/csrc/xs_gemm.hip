@@ -13,6 +13,7 @@ enum { KIND_PLAIN = 0, KIND_ROW_BLOCK = 1, KIND_HEAD_GROUP = 2 };
 struct ScatterArgs {
   int rpd;
   int n_proj, n_heads, head_dim, hpg;
+  int group_aligned;   // every 256-column tile lies inside one projection and one head group
 };
 
 // Instance id with consecutive ids on one XCD: workgroups are dealt to the 8 XCDs round
@@ -97,10 +98,32 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tiles_kernel(
     stage_tile(acc, lds);
     __syncthreads();
     if (KIND == KIND_HEAD_GROUP) {
-      const int pc = tid & 31;
-      for (int r = tid >> 5; r < rows; r += kThreads / 32) {
-        u32x4 v = *reinterpret_cast<const u32x4*>(lds + (r * kEpiPitch + pc * 8) * 2);
-        *reinterpret_cast<u32x4*>(head_group_dst(win, sa, M, m0 + r, n0 + pc * 8)) = v;
+      if (sa.group_aligned) {
+        // The tile's columns are heads [head0, head0 + 256 / head_dim) of one projection and
+        // one group: store head by head, consecutive lanes on consecutive 16-byte pieces of
+        // consecutive rows, which are contiguous in a head plane (a wave stores 1 KiB runs).
+        const int per_proj = sa.n_heads * sa.head_dim;
+        const int p = n0 / per_proj;
+        const int head0 = (n0 - p * per_proj) / sa.head_dim;
+        const int g = head0 / sa.hpg;
+        const int pph = sa.head_dim / 8;                 // 16-byte pieces per head row
+        const int64_t stride = win.stride[g];
+        char* plane0 = win.base[g] + (static_cast<int64_t>(p * sa.hpg + head0 - g * sa.hpg) * M + m0) * stride;
+        const int64_t plane_bytes = static_cast<int64_t>(M) * stride;
+        const int n = (kBN / sa.head_dim) * rows * pph;
+        for (int i = tid; i < n; i += kThreads) {
+          const int piece = i % pph;
+          const int hr = i / pph;
+          const int hsel = hr / rows, r = hr - hsel * rows;
+          u32x4 v = *reinterpret_cast<const u32x4*>(lds + (r * kEpiPitch + hsel * sa.head_dim + piece * 8) * 2);
+          *reinterpret_cast<u32x4*>(plane0 + hsel * plane_bytes + r * stride + piece * 16) = v;
+        }
+      } else {
+        const int pc = tid & 31;
+        for (int r = tid >> 5; r < rows; r += kThreads / 32) {
+          u32x4 v = *reinterpret_cast<const u32x4*>(lds + (r * kEpiPitch + pc * 8) * 2);
+          *reinterpret_cast<u32x4*>(head_group_dst(win, sa, M, m0 + r, n0 + pc * 8)) = v;
+        }
       }
     } else {
       store_rows(lds, kEpiPitch, kBN, rows, rowptr);
@@ -202,6 +225,8 @@ static int scatter_setup(const xs_scatter_desc* desc, int32_t M, int32_t N, cons
     sa->n_heads = nh;
     sa->head_dim = hd;
     sa->hpg = hpg;
+    // tiles inside one projection and one head group, heads not straddling a tile
+    sa->group_aligned = (nh * hd) % kBN == 0 && (hpg * hd) % kBN == 0 && kBN % hd == 0;
     int rc = xs_host::make_winset(win, W, static_cast<int64_t>(hd) * 2, ws);
     if (rc) return rc;
     for (int d = 0; d < W; ++d)

@@ -12,6 +12,7 @@ each policy (Expert-Wave burst issue, Alg. 1 interleave at the anti-starvation l
 chunked bursts, the model-driven AUTO) and producer cap, the fused layer is timed with HIP
 events around the persistent kernel and its device trace gives every Linear-2 tile's issue
 span (mainloop end -> last store issued):
+  (interleave_dyn: the same rule with tiles claimed from shared counters, XS_CLAIM_DYNAMIC)
   * measured stall = sum over tiles of [span - median span of the HBM control]_+, and its
     share of the producers' time (stall / (producers x kernel time));
   * predicted stall = xs_model_predict (Eqs. 3-6) on the burst sequence reconstructed from
@@ -98,10 +99,10 @@ def sweep_layer(cfg, host_model, caps, chunks, reps, rate):
     tile_bytes = (cfg.T * cfg.k // cfg.E) * 256 * 2   # rows of an expert's M-block x 256 columns
     tile_bytes = min(tile_bytes, 256 * 256 * 2)
     P1 = cfg.I // 128
-    configs = [("burst", X.XS_POLICY_BURST, 0, 0)]
-    configs += [(f"chunk{c}", X.XS_POLICY_CHUNK, c, 0) for c in chunks]
-    configs += [("interleave", X.XS_POLICY_INTERLEAVE, 0, 0), ("interleave_4xlead", X.XS_POLICY_INTERLEAVE, 0, 4),
-                ("auto", X.XS_POLICY_AUTO, 0, 0)]
+    configs = [("burst", X.XS_POLICY_BURST, 0, 0, 0)]
+    configs += [(f"chunk{c}", X.XS_POLICY_CHUNK, c, 0, 0) for c in chunks]
+    configs += [("interleave", X.XS_POLICY_INTERLEAVE, 0, 0, 0), ("interleave_4xlead", X.XS_POLICY_INTERLEAVE, 0, 4, 0),
+                ("auto", X.XS_POLICY_AUTO, 0, 0, 0), ("interleave_dyn", X.XS_POLICY_INTERLEAVE, 0, 0, 1)]
     results, control = [], {}
     for where in ("hbm", "host"):
         lay = EPLayer(s, combine_host=(where == "host"))
@@ -110,18 +111,18 @@ def sweep_layer(cfg, host_model, caps, chunks, reps, rate):
         cnt = torch.zeros((1,), dtype=torch.int32, device="cuda")
         e0, e1 = X.HipEvents(1), X.HipEvents(1)
         for cap in caps:
-            for name, pol, chunk, lead_mult in configs:
+            for name, pol, chunk, lead_mult, claim in configs:
                 knee = -(-(cap or 256) // P1)          # App. A.2 anti-starvation lead
                 p = pacing(pol, lead=lead_mult * knee, chunk=chunk, max_producers=cap,
-                           model=host_model if pol == X.XS_POLICY_AUTO else None)
+                           model=host_model if pol == X.XS_POLICY_AUTO else None, claim=claim)
                 times = []
                 for _ in range(reps):
                     cnt.zero_()
-                    lay.L.ffn_event_begin, lay.L.ffn_event_end = e0.ev[0], e1.ev[0]
+                    lay.L.events[X.XS_EV_FFN], lay.L.events[X.XS_EV_FFN_END] = e0.ev[0], e1.ev[0]
                     lay.fused(p, X.xs_trace(buf.data_ptr(), buf.shape[0], cnt.data_ptr()))
                     torch.cuda.synchronize()
                     times.append(X.HipEvents.elapsed_ms_pair(e0.ev[0], e1.ev[0]) * 1e3)
-                lay.L.ffn_event_begin, lay.L.ffn_event_end = None, None
+                lay.L.events[X.XS_EV_FFN], lay.L.events[X.XS_EV_FFN_END] = None, None
                 if int(lay.status.item()):
                     raise RuntimeError(f"device status {int(lay.status.item())}")
                 start, span, kern_us = trace_l2(buf, cnt, rate)

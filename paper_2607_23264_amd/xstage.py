@@ -23,6 +23,8 @@ XS_MAX_WINDOWS = 64
 XS_EXPERT_SWIGLU, XS_EXPERT_IDENTITY = 0, 1
 XS_POLICY_BURST, XS_POLICY_INTERLEAVE, XS_POLICY_CHUNK, XS_POLICY_AUTO = 0, 1, 2, 3
 XS_CLAIM_STATIC, XS_CLAIM_DYNAMIC = 0, 1
+(XS_EV_ROUTE, XS_EV_LAYOUT, XS_EV_DISPATCH, XS_EV_PLAN, XS_EV_FFN, XS_EV_FFN_END, XS_EV_REDUCE,
+ XS_EV_END) = range(8)
 XS_SCATTER_ROW_BLOCK, XS_SCATTER_HEAD_GROUP = 0, 1
 XS_MB_PERIODIC, XS_MB_COMPLETION = 0, 1
 
@@ -61,7 +63,7 @@ class xs_ep_layer(C.Structure):
                 ("expert_counts", vp), ("src_base", vp), ("expert_offsets", vp), ("dest_counts", vp),
                 ("slot_row", vp), ("row_src", vp), ("dispatch_win", C.POINTER(xs_window)),
                 ("combine_win", C.POINTER(xs_window)), ("h_ws", vp), ("h_rows", i64), ("y_ws", vp),
-                ("out", vp), ("ffn_event_begin", vp), ("ffn_event_end", vp)]
+                ("out", vp), ("events", vp * 8)]
 
 
 class xs_scatter_desc(C.Structure):

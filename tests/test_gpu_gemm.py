@@ -112,8 +112,10 @@ def _sp(x_bits, w_bits, nh, hd, hpg, serial=False):
     return host_bits(win)
 
 
-def test_sp_small_matches_oracle_bitexact_on_identity():
-    S, nh, hd, hpg = 300, 8, 32, 2
+@pytest.mark.parametrize("S,nh,hd,hpg", [(300, 8, 32, 2),     # heads straddle tile groups: generic path
+                                          (300, 8, 64, 4),     # one group per tile, 4 heads per tile
+                                          (257, 4, 256, 1)])   # one head per tile, ragged rows
+def test_sp_small_matches_oracle_bitexact_on_identity(S, nh, hd, hpg):
     N = 3 * nh * hd
     x = synth.normal_bf16(0, 7, (S, N))
     w = synth.to_bf16_bits(np.eye(N, dtype=np.float32))
