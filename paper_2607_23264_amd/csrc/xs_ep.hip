@@ -1,7 +1,8 @@
 // Expert-parallel routing, dispatch layout, dispatch stores and combine-reduce.
 //
-// Routing: one wavefront per token; top-k by repeated wave arg-max over the fp32 logits
-// (ties to the lower expert index) and a softmax over all E experts.
+// Routing: top-k by repeated arg-max over the fp32 logits (ties to the lower expert index)
+// and a softmax over all E experts; sixteen lanes per token with DPP reductions for
+// E <= 256 and k <= 16, one wavefront per token otherwise.
 // Layout: per 256-token chunk, every wave builds a 64-bit lane mask per expert in LDS
 // (ds_or_b64), so a slot's rank among earlier tokens of the chunk routed to the same expert
 // is a popcount: a deterministic, stable slot assignment. Chunk counts are scanned per
@@ -81,6 +82,108 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict
   if (lane < k) {
     topk_idx[static_cast<int64_t>(t) * k + lane] = my_idx;
     topk_w[static_cast<int64_t>(t) * k + lane] = my_w;
+  }
+}
+
+// Sixteen lanes per token (four tokens per wave), for E <= 16 * VPL and k <= 16. Lane s of
+// a token holds the logits e = 64 q + 4 s + c (q < VPL / 4, c < 4): 16 contiguous bytes per
+// lane and q, so a quarter-wave reads 256 contiguous bytes. The arg-max of each round and
+// the softmax sum reduce over the 16 lanes with DPP row rotations (no LDS round trips).
+template <int CTRL>
+__device__ __forceinline__ void argmax_dpp(float& bv, int& bi) {
+  const float ov = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(bv), CTRL, 0xF, 0xF, false));
+  const int oi = __builtin_amdgcn_update_dpp(0, bi, CTRL, 0xF, 0xF, false);
+  if (ov > bv || (ov == bv && oi < bi)) {
+    bv = ov;
+    bi = oi;
+  }
+}
+
+template <int CTRL>
+__device__ __forceinline__ float sum_dpp(float x) {
+  return x + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// all 16 lanes of a DPP row end with the reduction over the row: rotate by 8, 4, 2, 1
+constexpr int kRor8 = 0x128, kRor4 = 0x124, kRor2 = 0x122, kRor1 = 0x121;
+
+template <int VPL>
+__global__ __launch_bounds__(256) void route_topk16_kernel(const float* __restrict__ logits, int T,
+                                                           int E, int k, int renorm,
+                                                           int* __restrict__ topk_idx,
+                                                           float* __restrict__ topk_w) {
+  const int sub = threadIdx.x & 15;
+  const int t = (blockIdx.x * 256 + threadIdx.x) >> 4;
+  // every lane takes part in the row reductions: tokens past T read the last row, store nothing
+  const float* row = logits + static_cast<int64_t>(t < T ? t : T - 1) * E;
+  float v[VPL];
+  if ((E & 3) == 0) {
+    // rows start 16-byte aligned: one 128-bit load per lane and q
+#pragma unroll
+    for (int q = 0; q < VPL / 4; ++q) {
+      const int e = 64 * q + 4 * sub;
+      const f32x4 x = e < E ? *reinterpret_cast<const f32x4*>(row + e)
+                            : f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+      for (int c = 0; c < 4; ++c) v[4 * q + c] = x[c];
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < VPL / 4; ++q)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int e = 64 * q + 4 * sub + c;
+        v[4 * q + c] = e < E ? row[e] : -INFINITY;
+      }
+  }
+  uint32_t taken = 0;
+  float m = 0.f, my_v = -INFINITY;
+  int my_idx = 0;
+  for (int j = 0; j < k; ++j) {
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+#pragma unroll
+    for (int q = 0; q < VPL / 4; ++q)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int e = 64 * q + 4 * sub + c;
+        if (e < E && !((taken >> (4 * q + c)) & 1u) && v[4 * q + c] > bv) {
+          bv = v[4 * q + c];
+          bi = e;
+        }
+      }
+    argmax_dpp<kRor8>(bv, bi);
+    argmax_dpp<kRor4>(bv, bi);
+    argmax_dpp<kRor2>(bv, bi);
+    argmax_dpp<kRor1>(bv, bi);
+    if (j == 0) m = bv;   // the first winner is the row maximum
+    if (((bi >> 2) & 15) == sub) taken |= 1u << ((bi >> 6) * 4 + (bi & 3));
+    if (sub == j) {
+      my_idx = bi;
+      my_v = bv;
+    }
+  }
+  // softmax denominator over all experts: lane partials in ascending e, then the row sum
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < VPL; ++i)
+    if (64 * (i / 4) + 4 * sub + (i % 4) < E) s += expf(v[i] - m);
+  s = sum_dpp<kRor8>(s);
+  s = sum_dpp<kRor4>(s);
+  s = sum_dpp<kRor2>(s);
+  s = sum_dpp<kRor1>(s);
+  float my_w = expf(my_v - m) / s;
+  if (renorm) {
+    float ws = sub < k ? my_w : 0.f;
+    ws = sum_dpp<kRor8>(ws);
+    ws = sum_dpp<kRor4>(ws);
+    ws = sum_dpp<kRor2>(ws);
+    ws = sum_dpp<kRor1>(ws);
+    my_w = my_w / ws;
+  }
+  if (t < T && sub < k) {
+    topk_idx[static_cast<int64_t>(t) * k + sub] = my_idx;
+    topk_w[static_cast<int64_t>(t) * k + sub] = my_w;
   }
 }
 
@@ -267,24 +370,37 @@ __global__ __launch_bounds__(256) void combine_reduce_kernel(const char* __restr
   const float wl = lane < k ? w[static_cast<int64_t>(t) * k + lane] : 0.f;
   const int nch = H >> 3;
   u32x4* dst = reinterpret_cast<u32x4*>(out + static_cast<int64_t>(t) * H);
-  for (int c = lane; c < nch; c += 64) {
-    float acc[8];
+  const char* rows = cbuf + static_cast<int64_t>(t) * k * cstride;
+  // two 16-byte pieces per lane per pass: 2k independent loads in flight before the sums
+  for (int c0 = lane; c0 < nch; c0 += 128) {
+    const int c1 = c0 + 64;
+    const bool two = c1 < nch;
+    float acc[2][8];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) acc[h][q] = 0.f;
     for (int j = 0; j < k; ++j) {
-      float wj = __shfl(wl, j);
-      const u32x4 p = reinterpret_cast<const u32x4*>(
-          cbuf + (static_cast<int64_t>(t) * k + j) * cstride)[c];
+      const float wj = __shfl(wl, j);
+      const u32x4* r = reinterpret_cast<const u32x4*>(rows + static_cast<int64_t>(j) * cstride);
+      const u32x4 p0 = r[c0];
+      const u32x4 p1 = two ? r[c1] : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        acc[2 * q] += wj * bf_lo(p[q]);
-        acc[2 * q + 1] += wj * bf_hi(p[q]);
+        acc[0][2 * q] += wj * bf_lo(p0[q]);
+        acc[0][2 * q + 1] += wj * bf_hi(p0[q]);
+        acc[1][2 * q] += wj * bf_lo(p1[q]);
+        acc[1][2 * q + 1] += wj * bf_hi(p1[q]);
       }
     }
-    u32x4 o;
+    u32x4 o0, o1;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) o[q] = pack_bf16x2(acc[2 * q], acc[2 * q + 1]);
-    dst[c] = o;
+    for (int q = 0; q < 4; ++q) {
+      o0[q] = pack_bf16x2(acc[0][2 * q], acc[0][2 * q + 1]);
+      o1[q] = pack_bf16x2(acc[1][2 * q], acc[1][2 * q + 1]);
+    }
+    dst[c0] = o0;
+    if (two) dst[c1] = o1;
   }
 }
 
@@ -321,6 +437,16 @@ extern "C" int xs_route_topk_softmax(const float* logits, int32_t T, int32_t E, 
     return XS_EINVAL;
   if (T == 0) return XS_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if (E <= 256 && k <= 16) {
+    const dim3 g16((T + 15) / 16), b16(256);
+    if (E <= 64)
+      hipLaunchKernelGGL(route_topk16_kernel<4>, g16, b16, 0, st, logits, T, E, k, renormalize, topk_idx, topk_w);
+    else if (E <= 128)
+      hipLaunchKernelGGL(route_topk16_kernel<8>, g16, b16, 0, st, logits, T, E, k, renormalize, topk_idx, topk_w);
+    else
+      hipLaunchKernelGGL(route_topk16_kernel<16>, g16, b16, 0, st, logits, T, E, k, renormalize, topk_idx, topk_w);
+    return xs_host::launch_status();
+  }
   dim3 grid((T + 3) / 4), block(256);
   const int epl = (E + 63) / 64;
 #define XS_ROUTE(N)                                                                        \

@@ -37,7 +37,7 @@ def _route_gpu(logits, k, renorm=0):
 
 
 @pytest.mark.parametrize("case", ["tiny", "dsv3_uniform", "dsv3_zipf", "ties_E1000_k32", "one_token",
-                                  "k_equals_E", "renorm"])
+                                  "k_equals_E", "renorm", "ties_E200_k16", "E100_k3_T17"])
 def test_route_matches_oracle(case):
     g = np.random.default_rng(11)
     renorm = 0
@@ -54,6 +54,12 @@ def test_route_matches_oracle(case):
         lg, k = g.standard_normal((1, 64)).astype(np.float32), 4
     elif case == "k_equals_E":
         lg, k = g.standard_normal((9, 8)).astype(np.float32), 8
+    elif case == "ties_E200_k16":   # sixteen-lane kernel: ties, E not a multiple of 64, k = 16
+        lg, k = (np.round(g.standard_normal((41, 200)) * 2) / 2).astype(np.float32), 16
+        lg[3] = 0.0
+        lg[7, 150:] = 9.0
+    elif case == "E100_k3_T17":     # sixteen-lane kernel with 8 logits per lane, T not a multiple of 16
+        lg, k = g.standard_normal((17, 100)).astype(np.float32), 3
     else:
         lg, k, renorm = synth.uniform_logits(0, 2, 200, 64), 6, 1
     idx, w = _route_gpu(lg, k, renorm)
