@@ -37,8 +37,14 @@ __device__ __forceinline__ uint32_t f2bf(float f) {
   return u >> 16;
 }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two fp32 -> packed bf16 (lo in bits 0..15) with gfx950's v_cvt_pk_bf16_f32: round to
+// nearest even, as f2bf, in one instruction and without a branch.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return f2bf(lo) | (f2bf(hi) << 16);
+  const bf16x2_t b = __builtin_convertvector(f32x2{lo, hi}, bf16x2_t);
+  return __builtin_bit_cast(uint32_t, b);
 }
 
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }

@@ -290,7 +290,9 @@ __device__ __forceinline__ void stage_swiglu(const Acc& acc, char* lds) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const float gt = acc[i][0][4 * g + q], up = acc[i][1][4 * g + q];
-        h[q] = gt / (1.f + __expf(-gt)) * up;
+        // silu(g) = g / (1 + e^-g), with the hardware reciprocal (about 1 ulp) in place of an
+        // IEEE division sequence
+        h[q] = gt * __builtin_amdgcn_rcpf(1.f + __expf(-gt)) * up;
       }
       uint2 v;
       v.x = pack_bf16x2(h[0], h[1]);
@@ -304,17 +306,22 @@ __device__ __forceinline__ void stage_swiglu(const Acc& acc, char* lds) {
 // skipped). cols = 256 (plain) or 128 (SwiGLU). Every piece is one 128-bit store.
 __device__ __forceinline__ void store_rows(const char* lds_bytes, int pitch, int cols, int rows,
                                            char* const* rowptr) {
+  typedef __attribute__((address_space(1))) u32x4 global_u32x4;
   const uint16_t* lds = reinterpret_cast<const uint16_t*>(lds_bytes);
   const int tid = threadIdx.x;
   const int per_row = cols / 8;                // 16-byte pieces per row
   const int rows_per_pass = kThreads / per_row;
   const int pc = tid % per_row;
+  // global-address stores (a generic pointer would make them flat stores, which also count
+  // against the LDS wait counter); no unrolling, so no per-row LDS addresses are held (and
+  // spilled) across the loop. (Measured: nontemporal stores here slow the next tiles'
+  // mainloops by about 5 %.)
+#pragma unroll 1
   for (int r = tid / per_row; r < rows; r += rows_per_pass) {
     char* p = rowptr[r];
     if (!p) continue;
-    u32x4 v = *reinterpret_cast<const u32x4*>(lds + r * pitch + pc * 8);
-    // (measured: nontemporal stores here slow the next tiles' mainloops by about 5 %)
-    *reinterpret_cast<u32x4*>(p + pc * 16) = v;
+    const u32x4 v = *reinterpret_cast<const u32x4*>(lds + r * pitch + pc * 8);
+    *(global_u32x4*)(p + pc * 16) = v;
   }
 }
 
