@@ -35,7 +35,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--routing", choices=["uniform", "zipf"], default="uniform")
     p.add_argument("--policy", choices=["burst", "interleave", "chunk"], default="interleave")
-    p.add_argument("--lead", type=int, default=0, help="0 = the anti-starvation knee")
+    p.add_argument("--lead", type=int, default=64,
+                   help="lead D in rows (0 = the anti-starvation knee, ceil(grid / P1) = 16 here); "
+                        "64 = four knees, the fastest interleave measured on this share")
     p.add_argument("--chunk", type=int, default=2)
     p.add_argument("--claim", choices=["static", "dynamic"], default="dynamic",
                    help="how producers take tiles (dynamic: shared counters, same tile rule)")
