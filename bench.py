@@ -44,7 +44,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-phases", action="store_true")
     p.add_argument("--no-scatter", action="store_true", help="skip the TP / SP scatter GEMM lines")
-    p.add_argument("--no-slow-sink", action="store_true", help="skip the host-coherent sink line")
+    p.add_argument("--slow-sink", action="store_true",
+                   help="also run the host-coherent sink line (the tiny layer: it launches the same "
+                        "fused kernel, so it stays out of the default run and its kernel statistics)")
     p.add_argument("--policies", action="store_true",
                    help="also time the fused layer under every pacing policy (phases)")
     p.add_argument("--seed", type=int, default=0)
@@ -384,7 +386,7 @@ def main():
         log("[bench] TP / SP scatter GEMMs")
         res["scatter"] = scatter_lines(X, torch, synth)
         log("[bench] " + json.dumps(res["scatter"]))
-    if not a.no_slow_sink:
+    if a.slow_sink:
         log("[bench] slow sink (host-coherent combine windows)")
         res["slow_sink"] = slow_sink_line(X, torch, synth)
         log("[bench] " + json.dumps(res["slow_sink"]["layers"]))

@@ -128,7 +128,7 @@ def cmd_traffic(a):
            f"| copy FETCH_SIZE / WRITE_SIZE, KiB | {cf:.0f} / {cw:.0f} |",
            f"| fetched bytes per dispatch (scaled) | {fb / 1e9:.3f} GB |",
            f"| written bytes per dispatch (scaled) | {wb / 1e9:.3f} GB |",
-           f"| total HBM bytes per dispatch | {(fb + wb) / 1e9:.3f} GB |"]
+           f"| total bytes per dispatch (HBM traffic as these counters see it; MALL hits included) | {(fb + wb) / 1e9:.3f} GB |"]
     if a.algorithmic_bytes:
         out.append(f"| algorithmic bytes per dispatch | {a.algorithmic_bytes / 1e9:.3f} GB |")
         out.append(f"| traffic / algorithmic | {(fb + wb) / a.algorithmic_bytes:.2f} |")
