@@ -313,7 +313,9 @@ __global__ __launch_bounds__(256) void layout_finalize_kernel(
 }
 
 // ------------------------------------------------------------------------------ dispatch
-// One wave per token. Lanes hold up to 8 16-byte pieces of the row per round.
+// One wave per token (measured: a quarter row per wave, four waves per token, is slower).
+// Lanes hold up to 8 16-byte pieces of the row per round and store them into the k
+// destination rows.
 __global__ __launch_bounds__(256) void dispatch_kernel(const uint16_t* __restrict__ x, int T, int H,
                                                        const int* __restrict__ idx,
                                                        const int* __restrict__ slot_row, int k,
@@ -351,7 +353,7 @@ __global__ __launch_bounds__(256) void dispatch_kernel(const uint16_t* __restric
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         int c = c0 + u * 64 + lane;
-        if (c < nch) dst[c] = v[u];
+        if (c < nch) dst[c] = v[u];   // (measured: nontemporal stores here are slower)
       }
     }
   }
@@ -365,32 +367,50 @@ __global__ __launch_bounds__(256) void combine_reduce_kernel(const char* __restr
                                                              int k, int H,
                                                              uint16_t* __restrict__ out) {
   const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  // four waves per token, each over a quarter of the row's 16-byte pieces (one wave per
+  // token left 16 waves per CU at T = 4096, too few loads in flight to stream HBM)
+  const int wv = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int t = wv >> 2;
   if (t >= T) return;
   const float wl = lane < k ? w[static_cast<int64_t>(t) * k + lane] : 0.f;
   const int nch = H >> 3;
+  const int per = (nch + 3) >> 2;
+  const int c_begin = (wv & 3) * per;
+  const int c_end = min(nch, c_begin + per);
   u32x4* dst = reinterpret_cast<u32x4*>(out + static_cast<int64_t>(t) * H);
   const char* rows = cbuf + static_cast<int64_t>(t) * k * cstride;
-  // two 16-byte pieces per lane per pass: 2k independent loads in flight before the sums
-  for (int c0 = lane; c0 < nch; c0 += 128) {
+  // two 16-byte pieces per lane per pass, the slots' loads issued in blocks of eight before
+  // any sum (a loop over the runtime k kept only two loads in flight)
+  for (int c0 = c_begin + lane; c0 < c_end; c0 += 128) {
     const int c1 = c0 + 64;
-    const bool two = c1 < nch;
+    const bool two = c1 < c_end;
     float acc[2][8];
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int q = 0; q < 8; ++q) acc[h][q] = 0.f;
-    for (int j = 0; j < k; ++j) {
-      const float wj = __shfl(wl, j);
-      const u32x4* r = reinterpret_cast<const u32x4*>(rows + static_cast<int64_t>(j) * cstride);
-      const u32x4 p0 = r[c0];
-      const u32x4 p1 = two ? r[c1] : u32x4{0u, 0u, 0u, 0u};
+    for (int j0 = 0; j0 < k; j0 += 8) {
+      u32x4 p0[8], p1[8];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        acc[0][2 * q] += wj * bf_lo(p0[q]);
-        acc[0][2 * q + 1] += wj * bf_hi(p0[q]);
-        acc[1][2 * q] += wj * bf_lo(p1[q]);
-        acc[1][2 * q + 1] += wj * bf_hi(p1[q]);
+      for (int jj = 0; jj < 8; ++jj) {
+        p0[jj] = p1[jj] = u32x4{0u, 0u, 0u, 0u};
+        if (j0 + jj < k) {
+          const u32x4* r = reinterpret_cast<const u32x4*>(rows + static_cast<int64_t>(j0 + jj) * cstride);
+          p0[jj] = __builtin_nontemporal_load(r + c0);   // each combine row is read once
+          if (two) p1[jj] = __builtin_nontemporal_load(r + c1);
+        }
+      }
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) {
+        if (j0 + jj >= k) break;
+        const float wj = __shfl(wl, j0 + jj);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc[0][2 * q] += wj * bf_lo(p0[jj][q]);
+          acc[0][2 * q + 1] += wj * bf_hi(p0[jj][q]);
+          acc[1][2 * q] += wj * bf_lo(p1[jj][q]);
+          acc[1][2 * q + 1] += wj * bf_hi(p1[jj][q]);
+        }
       }
     }
     u32x4 o0, o1;
@@ -527,7 +547,7 @@ int dispatch(const void* x, int32_t T, int32_t H, const int32_t* topk_idx, const
 int combine_reduce(const void* cbuf, int64_t cstride, const float* w, int32_t T, int32_t k,
                    int32_t H, void* out, hipStream_t st) {
   if (T == 0) return XS_OK;
-  hipLaunchKernelGGL(combine_reduce_kernel, dim3((T + 3) / 4), dim3(256), 0, st,
+  hipLaunchKernelGGL(combine_reduce_kernel, dim3(T), dim3(256), 0, st,
                      static_cast<const char*>(cbuf), cstride, w, T, k, H,
                      static_cast<uint16_t*>(out));
   return launch_status();
