@@ -17,9 +17,10 @@ Modules:
   scatter         TP row-block and Ulysses head-group GEMM scatter epilogues
   xstage_model    Burst-Gap model (Eqs. 1-9), calibration fit, audit helpers
   schedule        tile orders: Expert-Wave, cross-wave interleave (Alg. 1), chunked
+  attention       softmax attention and the post-attention Ulysses exchange
 
 Parity status: every function here is pinned by tests under ``tests/`` against
 closed forms, worked numbers the paper prints, brute force or library routines,
 except where a function's docstring says "parity unpinned".
 """
-from . import ep, scatter, xstage_model, schedule  # noqa: F401
+from . import attention, ep, scatter, xstage_model, schedule  # noqa: F401

@@ -217,3 +217,24 @@ def sp_inputs(cfg: SPConfig, seed: int = 0):
     """X [S,Dm] ~ N(0,1) and Wqkv logically [Dm, 3*Dm] ~ N(0, w_std^2), bf16 bits."""
     return {"x": normal_bf16(seed, 7, (cfg.S, cfg.Dm)),
             "w": normal_bf16(seed, 8, (cfg.Dm, 3 * cfg.n_heads * cfg.head_dim), std=cfg.w_std)}
+
+
+@dataclass(frozen=True)
+class AttnConfig:
+    """One rank's Ulysses attention share: all M tokens of its local heads."""
+    name: str
+    M: int                # sequence length (all tokens, after the pre-attention exchange)
+    heads: int            # local heads
+    head_dim: int
+    W: int                # sequence chunks = destination windows of the post-attention exchange
+
+
+ATTN_UP_8K = AttnConfig("attn_up_M8192_h8_d128_W8", M=8192, heads=8, head_dim=128, W=8)
+ATTN_UP_16K = AttnConfig("attn_up_M16384_h8_d128_W8", M=16384, heads=8, head_dim=128, W=8)
+ATTN_UP_32K = AttnConfig("attn_up_M32768_h8_d128_W8", M=32768, heads=8, head_dim=128, W=8)
+
+
+def attn_inputs(cfg: AttnConfig, seed: int = 0):
+    """Q, K, V [heads][M][head_dim] ~ N(0, 1), bf16 bits."""
+    sh = (cfg.heads, cfg.M, cfg.head_dim)
+    return {"q": normal_bf16(seed, 900, sh), "k": normal_bf16(seed, 901, sh), "v": normal_bf16(seed, 902, sh)}
