@@ -298,6 +298,55 @@ int xs_gemm_scatter(const void* a, int64_t lda, const void* b, int64_t ldb, int3
 int xs_scatter_copy(const void* c, int64_t ldc, int32_t M, int32_t N, const xs_scatter_desc* desc,
                     const xs_window* win, int32_t W, void* stream);
 
+/* ----------------------------------------------------------------------------- attention
+ * Attention with the post-attention Ulysses exchange (Sec. 4.4, App. B; Table 4). One
+ * rank's share after the pre-attention exchange: all M tokens of `heads` local heads.
+ *   O[h][t][:] = sum_u softmax_u(scale * Q[h][t] . K[h][u]) V[h][u]   (full, non-causal)
+ * computed as a flash-attention pass: every persistent workgroup takes 128-query output
+ * tiles of one head and streams the head's K/V in 64-token tiles (the Q-loop), with an
+ * online softmax in fp32 and bf16 probabilities for the second product.
+ *   q, k, v  device bf16 [heads][M][head_dim]; head_dim must be 128.
+ *   scale    0 = 1 / sqrt(head_dim).
+ *   M        multiple of 128; with windows, M / W must be a multiple of 128 (a tile never
+ *            straddles two destinations).
+ * Modes:
+ *   XS_ATTN_LOCAL    output o, device bf16 [heads][M][head_dim] ("FA-only").
+ *   XS_ATTN_WINDOWS  each finished output tile is stored by the workgroup that computed it
+ *                    into window g = t / (M / W): row t % (M / W), head slot h, i.e. at
+ *                    base + (t % (M / W)) * row_stride_bytes + h * head_dim * 2 (a window
+ *                    holds [M / W][heads][head_dim]); the next Q-loop is the drain window.
+ *                    Ready flags are set after the last tile.
+ * max_producers caps the persistent grid (0 = two workgroups per CU). The optional trace
+ * records one kind-4 record per output tile: rec[1] tile start, rec[2] end of its Q-loop,
+ * rec[3] after its stores were issued. q, k, v and o are 16-byte aligned; windows as for the
+ * other window calls (16-byte aligned base and row stride, stride >= heads * head_dim * 2,
+ * capacity >= M / W rows). The caller owns every buffer; nothing is allocated. Returns
+ * XS_EINVAL for null, misaligned or inconsistent arguments, XS_EUNSUPPORTED for a head_dim,
+ * M or M / W the kernel does not tile, XS_EHIP if a launch fails; nothing is launched on an
+ * argument error. Output tiles are computed in a fixed order of operations, so results do
+ * not depend on the grid size or on the mode. */
+enum { XS_ATTN_LOCAL = 0, XS_ATTN_WINDOWS = 1 };
+
+typedef struct xs_attn {
+  int32_t heads, M, head_dim, W;
+  float scale;
+  int32_t max_producers;
+  const void* q;              /* device bf16 [heads][M][head_dim] */
+  const void* k;
+  const void* v;
+  void* o;                    /* XS_ATTN_LOCAL: device bf16 [heads][M][head_dim] */
+  const xs_window* win;       /* XS_ATTN_WINDOWS: host array [W] */
+} xs_attn;
+
+int xs_attention(const xs_attn* a, int32_t mode, const xs_trace* trace, void* stream);
+
+/* The serial post-attention exchange: o (device bf16 [heads][M][head_dim], 16-byte aligned,
+ * head_dim a multiple of 8) copied into the windows of XS_ATTN_WINDOWS, then their ready flags
+ * set (the baseline the fused path is compared with). Returns XS_EINVAL for bad arguments,
+ * XS_EHIP if a launch fails. */
+int xs_ulysses_copy(const void* o, int32_t heads, int32_t M, int32_t head_dim,
+                    const xs_window* win, int32_t W, void* stream);
+
 /* ----------------------------------------------------------------------------- X-Stage
  * Burst-Gap model (Sec. 3.3-3.5). Units: bytes and microseconds.
  *   T0(V) = t0_a_us + t0_b_us_per_byte * V   recovered issue floor at K producers

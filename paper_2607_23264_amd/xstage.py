@@ -27,6 +27,7 @@ XS_CLAIM_STATIC, XS_CLAIM_DYNAMIC = 0, 1
  XS_EV_END) = range(8)
 XS_SCATTER_ROW_BLOCK, XS_SCATTER_HEAD_GROUP = 0, 1
 XS_MB_PERIODIC, XS_MB_COMPLETION = 0, 1
+XS_ATTN_LOCAL, XS_ATTN_WINDOWS = 0, 1
 
 vp = C.c_void_p
 i32 = C.c_int32
@@ -64,6 +65,12 @@ class xs_ep_layer(C.Structure):
                 ("slot_row", vp), ("row_src", vp), ("dispatch_win", C.POINTER(xs_window)),
                 ("combine_win", C.POINTER(xs_window)), ("h_ws", vp), ("h_rows", i64), ("y_ws", vp),
                 ("out", vp), ("events", vp * 8)]
+
+
+class xs_attn(C.Structure):
+    _fields_ = [("heads", i32), ("M", i32), ("head_dim", i32), ("W", i32), ("scale", C.c_float),
+                ("max_producers", i32), ("q", vp), ("k", vp), ("v", vp), ("o", vp),
+                ("win", C.POINTER(xs_window))]
 
 
 class xs_scatter_desc(C.Structure):
@@ -118,6 +125,8 @@ xs_gemm_scatter = _sig("xs_gemm_scatter", C.c_int, vp, i64, vp, i64, i32, i32, i
                        P(xs_window), i32, P(xs_trace), vp)
 xs_scatter_copy = _sig("xs_scatter_copy", C.c_int, vp, i64, i32, i32, P(xs_scatter_desc), P(xs_window),
                        i32, vp)
+xs_attention = _sig("xs_attention", C.c_int, P(xs_attn), i32, P(xs_trace), vp)
+xs_ulysses_copy = _sig("xs_ulysses_copy", C.c_int, vp, i32, i32, i32, P(xs_window), i32, vp)
 xs_model_predict = _sig("xs_model_predict", C.c_int, P(xs_model), P(xs_burst), i32, f64, P(xs_burst_pred))
 xs_model_fit = _sig("xs_model_fit", C.c_int, P(xs_calib), P(xs_model))
 xs_xstage_microbench = _sig("xs_xstage_microbench", C.c_int, P(xs_microbench_args), P(xs_trace), vp)
@@ -126,8 +135,8 @@ xs_clock_rate_hz = _sig("xs_clock_rate_hz", C.c_double)
 EXPORTED = ["xs_strerror", "xs_version", "xs_route_topk_softmax", "xs_dispatch_layout_workspace_bytes",
             "xs_dispatch_layout", "xs_dispatch", "xs_ep_layer_workspace_bytes", "xs_expert_ffn",
             "xs_combine_send", "xs_combine_reduce", "xs_fused_ep_layer", "xs_gemm", "xs_gemm_scatter",
-            "xs_scatter_copy", "xs_model_predict", "xs_model_fit", "xs_xstage_microbench",
-            "xs_clock_rate_hz"]
+            "xs_scatter_copy", "xs_attention", "xs_ulysses_copy", "xs_model_predict", "xs_model_fit",
+            "xs_xstage_microbench", "xs_clock_rate_hz"]
 
 
 class XStageError(RuntimeError):
