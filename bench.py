@@ -47,6 +47,8 @@ def parse():
     p.add_argument("--slow-sink", action="store_true",
                    help="also run the host-coherent sink line (the tiny layer: it launches the same "
                         "fused kernel, so it stays out of the default run and its kernel statistics)")
+    p.add_argument("--no-attn", action="store_true",
+                   help="skip the attention + Ulysses exchange line (HBM and host-coherent windows)")
     p.add_argument("--policies", action="store_true",
                    help="also time the fused layer under every pacing policy (phases)")
     p.add_argument("--seed", type=int, default=0)
@@ -386,6 +388,13 @@ def main():
         log("[bench] TP / SP scatter GEMMs")
         res["scatter"] = scatter_lines(X, torch, synth)
         log("[bench] " + json.dumps(res["scatter"]))
+    if not a.no_attn:
+        log("[bench] attention + post-attention Ulysses exchange (FA-only / serial / fused / coupled)")
+        from paper_2607_23264_amd import attn_a2a
+        rep = attn_a2a.run()
+        res["attention_a2a"] = {"workload": rep["workload"], "grid": rep["grid"], "summary": rep["summary"],
+                                "cells": rep["cells"]}
+        torch.cuda.empty_cache()
     if a.slow_sink:
         log("[bench] slow sink (host-coherent combine windows)")
         res["slow_sink"] = slow_sink_line(X, torch, synth)

@@ -316,6 +316,10 @@ int xs_scatter_copy(const void* c, int64_t ldc, int32_t M, int32_t N, const xs_s
  *                    base + (t % (M / W)) * row_stride_bytes + h * head_dim * 2 (a window
  *                    holds [M / W][heads][head_dim]); the next Q-loop is the drain window.
  *                    Ready flags are set after the last tile.
+ *   XS_ATTN_WINDOWS_COUPLED  as XS_ATTN_WINDOWS, but after each tile's stores the producer
+ *                    waits until they are visible at system scope before its next Q-loop:
+ *                    the completion-coupled issuer the paper argues against (Sec. 4.4, Fig. 7),
+ *                    kept as the measured counterfactual.
  * max_producers caps the persistent grid (0 = two workgroups per CU). The optional trace
  * records one kind-4 record per output tile: rec[1] tile start, rec[2] end of its Q-loop,
  * rec[3] after its stores were issued. q, k, v and o are 16-byte aligned; windows as for the
@@ -325,7 +329,7 @@ int xs_scatter_copy(const void* c, int64_t ldc, int32_t M, int32_t N, const xs_s
  * M or M / W the kernel does not tile, XS_EHIP if a launch fails; nothing is launched on an
  * argument error. Output tiles are computed in a fixed order of operations, so results do
  * not depend on the grid size or on the mode. */
-enum { XS_ATTN_LOCAL = 0, XS_ATTN_WINDOWS = 1 };
+enum { XS_ATTN_LOCAL = 0, XS_ATTN_WINDOWS = 1, XS_ATTN_WINDOWS_COUPLED = 2 };
 
 typedef struct xs_attn {
   int32_t heads, M, head_dim, W;

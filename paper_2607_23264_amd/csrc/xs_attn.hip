@@ -209,7 +209,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(Args a) {
     // epilogue: O[q][d] for d = 32 db + 8 g + 4 up + 0..3
     const float inv = 1.f / l;
     char* dst;
-    if (a.mode == XS_ATTN_WINDOWS) {
+    if (a.mode != XS_ATTN_LOCAL) {
       const int g = (qt * kBQ) / a.chunk;    // uniform: a tile lies in one sequence chunk
       dst = a.win.base[g] + static_cast<int64_t>(qrow - g * a.chunk) * a.win.stride[g] +
             static_cast<int64_t>(h) * kD * 2;
@@ -225,6 +225,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(Args a) {
                          pack_bf16x2(oacc[db][4 * g + 2] * inv, oacc[db][4 * g + 3] * inv)};
         *(__attribute__((address_space(1))) u32x2*)(dst + (32 * db + 8 * g + 4 * up) * 2) = v;
       }
+    // completion-coupled counterfactual: the producer waits until its stores are visible at
+    // system scope before it starts the next Q-loop
+    if (a.mode == XS_ATTN_WINDOWS_COUPLED) __threadfence_system();
     // the next tile's loads overwrite both stages: every wave must be done with them (the
     // stores above may still drain)
     __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
@@ -284,7 +287,7 @@ extern "C" int xs_attention(const xs_attn* A, int32_t mode, const xs_trace* trac
   if (!A || !A->q || !A->k || !A->v || A->heads < 1 || A->M < 1 || A->head_dim < 1 ||
       !(A->scale >= 0.f) || A->max_producers < 0)
     return XS_EINVAL;
-  if (mode != XS_ATTN_LOCAL && mode != XS_ATTN_WINDOWS) return XS_EINVAL;
+  if (mode != XS_ATTN_LOCAL && mode != XS_ATTN_WINDOWS && mode != XS_ATTN_WINDOWS_COUPLED) return XS_EINVAL;
   const auto misaligned = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) != 0; };
   if (misaligned(A->q) || misaligned(A->k) || misaligned(A->v)) return XS_EINVAL;
   if (A->head_dim != attn::kD || A->M % attn::kBQ) return XS_EUNSUPPORTED;
@@ -315,7 +318,7 @@ extern "C" int xs_attention(const xs_attn* A, int32_t mode, const xs_trace* trac
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipLaunchKernelGGL(attn::attn_kernel, dim3(grid), dim3(attn::kThreads), 0, st, a);
   if (xs_host::launch_status()) return XS_EHIP;
-  if (mode == XS_ATTN_WINDOWS) return xs_host::signal_windows(a.win, st);
+  if (mode != XS_ATTN_LOCAL) return xs_host::signal_windows(a.win, st);
   return XS_OK;
 }
 

@@ -26,6 +26,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 # sources that define the fused expert-FFN kernel's code (a change to any of them makes a
 # stored traffic measurement stale)
 FFN_KERNEL_SOURCES = ("csrc/xs_ep_ffn.hip", "csrc/xs_gemm.hpp", "csrc/xs_common.hpp", "build.py")
+ATTN_KERNEL_SOURCES = ("csrc/xs_attn.hip", "csrc/xs_common.hpp", "build.py")
+KERNEL_SOURCES = {"ffn": FFN_KERNEL_SOURCES, "attn": ATTN_KERNEL_SOURCES}
 
 
 def sources_hash(paths=FFN_KERNEL_SOURCES) -> str:
@@ -112,7 +114,7 @@ def cmd_traffic(a):
         sys.exit(f"no {a.kernel} dispatches in the counter files")
     mean = lambda v: sum(v) / len(v)
     fb, wb = mean(fetch) * 1024.0 * kf, mean(write) * 1024.0 * kw
-    rec = {"kernel": a.kernel, "sources_sha": sources_hash(), "fetch_bytes": fb, "write_bytes": wb,
+    rec = {"kernel": a.kernel, "sources_sha": sources_hash(KERNEL_SOURCES[a.sources]), "fetch_bytes": fb, "write_bytes": wb,
            "traffic_bytes": fb + wb, "fetch_scale": kf, "write_scale": kw,
            "dispatches": [len(fetch), len(write)], "algorithmic_bytes": a.algorithmic_bytes}
     out = ["# HBM traffic per dispatch (rocprofv3 counters)", "",
@@ -158,6 +160,8 @@ def main():
     t.add_argument("--copy-bytes", type=float, required=True)
     t.add_argument("--copy-kernel", default="__amd_rocclr_copyBuffer")
     t.add_argument("--algorithmic-bytes", type=float, default=0.0)
+    t.add_argument("--sources", choices=sorted(KERNEL_SOURCES), default="ffn",
+                   help="which kernel's sources key the record")
     t.add_argument("--commands", required=True, help="the counter commands, separated by ';;'")
     t.add_argument("--out", required=True)
     a = ap.parse_args()

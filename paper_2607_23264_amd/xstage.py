@@ -27,7 +27,7 @@ XS_CLAIM_STATIC, XS_CLAIM_DYNAMIC = 0, 1
  XS_EV_END) = range(8)
 XS_SCATTER_ROW_BLOCK, XS_SCATTER_HEAD_GROUP = 0, 1
 XS_MB_PERIODIC, XS_MB_COMPLETION = 0, 1
-XS_ATTN_LOCAL, XS_ATTN_WINDOWS = 0, 1
+XS_ATTN_LOCAL, XS_ATTN_WINDOWS, XS_ATTN_WINDOWS_COUPLED = 0, 1, 2
 
 vp = C.c_void_p
 i32 = C.c_int32

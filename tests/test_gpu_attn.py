@@ -53,13 +53,14 @@ def _windows(heads, M, W, pad_cols=0):
     return buf, flags, wins
 
 
-def _fused(q_bits, k_bits, v_bits, W, pad_cols=0, max_producers=0):
+def _fused(q_bits, k_bits, v_bits, W, pad_cols=0, max_producers=0, coupled=False):
     X = xs()
     heads, M, _ = q_bits.shape
     q, k, v = dev_bits(q_bits), dev_bits(k_bits), dev_bits(v_bits)
     buf, flags, wins = _windows(heads, M, W, pad_cols)
     a = _desc(heads, M, q, k, v, win=wins, W=W, max_producers=max_producers)
-    X.check(X.xs_attention(a, X.XS_ATTN_WINDOWS, None, _stream()))
+    mode = X.XS_ATTN_WINDOWS_COUPLED if coupled else X.XS_ATTN_WINDOWS
+    X.check(X.xs_attention(a, mode, None, _stream()))
     torch.cuda.synchronize()
     return host_bits(buf), flags.cpu().numpy()
 
@@ -127,6 +128,13 @@ def test_fused_windows_equal_local_output_scattered(heads, M, W, pad):
     assert_close(_windows_as_heads(win, heads), oa.ulysses_scatter(ref64, W), "fused windows")
 
 
+def test_completion_coupled_mode_stores_the_same_bits():
+    q, k, v = _inputs(2, 1024, seed=61)
+    a, fa = _fused(q, k, v, 4, max_producers=3)
+    b, fb = _fused(q, k, v, 4, max_producers=3, coupled=True)
+    assert np.array_equal(a, b) and (fa == 1).all() and (fb == 1).all()
+
+
 def test_serial_copy_equals_fused():
     X = xs()
     heads, M, W = 2, 512, 4
@@ -187,7 +195,7 @@ def test_bad_arguments_are_rejected():
         a.head_dim = hd
         assert X.xs_attention(a, X.XS_ATTN_LOCAL, None, _stream()) == X.XS_EUNSUPPORTED
     # bad mode, missing output, negative scale, misaligned input
-    assert X.xs_attention(ok, 2, None, _stream()) == X.XS_EINVAL
+    assert X.xs_attention(ok, 3, None, _stream()) == X.XS_EINVAL
     assert X.xs_attention(_desc(heads, M, q, q, q), X.XS_ATTN_LOCAL, None, _stream()) == X.XS_EINVAL
     a = _desc(heads, M, q, q, q, o=o, scale=-1.0)
     assert X.xs_attention(a, X.XS_ATTN_LOCAL, None, _stream()) == X.XS_EINVAL
