@@ -38,9 +38,12 @@ namespace xs {
 namespace attn {
 
 typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) char lds_char;
 typedef const __attribute__((address_space(1))) void glob_void;
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
 
 constexpr int kD = 128;                    // head_dim
 constexpr int kBQ = 128;                   // queries per output tile (4 waves x 32)
@@ -50,6 +53,9 @@ constexpr int kTileBytes = kBKV * kRowBytes;   // 16 KiB
 constexpr int kStage = 2 * kTileBytes;     // K + V
 constexpr int kLds = 2 * kStage;           // two stages: 64 KiB
 constexpr int kThreads = 256;
+// a query's running maximum is raised (and its sums rescaled) only when a block's maximum
+// exceeds it by more than this many powers of two; until then probabilities stay <= 2^8
+constexpr float kRescaleSlack = 8.f;
 
 __device__ __forceinline__ int k_swz(int r) { return r & 15; }
 __device__ __forceinline__ int v_swz(int r) { return 4 * (r & 3); }
@@ -68,8 +74,31 @@ struct Args {
 
 __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
+// The two halves of a wave hold the two key halves of the same 32 queries: lanes l and
+// l + 32 combine through one half swap (v_permlane32_swap: a's upper half <-> b's lower half),
+// after which one result holds every lane's lower-half value and the other its upper-half
+// value. The two results are reinterpreted as floats through one two-element vector: a bit
+// cast of each result on its own was compiled to read the first result twice.
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ f32x2_t both_halves(float x) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const u32x2_t t = {r[0], r[1]};
+  return __builtin_bit_cast(f32x2_t, t);
+}
+__device__ __forceinline__ float max_halves(float x) {
+  const f32x2_t h = both_halves(x);
+  return fmaxf(h.x, h.y);
+}
+__device__ __forceinline__ float add_halves(float x) {
+  const f32x2_t h = both_halves(x);
+  return h.x + h.y;
+}
+
 __global__ __launch_bounds__(kThreads, 2) void attn_kernel(Args a) {
-  __shared__ __attribute__((aligned(16))) char lds[kLds];
+  __shared__ __attribute__((aligned(16))) char lds_raw[kLds];
+  lds_char* const lds = (lds_char*)lds_raw;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -86,13 +115,25 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(Args a) {
     ko[i] = static_cast<uint32_t>(r * kRowBytes + (((lane & 15) ^ k_swz(r)) << 4));
     vo[i] = static_cast<uint32_t>(r * kRowBytes + (((lane & 15) ^ v_swz(r)) << 4));
   }
-  // transposing reads of the value columns: this lane's source address inside a V tile for
-  // key step s (16 keys), column block db (32 columns) and half (keys +0 or +4)
-  const int grp = lane >> 4, j16 = lane & 15;
-  const int tr_d = 16 * (grp & 1) + 4 * (j16 & 3);      // column within the 32-column block
-  const int tr_k = 8 * (grp >> 1) + (j16 >> 2);          // key within the 16-key step
-  // fragment reads of the K tile: row 32 blk + lane % 32, logical piece 2 kk + up
+  // K fragment reads: row 32 b + lane % 32, logical piece 2 kk + up, at piece ^ (row & 15)
+  // (the row's low bits do not depend on b, so b is an immediate offset)
   const int krow = lane & 31;
+  uint32_t kofs[8];
+#pragma unroll
+  for (int kk = 0; kk < 8; ++kk)
+    kofs[kk] = static_cast<uint32_t>(krow * kRowBytes + (((2 * kk + up) ^ k_swz(krow)) << 4));
+  // transposing reads of the value columns: for key step s (16 keys), column block db (32
+  // columns) and half hf (keys +0 / +4) this lane addresses row 16 s + tr_k + 4 hf, columns
+  // 32 db + tr_d .. + 3; the row's low two bits (the swizzle) do not depend on s or hf
+  const int grp = lane >> 4, j16 = lane & 15;
+  const int tr_d = 16 * (grp & 1) + 4 * (j16 & 3);
+  const int tr_k = 8 * (grp >> 1) + (j16 >> 2);
+  uint32_t vofs[4];
+#pragma unroll
+  for (int db = 0; db < 4; ++db) {
+    const int phys_piece = (4 * db + (tr_d >> 3)) ^ v_swz(tr_k);
+    vofs[db] = static_cast<uint32_t>(tr_k * kRowBytes + (phys_piece << 4) + ((tr_d >> 2) & 1) * 8);
+  }
 
   for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
     const int h = t / qtiles, qt = t - h * qtiles;
@@ -106,7 +147,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(Args a) {
     for (int kk = 0; kk < 8; ++kk)
       qf[kk] = *reinterpret_cast<const bf16x8*>(a.q + hoff + static_cast<int64_t>(qrow) * kD + 16 * kk + 8 * up);
     auto issue = [&](int j) {
-      char* st = lds + (j & 1) * kStage;
+      lds_char* st = lds + (j & 1) * kStage;
       const char* kb = kh + static_cast<int64_t>(j) * kTileBytes;
       const char* vb = vh + static_cast<int64_t>(j) * kTileBytes;
 #pragma unroll
@@ -127,59 +168,62 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(Args a) {
     __syncthreads();
     if (nkv > 1) issue(1);
     for (int j = 0; j < nkv; ++j) {
-      const char* ks = lds + (j & 1) * kStage;
-      const char* vs = ks + kTileBytes;
+      lds_char* const ks = lds + (j & 1) * kStage;
+      lds_char* const vs = ks + kTileBytes;
       // S' = K Q^T over two 32-key blocks
       f32x16 sacc[2];
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) sacc[b][e] = 0.f;
-        const int r = 32 * b + krow;
 #pragma unroll
         for (int kk = 0; kk < 8; ++kk) {
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks + r * kRowBytes + (((2 * kk + up) ^ k_swz(r)) << 4));
+          const bf16x8 kf = *(const lds_bf16x8*)(ks + b * 32 * kRowBytes + kofs[kk]);
           sacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], sacc[b], 0, 0, 0);
         }
       }
       // online softmax in base 2 for query lane % 32
-      float mx = -INFINITY;
+      float mx = fmaxf(sacc[0][0], sacc[0][1]);
 #pragma unroll
       for (int b = 0; b < 2; ++b)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[b][e]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m, mx * a.scale_log2e);
-      const float corr = __builtin_amdgcn_exp2f(m - m_new);
-      float rs = 0.f;
+        for (int e = (b ? 0 : 2); e < 16; ++e) mx = fmaxf(mx, sacc[b][e]);
+      const float mxs = max_halves(mx) * a.scale_log2e;
+      if (__builtin_amdgcn_ballot_w64(mxs > m + kRescaleSlack)) {    // wave-uniform
+        const float m_new = fmaxf(m, mxs);
+        const float corr = __builtin_amdgcn_exp2f(m - m_new);
+        l *= corr;
+#pragma unroll
+        for (int db = 0; db < 4; ++db)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) oacc[db][e] *= corr;
+        m = m_new;
+      }
+      // probabilities, packed to bf16; the row sum adds the packed values themselves, so the
+      // normaliser is the sum of exactly the weights the second product uses
       uint32_t pk[2][8];
+      float rs = 0.f;
+      const bf16x2_v ones = __builtin_bit_cast(bf16x2_v, 0x3F803F80u);
 #pragma unroll
       for (int b = 0; b < 2; ++b)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float p0 = __builtin_amdgcn_exp2f(sacc[b][2 * e] * a.scale_log2e - m_new);
-          const float p1 = __builtin_amdgcn_exp2f(sacc[b][2 * e + 1] * a.scale_log2e - m_new);
-          rs += p0 + p1;
+          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[b][2 * e], a.scale_log2e, -m));
+          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[b][2 * e + 1], a.scale_log2e, -m));
           pk[b][e] = pack_bf16x2(p0, p1);
+          rs = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_v, pk[b][e]), ones, rs, false);
         }
-      rs += __shfl_xor(rs, 32);
-      l = l * corr + rs;
-      m = m_new;
-#pragma unroll
-      for (int db = 0; db < 4; ++db)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) oacc[db][e] *= corr;
-      // P^T fragments: key step s covers keys 16 s .. 16 s + 15; the lower half needs keys
-      // +0..7 of the step, the upper +8..15 (register pairs 2 (s & 1) .. of block s / 2)
+      l += add_halves(rs);
+      // P^T fragments: key step s covers keys 16 s .. 16 s + 15 of block s / 2; the lower
+      // half needs keys +0..7 (its own pairs o, o + 1 and the upper half's), the upper half
+      // keys +8..15 (the lower half's pairs o + 2, o + 3 and its own): two half swaps
       bf16x8 pf[4];
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
         const int b = s >> 1, o = 4 * (s & 1);
-        const uint32_t send0 = up ? pk[b][o] : pk[b][o + 2];
-        const uint32_t send1 = up ? pk[b][o + 1] : pk[b][o + 3];
-        const uint32_t r0 = __shfl_xor(send0, 32), r1 = __shfl_xor(send1, 32);
-        const u32x4 pv = up ? u32x4{r0, r1, pk[b][o + 2], pk[b][o + 3]}
-                            : u32x4{pk[b][o], pk[b][o + 1], r0, r1};
+        const auto x = __builtin_amdgcn_permlane32_swap(pk[b][o], pk[b][o + 2], false, false);
+        const auto y = __builtin_amdgcn_permlane32_swap(pk[b][o + 1], pk[b][o + 3], false, false);
+        const u32x4 pv = {x[0], y[0], x[1], y[1]};
         pf[s] = __builtin_bit_cast(bf16x8, pv);
       }
       // O' += V^T P^T
@@ -187,16 +231,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(Args a) {
       for (int s = 0; s < 4; ++s)
 #pragma unroll
         for (int db = 0; db < 4; ++db) {
-          s16x4 rd[2];
-#pragma unroll
-          for (int hf = 0; hf < 2; ++hf) {
-            const int r = 16 * s + tr_k + 4 * hf;
-            const int col = 32 * db + tr_d;
-            const int piece = col >> 3, half = (col >> 2) & 1;
-            const char* p = vs + r * kRowBytes + ((piece ^ v_swz(r)) << 4) + half * 8;
-            rd[hf] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
-          }
-          const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(rd[0], rd[1], 0, 1, 2, 3, 4, 5, 6, 7));
+          const s16x4 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vs + (16 * s) * kRowBytes + vofs[db]));
+          const s16x4 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vs + (16 * s + 4) * kRowBytes + vofs[db]));
+          const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(r0, r1, 0, 1, 2, 3, 4, 5, 6, 7));
           oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[s], oacc[db], 0, 0, 0);
         }
       if (j + 1 < nkv) {
