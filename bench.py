@@ -394,6 +394,18 @@ def main():
         rep = attn_a2a.run()
         res["attention_a2a"] = {"workload": rep["workload"], "grid": rep["grid"], "summary": rep["summary"],
                                 "cells": rep["cells"]}
+        from paper_2607_23264_amd.profiling import ATTN_KERNEL_SOURCES, sources_hash
+        ref = next((c for c in rep["cells"] if c["sink"] == "hbm" and c["M"] == 16384), None)
+        if ref is not None:
+            atr = read_traffic(os.path.join(HERE, "profiles", "attn_kernel_M16384_h8_d128_traffic.md"),
+                               sources_hash(ATTN_KERNEL_SOURCES))
+            res["attention_a2a"]["roofline"] = {
+                "bound": "mfma", "kernel": "attn_kernel (FA-only launch, M=16384, 8 heads, d=128)",
+                "achieved": ref["fa_TFLOPs"], "peak": MFMA_PEAK_BF16 / 1e12, "unit": "TFLOP/s",
+                "frac": ref["fa_TFLOPs"] * 1e12 / MFMA_PEAK_BF16,
+                "traffic": atr["traffic_bytes"] if atr else None,
+                "flops_per_launch": 4.0 * 8 * 16384 ** 2 * 128,
+                "algorithmic_bytes_per_launch": 4.0 * 8 * 16384 * 128 * 2}
         torch.cuda.empty_cache()
     if a.slow_sink:
         log("[bench] slow sink (host-coherent combine windows)")

@@ -23,18 +23,22 @@ import re
 import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-# sources that define the fused expert-FFN kernel's code (a change to any of them makes a
-# stored traffic measurement stale)
-FFN_KERNEL_SOURCES = ("csrc/xs_ep_ffn.hip", "csrc/xs_gemm.hpp", "csrc/xs_common.hpp", "build.py")
-ATTN_KERNEL_SOURCES = ("csrc/xs_attn.hip", "csrc/xs_common.hpp", "build.py")
+# sources that define a kernel's code; they and the compiler flags key a stored traffic
+# measurement (a change to either makes it stale)
+FFN_KERNEL_SOURCES = ("csrc/xs_ep_ffn.hip", "csrc/xs_gemm.hpp", "csrc/xs_common.hpp")
+ATTN_KERNEL_SOURCES = ("csrc/xs_attn.hip", "csrc/xs_common.hpp")
 KERNEL_SOURCES = {"ffn": FFN_KERNEL_SOURCES, "attn": ATTN_KERNEL_SOURCES}
 
 
 def sources_hash(paths=FFN_KERNEL_SOURCES) -> str:
+    if os.path.dirname(HERE) not in sys.path:        # also when run as a script
+        sys.path.insert(0, os.path.dirname(HERE))
+    from paper_2607_23264_amd.build import FLAGS, HIPCC
     h = hashlib.sha256()
     for p in paths:
         with open(os.path.join(HERE, p), "rb") as f:
             h.update(f.read())
+    h.update(" ".join([os.path.basename(HIPCC)] + FLAGS).encode())
     return h.hexdigest()[:16]
 
 
