@@ -9,7 +9,9 @@ code 255 is NaN); the elements are
     (1 + m/8) 2^(E - 7) for E = 1..15 except E = 15, m = 7 (NaN); subnormals (m/8) 2^-6;
     largest finite 448, no infinities;
   * E2M1: 1 sign, 2 exponent bits (bias 1), 1 mantissa bit: 0, 0.5, 1, 1.5, 2, 3, 4, 6.
-Encoding is round to nearest, ties to the even code (the code whose mantissa ends in 0).
+Encoding is round to nearest, ties to the even code (the code whose mantissa ends in 0), and
+keeps the sign, also when the magnitude rounds to zero (-0 = the sign bit alone), as an IEEE
+round-to-nearest-even conversion does.
 Shared exponent (reading): the smallest integer e with amax <= fmax 2^e (fmax = 448 or 6), so
 no element of the block saturates; e is clamped to [-127, 127], and an all-zero block takes
 e = 0. With amax = M 2^E (1 <= M < 2) and fmax = Mf 2^Ef this is e = E - Ef + [M > Mf], an
@@ -68,8 +70,9 @@ def decode(codes, fmt):
 
 
 def encode(v, fmt):
-    """fp64 -> codes, round to nearest with ties to the even code. |v| above the largest
-    finite value saturates to it (the quantizer below never produces such values)."""
+    """fp64 -> codes, round to nearest with ties to the even code, sign kept (also for -0).
+    |v| above the largest finite value saturates to it (the quantizer below never produces
+    such values)."""
     v = np.asarray(v, dtype=np.float64)
     t = _TABLES[fmt]
     a = np.minimum(np.abs(v), t[-1])
@@ -79,8 +82,7 @@ def encode(v, fmt):
     pick_hi = (dhi < dlo) | ((dhi == dlo) & (hi % 2 == 0) & (hi != lo))
     mag = np.where(pick_hi, hi, lo)
     mag = np.where(a == t[hi], hi, mag)
-    neg = np.signbit(v) & (mag != 0)
-    return (mag | np.where(neg, _SIGN[fmt], 0)).astype(np.uint8)
+    return (mag | np.where(np.signbit(v), _SIGN[fmt], 0)).astype(np.uint8)
 
 
 def shared_exponent(amax, fmt):

@@ -27,9 +27,7 @@ def test_e4m3_encode_matches_torch_rne():
                         mids, -mids, t, -t, [0.0, -0.0, 2.0 ** -10, 3 * 2.0 ** -10]])
     ref = torch.from_numpy(v.astype(np.float32)).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
     ours = mx.encode(v.astype(np.float32).astype(np.float64), mx.E4M3)
-    # torch keeps the sign of -0 (0x80); the oracle writes +0 for a zero magnitude
-    ref = np.where((ref & 0x7F) == 0, 0, ref)
-    assert np.array_equal(ours, ref)
+    assert np.array_equal(ours, ref)                  # including -0 (0x80) for negative underflow
 
 
 def test_e2m1_table_and_ties_by_hand():
@@ -40,6 +38,8 @@ def test_e2m1_table_and_ties_by_hand():
     for v, want in cases:
         got = mx.decode(mx.encode(np.array([v]), mx.E2M1), mx.E2M1)[0]
         assert got == want, (v, got, want)
+    # the sign survives a zero result: -0.25 -> code 0x8 (-0)
+    assert mx.encode(np.array([-0.25, -0.0, 0.0]), mx.E2M1).tolist() == [8, 8, 0]
 
 
 @pytest.mark.parametrize("fmt,fmax", [(mx.E4M3, 448.0), (mx.E2M1, 6.0)])
