@@ -351,6 +351,36 @@ int xs_attention(const xs_attn* a, int32_t mode, const xs_trace* trace, void* st
 int xs_ulysses_copy(const void* o, int32_t heads, int32_t M, int32_t head_dim,
                     const xs_window* win, int32_t W, void* stream);
 
+/* ----------------------------------------------------------------------------- MX formats
+ * Quantized EP precisions (W8A8, W4A8: Sec. 5.2, the MegaMoE sweep; the paper does not fix the
+ * formats). Reading: OCP microscaling as the gfx950 matrix cores take it. A block of 32
+ * consecutive elements along the reduction axis shares one E8M0 scale 2^(s - 127); elements
+ * are E4M3 (OCP "FN": bias 7, largest 448, no infinities) or E2M1 (0, 0.5, 1, 1.5, 2, 3, 4, 6
+ * and negatives). Quantization: e = the smallest integer with amax <= fmax 2^e (fmax 448 or
+ * 6; e = 0 for an all-zero block; clamped to [-127, 127]), decided on the exponent and
+ * mantissa bits of the block's largest magnitude; codes = round-to-nearest-even of
+ * x / 2^e (never saturates). E2M1 codes pack two per byte, element 2 i in the low nibble. */
+enum { XS_FMT_E4M3 = 0, XS_FMT_E2M1 = 1 };
+
+/* Block quantizer: x bf16 [rows][cols] (ldx elements per row, 16-byte aligned rows) ->
+ * codes [rows][cols] bytes (E4M3; ld_codes a multiple of 8) or [rows][cols / 2] (E2M1;
+ * ld_codes a multiple of 4), scales [rows][cols / 32] bytes (ld_scales bytes per row).
+ * cols is a multiple of 32. Device pointers, caller-owned; stream-ordered. XS_EINVAL on bad
+ * arguments (nothing launched), XS_EHIP if the launch fails. */
+int xs_quantize_mx(const void* x, int64_t rows, int32_t cols, int64_t ldx, int32_t fmt,
+                   void* codes, int64_t ld_codes, void* scales, int64_t ld_scales, void* stream);
+
+/* MX GEMM: c (bf16 [M][N], ldc elements) = deq(a) deq(b)^T with a E4M3 codes [M][K] (lda
+ * bytes per row) and scales [M][K / 32] (lda_s bytes per row), b codes [N][K] in b_fmt
+ * (ldb bytes per row) and scales [N][K / 32] (ldb_s). fp32 accumulation on
+ * v_mfma_scale_f32_32x32x64_f8f6f4, one bf16 rounding at the end. N a multiple of 256, K of
+ * 128; code rows 16-byte aligned, scale rows 4-byte aligned. b_fmt XS_FMT_E2M1 is not yet
+ * supported (XS_EUNSUPPORTED). XS_EINVAL / XS_EUNSUPPORTED on bad arguments (nothing
+ * launched), XS_EHIP if the launch fails. */
+int xs_gemm_mx(const void* a, int64_t lda, const void* a_scales, int64_t lda_s, const void* b,
+               int64_t ldb, const void* b_scales, int64_t ldb_s, int32_t b_fmt, void* c,
+               int64_t ldc, int32_t M, int32_t N, int32_t K, const xs_trace* trace, void* stream);
+
 /* ----------------------------------------------------------------------------- X-Stage
  * Burst-Gap model (Sec. 3.3-3.5). Units: bytes and microseconds.
  *   T0(V) = t0_a_us + t0_b_us_per_byte * V   recovered issue floor at K producers

@@ -1,0 +1,252 @@
+// MXFP8 GEMM core for gfx950: E4M3 operands with one E8M0 scale per 32 elements along K, on
+// v_mfma_scale_f32_32x32x64_f8f6f4. 256 x 256 output tile, 256 threads = 4 waves, one per
+// SIMD, as 2 (M) x 2 (N) waves of 128 x 128 each = 4 x 4 blocks of 32 x 32 (256 fp32
+// accumulators per lane). An fp8 fragment is twice a bf16 one, so the bf16 core's two waves
+// per SIMD (128 x 64 each) cannot hold double-buffered fragments and the block scales within
+// their 256 registers; one wave per SIMD has 512, and a 128 x 128 wave reads half the LDS
+// bytes per MFMA.
+//
+// LDS: two stages, each with an A and a B operand tile of 256 rows x 128 bytes (here 128 K
+// elements; logical piece c of row r at c ^ ((r >> 1) & 7), as in the bf16 core) and the
+// 256 + 256 rows' scale words of the stage (one 32-bit word per row: its four 32-element
+// blocks), 132 KiB in all. Everything arrives by direct global -> LDS loads, the swizzle
+// applied on the global side (instruction i of wave w fills operand rows 32 i + 8 w .. + 7;
+// one dword load per lane fills the scale words of rows 64 w + lane). A stage is 32 MFMAs of
+// 64 cycles per wave (one wave per SIMD), so loading it one stage ahead gives the loads about
+// as long to land as the bf16 core's three-deep weight pipeline does.
+//
+// Operand layout of the scaled MFMA (measured on gfx950): lane 32 h + i holds row i's K
+// elements [16 h, 16 h + 16) in bytes 0..15 and [32 + 16 h, 48 + 16 h) in bytes 16..31 of its
+// eight dwords, and the scale of K block b (32 elements) of row i comes from lane 32 b + i, in
+// the byte op_sel names. Sub-step kk of a stage (K elements [64 kk, 64 kk + 64)) reads pieces
+// 4 kk + h and 4 kk + 2 + h of the row; a lane's scale word for the stage holds the row's four
+// block scales, and one byte permute puts the scale of block 2 kk + h into byte kk.
+#pragma once
+#include "xs_gemm.hpp"
+
+namespace xs {
+
+constexpr int kMxThreads = 256;
+constexpr int kMxStage = 2 * kOpBytes + 2048;    // A tile, B tile, A and B scale words: 66 KiB
+constexpr int kMxScaleOff = 2 * kOpBytes;
+constexpr int kMxLds = 2 * kMxStage;             // 132 KiB
+static_assert(kMxLds <= kLdsBytes, "the MX stages fit the LDS the kernels declare");
+typedef int v8i_t __attribute__((ext_vector_type(8)));
+typedef int v4i_t __attribute__((ext_vector_type(4)));
+typedef f32x16 AccMx[4][4];
+
+struct MxTile {
+  const char* a;          // A code base (tile row 0, k 0)
+  const char* b;          // B code base
+  const char* sa;         // A scale base (tile row 0)
+  const char* sb;         // B scale base
+  uint32_t oa[8], ob[8];  // per-lane byte offsets of the eight direct loads of each operand
+  uint32_t sao, sbo;      // per-lane byte offsets of the scale rows this lane loads
+  int arow, brow;         // LDS byte offsets of this lane's fragment rows
+  int w;
+};
+
+template <int NI>
+__device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& acc, char* lds) {
+  const int lane = threadIdx.x & 63;
+  const int w = t.w;
+  const int swz = (lane >> 1) & 7;
+  const int h = lane >> 5;
+  const uint32_t sel = h ? 0x0C0C0301u : 0x0C0C0200u;
+  // Addresses are the uniform base plus a 32-bit per-lane offset that includes the stage
+  // (a 32-bit sum that may wrap is not folded into loop-invariant 64-bit per-lane pointers,
+  // which would cost two registers per load): the loads keep the scalar-base + vector-offset
+  // form.
+  auto issue = [&](int kt) {
+    char* st = lds + (kt & 1) * kMxStage;
+    const uint32_t k0 = static_cast<uint32_t>(kt) * 128u, k4 = static_cast<uint32_t>(kt) * 4u;
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      __builtin_amdgcn_global_load_lds((glob_void*)(t.a + (t.oa[i] + k0)), (lds_void*)(st + (4 * i + w) * 1024),
+                                       16, 0, 0);
+    __builtin_amdgcn_global_load_lds((glob_void*)(t.sa + (t.sao + k4)), (lds_void*)(st + kMxScaleOff + w * 256),
+                                     4, 0, 0);
+    __builtin_amdgcn_global_load_lds((glob_void*)(t.sb + (t.sbo + k4)),
+                                     (lds_void*)(st + kMxScaleOff + 1024 + w * 256), 4, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      __builtin_amdgcn_global_load_lds((glob_void*)(t.b + (t.ob[i] + k0)),
+                                       (lds_void*)(st + kOpBytes + (4 * i + w) * 1024), 16, 0, 0);
+  };
+  uint32_t sw[8];         // this stage's scale words: A blocks 0..3, B blocks 0..3
+  auto read_s = [&](const char* st) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      sw[i] = *reinterpret_cast<const uint32_t*>(st + kMxScaleOff + (t.arow >> 7) * 4 + i * 128);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      sw[4 + j] = *reinterpret_cast<const uint32_t*>(st + kMxScaleOff + 1024 + (t.brow >> 7) * 4 + j * 128);
+  };
+  // A fragments double-buffered (by sub-step), B fragments single-buffered: a sub-step's B
+  // fragments are read again right after its last MFMA has issued
+  v8i_t af[2][4], bfr[4];
+  auto frag = [&](const char* base, int row_off, int kk) {
+    const v4i_t lo = *reinterpret_cast<const v4i_t*>(base + row_off + (((4 * kk + h) ^ swz) << 4));
+    const v4i_t hi = *reinterpret_cast<const v4i_t*>(base + row_off + (((4 * kk + 2 + h) ^ swz) << 4));
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  };
+  auto read_a = [&](const char* st, int kk, int buf) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) af[buf][i] = frag(st, t.arow + i * 32 * 128, kk);
+  };
+  auto read_b = [&](const char* st, int kk) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bfr[j] = frag(st + kOpBytes, t.brow + j * 32 * 128, kk);
+  };
+  // B fragment first: each lane's accumulators hold four consecutive output columns
+  auto mma = [&](int buf, int kk) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int sa = static_cast<int>(__builtin_amdgcn_perm(sw[i], sw[i], sel));
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int sb = static_cast<int>(__builtin_amdgcn_perm(sw[4 + j], sw[4 + j], sel));
+        if (kk == 0)
+          acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bfr[j], af[buf][i], acc[i][j],
+                                                                      0, 0, 0, sb, 0, sa);
+        else
+          acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bfr[j], af[buf][i], acc[i][j],
+                                                                      0, 0, 1, sb, 1, sa);
+      }
+    }
+  };
+  // prologue: stage 0 resident, stage 1 in flight
+  issue(0);
+  wait_vm0();
+  __builtin_amdgcn_s_barrier();
+  if (nk > 1) issue(1);
+  if (NI > 0) {
+    read_s(lds);
+    read_b(lds, 0);
+    read_a(lds, 0, 0);
+  }
+  for (int kt = 0; kt < nk; ++kt) {
+    const char* st = lds + (kt & 1) * kMxStage;
+    if (NI > 0) {
+      // sub-step 0 with sub-step 1's A fragments read in between, then its B fragments
+      read_a(st, 1, 1);
+      mma(0, 0);
+#pragma unroll
+      for (int g = 0; g < NI; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // two MFMAs
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // one A fragment
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2 * NI, 0);
+      read_b(st, 1);
+      mma(1, 1);   // sub-step 1
+    }
+    if (kt + 1 < nk) {
+      // this wave's loads of stage kt + 1 have landed (nothing newer is in flight) ...
+      wait_vm0();
+      // ... and every wave's, and stage kt is no longer read (its last fragments and scale
+      // words are in registers)
+      __builtin_amdgcn_s_barrier();
+      const char* nx = lds + ((kt + 1) & 1) * kMxStage;
+      if (NI > 0) {
+        read_s(nx);
+        read_b(nx, 0);
+        read_a(nx, 0, 0);
+      }
+      if (kt + 2 < nk) issue(kt + 2);   // into stage kt's buffers
+    }
+  }
+}
+
+// acc = deq(A)[0:256, 0:K] deq(B)[rows(0:256), 0:K]^T. A / B: E4M3 code rows (lda / ldb bytes
+// apart, 16-byte aligned), As / Bs: E8M0 scale rows ([K / 32] bytes, lda_s / ldb_s apart,
+// 4-byte aligned). K a multiple of 128. B rows map through b_row_map (SwiGLU interleave).
+// Rows of A at or beyond a_rows read row a_rows - 1; a wave skips the MFMAs of 32-row blocks
+// past a_rows. Ends with a block barrier. Accumulator acc[i][j][q] is output
+//   row wm*128 + 32 i + lane % 32, column wn*128 + 32 j + 8 (q / 4) + 4 (lane / 32) + q % 4.
+__device__ __forceinline__ void gemm_mainloop_mx(const uint8_t* __restrict__ A, int64_t lda,
+                                                 const uint8_t* __restrict__ As, int64_t lda_s,
+                                                 int a_rows, const uint8_t* __restrict__ B,
+                                                 int64_t ldb, const uint8_t* __restrict__ Bs,
+                                                 int64_t ldb_s, int b_n0, int b_half, bool swiglu,
+                                                 int K, AccMx& acc, char* lds) {
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = w >> 1, wn = w & 1;
+  MxTile t;
+  t.a = reinterpret_cast<const char*>(A);
+  t.b = reinterpret_cast<const char*>(B);
+  t.sa = reinterpret_cast<const char*>(As);
+  t.sb = reinterpret_cast<const char*>(Bs);
+  t.w = w;
+  const int lr = lane >> 3, lp = lane & 7;
+  const int c16 = (lp ^ ((4 * w + (lr >> 1)) & 7)) * 16;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int r = 32 * i + 8 * w + lr;
+    const int ar = r < a_rows ? r : a_rows - 1;
+    t.oa[i] = static_cast<uint32_t>(ar * lda + c16);
+    t.ob[i] = static_cast<uint32_t>(b_row_map(r, b_n0, b_half, swiglu) * ldb + c16);
+  }
+  const int rs = 64 * w + lane;            // the scale row this lane loads
+  t.sao = static_cast<uint32_t>((rs < a_rows ? rs : a_rows - 1) * lda_s);
+  t.sbo = static_cast<uint32_t>(b_row_map(rs, b_n0, b_half, swiglu) * ldb_s);
+  t.arow = (wm * 128 + (lane & 31)) * 128;
+  t.brow = (wn * 128 + (lane & 31)) * 128;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
+  const int nk = K / 128;
+  const int valid = a_rows - wm * 128;
+  const int ni = valid >= 128 ? 4 : (valid <= 0 ? 0 : (valid + 31) >> 5);
+  switch (__builtin_amdgcn_readfirstlane(ni)) {
+    case 4: mainloop_mx_ni<4>(t, nk, acc, lds); break;
+    case 3: mainloop_mx_ni<3>(t, nk, acc, lds); break;
+    case 2: mainloop_mx_ni<2>(t, nk, acc, lds); break;
+    case 1: mainloop_mx_ni<1>(t, nk, acc, lds); break;
+    default: mainloop_mx_ni<0>(t, nk, acc, lds); break;
+  }
+  __syncthreads();
+}
+
+// Accumulators -> bf16 tile in LDS, row-major [256][kEpiPitch].
+__device__ __forceinline__ void stage_tile_mx(const AccMx& acc, char* lds) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  const int row0 = wm * 128 + (lane & 31);
+  const int col0 = wn * 128 + 4 * (lane >> 5);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        uint2 v;
+        v.x = pack_bf16x2(acc[i][j][4 * g], acc[i][j][4 * g + 1]);
+        v.y = pack_bf16x2(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+        const int row = row0 + 32 * i, col = col0 + 32 * j + 8 * g;
+        *reinterpret_cast<uint2*>(lds + (row * kEpiPitch + col) * 2) = v;
+      }
+}
+
+// Stores staged rows [0, rows) through per-row destination pointers (null rows skipped):
+// pieces of 16 bytes, per_row pieces per row, pitch bytes between staged rows; NT threads.
+template <int NT>
+__device__ __forceinline__ void store_rows_n(const char* lds, int pitch, int per_row, int rows,
+                                             char* const* rowptr) {
+  typedef __attribute__((address_space(1))) u32x4 global_u32x4;
+  const int tid = threadIdx.x;
+  const int rows_per_pass = NT / per_row;
+  const int pc = tid % per_row;
+#pragma unroll 1
+  for (int r = tid / per_row; r < rows; r += rows_per_pass) {
+    char* p = rowptr[r];
+    if (!p) continue;
+    const u32x4 v = *reinterpret_cast<const u32x4*>(lds + r * pitch + pc * 16);
+    *(global_u32x4*)(p + pc * 16) = v;
+  }
+}
+
+}  // namespace xs

@@ -28,6 +28,7 @@ XS_CLAIM_STATIC, XS_CLAIM_DYNAMIC = 0, 1
 XS_SCATTER_ROW_BLOCK, XS_SCATTER_HEAD_GROUP = 0, 1
 XS_MB_PERIODIC, XS_MB_COMPLETION = 0, 1
 XS_ATTN_LOCAL, XS_ATTN_WINDOWS, XS_ATTN_WINDOWS_COUPLED = 0, 1, 2
+XS_FMT_E4M3, XS_FMT_E2M1 = 0, 1
 
 vp = C.c_void_p
 i32 = C.c_int32
@@ -127,6 +128,9 @@ xs_scatter_copy = _sig("xs_scatter_copy", C.c_int, vp, i64, i32, i32, P(xs_scatt
                        i32, vp)
 xs_attention = _sig("xs_attention", C.c_int, P(xs_attn), i32, P(xs_trace), vp)
 xs_ulysses_copy = _sig("xs_ulysses_copy", C.c_int, vp, i32, i32, i32, P(xs_window), i32, vp)
+xs_quantize_mx = _sig("xs_quantize_mx", C.c_int, vp, i64, i32, i64, i32, vp, i64, vp, i64, vp)
+xs_gemm_mx = _sig("xs_gemm_mx", C.c_int, vp, i64, vp, i64, vp, i64, vp, i64, i32, vp, i64, i32, i32, i32,
+                  P(xs_trace), vp)
 xs_model_predict = _sig("xs_model_predict", C.c_int, P(xs_model), P(xs_burst), i32, f64, P(xs_burst_pred))
 xs_model_fit = _sig("xs_model_fit", C.c_int, P(xs_calib), P(xs_model))
 xs_xstage_microbench = _sig("xs_xstage_microbench", C.c_int, P(xs_microbench_args), P(xs_trace), vp)
@@ -135,7 +139,8 @@ xs_clock_rate_hz = _sig("xs_clock_rate_hz", C.c_double)
 EXPORTED = ["xs_strerror", "xs_version", "xs_route_topk_softmax", "xs_dispatch_layout_workspace_bytes",
             "xs_dispatch_layout", "xs_dispatch", "xs_ep_layer_workspace_bytes", "xs_expert_ffn",
             "xs_combine_send", "xs_combine_reduce", "xs_fused_ep_layer", "xs_gemm", "xs_gemm_scatter",
-            "xs_scatter_copy", "xs_attention", "xs_ulysses_copy", "xs_model_predict", "xs_model_fit",
+            "xs_scatter_copy", "xs_attention", "xs_ulysses_copy", "xs_quantize_mx", "xs_gemm_mx",
+            "xs_model_predict", "xs_model_fit",
             "xs_xstage_microbench", "xs_clock_rate_hz"]
 
 

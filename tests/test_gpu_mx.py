@@ -1,0 +1,129 @@
+"""GPU parity of the MX (microscaled) quantizer and GEMM against the CPU oracle, through the C
+ABI: codes and scales bit-exact, the GEMM within the fp32-accumulation tolerance of the fp64
+product of the dequantized operands."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import mx
+from gpu_helpers import assert_close, dev_bits, host_bits, require_gpu, xs
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _bits_f64(b):
+    return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def _quantize(x_bits, fmt, pad_codes=0, pad_scales=0):
+    X = xs()
+    rows, cols = x_bits.shape
+    cb = cols if fmt == X.XS_FMT_E4M3 else cols // 2
+    ldc, lds = cb + pad_codes, cols // 32 + pad_scales
+    x = dev_bits(x_bits)
+    codes = torch.full((rows, ldc), 0x5A, dtype=torch.uint8, device="cuda")
+    scales = torch.full((rows, lds), 0xA5, dtype=torch.uint8, device="cuda")
+    X.check(X.xs_quantize_mx(x.data_ptr(), rows, cols, cols, fmt, codes.data_ptr(), ldc,
+                             scales.data_ptr(), lds, _stream()))
+    torch.cuda.synchronize()
+    return codes.cpu().numpy(), scales.cpu().numpy(), cb
+
+
+def _special_rows(cols):
+    """Rows that hit the exponent rule's edges and the encoder's ties."""
+    t = mx.fmt_values(mx.E4M3)
+    rows = [np.zeros(cols),                                    # all-zero blocks
+            np.full(cols, 448.0), np.full(cols, 449.0),        # amax exactly fmax / just above
+            np.tile((t[1:] + t[:-1])[:32] / 2, cols // 32),     # exact midpoints of E4M3
+            np.tile(np.r_[1.75, np.linspace(-1, 1, 31)], cols // 32),
+            np.tile(np.r_[2.0 ** -130, np.zeros(31)], cols // 32)]   # a bf16 subnormal maximum
+    return synth.to_bf16_bits(np.array(rows, dtype=np.float32))
+
+
+@pytest.mark.parametrize("fmt_name", ["E4M3", "E2M1"])
+@pytest.mark.parametrize("rows,cols", [(1, 32), (7, 96), (130, 7168), (257, 2048)])
+def test_quantize_bitexact(fmt_name, rows, cols):
+    X = xs()
+    fmt = getattr(X, f"XS_FMT_{fmt_name}")
+    ofmt = getattr(mx, fmt_name)
+    g = np.random.default_rng(rows + cols)
+    x = synth.to_bf16_bits((g.standard_normal((rows, cols)) * np.exp(g.uniform(-4, 4, (rows, 1)))).astype(np.float32))
+    if rows >= 6:
+        x[:6] = _special_rows(cols)
+    codes, scales, cb = _quantize(x, fmt, pad_codes=16, pad_scales=4)
+    ref_c, ref_s = mx.quantize_mx(_bits_f64(x), ofmt)
+    if ofmt == mx.E2M1:
+        ref_c = mx.pack_e2m1(ref_c)
+    assert np.array_equal(scales[:, :cols // 32], ref_s)
+    assert np.array_equal(codes[:, :cb], ref_c)
+    assert (codes[:, cb:] == 0x5A).all() and (scales[:, cols // 32:] == 0xA5).all()   # padding untouched
+
+
+def _gemm_mx(a_bits, b_bits):
+    """Quantize both operands on the GPU, multiply; returns (c bits, oracle fp64)."""
+    X = xs()
+    M, K = a_bits.shape
+    N = b_bits.shape[0]
+    ac, as_, _ = _quantize(a_bits, X.XS_FMT_E4M3)
+    bc, bs, _ = _quantize(b_bits, X.XS_FMT_E4M3)
+    da, das = torch.from_numpy(ac).cuda(), torch.from_numpy(as_).cuda()
+    db, dbs = torch.from_numpy(bc).cuda(), torch.from_numpy(bs).cuda()
+    c = torch.full((M, N), -1, dtype=torch.int16, device="cuda")
+    X.check(X.xs_gemm_mx(da.data_ptr(), K, das.data_ptr(), K // 32, db.data_ptr(), K, dbs.data_ptr(), K // 32,
+                         X.XS_FMT_E4M3, c.data_ptr(), N, M, N, K, None, _stream()))
+    torch.cuda.synchronize()
+    ref = mx.gemm_mx(ac, as_, mx.E4M3, bc, bs, mx.E4M3)
+    return host_bits(c), ref
+
+
+@pytest.mark.parametrize("M,N,K", [(256, 256, 128), (300, 512, 384), (1, 256, 256), (513, 768, 1024), (77, 256, 7168)])
+def test_gemm_mx_matches_oracle(M, N, K):
+    a = synth.normal_bf16(0, 20, (M, K))
+    b = synth.normal_bf16(0, 21, (N, K), std=0.05)
+    c, ref = _gemm_mx(a, b)
+    assert_close(c, ref, f"gemm_mx {M}x{N}x{K}")
+
+
+def test_gemm_mx_integer_operands_bitexact():
+    # small integers are exact in E4M3 with scale 2^0 when every block holds a value of 256..448
+    # (scale exponent 0) - here blocks are integers in [-8, 8] plus one 256: scale 2^0, exact
+    # codes, and |sums| < 2^24, so fp32 accumulation is exact in any order
+    g = np.random.default_rng(9)
+    M, N, K = 300, 256, 512
+    a = g.integers(-8, 9, (M, K)).astype(np.float32)
+    b = g.integers(-8, 9, (N, K)).astype(np.float32)
+    a[:, ::32] = 256.0
+    b[:, ::32] = 256.0
+    c, ref = _gemm_mx(synth.to_bf16_bits(a), synth.to_bf16_bits(b))
+    from oracle.ep import f64_to_bf16_bits
+    assert np.array_equal(c, f64_to_bf16_bits(a.astype(np.float64) @ b.astype(np.float64).T))
+    assert np.array_equal(c, f64_to_bf16_bits(ref))
+
+
+def test_mx_bad_arguments():
+    X = xs()
+    x = torch.zeros((4, 64), dtype=torch.int16, device="cuda")
+    c = torch.zeros((4, 64), dtype=torch.uint8, device="cuda")
+    s = torch.zeros((4, 2), dtype=torch.uint8, device="cuda")
+    assert X.xs_quantize_mx(x.data_ptr(), 4, 48, 64, X.XS_FMT_E4M3, c.data_ptr(), 64, s.data_ptr(), 2, _stream()) == X.XS_EINVAL
+    assert X.xs_quantize_mx(x.data_ptr(), 4, 64, 64, 7, c.data_ptr(), 64, s.data_ptr(), 2, _stream()) == X.XS_EINVAL
+    assert X.xs_quantize_mx(x.data_ptr(), 4, 64, 64, X.XS_FMT_E4M3, c.data_ptr(), 32, s.data_ptr(), 2, _stream()) == X.XS_EINVAL
+    a = torch.zeros((256, 256), dtype=torch.uint8, device="cuda")
+    sc = torch.zeros((256, 8), dtype=torch.uint8, device="cuda")
+    o = torch.zeros((256, 256), dtype=torch.int16, device="cuda")
+    args = lambda K, N, fmt: (a.data_ptr(), 256, sc.data_ptr(), 8, a.data_ptr(), 256, sc.data_ptr(), 8, fmt,
+                              o.data_ptr(), 256, 256, N, K, None, _stream())
+    assert X.xs_gemm_mx(*args(192, 256, X.XS_FMT_E4M3)) == X.XS_EUNSUPPORTED     # K % 128
+    assert X.xs_gemm_mx(*args(256, 200, X.XS_FMT_E4M3)) == X.XS_EUNSUPPORTED     # N % 256
+    assert X.xs_gemm_mx(*args(256, 256, 9)) == X.XS_EINVAL
+    torch.cuda.synchronize()
