@@ -18,6 +18,7 @@ Modules:
   xstage_model    Burst-Gap model (Eqs. 1-9), calibration fit, audit helpers
   schedule        tile orders: Expert-Wave, cross-wave interleave (Alg. 1), chunked
   attention       softmax attention and the post-attention Ulysses exchange
+  ep_mx           the EP layer with MXFP8 rows, weights and activations (W8A8)
   mx              microscaled formats (E4M3 / E2M1 elements, E8M0 block scales) of the
                   quantized EP path: encode, decode, block quantizer, dequantized GEMM
 
@@ -25,4 +26,4 @@ Parity status: every function here is pinned by tests under ``tests/`` against
 closed forms, worked numbers the paper prints, brute force or library routines,
 except where a function's docstring says "parity unpinned".
 """
-from . import attention, ep, mx, scatter, xstage_model, schedule  # noqa: F401
+from . import attention, ep, ep_mx, mx, scatter, xstage_model, schedule  # noqa: F401
