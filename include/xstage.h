@@ -119,6 +119,14 @@ int xs_dispatch(const void* x, int32_t T, int32_t H, const int32_t* topk_idx,
                 const int32_t* slot_row, int32_t k, int32_t E, const xs_window* win, int32_t W,
                 int32_t* dev_status, void* stream);
 
+/* The same one-sided row stores for rows of any byte length (a multiple of 16, rows
+ * row_stride bytes apart, 16-byte aligned): e.g. MXFP8 token rows of H codes then H / 32
+ * scales (xs_quantize_mx into caller staging, then this). Windows need row_stride_bytes >=
+ * row_bytes. Errors as xs_dispatch. */
+int xs_dispatch_rows(const void* rows, int64_t row_stride, int32_t row_bytes, int32_t T,
+                     const int32_t* topk_idx, const int32_t* slot_row, int32_t k, int32_t E,
+                     const xs_window* win, int32_t W, int32_t* dev_status, void* stream);
+
 /* ----------------------------------------------------------------------------- EP layer
  * One rank's share of an expert-parallel MoE layer (Sec. 4.3). Experts
  * [e_begin, e_begin + n_experts) are computed here; they must be whole windows
@@ -126,7 +134,22 @@ int xs_dispatch(const void* x, int32_t T, int32_t H, const int32_t* topk_idx,
  * tokens are dispatched and its output is reduced; routing and layout cover all n_src
  * sources (standing in for the count exchange between ranks).
  * Expert FFN (SwiGLU): h = bf16(silu(x Wg^T) * (x Wu^T)), y = bf16(h W2^T), fp32
- * accumulation; W1 rows [0, I) are the gate Wg and rows [I, 2I) the up projection Wu. */
+ * accumulation; W1 rows [0, I) are the gate Wg and rows [I, 2I) the up projection Wu.
+ * Precision (the paper's EP runs also at W8A8, Sec. 5.2):
+ *   XS_PREC_BF16   as above.
+ *   XS_PREC_MXFP8  MX formats (see "MX formats" below). Token rows are quantized once, in
+ *                  the dispatch phase, into workspace staging and dispatched as rows of H
+ *                  E4M3 codes followed by H / 32 E8M0 scales (dispatch window rows >= H +
+ *                  H / 32 bytes); w1 / w2 hold E4M3 codes ([n_experts][2I][H] and
+ *                  [n_experts][H][I] bytes) and w1_scale / w2_scale their scales
+ *                  ([n_experts][2I][H / 32], [n_experts][H][I / 32]); Linear-1 runs on the
+ *                  scaled MFMA, SwiGLU in fp32, and h is stored as MXFP8 rows of I codes and
+ *                  I / 32 scales (h_ws: [h_rows][I + I / 32] bytes); Linear-2 likewise, its
+ *                  output y rounded to bf16 for the unchanged combine. Requires H and I
+ *                  multiples of 512. Only xs_fused_ep_layer takes it (the unfused phase calls
+ *                  return XS_EUNSUPPORTED). */
+enum { XS_PREC_BF16 = 0, XS_PREC_MXFP8 = 1 };
+
 typedef struct xs_ep_layer {
   int32_t n_src, T, H, E, k, I, W;
   int32_t e_begin, n_experts;
@@ -154,6 +177,10 @@ typedef struct xs_ep_layer {
   void* out;                  /* device bf16 [T][H], combined output of source `src` */
   void* events[8];            /* optional hipEvent_t per phase boundary (NULL = not recorded),
                                  recorded on `stream`; see XS_EV_* */
+  int32_t precision;          /* XS_PREC_BF16 (0) or XS_PREC_MXFP8 */
+  int32_t reserved;           /* 0 */
+  const void* w1_scale;       /* XS_PREC_MXFP8: device E8M0 [n_experts][2I][H / 32] */
+  const void* w2_scale;       /* XS_PREC_MXFP8: device E8M0 [n_experts][H][I / 32] */
 } xs_ep_layer;
 
 /* Phase boundaries of the EP entry points: events[XS_EV_x] is recorded right before the

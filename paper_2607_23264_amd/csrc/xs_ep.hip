@@ -316,7 +316,8 @@ __global__ __launch_bounds__(256) void layout_finalize_kernel(
 // One wave per token (measured: a quarter row per wave, four waves per token, is slower).
 // Lanes hold up to 8 16-byte pieces of the row per round and store them into the k
 // destination rows.
-__global__ __launch_bounds__(256) void dispatch_kernel(const uint16_t* __restrict__ x, int T, int H,
+__global__ __launch_bounds__(256) void dispatch_kernel(const char* __restrict__ x, int64_t x_stride,
+                                                       int nch, int T,
                                                        const int* __restrict__ idx,
                                                        const int* __restrict__ slot_row, int k,
                                                        int E, WinSet win, int* status) {
@@ -337,8 +338,7 @@ __global__ __launch_bounds__(256) void dispatch_kernel(const uint16_t* __restric
       else my_dst = win.base[d] + static_cast<int64_t>(r) * win.stride[d];
     }
   }
-  const u32x4* src = reinterpret_cast<const u32x4*>(x + static_cast<int64_t>(t) * H);
-  const int nch = H >> 3;
+  const u32x4* src = reinterpret_cast<const u32x4*>(x + static_cast<int64_t>(t) * x_stride);
   for (int c0 = 0; c0 < nch; c0 += 64 * 8) {
     u32x4 v[8];
 #pragma unroll
@@ -534,14 +534,22 @@ int dispatch_layout(const int32_t* topk_idx, int32_t n_src, int32_t T, int32_t k
   return XS_OK;
 }
 
-int dispatch(const void* x, int32_t T, int32_t H, const int32_t* topk_idx, const int32_t* slot_row,
-             int32_t k, int32_t E, const WinSet& ws, int32_t* dev_status, hipStream_t st) {
+// Token rows of row_bytes bytes (a multiple of 16), x_stride apart, into the window rows of
+// their slots.
+int dispatch_rows(const void* x, int64_t x_stride, int32_t row_bytes, int32_t T,
+                  const int32_t* topk_idx, const int32_t* slot_row, int32_t k, int32_t E,
+                  const WinSet& ws, int32_t* dev_status, hipStream_t st) {
   if (T == 0) return signal_windows(ws, st);
-  hipLaunchKernelGGL(dispatch_kernel, dim3((T + 3) / 4), dim3(256), 0, st,
-                     static_cast<const uint16_t*>(x), T, H, topk_idx, slot_row, k, E, ws,
-                     dev_status);
+  hipLaunchKernelGGL(dispatch_kernel, dim3((T + 3) / 4), dim3(256), 0, st, static_cast<const char*>(x),
+                     x_stride, row_bytes / 16, T, topk_idx, slot_row, k, E, ws, dev_status);
   if (launch_status()) return XS_EHIP;
   return signal_windows(ws, st);
+}
+
+int dispatch(const void* x, int32_t T, int32_t H, const int32_t* topk_idx, const int32_t* slot_row,
+             int32_t k, int32_t E, const WinSet& ws, int32_t* dev_status, hipStream_t st) {
+  return dispatch_rows(x, static_cast<int64_t>(H) * 2, H * 2, T, topk_idx, slot_row, k, E, ws,
+                       dev_status, st);
 }
 
 int combine_reduce(const void* cbuf, int64_t cstride, const float* w, int32_t T, int32_t k,
@@ -577,6 +585,20 @@ extern "C" int xs_dispatch(const void* x, int32_t T, int32_t H, const int32_t* t
   if (rc) return rc;
   return xs_host::dispatch(x, T, H, topk_idx, slot_row, k, E, ws, dev_status,
                            static_cast<hipStream_t>(stream));
+}
+
+extern "C" int xs_dispatch_rows(const void* rows, int64_t row_stride, int32_t row_bytes, int32_t T,
+                                const int32_t* topk_idx, const int32_t* slot_row, int32_t k, int32_t E,
+                                const xs_window* win, int32_t W, int32_t* dev_status, void* stream) {
+  if (!rows || !topk_idx || !slot_row || T < 0 || row_bytes < 16 || k < 1 || k > 32 || k > E ||
+      E < 1 || W < 1 || E % W || row_stride < row_bytes)
+    return XS_EINVAL;
+  if (row_bytes % 16 || row_stride % 16 || (reinterpret_cast<uintptr_t>(rows) & 15)) return XS_EUNSUPPORTED;
+  WinSet ws;
+  int rc = xs_host::make_winset(win, W, row_bytes, &ws);
+  if (rc) return rc;
+  return xs_host::dispatch_rows(rows, row_stride, row_bytes, T, topk_idx, slot_row, k, E, ws, dev_status,
+                                static_cast<hipStream_t>(stream));
 }
 
 extern "C" int xs_combine_reduce(const void* cbuf, int64_t cbuf_stride_bytes, const float* topk_w,

@@ -24,7 +24,7 @@
 #include <algorithm>
 #include <cmath>
 
-#include "xs_gemm.hpp"
+#include "xs_gemm_mx.hpp"
 
 namespace xs {
 
@@ -45,6 +45,9 @@ struct EpArgs {
   const uint16_t* w2;
   uint16_t* h;
   uint16_t* y;
+  const uint8_t* w1s;          // MXFP8: weight scales (w1 / w2 then hold E4M3 codes)
+  const uint8_t* w2s;
+  int64_t h_stride;            // MXFP8: bytes per h row (I codes, then I / 32 scales)
   const int* meta;             // [0] rows P, [1] waves, [2] wave-list length, [3] computed rows
   const int* row_expert;
   const int* exp_m;
@@ -258,6 +261,123 @@ __device__ __forceinline__ int xcd_instance_ep(int b, int G) {
   return (G % 8) ? b : (b % 8) * (G / 8) + b / 8;
 }
 
+// MXFP8 tiles (256 threads, the MX core). Linear-1: the dispatch window rows hold H codes
+// then H / 32 scales; the SwiGLU output is quantized in the epilogue into h rows of I codes
+// then I / 32 scales (this tile's 128 columns: codes at 128 nt, scales at I + 4 nt).
+__device__ __forceinline__ void ep_l1_tile_mx(const EpArgs& a, int p, int nt, bool fused, char* lds,
+                                              char** rowptr) {
+  const int tid = threadIdx.x;
+  const int x = a.row_expert[p];
+  const int e = a.e_begin + x;
+  const int dl = e / a.epw - a.d_first;
+  const int m0 = (p - a.exp_rowfirst[x]) * kBM;
+  const int rows = min(kBM, a.exp_m[x] - m0);
+  const uint64_t t0 = a.tr.buf ? wall_ticks() : 0;
+  const int64_t ws = a.dwin.stride[dl];
+  const uint8_t* A = reinterpret_cast<const uint8_t*>(a.dwin.base[dl] +
+                                                      static_cast<int64_t>(a.expert_offsets[e] + m0) * ws);
+  const int64_t wrows = static_cast<int64_t>(x) * 2 * a.I;
+  const uint8_t* B = reinterpret_cast<const uint8_t*>(a.w1) + wrows * a.H;
+  const uint8_t* Bs = a.w1s + wrows * (a.H / 32);
+  AccMx acc;
+  gemm_mainloop_mx(A, ws, A + a.H, ws, rows, B, a.H, Bs, a.H / 32, nt * (kBN / 2), a.I, true, a.H, acc, lds);
+  const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
+  if (tid < rows)
+    rowptr[tid] = reinterpret_cast<char*>(a.h) + static_cast<int64_t>(a.exp_hrow[x] + m0 + tid) * a.h_stride;
+  stage_swiglu_mxq(acc, lds);
+  __syncthreads();
+  typedef __attribute__((address_space(1))) u32x4 global_u32x4;
+#pragma unroll 1
+  for (int i = tid; i < rows * 8; i += kMxThreads) {
+    const int r = i >> 3, pc = i & 7;
+    *(global_u32x4*)(rowptr[r] + nt * 128 + pc * 16) = *reinterpret_cast<const u32x4*>(lds + r * kHqPitch + pc * 16);
+  }
+  if (tid < rows)
+    *(__attribute__((address_space(1))) uint32_t*)(rowptr[tid] + a.I + nt * 4) =
+        *reinterpret_cast<const uint32_t*>(lds + kHqScaleOff + tid * 4);
+  if (fused) {
+    __syncthreads();
+    if (tid == 0 && p != a.withhold_row)
+      __hip_atomic_fetch_add(&a.l1_done[p], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  } else {
+    lds_barrier();
+  }
+  if (a.tr.buf && tid == 0) {
+    uint32_t i = atomicAdd(a.tr.count, 1u);
+    if (static_cast<int64_t>(i) < a.tr.capacity) {
+      uint64_t* r = a.tr.buf + static_cast<int64_t>(i) * 4;
+      r[0] = (1ull << 56) | (static_cast<uint64_t>(blockIdx.x) << 32) | static_cast<uint32_t>(p * a.P1 + nt);
+      r[1] = t0;
+      r[2] = t1;
+      r[3] = wall_ticks();
+    }
+  }
+}
+
+// Linear-2 on MXFP8 h rows; bf16 output rows into the combine windows as in the bf16 tile.
+__device__ __forceinline__ void ep_l2_tile_mx(const EpArgs& a, int p, int nt, bool fused, char* lds,
+                                              char** rowptr, int* flag) {
+  const int tid = threadIdx.x;
+  const uint64_t t0 = a.tr.buf ? wall_ticks() : 0;
+  if (fused && !ep_wait_row(a, p, flag)) return;
+  const int x = a.row_expert[p];
+  const int e = a.e_begin + x;
+  const int m0 = (p - a.exp_rowfirst[x]) * kBM;
+  const int rows = min(kBM, a.exp_m[x] - m0);
+  const uint8_t* A = reinterpret_cast<const uint8_t*>(a.h) + static_cast<int64_t>(a.exp_hrow[x] + m0) * a.h_stride;
+  const int64_t wrows = static_cast<int64_t>(x) * a.H;
+  const uint8_t* B = reinterpret_cast<const uint8_t*>(a.w2) + wrows * a.I;
+  const uint8_t* Bs = a.w2s + wrows * (a.I / 32);
+  const int n0 = nt * kBN;
+  int code = -1;
+  if (a.l2_combine && tid < rows)
+    code = a.row_src[static_cast<int64_t>(e / a.epw) * a.cap + a.expert_offsets[e] + m0 + tid];
+  AccMx acc;
+  gemm_mainloop_mx(A, a.h_stride, A + a.I, a.h_stride, rows, B, a.I, Bs, a.I / 32, n0, 0, false, a.I, acc, lds);
+  const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
+  if (tid < rows) {
+    char* ptr = nullptr;
+    const int src = code >> 24, slot = code & 0xffffff;
+    if (code >= 0 && src < a.n_src && slot < a.tk)
+      ptr = a.cwin.base[src] + static_cast<int64_t>(slot) * a.cwin.stride[src] + static_cast<int64_t>(n0) * 2;
+    else
+      set_status(a.status, XS_EBADINPUT);
+    rowptr[tid] = ptr;
+  }
+  stage_tile_mx(acc, lds);
+  __syncthreads();
+  store_rows_n<kMxThreads>(lds, kEpiPitch * 2, kBN * 2 / 16, rows, rowptr);
+  lds_barrier();
+  if (tid == 0) {
+    const uint64_t t2 = a.tr.buf ? wall_ticks() : 0;
+    if (a.tr.buf) {
+      uint32_t i = atomicAdd(a.tr.count, 1u);
+      if (static_cast<int64_t>(i) < a.tr.capacity) {
+        uint64_t* r = a.tr.buf + static_cast<int64_t>(i) * 4;
+        r[0] = (2ull << 56) | (static_cast<uint64_t>(blockIdx.x) << 32) | static_cast<uint32_t>(p * a.P2 + nt);
+        r[1] = t0;
+        r[2] = t1;
+        r[3] = t2;
+      }
+    }
+    spin_ticks(static_cast<uint64_t>(a.gap_ticks));
+  }
+  if (a.gap_ticks) __syncthreads();
+}
+
+// Tile dispatch by precision (PREC 0: bf16, 1: MXFP8).
+template <int PREC>
+__device__ __forceinline__ void l1_tile(const EpArgs& a, int p, int nt, bool fused, char* lds, char** rowptr) {
+  if constexpr (PREC == 1) ep_l1_tile_mx(a, p, nt, fused, lds, rowptr);
+  else ep_l1_tile(a, p, nt, fused, lds, rowptr);
+}
+template <int PREC>
+__device__ __forceinline__ void l2_tile(const EpArgs& a, int p, int nt, bool fused, char* lds, char** rowptr,
+                                        int* flag) {
+  if constexpr (PREC == 1) ep_l2_tile_mx(a, p, nt, fused, lds, rowptr, flag);
+  else ep_l2_tile(a, p, nt, fused, lds, rowptr, flag);
+}
+
 // Dynamic claiming. Thread 0 takes the next tile and broadcasts it through LDS:
 //   > 0: Linear-1 entry (value - 1), < -1: Linear-2 entry (-value - 2), -1: no work left.
 // Linear-2 entries are taken as tickets (one fetch_add, no retry loop): a producer holds at
@@ -302,7 +422,7 @@ __device__ __forceinline__ int ep_claim(const EpArgs& a, int n1, int n2, int& ru
   }
 }
 
-template <int MODE>
+template <int MODE, int PREC>
 __device__ __forceinline__ void ep_dynamic(const EpArgs& a, int n1, int n2, char* lds, char** rowptr,
                                            int* flag) {
   constexpr bool fused = MODE == 3;
@@ -322,10 +442,10 @@ __device__ __forceinline__ void ep_dynamic(const EpArgs& a, int n1, int n2, char
       const int r0 = a.wave_row[w], nl1 = (a.wave_row[w + 1] - r0) * a.P1;
       if (off < nl1) {
         const int k1 = r0 * a.P1 + off;
-        ep_l1_tile(a, k1 / a.P1, k1 % a.P1, true, lds, rowptr);
+        l1_tile<PREC>(a, k1 / a.P1, k1 % a.P1, true, lds, rowptr);
       } else {
         const int k2 = r0 * a.P2 + (off - nl1);
-        ep_l2_tile(a, k2 / a.P2, k2 % a.P2, true, lds, rowptr, flag);
+        l2_tile<PREC>(a, k2 / a.P2, k2 % a.P2, true, lds, rowptr, flag);
       }
     }
   }
@@ -337,19 +457,18 @@ __device__ __forceinline__ void ep_dynamic(const EpArgs& a, int n1, int n2, char
     if (t == -1) return;
     if (t > 0) {
       const int k1 = t - 1;
-      ep_l1_tile(a, k1 / a.P1, k1 % a.P1, fused, lds, rowptr);
+      l1_tile<PREC>(a, k1 / a.P1, k1 % a.P1, fused, lds, rowptr);
     } else {
       const int k2 = -t - 2;
-      ep_l2_tile(a, k2 / a.P2, k2 % a.P2, fused, lds, rowptr, flag);
+      l2_tile<PREC>(a, k2 / a.P2, k2 % a.P2, fused, lds, rowptr, flag);
     }
   }
 }
 
 // MODE 3: fused Linear-1 + Linear-2 (the EP layer); 1 / 2: one GEMM stream only (unfused
 // expert FFN). A template parameter so each variant is its own kernel in a trace.
-template <int MODE>
-__global__ __launch_bounds__(kThreads, 1) void ep_ffn_kernel(EpArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
+template <int MODE, int PREC>
+__device__ __forceinline__ void ep_ffn_body(const EpArgs& a, char* smem) {
   char* lds = smem;
   char** rowptr = reinterpret_cast<char**>(smem + kLdsRowPtrOff);
   int* flag = reinterpret_cast<int*>(smem + kLdsMiscOff);
@@ -368,16 +487,16 @@ __global__ __launch_bounds__(kThreads, 1) void ep_ffn_kernel(EpArgs a) {
       const int r0 = a.wave_row[w], nl1 = (a.wave_row[w + 1] - r0) * a.P1;
       if (off < nl1) {
         const int k1 = r0 * a.P1 + off;
-        ep_l1_tile(a, k1 / a.P1, k1 % a.P1, true, lds, rowptr);
+        l1_tile<PREC>(a, k1 / a.P1, k1 % a.P1, true, lds, rowptr);
       } else {
         const int k2 = r0 * a.P2 + (off - nl1);
-        ep_l2_tile(a, k2 / a.P2, k2 % a.P2, true, lds, rowptr, flag);
+        l2_tile<PREC>(a, k2 / a.P2, k2 % a.P2, true, lds, rowptr, flag);
       }
     }
     return;
   }
   if (a.claim == XS_CLAIM_DYNAMIC) {
-    ep_dynamic<MODE>(a, n1, n2, lds, rowptr, flag);
+    ep_dynamic<MODE, PREC>(a, n1, n2, lds, rowptr, flag);
     return;
   }
   const int D = a.lead, c = a.chunk;
@@ -388,15 +507,28 @@ __global__ __launch_bounds__(kThreads, 1) void ep_ffn_kernel(EpArgs a) {
     bool take2 = k2 < n2 && p2 + D <= p1;
     if (take2 && c > 0 && run >= c && k1 < n1) take2 = false;
     if (take2) {
-      ep_l2_tile(a, p2, k2 % a.P2, fused, lds, rowptr, flag);
+      l2_tile<PREC>(a, p2, k2 % a.P2, fused, lds, rowptr, flag);
       k2 += G;
       ++run;
     } else {
-      ep_l1_tile(a, p1, k1 % a.P1, fused, lds, rowptr);
+      l1_tile<PREC>(a, p1, k1 % a.P1, fused, lds, rowptr);
       k1 += G;
       run = 0;
     }
   }
+}
+
+template <int MODE>
+__global__ __launch_bounds__(kThreads, 1) void ep_ffn_kernel(EpArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
+  ep_ffn_body<MODE, 0>(a, smem);
+}
+
+// The same schedule with MXFP8 tiles on the four-wave MX core.
+template <int MODE>
+__global__ __launch_bounds__(kMxThreads, 1) void ep_ffn_mx_kernel(EpArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
+  ep_ffn_body<MODE, 1>(a, smem);
 }
 
 // Prefix of the rows each computed window holds (rows past capacity were never stored).
@@ -464,6 +596,8 @@ namespace xs_host {
 int dispatch_layout(const int32_t*, int32_t, int32_t, int32_t, int32_t, int32_t, int32_t, int32_t*,
                     int32_t*, int32_t*, int32_t*, int32_t*, int32_t*, void*, int64_t, int32_t*,
                     hipStream_t);
+int dispatch_rows(const void*, int64_t, int32_t, int32_t, const int32_t*, const int32_t*, int32_t,
+                  int32_t, const WinSet&, int32_t*, hipStream_t);
 int dispatch(const void*, int32_t, int32_t, const int32_t*, const int32_t*, int32_t, int32_t,
              const WinSet&, int32_t*, hipStream_t);
 int combine_reduce(const void*, int64_t, const float*, int32_t, int32_t, int32_t, void*,
@@ -480,9 +614,20 @@ int64_t align_up(int64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct EpWorkspace {
   int64_t layout_off, layout_bytes;
   int64_t meta_off, exp_off, rowexp_off, wave_pos_off, wave_row_off, l1_off;
+  int64_t xq_off;              // MXFP8: quantized token rows of this source [T][H + H / 32]
   int64_t total;
   int64_t max_rows;
 };
+
+bool is_mx(const xs_ep_layer* L) { return L->precision == XS_PREC_MXFP8; }
+
+// Bytes of one dispatched token row and of one h row.
+int64_t token_row_bytes(const xs_ep_layer* L) {
+  return is_mx(L) ? static_cast<int64_t>(L->H) + L->H / 32 : static_cast<int64_t>(L->H) * 2;
+}
+int64_t h_row_bytes(const xs_ep_layer* L) {
+  return is_mx(L) ? static_cast<int64_t>(L->I) + L->I / 32 : static_cast<int64_t>(L->I) * 2;
+}
 
 int n_cwin_of(const xs_ep_layer* L) { return L->n_experts / (L->E / L->W); }
 
@@ -506,6 +651,8 @@ EpWorkspace ep_workspace(const xs_ep_layer* L) {
   o += align_up((max_rows + 2) * 4);
   w.l1_off = o;
   o += align_up(max_rows * 4);
+  w.xq_off = o;
+  if (is_mx(L)) o += align_up(static_cast<int64_t>(L->T) * token_row_bytes(L));
   w.total = o;
   return w;
 }
@@ -526,6 +673,20 @@ int validate(const xs_ep_layer* L, bool need_out) {
     return XS_EINVAL;
   if (need_out && (!L->x || !L->logits || !L->out)) return XS_EINVAL;
   if (L->expert_mode != XS_EXPERT_SWIGLU && L->expert_mode != XS_EXPERT_IDENTITY) return XS_EINVAL;
+  if (L->precision != XS_PREC_BF16 && L->precision != XS_PREC_MXFP8) return XS_EINVAL;
+  if (L->reserved != 0) return XS_EINVAL;
+  if (is_mx(L)) {
+    if (L->expert_mode != XS_EXPERT_SWIGLU) return XS_EUNSUPPORTED;
+    if (!L->w1_scale || !L->w2_scale) return XS_EINVAL;
+    // 16-byte code rows and 4-byte scale rows, whole 256 x 256 tiles along H, 128-column
+    // SwiGLU tiles and 128-deep K stages along I
+    if (L->H % 512 || L->I % 512) return XS_EUNSUPPORTED;
+    if ((reinterpret_cast<uintptr_t>(L->w1) | reinterpret_cast<uintptr_t>(L->w2) |
+         reinterpret_cast<uintptr_t>(L->h_ws)) & 15)
+      return XS_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(L->w1_scale) | reinterpret_cast<uintptr_t>(L->w2_scale)) & 3)
+      return XS_EINVAL;
+  }
   if (L->H % 8) return XS_EUNSUPPORTED;
   if (L->expert_mode == XS_EXPERT_SWIGLU) {
     if (!L->w1 || !L->w2 || !L->h_ws || L->I < 1) return XS_EINVAL;
@@ -536,7 +697,7 @@ int validate(const xs_ep_layer* L, bool need_out) {
 }
 
 int fill_args(const xs_ep_layer* L, void* workspace, EpArgs* a, WinSet* dws, WinSet* cws) {
-  int rc = xs_host::make_winset(L->dispatch_win, L->W, static_cast<int64_t>(L->H) * 2, dws);
+  int rc = xs_host::make_winset(L->dispatch_win, L->W, token_row_bytes(L), dws);
   if (rc) return rc;
   for (int d = 0; d < L->W; ++d)
     if (dws->cap[d] < L->cap) return XS_EINVAL;
@@ -573,6 +734,9 @@ int fill_args(const xs_ep_layer* L, void* workspace, EpArgs* a, WinSet* dws, Win
   a->w2 = static_cast<const uint16_t*>(L->w2);
   a->h = static_cast<uint16_t*>(L->h_ws);
   a->y = static_cast<uint16_t*>(L->y_ws);
+  a->w1s = static_cast<const uint8_t*>(L->w1_scale);
+  a->w2s = static_cast<const uint8_t*>(L->w2_scale);
+  a->h_stride = h_row_bytes(L);
   int* meta = reinterpret_cast<int*>(ws + w.meta_off);
   int* exp = reinterpret_cast<int*>(ws + w.exp_off);
   a->meta = meta;
@@ -655,7 +819,9 @@ static int run_ffn(const xs_ep_layer* L, const EpArgs& base, int mode, int l2_co
   a.gap_ticks = pc ? xs_host::ns_to_ticks(pc->gap_ns) : 0;
   const int64_t tmo_us = pc && pc->spin_timeout_us > 0 ? pc->spin_timeout_us : 2000000;
   a.timeout_ticks = xs_host::ns_to_ticks(tmo_us * 1000);
-  if (mode == 1)
+  if (is_mx(L))
+    hipLaunchKernelGGL(ep_ffn_mx_kernel<3>, dim3(grid), dim3(kMxThreads), 0, st, a);
+  else if (mode == 1)
     hipLaunchKernelGGL(ep_ffn_kernel<1>, dim3(grid), dim3(kThreads), 0, st, a);
   else if (mode == 2)
     hipLaunchKernelGGL(ep_ffn_kernel<2>, dim3(grid), dim3(kThreads), 0, st, a);
@@ -668,6 +834,7 @@ extern "C" int xs_expert_ffn(const xs_ep_layer* L, void* workspace, int64_t work
                              int32_t* dev_status, void* stream) {
   int rc = validate(L, false);
   if (rc) return rc;
+  if (is_mx(L)) return XS_EUNSUPPORTED;
   if (!L->y_ws) return XS_EINVAL;
   if (!workspace || workspace_bytes < ep_workspace(L).total) return XS_EWORKSPACE;
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -695,6 +862,7 @@ extern "C" int xs_expert_ffn(const xs_ep_layer* L, void* workspace, int64_t work
 extern "C" int xs_combine_send(const xs_ep_layer* L, int32_t* dev_status, void* stream) {
   int rc = validate(L, false);
   if (rc) return rc;
+  if (is_mx(L)) return XS_EUNSUPPORTED;
   if (!L->y_ws) return XS_EINVAL;
   hipStream_t st = static_cast<hipStream_t>(stream);
   EpArgs a;
@@ -741,8 +909,19 @@ extern "C" int xs_fused_ep_layer(const xs_ep_layer* L, const xs_pacing* pacing,
   if (rc) return rc;
   const int64_t so = static_cast<int64_t>(L->src) * L->T * L->k;
   if ((rc = record_event(L, XS_EV_DISPATCH, st))) return rc;
-  rc = xs_host::dispatch(L->x, L->T, L->H, L->topk_idx + so, L->slot_row + so, L->k, L->E, dws,
-                         dev_status, st);
+  if (is_mx(L)) {
+    // quantize this source's token rows once (codes, then scales, in each staged row) and
+    // dispatch the staged rows
+    const int64_t rb = token_row_bytes(L);
+    char* xq = static_cast<char*>(workspace) + w.xq_off;
+    rc = xs_quantize_mx(L->x, L->T, L->H, L->H, XS_FMT_E4M3, xq, rb, xq + L->H, rb, stream);
+    if (rc) return rc;
+    rc = xs_host::dispatch_rows(xq, rb, static_cast<int32_t>(rb), L->T, L->topk_idx + so, L->slot_row + so,
+                                L->k, L->E, dws, dev_status, st);
+  } else {
+    rc = xs_host::dispatch(L->x, L->T, L->H, L->topk_idx + so, L->slot_row + so, L->k, L->E, dws,
+                           dev_status, st);
+  }
   if (rc) return rc;
   a.status = dev_status;
   if ((rc = record_event(L, XS_EV_PLAN, st))) return rc;

@@ -231,6 +231,72 @@ __device__ __forceinline__ void stage_tile_mx(const AccMx& acc, char* lds) {
       }
 }
 
+// Shared exponent of an MXFP8 (E4M3) block from the bits of its largest magnitude as an fp32
+// value: the smallest e with amax <= 448 2^e (448 = 1.75 2^8), i.e. e = E - 8 + [M > 1.75] for
+// amax = M 2^E; 0 for an all-zero block; clamped to [-127, 127]. Integer arithmetic only.
+__device__ __forceinline__ int mx_exp_e4m3_f32(uint32_t amax_bits) {
+  if (amax_bits == 0) return 0;
+  const int F = static_cast<int>(amax_bits >> 23);
+  const uint32_t m = amax_bits & 0x7FFFFFu;
+  int E, above;
+  if (F != 0) {
+    E = F - 127;
+    above = m > 0x600000u;
+  } else {                                       // fp32 subnormal: m 2^-149
+    const int p = 31 - __builtin_clz(m);
+    E = p - 149;
+    above = static_cast<uint64_t>(m) * 4 > (7ull << p);
+  }
+  const int e = E - 8 + above;
+  return e < -127 ? -127 : (e > 127 ? 127 : e);
+}
+
+// Staged MXFP8 h tile: 256 rows of 128 codes (pitch kHqPitch bytes) and, after them, 256
+// rows of 4 scale bytes.
+constexpr int kHqPitch = 144;
+constexpr int kHqScaleOff = kBM * kHqPitch;
+
+// SwiGLU of a gate/up tile, quantized to MXFP8 along its 128 output columns (four blocks of
+// 32). B blocks 2 jj and 2 jj + 1 of a wave hold the gate and up rows of the same 32 output
+// columns (block 2 wn + jj of the tile); a lane holds 16 of a row's 32 values of that block
+// and lane ^ 32 the other 16, so the block maximum takes one half swap. Codes: the exact
+// power-of-two scaling and the hardware round-to-nearest-even E4M3 conversion.
+__device__ __forceinline__ void stage_swiglu_mxq(const AccMx& acc, char* lds) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  const int up = lane >> 5;
+  typedef uint32_t u32x2_ __attribute__((ext_vector_type(2)));
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = wm * 128 + 32 * i + (lane & 31);
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+      float hv[16];
+      uint32_t amax = 0;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const float gt = acc[i][2 * jj][q], u = acc[i][2 * jj + 1][q];
+        hv[q] = gt * __builtin_amdgcn_rcpf(1.f + __expf(-gt)) * u;
+        amax = max(amax, __builtin_bit_cast(uint32_t, hv[q]) & 0x7FFFFFFFu);
+      }
+      const auto r = __builtin_amdgcn_permlane32_swap(amax, amax, false, false);
+      const u32x2_ both = {r[0], r[1]};
+      const int e = mx_exp_e4m3_f32(max(both.x, both.y));
+      const int col0 = 32 * (2 * wn + jj) + 4 * up;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        uint32_t c = static_cast<uint32_t>(__builtin_amdgcn_cvt_pk_fp8_f32(
+            __builtin_amdgcn_ldexpf(hv[4 * g], -e), __builtin_amdgcn_ldexpf(hv[4 * g + 1], -e), 0, false));
+        c = static_cast<uint32_t>(__builtin_amdgcn_cvt_pk_fp8_f32(
+            __builtin_amdgcn_ldexpf(hv[4 * g + 2], -e), __builtin_amdgcn_ldexpf(hv[4 * g + 3], -e),
+            static_cast<int>(c), true));
+        *reinterpret_cast<uint32_t*>(lds + row * kHqPitch + col0 + 8 * g) = c;
+      }
+      if (up == 0) lds[kHqScaleOff + row * 4 + 2 * wn + jj] = static_cast<char>(e + 127);
+    }
+  }
+}
+
 // Stores staged rows [0, rows) through per-row destination pointers (null rows skipped):
 // pieces of 16 bytes, per_row pieces per row, pitch bytes between staged rows; NT threads.
 template <int NT>

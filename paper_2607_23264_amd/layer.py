@@ -47,8 +47,14 @@ class Shape:
 class EPLayer:
     """Owns every device buffer of one EP layer call (inputs, layout, windows, outputs)."""
 
-    def __init__(self, s: Shape, device="cuda", combine_host: bool = False, sentinel: bool = True):
+    def __init__(self, s: Shape, device="cuda", combine_host: bool = False, sentinel: bool = True,
+                 precision: int = X.XS_PREC_BF16):
         self.s = s
+        self.precision = precision
+        mxp = precision == X.XS_PREC_MXFP8
+        # bytes per dispatched token row and per h row (MXFP8: codes, then one scale per 32)
+        self.row_bytes = s.H + s.H // 32 if mxp else 2 * s.H
+        self.h_bytes = s.I + s.I // 32 if mxp else 2 * s.I
         self.dev = torch.device(device)
         cap = s.cap if s.cap is not None else s.n_src * s.T * min(s.k, s.epw)
         self.cap = cap
@@ -69,8 +75,12 @@ class EPLayer:
         self.slot_row = torch.zeros((s.n_src, s.T, s.k), dtype=i32, device=d)
         self.row_src = torch.full((s.W, cap), -1, dtype=i32, device=d)
         fill = -1 if sentinel else 0
-        self.dwin = torch.full((s.W, cap, s.H), fill, dtype=torch.int16, device=d) if sentinel \
-            else torch.empty((s.W, cap, s.H), dtype=torch.int16, device=d)
+        if mxp:
+            self.dwin = torch.full((s.W, cap, self.row_bytes), 0xFF if sentinel else 0, dtype=torch.uint8, device=d)
+            self.xq = torch.zeros((s.T, self.row_bytes), dtype=torch.uint8, device=d)
+        else:
+            self.dwin = torch.full((s.W, cap, s.H), fill, dtype=torch.int16, device=d) if sentinel \
+                else torch.empty((s.W, cap, s.H), dtype=torch.int16, device=d)
         self.combine_host = combine_host
         if combine_host:
             self._host = HostCoherent(s.n_src * s.T * s.k * s.H * 2)
@@ -80,7 +90,15 @@ class EPLayer:
             self.cwin = torch.full((s.n_src, s.T * s.k, s.H), fill, dtype=torch.int16, device=d) if sentinel \
                 else torch.empty((s.n_src, s.T * s.k, s.H), dtype=torch.int16, device=d)
         h_rows = s.n_cwin * cap
-        self.h_ws = torch.zeros((h_rows, s.I if s.I else 1), dtype=torch.int16, device=d)
+        if mxp:
+            self.h_ws = torch.zeros((h_rows, self.h_bytes), dtype=torch.uint8, device=d)
+            E_, I_, H_ = s.n_experts, s.I, s.H
+            self.w1q = torch.zeros((E_, 2 * I_, H_), dtype=torch.uint8, device=d)
+            self.w1s = torch.zeros((E_, 2 * I_, H_ // 32), dtype=torch.uint8, device=d)
+            self.w2q = torch.zeros((E_, H_, I_), dtype=torch.uint8, device=d)
+            self.w2s = torch.zeros((E_, H_, I_ // 32), dtype=torch.uint8, device=d)
+        else:
+            self.h_ws = torch.zeros((h_rows, s.I if s.I else 1), dtype=torch.int16, device=d)
         self.y_ws = torch.zeros((h_rows, s.H), dtype=torch.int16, device=d)
         self.out = torch.zeros((s.T, s.H), dtype=torch.int16, device=d)
         self.status = torch.zeros((1,), dtype=i32, device=d)
@@ -104,8 +122,13 @@ class EPLayer:
         L.cap = self.cap
         L.logits = self.logits.data_ptr()
         L.x = self.x_all[s.src].data_ptr()
-        L.w1 = X.ptr(self.w1)
-        L.w2 = X.ptr(self.w2)
+        L.precision = self.precision
+        if self.precision == X.XS_PREC_MXFP8:
+            L.w1, L.w2 = self.w1q.data_ptr(), self.w2q.data_ptr()
+            L.w1_scale, L.w2_scale = self.w1s.data_ptr(), self.w2s.data_ptr()
+        else:
+            L.w1 = X.ptr(self.w1)
+            L.w2 = X.ptr(self.w2)
         L.topk_idx = self.topk_idx.data_ptr()
         L.topk_w = self.topk_w.data_ptr()
         L.expert_counts = self.expert_counts.data_ptr()
@@ -130,7 +153,18 @@ class EPLayer:
             for i in range(w1_bits.shape[0]):   # expert by expert to bound host staging
                 self.w1[i].copy_(_dev_bits(w1_bits[i], "cpu"))
                 self.w2[i].copy_(_dev_bits(w2_bits[i], "cpu"))
+            if self.precision == X.XS_PREC_MXFP8:
+                self.quantize_weights()
         torch.cuda.synchronize(self.dev)
+
+    def quantize_weights(self):
+        """MXFP8 codes and scales of W1 (along H) and W2 (along I), on the GPU."""
+        s = self.s
+        st = self.stream
+        X.check(X.xs_quantize_mx(self.w1.data_ptr(), s.n_experts * 2 * s.I, s.H, s.H, X.XS_FMT_E4M3,
+                                 self.w1q.data_ptr(), s.H, self.w1s.data_ptr(), s.H // 32, st), "quantize w1")
+        X.check(X.xs_quantize_mx(self.w2.data_ptr(), s.n_experts * s.H, s.I, s.I, X.XS_FMT_E4M3,
+                                 self.w2q.data_ptr(), s.I, self.w2s.data_ptr(), s.I // 32, st), "quantize w2")
 
     @property
     def stream(self):
@@ -154,6 +188,14 @@ class EPLayer:
 
     def dispatch(self, src: int):
         s = self.s
+        if self.precision == X.XS_PREC_MXFP8:
+            rb = self.row_bytes
+            X.check(X.xs_quantize_mx(self.x_all[src].data_ptr(), s.T, s.H, s.H, X.XS_FMT_E4M3, self.xq.data_ptr(),
+                                     rb, self.xq.data_ptr() + s.H, rb, self.stream), "quantize x")
+            X.check(X.xs_dispatch_rows(self.xq.data_ptr(), rb, rb, s.T, self.topk_idx[src].data_ptr(),
+                                       self.slot_row[src].data_ptr(), s.k, s.E, self._dwins, s.W,
+                                       self.status.data_ptr(), self.stream), "dispatch rows")
+            return
         X.check(X.xs_dispatch(self.x_all[src].data_ptr(), s.T, s.H, self.topk_idx[src].data_ptr(),
                               self.slot_row[src].data_ptr(), s.k, s.E, self._dwins, s.W,
                               self.status.data_ptr(), self.stream), "dispatch")

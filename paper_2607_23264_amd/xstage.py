@@ -29,6 +29,7 @@ XS_SCATTER_ROW_BLOCK, XS_SCATTER_HEAD_GROUP = 0, 1
 XS_MB_PERIODIC, XS_MB_COMPLETION = 0, 1
 XS_ATTN_LOCAL, XS_ATTN_WINDOWS, XS_ATTN_WINDOWS_COUPLED = 0, 1, 2
 XS_FMT_E4M3, XS_FMT_E2M1 = 0, 1
+XS_PREC_BF16, XS_PREC_MXFP8 = 0, 1
 
 vp = C.c_void_p
 i32 = C.c_int32
@@ -65,7 +66,8 @@ class xs_ep_layer(C.Structure):
                 ("expert_counts", vp), ("src_base", vp), ("expert_offsets", vp), ("dest_counts", vp),
                 ("slot_row", vp), ("row_src", vp), ("dispatch_win", C.POINTER(xs_window)),
                 ("combine_win", C.POINTER(xs_window)), ("h_ws", vp), ("h_rows", i64), ("y_ws", vp),
-                ("out", vp), ("events", vp * 8)]
+                ("out", vp), ("events", vp * 8), ("precision", i32), ("reserved", i32),
+                ("w1_scale", vp), ("w2_scale", vp)]
 
 
 class xs_attn(C.Structure):
@@ -128,6 +130,8 @@ xs_scatter_copy = _sig("xs_scatter_copy", C.c_int, vp, i64, i32, i32, P(xs_scatt
                        i32, vp)
 xs_attention = _sig("xs_attention", C.c_int, P(xs_attn), i32, P(xs_trace), vp)
 xs_ulysses_copy = _sig("xs_ulysses_copy", C.c_int, vp, i32, i32, i32, P(xs_window), i32, vp)
+xs_dispatch_rows = _sig("xs_dispatch_rows", C.c_int, vp, i64, i32, i32, vp, vp, i32, i32, P(xs_window), i32,
+                        vp, vp)
 xs_quantize_mx = _sig("xs_quantize_mx", C.c_int, vp, i64, i32, i64, i32, vp, i64, vp, i64, vp)
 xs_gemm_mx = _sig("xs_gemm_mx", C.c_int, vp, i64, vp, i64, vp, i64, vp, i64, i32, vp, i64, i32, i32, i32,
                   P(xs_trace), vp)
@@ -139,7 +143,7 @@ xs_clock_rate_hz = _sig("xs_clock_rate_hz", C.c_double)
 EXPORTED = ["xs_strerror", "xs_version", "xs_route_topk_softmax", "xs_dispatch_layout_workspace_bytes",
             "xs_dispatch_layout", "xs_dispatch", "xs_ep_layer_workspace_bytes", "xs_expert_ffn",
             "xs_combine_send", "xs_combine_reduce", "xs_fused_ep_layer", "xs_gemm", "xs_gemm_scatter",
-            "xs_scatter_copy", "xs_attention", "xs_ulysses_copy", "xs_quantize_mx", "xs_gemm_mx",
+            "xs_scatter_copy", "xs_attention", "xs_ulysses_copy", "xs_quantize_mx", "xs_gemm_mx", "xs_dispatch_rows",
             "xs_model_predict", "xs_model_fit",
             "xs_xstage_microbench", "xs_clock_rate_hz"]
 

@@ -1,0 +1,331 @@
+"""GPU parity of the MXFP8 (W8A8) expert-parallel layer against the CPU oracle, through the C
+ABI: dispatch windows of quantized token rows (bit-exact), the quantized h rows, the combine
+rows and the combined output; every pacing policy gives the same bits."""
+import ctypes as C
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import ep as oep
+from oracle import ep_mx as omx
+from oracle import mx as omxf
+from gpu_helpers import assert_close, bits_f64, host_bits, require_gpu, xs
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+    torch.cuda.set_device(0)
+
+
+def _mx_layer(cfg, **kw):
+    from paper_2607_23264_amd.layer import EPLayer, Shape
+    X = xs()
+    experts = synth.computed_experts(cfg)
+    s = Shape(cfg.n_src, cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.W, experts[0], len(experts), src=cfg.rank,
+              **kw)
+    return EPLayer(s, precision=X.XS_PREC_MXFP8)
+
+
+def _policies():
+    from paper_2607_23264_amd.layer import pacing
+    X = xs()
+    return {"burst": pacing(X.XS_POLICY_BURST), "interleave_D1": pacing(X.XS_POLICY_INTERLEAVE, lead=1),
+            "chunk2_p8": pacing(X.XS_POLICY_CHUNK, lead=2, chunk=2, max_producers=8),
+            "auto_nomodel": pacing(X.XS_POLICY_AUTO),
+            "interleave_dyn": pacing(X.XS_POLICY_INTERLEAVE, lead=1, claim=X.XS_CLAIM_DYNAMIC),
+            "burst_w4_dyn": pacing(X.XS_POLICY_BURST, wave_tiles=4, claim=X.XS_CLAIM_DYNAMIC)}
+
+
+def _h_within_fp32_bound(got_codes, got_scales, xq, w1q, what):
+    """The GPU's quantized h rows against the exact SwiGLU of the dequantized operands.
+
+    The GPU accumulates Linear-1 in fp32 and evaluates SwiGLU in fp32, so its h differs from
+    the exact value by at most bh = |dh/dg| bg + |dh/du| bu + (8 + 2|g|) 2^-24 |h|, where
+    bg, bu = 2 K 2^-24 sum_k |x_k w_k| bound the accumulation error of the gate and up
+    sums (K terms) and the last term covers the exp, reciprocal and products. Each block's
+    scale must be the shared exponent of some values within that bound, and each code the
+    round-to-nearest-even of some value within it: codes may differ from the oracle's only
+    where its value lies that close to a rounding midpoint (or a block maximum that close to a
+    power-of-two threshold)."""
+    X = omxf.dequantize_mx(*xq, omxf.E4M3)
+    W1 = omxf.dequantize_mx(*w1q, omxf.E4M3)
+    I = W1.shape[0] // 2
+    K = X.shape[1]
+    g, u = X @ W1[:I].T, X @ W1[I:].T
+    u_eps = 2.0 ** -24
+    bg = 2 * K * u_eps * (np.abs(X) @ np.abs(W1[:I]).T)
+    bu = 2 * K * u_eps * (np.abs(X) @ np.abs(W1[I:]).T)
+    with np.errstate(over="ignore"):
+        sig = 1.0 / (1.0 + np.exp(-g))
+    h = g * sig * u
+    dh_dg = np.abs(u * sig * (1 + g * (1 - sig)))
+    bh = dh_dg * bg + np.abs(g * sig) * bu + (8 + 2 * np.abs(g)) * u_eps * np.abs(h)
+    lo, hi = h - bh, h + bh
+    m = h.shape[0]
+    es = got_scales.astype(np.int64) - 127                       # [m][I / 32]
+    # admissible scales: the exponent of some block maximum in [max|lo..hi|]
+    amax_lo = np.where((lo > 0) | (hi < 0), np.minimum(np.abs(lo), np.abs(hi)), 0.0)
+    amax_hi = np.maximum(np.abs(lo), np.abs(hi))
+    e_lo = omxf.shared_exponent(amax_lo.reshape(m, -1, 32).max(-1), omxf.E4M3)
+    e_hi = omxf.shared_exponent(amax_hi.reshape(m, -1, 32).max(-1), omxf.E4M3)
+    bad_scale = (es < e_lo) | (es > e_hi)
+    assert not bad_scale.any(), f"{what}: {bad_scale.sum()} block scales outside the fp32 bound"
+    sc = np.repeat(np.ldexp(1.0, es), 32, axis=1)
+    vals = omxf.decode(got_codes, omxf.E4M3)
+    c_lo = omxf.decode(omxf.encode(lo / sc, omxf.E4M3), omxf.E4M3)
+    c_hi = omxf.decode(omxf.encode(hi / sc, omxf.E4M3), omxf.E4M3)
+    bad = (vals < c_lo) | (vals > c_hi)
+    assert not bad.any(), f"{what}: {bad.sum()} codes outside the fp32 bound, first at {np.argwhere(bad)[0]}"
+    want, _ = omxf.quantize_mx(h, omxf.E4M3)
+    return int((got_codes != want).sum())
+
+
+def _window_bases(lay):
+    """Row of the h workspace where each computed window's rows begin."""
+    s = lay.s
+    counts = lay.dest_counts.cpu().numpy()
+    first = s.e_begin // s.epw
+    base, out = 0, {}
+    for d in range(first, first + s.n_cwin):
+        out[d] = base
+        base += min(int(counts[d]), lay.cap)
+    return out
+
+
+def test_tiny_layer_matches_oracle_for_every_policy():
+    cfg = synth.EP_TINY
+    inp = synth.ep_inputs(cfg, 0)
+    ref = omx.ep_layer_mx(inp["x"], inp["logits"], inp["w1"], inp["w2"], cfg.k, cfg.E, cfg.W, cap=cfg.T * cfg.k)
+    lay = _mx_layer(cfg)
+    lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
+    outs = {}
+    for name, p in _policies().items():
+        lay.out.zero_()
+        lay.cwin.fill_(-1)
+        lay.fused(p)
+        torch.cuda.synchronize()
+        assert int(lay.status.item()) == 0, name
+        outs[name] = host_bits(lay.out)
+        assert_close(outs[name], ref["out64"], f"tiny MXFP8 layer {name}")
+    first = next(iter(outs.values()))
+    for name, o in outs.items():
+        assert np.array_equal(o, first), f"policy {name} changed the output bits"
+    assert np.array_equal(lay.topk_idx.cpu().numpy(), ref["idx"])
+    assert np.array_equal(lay.slot_row.cpu().numpy(), ref["layout"]["slot_row"])
+    # dispatch windows: the quantized token rows, codes then scales, bit for bit
+    win = lay.dwin.cpu().numpy()
+    H = cfg.H
+    for d in range(cfg.W):
+        n = int(ref["layout"]["dest_counts"][d])
+        assert np.array_equal(win[d, :n, :H], ref["win_codes"][d, :n]), f"window {d} codes"
+        assert np.array_equal(win[d, :n, H:H + H // 32], ref["win_scales"][d, :n]), f"window {d} scales"
+        assert (win[d, n:] == 0xFF).all(), f"window {d} rows past the count were written"
+    # h rows of every expert: I codes then I / 32 scales
+    h = lay.h_ws.cpu().numpy()
+    bases = _window_bases(lay)
+    epw = cfg.E // cfg.W
+    flips = 0
+    for e, (hc, hs) in ref["h"].items():
+        d, r0 = e // epw, int(ref["layout"]["expert_offsets"][e])
+        m = hc.shape[0]
+        rows = h[bases[d] + r0:bases[d] + r0 + m]
+        xq = (ref["win_codes"][d, r0:r0 + m], ref["win_scales"][d, r0:r0 + m])
+        flips += _h_within_fp32_bound(rows[:, :cfg.I], rows[:, cfg.I:], xq, omx.quantize_rows(inp["w1"][e]),
+                                      f"h of expert {e}")
+    print(f"h codes that differ from the oracle's (all within the fp32 bound): {flips}")
+    # combine rows (bf16 expert outputs) against the oracle's rounded rows
+    comb = host_bits(lay.cwin)
+    assert_close(comb[0], bits_f64(ref["combine"][0]), "combine rows")
+
+
+def test_multi_source_ragged_share():
+    # 3 sources, this GPU = rank 1 owning experts 4..7; T not a multiple of the 256-row tile
+    cfg = synth.EPConfig("t", T=300, H=512, E=16, k=3, I=512, W=4, n_src=3, rank=1)
+    inp = synth.ep_inputs(cfg, 7)
+    experts = synth.computed_experts(cfg)
+    fill = synth.normal_bf16(0, 200, (cfg.T * cfg.k, cfg.H))
+    ref = omx.ep_layer_mx(inp["x"], inp["logits"], inp["w1"], inp["w2"], cfg.k, cfg.E, cfg.W,
+                          cap=cfg.n_src * cfg.T * cfg.k, experts=experts, combine_fill=fill, out_src=cfg.rank)
+    lay = _mx_layer(cfg)
+    lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
+    lay.prefill_other_sources(fill)
+    from paper_2607_23264_amd.layer import pacing
+    lay.fused(pacing(xs().XS_POLICY_INTERLEAVE, lead=1))
+    torch.cuda.synchronize()
+    assert int(lay.status.item()) == 0
+    assert_close(host_bits(lay.out), ref["out64"], "ragged MXFP8 share output")
+    # the computed window holds every source's quantized rows bit for bit
+    d = cfg.rank
+    n = int(ref["layout"]["dest_counts"][d])
+    win = lay.dwin.cpu().numpy()
+    assert np.array_equal(win[d, :n, :cfg.H], ref["win_codes"][d, :n])
+    assert np.array_equal(win[d, :n, cfg.H:], ref["win_scales"][d, :n])
+    # combine windows of every source: computed rows close to the oracle's, the rest untouched
+    comb = host_bits(lay.cwin)
+    epw = cfg.E // cfg.W
+    own = np.isin(ref["idx"] // epw, [cfg.rank]).reshape(cfg.n_src, cfg.T * cfg.k)
+    for s in range(cfg.n_src):
+        assert_close(comb[s][own[s]], bits_f64(ref["combine"][s][own[s]]), f"combine rows of source {s}")
+        if s != cfg.rank:
+            assert (comb[s][~own[s]] == 0xFFFF).all()
+
+
+def _local_token_sample(idx_r, experts, T, n_tokens, max_experts, seed):
+    """Tokens 0 and T - 1 and random others whose locally computed experts stay within a set
+    of at most max_experts (bounds the oracle's weight quantization)."""
+    g = np.random.default_rng(seed)
+    local = set(experts)
+    chosen, used = [], set()
+    for t in [0, T - 1] + list(g.permutation(T)):
+        mine = {int(e) for e in idx_r[t] if int(e) in local}
+        if len(used | mine) > max_experts or t in chosen:
+            continue
+        chosen.append(int(t))
+        used |= mine
+        if len(chosen) == n_tokens:
+            break
+    return chosen
+
+
+@pytest.mark.parametrize("routing,claim", [("uniform", 0), ("zipf", 1)])
+def test_dsv3_share_full_size_sampled(routing, claim):
+    cfg = dataclasses.replace(synth.EP_DSV3_SHARE, routing=routing)
+    if routing == "zipf":
+        idx = np.stack([oep.route_topk_softmax(synth.zipf_logits(0, s, cfg.T, cfg.E), cfg.k)[0]
+                        for s in range(cfg.n_src)])
+        loads = np.bincount((idx // cfg.E_local).ravel(), minlength=cfg.W)
+        cfg = dataclasses.replace(cfg, rank=int(loads.argmax()))
+    inp = synth.ep_inputs(cfg, 0)
+    experts = synth.computed_experts(cfg)
+    fill = synth.ep_remote_combine_fill(cfg, 0)
+    lay = _mx_layer(cfg)
+    lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
+    lay.prefill_other_sources(fill)
+    from paper_2607_23264_amd.layer import pacing
+    lay.fused(pacing(xs().XS_POLICY_INTERLEAVE, lead=0, claim=claim))
+    torch.cuda.synchronize()
+    assert int(lay.status.item()) == 0
+    r = cfg.rank
+    idx, w = oep.route_topk_softmax(inp["logits"][r], cfg.k)
+    assert np.array_equal(lay.topk_idx[r].cpu().numpy(), idx)
+    slot_row = lay.slot_row[r].cpu().numpy()
+    toks = _local_token_sample(idx, experts, cfg.T, 10, 4, seed=1)
+    out = host_bits(lay.out)
+    win = lay.dwin.cpu().numpy()
+    pos = {e: i for i, e in enumerate(experts)}
+    wq = {}
+    for t in toks:
+        xq = omx.quantize_rows(inp["x"][r, t:t + 1])
+        acc = np.zeros(cfg.H)
+        for j in range(cfg.k):
+            e = int(idx[t, j])
+            d = e // cfg.E_local
+            # this source's token row in its destination window, codes and scales
+            assert np.array_equal(win[d, slot_row[t, j], :cfg.H], xq[0][0]), (t, j)
+            assert np.array_equal(win[d, slot_row[t, j], cfg.H:], xq[1][0]), (t, j)
+            if e in pos:
+                if e not in wq:
+                    i = pos[e]
+                    wq[e] = (omx.quantize_rows(inp["w1"][i]), omx.quantize_rows(inp["w2"][i]))
+                _, _, _, yb = omx.expert_ffn_mx(xq, *wq[e])
+                row = bits_f64(yb[0])
+            else:
+                row = bits_f64(fill[t * cfg.k + j])
+            acc += np.float64(w[t, j]) * row
+        assert_close(out[t], acc, f"{routing} token {t}")
+
+
+def _fused_rc(L, lay):
+    X = xs()
+    ws = lay.workspace
+    return X.xs_fused_ep_layer(C.byref(L), None, None, ws.data_ptr(), ws.numel(), lay.status.data_ptr(),
+                               lay.stream)
+
+
+def test_bad_arguments():
+    X = xs()
+    cfg = synth.EP_TINY
+    lay = _mx_layer(cfg)
+    ws = lay.workspace
+
+    def variant(**fields):
+        L = X.xs_ep_layer.from_buffer_copy(lay.L)
+        for k, v in fields.items():
+            setattr(L, k, v)
+        return L
+
+    assert _fused_rc(variant(precision=2), lay) == X.XS_EINVAL
+    assert _fused_rc(variant(reserved=1), lay) == X.XS_EINVAL
+    assert _fused_rc(variant(w1_scale=None), lay) == X.XS_EINVAL
+    assert _fused_rc(variant(w2_scale=None), lay) == X.XS_EINVAL
+    assert _fused_rc(variant(expert_mode=X.XS_EXPERT_IDENTITY), lay) == X.XS_EUNSUPPORTED
+    assert _fused_rc(variant(I=768), lay) == X.XS_EUNSUPPORTED
+    assert _fused_rc(variant(w1=lay.w1q.data_ptr() + 8), lay) == X.XS_EINVAL
+    assert _fused_rc(variant(w2_scale=lay.w2s.data_ptr() + 2), lay) == X.XS_EINVAL
+    # the unfused phase calls take bf16 only
+    assert X.xs_expert_ffn(C.byref(lay.L), ws.data_ptr(), ws.numel(), lay.status.data_ptr(),
+                           lay.stream) == X.XS_EUNSUPPORTED
+    assert X.xs_combine_send(C.byref(lay.L), lay.status.data_ptr(), lay.stream) == X.XS_EUNSUPPORTED
+    # a workspace sized for bf16 is too small: the quantized rows are staged in it
+    nb = C.c_int64()
+    X.check(X.xs_ep_layer_workspace_bytes(C.byref(variant(precision=X.XS_PREC_BF16)), C.byref(nb)))
+    assert X.xs_fused_ep_layer(C.byref(lay.L), None, None, ws.data_ptr(), nb.value, lay.status.data_ptr(),
+                               lay.stream) == X.XS_EWORKSPACE
+    # windows narrower than a quantized row
+    narrow = X.windows([X.window(lay.dwin[w], row_bytes=cfg.H) for w in range(cfg.W)])
+    assert _fused_rc(variant(dispatch_win=C.cast(narrow, C.POINTER(X.xs_window))), lay) != X.XS_OK
+    torch.cuda.synchronize()
+    assert int(lay.status.item()) == 0
+
+
+def test_dispatch_rows_bitexact():
+    X = xs()
+    g = np.random.default_rng(3)
+    T, k, E, W, row_bytes, stride = 301, 3, 12, 3, 80, 96
+    idx = np.argsort(g.random((1, T, E)), axis=2)[:, :, :k].astype(np.int32)
+    lay = oep.dispatch_layout(idx, E, W, T * k)
+    rows = g.integers(0, 256, (T, stride), dtype=np.uint8)
+    d_rows = torch.from_numpy(rows).cuda()
+    d_idx = torch.from_numpy(idx[0]).cuda()
+    d_slot = torch.from_numpy(np.ascontiguousarray(lay["slot_row"][0])).cuda()
+    win = torch.full((W, T * k, 112), 0xAB, dtype=torch.uint8, device="cuda")
+    wins = X.windows([X.window(win[d]) for d in range(W)])
+    st = torch.zeros((1,), dtype=torch.int32, device="cuda")
+    X.check(X.xs_dispatch_rows(d_rows.data_ptr(), stride, row_bytes, T, d_idx.data_ptr(), d_slot.data_ptr(), k, E,
+                               wins, W, st.data_ptr(), torch.cuda.current_stream().cuda_stream))
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    want = np.full((W, T * k, 112), 0xAB, dtype=np.uint8)
+    epw = E // W
+    for t in range(T):
+        for j in range(k):
+            want[idx[0, t, j] // epw, lay["slot_row"][0, t, j], :row_bytes] = rows[t, :row_bytes]
+    assert np.array_equal(win.cpu().numpy(), want)
+    # argument checks
+    cs = torch.cuda.current_stream().cuda_stream
+    args = (d_idx.data_ptr(), d_slot.data_ptr(), k, E, wins, W, st.data_ptr(), cs)
+    assert X.xs_dispatch_rows(d_rows.data_ptr(), stride, 8, T, *args) == X.XS_EINVAL
+    assert X.xs_dispatch_rows(d_rows.data_ptr(), stride, 24, T, *args) == X.XS_EUNSUPPORTED
+    assert X.xs_dispatch_rows(d_rows.data_ptr(), 72, row_bytes, T, *args) == X.XS_EINVAL
+    assert X.xs_dispatch_rows(d_rows.data_ptr() + 8, stride, row_bytes, T, *args) == X.XS_EUNSUPPORTED
+    assert X.xs_dispatch_rows(d_rows.data_ptr(), stride, 128, T, *args) != X.XS_OK   # windows too narrow
+    assert X.xs_dispatch_rows(d_rows.data_ptr(), stride, row_bytes, 0, *args) == X.XS_OK
+    torch.cuda.synchronize()
+
+
+def test_weight_quantization_matches_oracle():
+    cfg = synth.EP_TINY
+    inp = synth.ep_inputs(cfg, 2)
+    lay = _mx_layer(cfg)
+    lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
+    for i in (0, cfg.E - 1):
+        c1, s1 = omx.quantize_rows(inp["w1"][i])
+        c2, s2 = omx.quantize_rows(inp["w2"][i])
+        assert np.array_equal(lay.w1q[i].cpu().numpy(), c1) and np.array_equal(lay.w1s[i].cpu().numpy(), s1)
+        assert np.array_equal(lay.w2q[i].cpu().numpy(), c2) and np.array_equal(lay.w2s[i].cpu().numpy(), s2)
