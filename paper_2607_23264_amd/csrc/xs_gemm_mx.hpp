@@ -22,6 +22,8 @@
 // 4 kk + h and 4 kk + 2 + h of the row; a lane's scale word for the stage holds the row's four
 // block scales, and one byte permute puts the scale of block 2 kk + h into byte kk.
 #pragma once
+#include <type_traits>
+
 #include "xs_gemm.hpp"
 
 namespace xs {
@@ -73,7 +75,8 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
       __builtin_amdgcn_global_load_lds((glob_void*)(t.b + (t.ob[i] + k0)),
                                        (lds_void*)(st + kOpBytes + (4 * i + w) * 1024), 16, 0, 0);
   };
-  uint32_t sw[8];         // this stage's scale words: A blocks 0..3, B blocks 0..3
+  uint32_t sw[8];         // a stage's scale words as read: A blocks 0..3, B blocks 0..3
+  int sc[8];              // the same, byte kk = scale of K block 2 kk + h (the MFMA's op_sel)
   auto read_s = [&](const char* st) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -82,79 +85,113 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
     for (int j = 0; j < 4; ++j)
       sw[4 + j] = *reinterpret_cast<const uint32_t*>(st + kMxScaleOff + 1024 + (t.brow >> 7) * 4 + j * 128);
   };
-  // A fragments double-buffered (by sub-step), B fragments single-buffered: a sub-step's B
-  // fragments are read again right after its last MFMA has issued
-  v8i_t af[2][4], bfr[4];
+  auto perm_s = [&]() {
+#pragma unroll
+    for (int n = 0; n < 8; ++n) sc[n] = static_cast<int>(__builtin_amdgcn_perm(sw[n], sw[n], sel));
+  };
+  // fragments of sub-step 0 (K elements [0, 64) of a stage) and of sub-step 1 ([64, 128))
+  v8i_t a0[4], b0[4], a1[4], b1[4];
   auto frag = [&](const char* base, int row_off, int kk) {
     const v4i_t lo = *reinterpret_cast<const v4i_t*>(base + row_off + (((4 * kk + h) ^ swz) << 4));
     const v4i_t hi = *reinterpret_cast<const v4i_t*>(base + row_off + (((4 * kk + 2 + h) ^ swz) << 4));
     return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   };
-  auto read_a = [&](const char* st, int kk, int buf) {
+  auto read_frags = [&](const char* st, int kk, v8i_t (&a)[4], v8i_t (&b)[4]) {
 #pragma unroll
-    for (int i = 0; i < NI; ++i) af[buf][i] = frag(st, t.arow + i * 32 * 128, kk);
-  };
-  auto read_b = [&](const char* st, int kk) {
+    for (int j = 0; j < 4; ++j) b[j] = frag(st + kOpBytes, t.brow + j * 32 * 128, kk);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) bfr[j] = frag(st + kOpBytes, t.brow + j * 32 * 128, kk);
+    for (int i = 0; i < NI; ++i) a[i] = frag(st, t.arow + i * 32 * 128, kk);
   };
   // B fragment first: each lane's accumulators hold four consecutive output columns
-  auto mma = [&](int buf, int kk) {
+  auto mma0 = [&]() {
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int sa = static_cast<int>(__builtin_amdgcn_perm(sw[i], sw[i], sel));
+    for (int i = 0; i < NI; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int sb = static_cast<int>(__builtin_amdgcn_perm(sw[4 + j], sw[4 + j], sel));
-        if (kk == 0)
-          acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bfr[j], af[buf][i], acc[i][j],
-                                                                      0, 0, 0, sb, 0, sa);
-        else
-          acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bfr[j], af[buf][i], acc[i][j],
-                                                                      0, 0, 1, sb, 1, sa);
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b0[j], a0[i], acc[i][j], 0, 0, 0, sc[4 + j],
+                                                                    0, sc[i]);
+  };
+  auto mma1 = [&]() {
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b1[j], a1[i], acc[i][j], 0, 0, 1, sc[4 + j],
+                                                                    1, sc[i]);
+  };
+  constexpr int kMfma = 4 * NI;             // MFMAs per sub-step
+  constexpr int kFragReads = 8 + 2 * NI;    // ds_read_b128 per sub-step's fragments
+  // One stage. The schedule is fixed by hand (the compiler, left alone, sinks every MFMA of
+  // the stage below the barrier and leaves the fragment reads exposed):
+  //   A: sub-step 0's MFMAs, each followed by reads of sub-step 1's fragments;
+  //   barrier: this wave's reads of the stage are done and the next stage has landed in every
+  //     wave's share;
+  //   B: sub-step 1's MFMAs, interleaved with the next stage's scale-word and sub-step-0
+  //     fragment reads and the global loads of the stage after next (into this stage's
+  //     buffers, which no wave reads any more).
+  // NEXT: a stage follows; ISSUE: the stage after next exists. Compile-time, so the steady
+  // loop body has no branches.
+  auto stage = [&](int kt, auto next_c, auto issue_c) {
+    constexpr bool kNext = decltype(next_c)::value;
+    constexpr bool kIssue = decltype(issue_c)::value;
+    const char* st = lds + (kt & 1) * kMxStage;
+    const char* nx = lds + ((kt + 1) & 1) * kMxStage;
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (NI > 0) {
+      read_frags(st, 1, a1, b1);
+      mma0();
+#pragma unroll
+      for (int g = 0; g < kMfma; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                       // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, (kFragReads + kMfma - 1) / kMfma, 0);   // DS reads
       }
     }
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (kNext) {
+      __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0)
+      __builtin_amdgcn_s_barrier();
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (NI > 0) mma1();
+    if constexpr (kNext) {
+      if constexpr (NI > 0) {
+        read_s(nx);
+        read_frags(nx, 0, a0, b0);
+      }
+    }
+    if constexpr (kIssue) issue(kt + 2);
+    if constexpr (NI > 0) {
+      constexpr int kReads = kNext ? (kFragReads + 8 + kMfma - 1) / kMfma : 0;   // per MFMA
+      constexpr int kLoads = kIssue ? (18 + kMfma - 1) / kMfma : 0;
+#pragma unroll
+      for (int g = 0; g < kMfma; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if constexpr (kReads > 0) __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+        if constexpr (kLoads > 0) __builtin_amdgcn_sched_group_barrier(0x010, kLoads, 0);   // global loads
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (kNext && NI > 0) perm_s();
   };
-  // prologue: stage 0 resident, stage 1 in flight
+  // prologue: stage 0 resident, stage 1 in flight, stage 0's sub-step-0 operands in registers
   issue(0);
   wait_vm0();
   __builtin_amdgcn_s_barrier();
   if (nk > 1) issue(1);
-  if (NI > 0) {
+  if constexpr (NI > 0) {
     read_s(lds);
-    read_b(lds, 0);
-    read_a(lds, 0, 0);
+    read_frags(lds, 0, a0, b0);
+    perm_s();
   }
-  for (int kt = 0; kt < nk; ++kt) {
-    const char* st = lds + (kt & 1) * kMxStage;
-    if (NI > 0) {
-      // sub-step 0 with sub-step 1's A fragments read in between, then its B fragments
-      read_a(st, 1, 1);
-      mma(0, 0);
-#pragma unroll
-      for (int g = 0; g < NI; ++g) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // two MFMAs
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // one A fragment
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, 2 * NI, 0);
-      read_b(st, 1);
-      mma(1, 1);   // sub-step 1
-    }
-    if (kt + 1 < nk) {
-      // this wave's loads of stage kt + 1 have landed (nothing newer is in flight) ...
-      wait_vm0();
-      // ... and every wave's, and stage kt is no longer read (its last fragments and scale
-      // words are in registers)
-      __builtin_amdgcn_s_barrier();
-      const char* nx = lds + ((kt + 1) & 1) * kMxStage;
-      if (NI > 0) {
-        read_s(nx);
-        read_b(nx, 0);
-        read_a(nx, 0, 0);
-      }
-      if (kt + 2 < nk) issue(kt + 2);   // into stage kt's buffers
-    }
+  const std::true_type yes;
+  const std::false_type no;
+  int kt = 0;
+  for (; kt + 2 < nk; ++kt) stage(kt, yes, yes);
+  if (kt + 1 < nk) {
+    stage(kt, yes, no);
+    ++kt;
   }
+  stage(kt, no, no);
 }
 
 // acc = deq(A)[0:256, 0:K] deq(B)[rows(0:256), 0:K]^T. A / B: E4M3 code rows (lda / ldb bytes

@@ -25,7 +25,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 # sources that define a kernel's code; they and the compiler flags key a stored traffic
 # measurement (a change to either makes it stale)
-FFN_KERNEL_SOURCES = ("csrc/xs_ep_ffn.hip", "csrc/xs_gemm.hpp", "csrc/xs_common.hpp")
+FFN_KERNEL_SOURCES = ("csrc/xs_ep_ffn.hip", "csrc/xs_gemm.hpp", "csrc/xs_gemm_mx.hpp", "csrc/xs_common.hpp")
 ATTN_KERNEL_SOURCES = ("csrc/xs_attn.hip", "csrc/xs_common.hpp")
 KERNEL_SOURCES = {"ffn": FFN_KERNEL_SOURCES, "attn": ATTN_KERNEL_SOURCES}
 
