@@ -102,35 +102,36 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
 #pragma unroll
     for (int i = 0; i < NI; ++i) a[i] = frag(st, t.arow + i * 32 * 128, kk);
   };
-  // B fragment first: each lane's accumulators hold four consecutive output columns
-  auto mma0 = [&]() {
-#pragma unroll
-    for (int i = 0; i < NI; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b0[j], a0[i], acc[i][j], 0, 0, 0, sc[4 + j],
-                                                                    0, sc[i]);
-  };
-  auto mma1 = [&]() {
-#pragma unroll
-    for (int i = 0; i < NI; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b1[j], a1[i], acc[i][j], 0, 0, 1, sc[4 + j],
-                                                                    1, sc[i]);
-  };
   constexpr int kMfma = 4 * NI;             // MFMAs per sub-step
-  constexpr int kFragReads = 8 + 2 * NI;    // ds_read_b128 per sub-step's fragments
-  // One stage. The schedule is fixed by hand (the compiler, left alone, sinks every MFMA of
-  // the stage below the barrier and leaves the fragment reads exposed):
-  //   A: sub-step 0's MFMAs, each followed by reads of sub-step 1's fragments;
+  // One stage. The schedule is fixed by hand, one MFMA and what follows it per fenced group
+  // (left alone, the compiler sinks every MFMA of the stage below the barrier, leaves the
+  // fragment reads exposed and issues the global loads in one burst):
+  //   A: sub-step 0's MFMAs, the first eight each followed by one fragment read (two
+  //     ds_read_b128) of sub-step 1;
   //   barrier: this wave's reads of the stage are done and the next stage has landed in every
   //     wave's share;
-  //   B: sub-step 1's MFMAs, interleaved with the next stage's scale-word and sub-step-0
-  //     fragment reads and the global loads of the stage after next (into this stage's
-  //     buffers, which no wave reads any more).
+  //   B: sub-step 1's MFMAs, each followed by two global loads of the stage after next (into
+  //     this stage's buffers, which no wave reads any more) and one read of the next stage's
+  //     scale words or sub-step-0 fragments.
   // NEXT: a stage follows; ISSUE: the stage after next exists. Compile-time, so the steady
   // loop body has no branches.
+  // one direct load n of stage kt: 0..7 A pieces, 8 / 9 A / B scale words, 10..17 B pieces
+  auto issue_one = [&](int kt, int n) {
+    char* st = lds + (kt & 1) * kMxStage;
+    const uint32_t k0 = static_cast<uint32_t>(kt) * 128u, k4 = static_cast<uint32_t>(kt) * 4u;
+    if (n < 8)
+      __builtin_amdgcn_global_load_lds((glob_void*)(t.a + (t.oa[n] + k0)), (lds_void*)(st + (4 * n + w) * 1024),
+                                       16, 0, 0);
+    else if (n == 8)
+      __builtin_amdgcn_global_load_lds((glob_void*)(t.sa + (t.sao + k4)), (lds_void*)(st + kMxScaleOff + w * 256),
+                                       4, 0, 0);
+    else if (n == 9)
+      __builtin_amdgcn_global_load_lds((glob_void*)(t.sb + (t.sbo + k4)),
+                                       (lds_void*)(st + kMxScaleOff + 1024 + w * 256), 4, 0, 0);
+    else
+      __builtin_amdgcn_global_load_lds((glob_void*)(t.b + (t.ob[n - 10] + k0)),
+                                       (lds_void*)(st + kOpBytes + (4 * (n - 10) + w) * 1024), 16, 0, 0);
+  };
   auto stage = [&](int kt, auto next_c, auto issue_c) {
     constexpr bool kNext = decltype(next_c)::value;
     constexpr bool kIssue = decltype(issue_c)::value;
@@ -138,12 +139,19 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
     const char* nx = lds + ((kt + 1) & 1) * kMxStage;
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (NI > 0) {
-      read_frags(st, 1, a1, b1);
-      mma0();
 #pragma unroll
       for (int g = 0; g < kMfma; ++g) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                       // one MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, (kFragReads + kMfma - 1) / kMfma, 0);   // DS reads
+        const int i = g >> 2, j = g & 3;   // B fragment first: a lane's accumulators hold 4 columns
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b0[j], a0[i], acc[i][j], 0, 0, 0, sc[4 + j],
+                                                                    0, sc[i]);
+        if (g < 4) b1[g] = frag(st + kOpBytes, t.brow + g * 32 * 128, 1);
+        else if (g - 4 < NI) a1[g - 4] = frag(st, t.arow + (g - 4) * 32 * 128, 1);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int r = kMfma; r < 4 + NI; ++r) {   // reads left over when there are few MFMAs
+        if (r < 4) b1[r] = frag(st + kOpBytes, t.brow + r * 32 * 128, 1);
+        else a1[r - 4] = frag(st, t.arow + (r - 4) * 32 * 128, 1);
       }
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -152,23 +160,38 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
       __builtin_amdgcn_s_barrier();
     }
     __builtin_amdgcn_sched_barrier(0);
-    if constexpr (NI > 0) mma1();
-    if constexpr (kNext) {
-      if constexpr (NI > 0) {
-        read_s(nx);
-        read_frags(nx, 0, a0, b0);
-      }
-    }
-    if constexpr (kIssue) issue(kt + 2);
     if constexpr (NI > 0) {
-      constexpr int kReads = kNext ? (kFragReads + 8 + kMfma - 1) / kMfma : 0;   // per MFMA
-      constexpr int kLoads = kIssue ? (18 + kMfma - 1) / kMfma : 0;
 #pragma unroll
       for (int g = 0; g < kMfma; ++g) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        if constexpr (kReads > 0) __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
-        if constexpr (kLoads > 0) __builtin_amdgcn_sched_group_barrier(0x010, kLoads, 0);   // global loads
+        const int i = g >> 2, j = g & 3;
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b1[j], a1[i], acc[i][j], 0, 0, 1, sc[4 + j],
+                                                                    1, sc[i]);
+        if constexpr (kIssue) {
+          if (2 * g < 18) issue_one(kt + 2, 2 * g);
+          if (2 * g + 1 < 18) issue_one(kt + 2, 2 * g + 1);
+        }
+        if constexpr (kNext) {
+          if (g == 0) read_s(nx);
+          else if (g - 1 < 4) b0[g - 1] = frag(nx + kOpBytes, t.brow + (g - 1) * 32 * 128, 0);
+          else if (g - 5 < NI) a0[g - 5] = frag(nx, t.arow + (g - 5) * 32 * 128, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
       }
+      // what did not fit beside the MFMAs
+      if constexpr (kIssue) {
+#pragma unroll
+        for (int n = 2 * kMfma; n < 18; ++n) issue_one(kt + 2, n);
+      }
+      if constexpr (kNext) {
+#pragma unroll
+        for (int r = kMfma; r < 5 + NI; ++r) {
+          if (r == 0) read_s(nx);
+          else if (r - 1 < 4) b0[r - 1] = frag(nx + kOpBytes, t.brow + (r - 1) * 32 * 128, 0);
+          else a0[r - 5] = frag(nx, t.arow + (r - 5) * 32 * 128, 0);
+        }
+      }
+    } else if constexpr (kIssue) {
+      issue(kt + 2);
     }
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (kNext && NI > 0) perm_s();
