@@ -1,12 +1,14 @@
-"""Oracle for the quantized (MXFP8, "W8A8") EP layer (test infrastructure only).
+"""Oracle for the quantized EP layer, W8A8 (MXFP8) and W4A8 (test infrastructure only).
 
 The paper runs its EP kernel at W8A8 as well as W4A8 (Sec. 5.2); the path is the same
 route -> dispatch -> grouped SwiGLU FFN -> combine, with narrower operands. Readings:
   * token rows are quantized once, at dispatch, to MXFP8 along H (E4M3 codes, one E8M0
     scale per 32 elements; oracle/mx.py); a dispatch window row holds the H codes followed by
     the H / 32 scales;
-  * W1 [2I][H] and W2 [H][I] are quantized the same way along their reduction axis (H for W1,
-    I for W2);
+  * W1 [2I][H] and W2 [H][I] are quantized along their reduction axis (H for W1, I for W2)
+    with one E8M0 scale per 32 elements, to E4M3 (W8A8) or to E2M1 (W4A8: MXFP4 weights,
+    8-bit activations); codes are kept one per element here (the GPU packs E2M1 two per
+    byte, low nibble first);
   * Linear-1 in fp64 from the dequantized operands, SwiGLU in fp64, and the activation h is
     quantized to MXFP8 along I straight from that value (the quantized path stores h as MXFP8
     where the bf16 path stores bf16);
@@ -22,17 +24,18 @@ from . import ep, mx
 __all__ = ["quantize_rows", "expert_ffn_mx", "ep_layer_mx", "ep_layer_mx_dense"]
 
 
-def quantize_rows(bits):
-    """bf16 bits [..., K] -> (E4M3 codes [..., K], scales [..., K / 32])."""
-    return mx.quantize_mx(ep.bf16_bits_to_f64(np.asarray(bits)), mx.E4M3)
+def quantize_rows(bits, fmt=mx.E4M3):
+    """bf16 bits [..., K] -> (codes [..., K] of format fmt, scales [..., K / 32])."""
+    return mx.quantize_mx(ep.bf16_bits_to_f64(np.asarray(bits)), fmt)
 
 
-def expert_ffn_mx(xq, w1q, w2q):
+def expert_ffn_mx(xq, w1q, w2q, wfmt=mx.E4M3):
     """One expert's SwiGLU FFN on MXFP8 rows. xq = (codes, scales) of [M][H]; w1q of
-    [2I][H]; w2q of [H][I]. Returns (h codes, h scales, y64 [M][H], y bits)."""
+    [2I][H] and w2q of [H][I] in format wfmt. Returns (h codes, h scales, y64 [M][H],
+    y bits)."""
     X = mx.dequantize_mx(*xq, mx.E4M3)
-    W1 = mx.dequantize_mx(*w1q, mx.E4M3)
-    W2 = mx.dequantize_mx(*w2q, mx.E4M3)
+    W1 = mx.dequantize_mx(*w1q, wfmt)
+    W2 = mx.dequantize_mx(*w2q, wfmt)
     I = W1.shape[0] // 2
     g = X @ W1[:I].T
     u = X @ W1[I:].T
@@ -44,8 +47,9 @@ def expert_ffn_mx(xq, w1q, w2q):
 
 
 def ep_layer_mx(x_bits, logits, w1_bits, w2_bits, k, E, W, cap, experts=None, renormalize=False,
-                combine_fill=None, out_src=0):
-    """The layer of oracle/ep.ep_layer with MXFP8 rows, weights and activations.
+                combine_fill=None, out_src=0, wfmt=mx.E4M3):
+    """The layer of oracle/ep.ep_layer with MXFP8 rows and activations and weights in format
+    wfmt (E4M3: W8A8, E2M1: W4A8).
 
     x_bits [n_src][T][H], logits [n_src][T][E], w1_bits [n_exp][2I][H], w2_bits [n_exp][H][I]
     (indexed by position in ``experts``). Returns every intermediate, including the dispatch
@@ -84,9 +88,9 @@ def ep_layer_mx(x_bits, logits, w1_bits, w2_bits, k, E, W, cap, experts=None, re
         r1 = r0 + int(total[e])
         if r1 == r0:
             continue
-        w1q = quantize_rows(w1_bits[i])
-        w2q = quantize_rows(w2_bits[i])
-        hc, hs, _, yb = expert_ffn_mx((win_c[d, r0:r1], win_s[d, r0:r1]), w1q, w2q)
+        w1q = quantize_rows(w1_bits[i], wfmt)
+        w2q = quantize_rows(w2_bits[i], wfmt)
+        hc, hs, _, yb = expert_ffn_mx((win_c[d, r0:r1], win_s[d, r0:r1]), w1q, w2q, wfmt)
         h[e] = (hc, hs)
         ep.combine_send(np.concatenate([np.zeros((r0, H), np.uint16), yb]), lay["row_src"][d], comb, k,
                         rows=range(r0, r1))
@@ -95,7 +99,7 @@ def ep_layer_mx(x_bits, logits, w1_bits, w2_bits, k, E, W, cap, experts=None, re
             "h": h, "combine": comb, "out64": out64, "out_bits": out_bits}
 
 
-def ep_layer_mx_dense(x_bits, logits, w1_bits, w2_bits, k, renormalize=False):
+def ep_layer_mx_dense(x_bits, logits, w1_bits, w2_bits, k, renormalize=False, wfmt=mx.E4M3):
     """Brute force for one source with no layout or windows: each token's row is quantized,
     run through each of its top-k experts on its own, and the bf16 outputs are summed with
     the routing weights in ascending slot order. Tiny shapes only."""
@@ -107,6 +111,6 @@ def ep_layer_mx_dense(x_bits, logits, w1_bits, w2_bits, k, renormalize=False):
         xq = quantize_rows(x_bits[t:t + 1])
         for j in range(k):
             e = int(idx[t, j])
-            _, _, _, yb = expert_ffn_mx(xq, quantize_rows(w1_bits[e]), quantize_rows(w2_bits[e]))
+            _, _, _, yb = expert_ffn_mx(xq, quantize_rows(w1_bits[e], wfmt), quantize_rows(w2_bits[e], wfmt), wfmt)
             out[t] += np.float64(w[t, j]) * ep.bf16_bits_to_f64(yb[0])
     return out, ep.f64_to_bf16_bits(out)

@@ -1,8 +1,9 @@
-"""Pins of the quantized (MXFP8) EP layer oracle: its layout / dispatch / combine plumbing
-against a dense per-token brute force (bit-exact on operands MXFP8 holds exactly), the
-dispatch windows' contents, and its distance from the bf16 layer (the size of the
-quantization error)."""
+"""Pins of the quantized (W8A8 MXFP8 and W4A8) EP layer oracle: its layout / dispatch / combine
+plumbing against a dense per-token brute force (bit-exact on operands the formats hold
+exactly), the dispatch windows' contents, and its distance from the bf16 layer (the size of
+the quantization error)."""
 import numpy as np
+import pytest
 
 import synth
 from oracle import ep, ep_mx, mx
@@ -12,17 +13,25 @@ def _int_bits(g, shape):
     return synth.to_bf16_bits(g.integers(-8, 9, shape).astype(np.float32))
 
 
-def test_layer_equals_dense_brute_force_bitexact():
-    # integers in [-8, 8] are exact in E4M3 under any block scale, so every product and sum is
-    # exact and the two paths round h and y identically
+def _e2m1_int_bits(g, shape):
+    # integers that E2M1 holds under any block scale: amax 6 or 4 takes scale 1, amax 3 or 2
+    # scale 1/2, amax 1 scale 1/4, and every smaller member stays on the grid
+    return synth.to_bf16_bits(g.choice([0, 1, -1, 2, -2, 3, -3, 4, -4, 6, -6], shape).astype(np.float32))
+
+
+@pytest.mark.parametrize("wfmt", [mx.E4M3, mx.E2M1])
+def test_layer_equals_dense_brute_force_bitexact(wfmt):
+    # integers in [-8, 8] are exact in E4M3 under any block scale (and the E2M1 set above in
+    # E2M1), so every product and sum is exact and the two paths round h and y identically
     g = np.random.default_rng(0)
     T, H, E, k, I = 24, 64, 6, 2, 64
     x = _int_bits(g, (T, H))
     logits = g.standard_normal((T, E)).astype(np.float32)
-    w1 = _int_bits(g, (E, 2 * I, H))
-    w2 = _int_bits(g, (E, H, I))
-    res = ep_mx.ep_layer_mx(x, logits, w1, w2, k, E, 3, T * k)
-    dense64, dense_bits = ep_mx.ep_layer_mx_dense(x, logits, w1, w2, k)
+    wbits = _int_bits if wfmt == mx.E4M3 else _e2m1_int_bits
+    w1 = wbits(g, (E, 2 * I, H))
+    w2 = wbits(g, (E, H, I))
+    res = ep_mx.ep_layer_mx(x, logits, w1, w2, k, E, 3, T * k, wfmt=wfmt)
+    dense64, dense_bits = ep_mx.ep_layer_mx_dense(x, logits, w1, w2, k, wfmt=wfmt)
     assert res["status"] == ep.STATUS_OK
     assert np.array_equal(res["out_bits"], dense_bits)
     assert np.array_equal(res["out64"], dense64)
@@ -53,13 +62,19 @@ def test_quantized_layer_is_within_the_format_error_of_the_bf16_layer():
     cfg = synth.EP_TINY
     inp = synth.ep_inputs(cfg, 0)
     ref = ep.ep_layer(inp["x"], inp["logits"], inp["w1"], inp["w2"], cfg.k, cfg.E, cfg.W, cap=cfg.T * cfg.k)
-    q = ep_mx.ep_layer_mx(inp["x"], inp["logits"], inp["w1"], inp["w2"], cfg.k, cfg.E, cfg.W, cfg.T * cfg.k)
-    a, b = q["out64"], ref["out64"]
-    rl2 = np.linalg.norm(a - b) / np.linalg.norm(b)
+    rl2 = {}
+    for wfmt in (mx.E4M3, mx.E2M1):
+        q = ep_mx.ep_layer_mx(inp["x"], inp["logits"], inp["w1"], inp["w2"], cfg.k, cfg.E, cfg.W, cfg.T * cfg.k,
+                              wfmt=wfmt)
+        a, b = q["out64"], ref["out64"]
+        rl2[wfmt] = np.linalg.norm(a - b) / np.linalg.norm(b)
     # E4M3 keeps 3 mantissa bits: each quantized operand carries a relative rounding error of
     # up to 2^-4 (about 2^-4 / sqrt(3) rms); x, W1, h and W2 are quantized, so the output's
     # relative error is a few percent, and clearly nonzero
-    assert 0.005 < rl2 < 0.12, rl2
+    assert 0.005 < rl2[mx.E4M3] < 0.12, rl2
+    # E2M1 weights keep 1 mantissa bit (steps of up to 2^-2 relative, and values below a
+    # twelfth of the block maximum flush to 0 or 0.5 steps): a larger error, still bounded
+    assert 2 * rl2[mx.E4M3] < rl2[mx.E2M1] < 0.5, rl2
 
 
 def test_h_is_the_quantized_swiglu_output():
