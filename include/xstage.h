@@ -147,8 +147,11 @@ int xs_dispatch_rows(const void* rows, int64_t row_stride, int32_t row_bytes, in
  *                  I / 32 scales (h_ws: [h_rows][I + I / 32] bytes); Linear-2 likewise, its
  *                  output y rounded to bf16 for the unchanged combine. Requires H and I
  *                  multiples of 512. Only xs_fused_ep_layer takes it (the unfused phase calls
- *                  return XS_EUNSUPPORTED). */
-enum { XS_PREC_BF16 = 0, XS_PREC_MXFP8 = 1 };
+ *                  return XS_EUNSUPPORTED).
+ *   XS_PREC_W4A8   as XS_PREC_MXFP8 with E2M1 weights: w1 / w2 hold packed E2M1 codes
+ *                  ([n_experts][2I][H / 2] and [n_experts][H][I / 2] bytes, element 2 i in the
+ *                  low nibble) under the same E8M0 scales; token rows and h stay MXFP8. */
+enum { XS_PREC_BF16 = 0, XS_PREC_MXFP8 = 1, XS_PREC_W4A8 = 2 };
 
 typedef struct xs_ep_layer {
   int32_t n_src, T, H, E, k, I, W;
@@ -177,10 +180,10 @@ typedef struct xs_ep_layer {
   void* out;                  /* device bf16 [T][H], combined output of source `src` */
   void* events[8];            /* optional hipEvent_t per phase boundary (NULL = not recorded),
                                  recorded on `stream`; see XS_EV_* */
-  int32_t precision;          /* XS_PREC_BF16 (0) or XS_PREC_MXFP8 */
+  int32_t precision;          /* XS_PREC_BF16 (0), XS_PREC_MXFP8 or XS_PREC_W4A8 */
   int32_t reserved;           /* 0 */
-  const void* w1_scale;       /* XS_PREC_MXFP8: device E8M0 [n_experts][2I][H / 32] */
-  const void* w2_scale;       /* XS_PREC_MXFP8: device E8M0 [n_experts][H][I / 32] */
+  const void* w1_scale;       /* MX precisions: device E8M0 [n_experts][2I][H / 32] */
+  const void* w2_scale;       /* MX precisions: device E8M0 [n_experts][H][I / 32] */
 } xs_ep_layer;
 
 /* Phase boundaries of the EP entry points: events[XS_EV_x] is recorded right before the
@@ -398,12 +401,12 @@ int xs_quantize_mx(const void* x, int64_t rows, int32_t cols, int64_t ldx, int32
                    void* codes, int64_t ld_codes, void* scales, int64_t ld_scales, void* stream);
 
 /* MX GEMM: c (bf16 [M][N], ldc elements) = deq(a) deq(b)^T with a E4M3 codes [M][K] (lda
- * bytes per row) and scales [M][K / 32] (lda_s bytes per row), b codes [N][K] in b_fmt
- * (ldb bytes per row) and scales [N][K / 32] (ldb_s). fp32 accumulation on
- * v_mfma_scale_f32_32x32x64_f8f6f4, one bf16 rounding at the end. N a multiple of 256, K of
- * 128; code rows 16-byte aligned, scale rows 4-byte aligned. b_fmt XS_FMT_E2M1 is not yet
- * supported (XS_EUNSUPPORTED). XS_EINVAL / XS_EUNSUPPORTED on bad arguments (nothing
- * launched), XS_EHIP if the launch fails. */
+ * bytes per row) and scales [M][K / 32] (lda_s bytes per row), b codes in b_fmt, [N][K]
+ * bytes (E4M3) or [N][K / 2] packed (E2M1, ldb >= K / 2), ldb bytes per row, and scales
+ * [N][K / 32] (ldb_s). fp32 accumulation on v_mfma_scale_f32_32x32x64_f8f6f4, one bf16
+ * rounding at the end. N a multiple of 256, K of 128; code rows 16-byte aligned, scale rows
+ * 4-byte aligned. XS_EINVAL / XS_EUNSUPPORTED on bad arguments (nothing launched), XS_EHIP
+ * if the launch fails. */
 int xs_gemm_mx(const void* a, int64_t lda, const void* a_scales, int64_t lda_s, const void* b,
                int64_t ldb, const void* b_scales, int64_t ldb_s, int32_t b_fmt, void* c,
                int64_t ldc, int32_t M, int32_t N, int32_t K, const xs_trace* trace, void* stream);

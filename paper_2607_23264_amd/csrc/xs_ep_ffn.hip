@@ -261,9 +261,11 @@ __device__ __forceinline__ int xcd_instance_ep(int b, int G) {
   return (G % 8) ? b : (b % 8) * (G / 8) + b / 8;
 }
 
-// MXFP8 tiles (256 threads, the MX core). Linear-1: the dispatch window rows hold H codes
-// then H / 32 scales; the SwiGLU output is quantized in the epilogue into h rows of I codes
-// then I / 32 scales (this tile's 128 columns: codes at 128 nt, scales at I + 4 nt).
+// MX tiles (256 threads, the MX core); BF4: the weights are packed E2M1 (W4A8), else E4M3.
+// Linear-1: the dispatch window rows hold H codes then H / 32 scales; the SwiGLU output is
+// quantized in the epilogue into h rows of I codes then I / 32 scales (this tile's 128
+// columns: codes at 128 nt, scales at I + 4 nt).
+template <bool BF4>
 __device__ __forceinline__ void ep_l1_tile_mx(const EpArgs& a, int p, int nt, bool fused, char* lds,
                                               char** rowptr) {
   const int tid = threadIdx.x;
@@ -277,10 +279,12 @@ __device__ __forceinline__ void ep_l1_tile_mx(const EpArgs& a, int p, int nt, bo
   const uint8_t* A = reinterpret_cast<const uint8_t*>(a.dwin.base[dl] +
                                                       static_cast<int64_t>(a.expert_offsets[e] + m0) * ws);
   const int64_t wrows = static_cast<int64_t>(x) * 2 * a.I;
-  const uint8_t* B = reinterpret_cast<const uint8_t*>(a.w1) + wrows * a.H;
+  const int64_t ldb = BF4 ? a.H / 2 : a.H;
+  const uint8_t* B = reinterpret_cast<const uint8_t*>(a.w1) + wrows * ldb;
   const uint8_t* Bs = a.w1s + wrows * (a.H / 32);
   AccMx acc;
-  gemm_mainloop_mx(A, ws, A + a.H, ws, rows, B, a.H, Bs, a.H / 32, nt * (kBN / 2), a.I, true, a.H, acc, lds);
+  gemm_mainloop_mx<BF4>(A, ws, A + a.H, ws, rows, B, ldb, Bs, a.H / 32, nt * (kBN / 2), a.I, true, a.H, acc,
+                        lds);
   const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
   if (tid < rows)
     rowptr[tid] = reinterpret_cast<char*>(a.h) + static_cast<int64_t>(a.exp_hrow[x] + m0 + tid) * a.h_stride;
@@ -315,6 +319,7 @@ __device__ __forceinline__ void ep_l1_tile_mx(const EpArgs& a, int p, int nt, bo
 }
 
 // Linear-2 on MXFP8 h rows; bf16 output rows into the combine windows as in the bf16 tile.
+template <bool BF4>
 __device__ __forceinline__ void ep_l2_tile_mx(const EpArgs& a, int p, int nt, bool fused, char* lds,
                                               char** rowptr, int* flag) {
   const int tid = threadIdx.x;
@@ -326,14 +331,16 @@ __device__ __forceinline__ void ep_l2_tile_mx(const EpArgs& a, int p, int nt, bo
   const int rows = min(kBM, a.exp_m[x] - m0);
   const uint8_t* A = reinterpret_cast<const uint8_t*>(a.h) + static_cast<int64_t>(a.exp_hrow[x] + m0) * a.h_stride;
   const int64_t wrows = static_cast<int64_t>(x) * a.H;
-  const uint8_t* B = reinterpret_cast<const uint8_t*>(a.w2) + wrows * a.I;
+  const int64_t ldb = BF4 ? a.I / 2 : a.I;
+  const uint8_t* B = reinterpret_cast<const uint8_t*>(a.w2) + wrows * ldb;
   const uint8_t* Bs = a.w2s + wrows * (a.I / 32);
   const int n0 = nt * kBN;
   int code = -1;
   if (a.l2_combine && tid < rows)
     code = a.row_src[static_cast<int64_t>(e / a.epw) * a.cap + a.expert_offsets[e] + m0 + tid];
   AccMx acc;
-  gemm_mainloop_mx(A, a.h_stride, A + a.I, a.h_stride, rows, B, a.I, Bs, a.I / 32, n0, 0, false, a.I, acc, lds);
+  gemm_mainloop_mx<BF4>(A, a.h_stride, A + a.I, a.h_stride, rows, B, ldb, Bs, a.I / 32, n0, 0, false, a.I, acc,
+                        lds);
   const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
   if (tid < rows) {
     char* ptr = nullptr;
@@ -365,16 +372,16 @@ __device__ __forceinline__ void ep_l2_tile_mx(const EpArgs& a, int p, int nt, bo
   if (a.gap_ticks) __syncthreads();
 }
 
-// Tile dispatch by precision (PREC 0: bf16, 1: MXFP8).
+// Tile dispatch by precision (PREC 0: bf16, 1: MXFP8, 2: W4A8).
 template <int PREC>
 __device__ __forceinline__ void l1_tile(const EpArgs& a, int p, int nt, bool fused, char* lds, char** rowptr) {
-  if constexpr (PREC == 1) ep_l1_tile_mx(a, p, nt, fused, lds, rowptr);
+  if constexpr (PREC > 0) ep_l1_tile_mx<PREC == 2>(a, p, nt, fused, lds, rowptr);
   else ep_l1_tile(a, p, nt, fused, lds, rowptr);
 }
 template <int PREC>
 __device__ __forceinline__ void l2_tile(const EpArgs& a, int p, int nt, bool fused, char* lds, char** rowptr,
                                         int* flag) {
-  if constexpr (PREC == 1) ep_l2_tile_mx(a, p, nt, fused, lds, rowptr, flag);
+  if constexpr (PREC > 0) ep_l2_tile_mx<PREC == 2>(a, p, nt, fused, lds, rowptr, flag);
   else ep_l2_tile(a, p, nt, fused, lds, rowptr, flag);
 }
 
@@ -531,6 +538,13 @@ __global__ __launch_bounds__(kMxThreads, 1) void ep_ffn_mx_kernel(EpArgs a) {
   ep_ffn_body<MODE, 1>(a, smem);
 }
 
+// The same with E2M1 weights (W4A8).
+template <int MODE>
+__global__ __launch_bounds__(kMxThreads, 1) void ep_ffn_w4a8_kernel(EpArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
+  ep_ffn_body<MODE, 2>(a, smem);
+}
+
 // Prefix of the rows each computed window holds (rows past capacity were never stored).
 __device__ __forceinline__ int window_prefix(const EpArgs& a, const int* dest_counts, int n_cwin,
                                              int* base) {
@@ -619,7 +633,7 @@ struct EpWorkspace {
   int64_t max_rows;
 };
 
-bool is_mx(const xs_ep_layer* L) { return L->precision == XS_PREC_MXFP8; }
+bool is_mx(const xs_ep_layer* L) { return L->precision == XS_PREC_MXFP8 || L->precision == XS_PREC_W4A8; }
 
 // Bytes of one dispatched token row and of one h row.
 int64_t token_row_bytes(const xs_ep_layer* L) {
@@ -673,7 +687,8 @@ int validate(const xs_ep_layer* L, bool need_out) {
     return XS_EINVAL;
   if (need_out && (!L->x || !L->logits || !L->out)) return XS_EINVAL;
   if (L->expert_mode != XS_EXPERT_SWIGLU && L->expert_mode != XS_EXPERT_IDENTITY) return XS_EINVAL;
-  if (L->precision != XS_PREC_BF16 && L->precision != XS_PREC_MXFP8) return XS_EINVAL;
+  if (L->precision != XS_PREC_BF16 && L->precision != XS_PREC_MXFP8 && L->precision != XS_PREC_W4A8)
+    return XS_EINVAL;
   if (L->reserved != 0) return XS_EINVAL;
   if (is_mx(L)) {
     if (L->expert_mode != XS_EXPERT_SWIGLU) return XS_EUNSUPPORTED;
@@ -819,7 +834,9 @@ static int run_ffn(const xs_ep_layer* L, const EpArgs& base, int mode, int l2_co
   a.gap_ticks = pc ? xs_host::ns_to_ticks(pc->gap_ns) : 0;
   const int64_t tmo_us = pc && pc->spin_timeout_us > 0 ? pc->spin_timeout_us : 2000000;
   a.timeout_ticks = xs_host::ns_to_ticks(tmo_us * 1000);
-  if (is_mx(L))
+  if (L->precision == XS_PREC_W4A8)
+    hipLaunchKernelGGL(ep_ffn_w4a8_kernel<3>, dim3(grid), dim3(kMxThreads), 0, st, a);
+  else if (is_mx(L))
     hipLaunchKernelGGL(ep_ffn_mx_kernel<3>, dim3(grid), dim3(kMxThreads), 0, st, a);
   else if (mode == 1)
     hipLaunchKernelGGL(ep_ffn_kernel<1>, dim3(grid), dim3(kThreads), 0, st, a);

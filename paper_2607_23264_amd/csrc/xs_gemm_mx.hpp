@@ -17,10 +17,16 @@
 //
 // Operand layout of the scaled MFMA (measured on gfx950): lane 32 h + i holds row i's K
 // elements [16 h, 16 h + 16) in bytes 0..15 and [32 + 16 h, 48 + 16 h) in bytes 16..31 of its
-// eight dwords, and the scale of K block b (32 elements) of row i comes from lane 32 b + i, in
+// eight dwords (an fp4 operand: elements [32 h, 32 h + 32), two per byte, in the first four
+// dwords), and the scale of K block b (32 elements) of row i comes from lane 32 b + i, in
 // the byte op_sel names. Sub-step kk of a stage (K elements [64 kk, 64 kk + 64)) reads pieces
-// 4 kk + h and 4 kk + 2 + h of the row; a lane's scale word for the stage holds the row's four
-// block scales, and one byte permute puts the scale of block 2 kk + h into byte kk.
+// 4 kk + h and 4 kk + 2 + h of an fp8 row, or piece 2 kk + h of an fp4 row; a lane's scale
+// word for the stage holds the row's four block scales, and one byte permute puts the scale
+// of block 2 kk + h into byte kk.
+//
+// B may be E2M1 (W4A8): its tile rows are then 64 bytes per stage (four 16-byte pieces,
+// piece c at c ^ ((row >> 2) & 3), so the 16 rows of each ds_read_b128 phase hit 16 distinct
+// bank groups) in the first half of the B area; the MFMA rate is that of fp8.
 #pragma once
 #include <type_traits>
 
@@ -44,78 +50,30 @@ struct MxTile {
   const char* sb;         // B scale base
   uint32_t oa[8], ob[8];  // per-lane byte offsets of the eight direct loads of each operand
   uint32_t sao, sbo;      // per-lane byte offsets of the scale rows this lane loads
-  int arow, brow;         // LDS byte offsets of this lane's fragment rows
+  int ar, br;             // this lane's fragment rows in the A and B tiles
+  int arow, brow;         // their LDS byte offsets within an operand tile
   int w;
 };
 
-template <int NI>
+template <int NI, bool BF4>
 __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& acc, char* lds) {
   const int lane = threadIdx.x & 63;
   const int w = t.w;
-  const int swz = (lane >> 1) & 7;
+  const int swz = (lane >> 1) & 7;          // fp8 rows: 8 pieces, piece c at c ^ ((row >> 1) & 7)
+  const int swz4 = (lane >> 2) & 3;         // fp4 rows: 4 pieces, piece c at c ^ ((row >> 2) & 3)
   const int h = lane >> 5;
   const uint32_t sel = h ? 0x0C0C0301u : 0x0C0C0200u;
+  // B as E2M1 (BF4): 64-byte tile rows per stage (four direct loads per wave instead of
+  // eight), one 16-byte fragment read per sub-step, and the MFMA told its first operand is fp4
+  constexpr int kBLoads = BF4 ? 4 : 8;
+  constexpr int kLoads = 10 + kBLoads;                 // direct loads per wave and stage
+  constexpr uint32_t kBStep = BF4 ? 64u : 128u;        // B bytes per row and stage
+  constexpr int kBRow = BF4 ? 64 : 128;                // B tile row pitch in LDS
+  constexpr int kFmtB = BF4 ? 4 : 0;
   // Addresses are the uniform base plus a 32-bit per-lane offset that includes the stage
   // (a 32-bit sum that may wrap is not folded into loop-invariant 64-bit per-lane pointers,
   // which would cost two registers per load): the loads keep the scalar-base + vector-offset
-  // form.
-  auto issue = [&](int kt) {
-    char* st = lds + (kt & 1) * kMxStage;
-    const uint32_t k0 = static_cast<uint32_t>(kt) * 128u, k4 = static_cast<uint32_t>(kt) * 4u;
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      __builtin_amdgcn_global_load_lds((glob_void*)(t.a + (t.oa[i] + k0)), (lds_void*)(st + (4 * i + w) * 1024),
-                                       16, 0, 0);
-    __builtin_amdgcn_global_load_lds((glob_void*)(t.sa + (t.sao + k4)), (lds_void*)(st + kMxScaleOff + w * 256),
-                                     4, 0, 0);
-    __builtin_amdgcn_global_load_lds((glob_void*)(t.sb + (t.sbo + k4)),
-                                     (lds_void*)(st + kMxScaleOff + 1024 + w * 256), 4, 0, 0);
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      __builtin_amdgcn_global_load_lds((glob_void*)(t.b + (t.ob[i] + k0)),
-                                       (lds_void*)(st + kOpBytes + (4 * i + w) * 1024), 16, 0, 0);
-  };
-  uint32_t sw[8];         // a stage's scale words as read: A blocks 0..3, B blocks 0..3
-  int sc[8];              // the same, byte kk = scale of K block 2 kk + h (the MFMA's op_sel)
-  auto read_s = [&](const char* st) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      sw[i] = *reinterpret_cast<const uint32_t*>(st + kMxScaleOff + (t.arow >> 7) * 4 + i * 128);
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      sw[4 + j] = *reinterpret_cast<const uint32_t*>(st + kMxScaleOff + 1024 + (t.brow >> 7) * 4 + j * 128);
-  };
-  auto perm_s = [&]() {
-#pragma unroll
-    for (int n = 0; n < 8; ++n) sc[n] = static_cast<int>(__builtin_amdgcn_perm(sw[n], sw[n], sel));
-  };
-  // fragments of sub-step 0 (K elements [0, 64) of a stage) and of sub-step 1 ([64, 128))
-  v8i_t a0[4], b0[4], a1[4], b1[4];
-  auto frag = [&](const char* base, int row_off, int kk) {
-    const v4i_t lo = *reinterpret_cast<const v4i_t*>(base + row_off + (((4 * kk + h) ^ swz) << 4));
-    const v4i_t hi = *reinterpret_cast<const v4i_t*>(base + row_off + (((4 * kk + 2 + h) ^ swz) << 4));
-    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-  };
-  auto read_frags = [&](const char* st, int kk, v8i_t (&a)[4], v8i_t (&b)[4]) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) b[j] = frag(st + kOpBytes, t.brow + j * 32 * 128, kk);
-#pragma unroll
-    for (int i = 0; i < NI; ++i) a[i] = frag(st, t.arow + i * 32 * 128, kk);
-  };
-  constexpr int kMfma = 4 * NI;             // MFMAs per sub-step
-  // One stage. The schedule is fixed by hand, one MFMA and what follows it per fenced group
-  // (left alone, the compiler sinks every MFMA of the stage below the barrier, leaves the
-  // fragment reads exposed and issues the global loads in one burst):
-  //   A: sub-step 0's MFMAs, the first eight each followed by one fragment read (two
-  //     ds_read_b128) of sub-step 1;
-  //   barrier: this wave's reads of the stage are done and the next stage has landed in every
-  //     wave's share;
-  //   B: sub-step 1's MFMAs, each followed by two global loads of the stage after next (into
-  //     this stage's buffers, which no wave reads any more) and one read of the next stage's
-  //     scale words or sub-step-0 fragments.
-  // NEXT: a stage follows; ISSUE: the stage after next exists. Compile-time, so the steady
-  // loop body has no branches.
-  // one direct load n of stage kt: 0..7 A pieces, 8 / 9 A / B scale words, 10..17 B pieces
+  // form. Direct load n of stage kt: 0..7 A pieces, 8 / 9 A / B scale words, 10.. B pieces.
   auto issue_one = [&](int kt, int n) {
     char* st = lds + (kt & 1) * kMxStage;
     const uint32_t k0 = static_cast<uint32_t>(kt) * 128u, k4 = static_cast<uint32_t>(kt) * 4u;
@@ -129,9 +87,63 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
       __builtin_amdgcn_global_load_lds((glob_void*)(t.sb + (t.sbo + k4)),
                                        (lds_void*)(st + kMxScaleOff + 1024 + w * 256), 4, 0, 0);
     else
-      __builtin_amdgcn_global_load_lds((glob_void*)(t.b + (t.ob[n - 10] + k0)),
+      __builtin_amdgcn_global_load_lds((glob_void*)(t.b + (t.ob[n - 10] + static_cast<uint32_t>(kt) * kBStep)),
                                        (lds_void*)(st + kOpBytes + (4 * (n - 10) + w) * 1024), 16, 0, 0);
   };
+  auto issue = [&](int kt) {
+#pragma unroll
+    for (int n = 0; n < kLoads; ++n) issue_one(kt, n);
+  };
+  uint32_t sw[8];         // a stage's scale words as read: A blocks 0..3, B blocks 0..3
+  int sc[8];              // the same, byte kk = scale of K block 2 kk + h (the MFMA's op_sel)
+  auto read_s = [&](const char* st) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      sw[i] = *reinterpret_cast<const uint32_t*>(st + kMxScaleOff + t.ar * 4 + i * 128);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      sw[4 + j] = *reinterpret_cast<const uint32_t*>(st + kMxScaleOff + 1024 + t.br * 4 + j * 128);
+  };
+  auto perm_s = [&]() {
+#pragma unroll
+    for (int n = 0; n < 8; ++n) sc[n] = static_cast<int>(__builtin_amdgcn_perm(sw[n], sw[n], sel));
+  };
+  // fragments of sub-step 0 (K elements [0, 64) of a stage) and of sub-step 1 ([64, 128))
+  v8i_t a0[4], b0[4], a1[4], b1[4];
+  auto frag = [&](const char* base, int row_off, int kk) {
+    const v4i_t lo = *reinterpret_cast<const v4i_t*>(base + row_off + (((4 * kk + h) ^ swz) << 4));
+    const v4i_t hi = *reinterpret_cast<const v4i_t*>(base + row_off + (((4 * kk + 2 + h) ^ swz) << 4));
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  };
+  // B fragment j of sub-step kk: an fp4 operand is 32 codes (16 bytes) per lane, in the low
+  // four registers (the MFMA ignores the upper four)
+  auto frag_b = [&](const char* st, int j, int kk) {
+    if constexpr (BF4) {
+      const char* base = st + kOpBytes + t.brow + j * 32 * kBRow;
+      const v4i_t v = *reinterpret_cast<const v4i_t*>(base + (((2 * kk + h) ^ swz4) << 4));
+      return __builtin_shufflevector(v, v, 0, 1, 2, 3, -1, -1, -1, -1);
+    } else {
+      return frag(st + kOpBytes, t.brow + j * 32 * kBRow, kk);
+    }
+  };
+  auto read_frags = [&](const char* st, int kk, v8i_t (&a)[4], v8i_t (&b)[4]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) b[j] = frag_b(st, j, kk);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) a[i] = frag(st, t.arow + i * 32 * 128, kk);
+  };
+  constexpr int kMfma = 4 * NI;             // MFMAs per sub-step
+  // One stage. The schedule is fixed by hand, one MFMA and what follows it per fenced group
+  // (left alone, the compiler sinks every MFMA of the stage below the barrier, leaves the
+  // fragment reads exposed and issues the global loads in one burst):
+  //   A: sub-step 0's MFMAs, the first eight each followed by one fragment read of sub-step 1;
+  //   barrier: this wave's reads of the stage are done and the next stage has landed in every
+  //     wave's share;
+  //   B: sub-step 1's MFMAs, each followed by two global loads of the stage after next (into
+  //     this stage's buffers, which no wave reads any more) and one read of the next stage's
+  //     scale words or sub-step-0 fragments.
+  // NEXT: a stage follows; ISSUE: the stage after next exists. Compile-time, so the steady
+  // loop body has no branches.
   auto stage = [&](int kt, auto next_c, auto issue_c) {
     constexpr bool kNext = decltype(next_c)::value;
     constexpr bool kIssue = decltype(issue_c)::value;
@@ -142,15 +154,15 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
 #pragma unroll
       for (int g = 0; g < kMfma; ++g) {
         const int i = g >> 2, j = g & 3;   // B fragment first: a lane's accumulators hold 4 columns
-        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b0[j], a0[i], acc[i][j], 0, 0, 0, sc[4 + j],
-                                                                    0, sc[i]);
-        if (g < 4) b1[g] = frag(st + kOpBytes, t.brow + g * 32 * 128, 1);
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b0[j], a0[i], acc[i][j], kFmtB, 0, 0,
+                                                                    sc[4 + j], 0, sc[i]);
+        if (g < 4) b1[g] = frag_b(st, g, 1);
         else if (g - 4 < NI) a1[g - 4] = frag(st, t.arow + (g - 4) * 32 * 128, 1);
         __builtin_amdgcn_sched_barrier(0);
       }
 #pragma unroll
       for (int r = kMfma; r < 4 + NI; ++r) {   // reads left over when there are few MFMAs
-        if (r < 4) b1[r] = frag(st + kOpBytes, t.brow + r * 32 * 128, 1);
+        if (r < 4) b1[r] = frag_b(st, r, 1);
         else a1[r - 4] = frag(st, t.arow + (r - 4) * 32 * 128, 1);
       }
     }
@@ -164,15 +176,15 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
 #pragma unroll
       for (int g = 0; g < kMfma; ++g) {
         const int i = g >> 2, j = g & 3;
-        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b1[j], a1[i], acc[i][j], 0, 0, 1, sc[4 + j],
-                                                                    1, sc[i]);
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b1[j], a1[i], acc[i][j], kFmtB, 0, 1,
+                                                                    sc[4 + j], 1, sc[i]);
         if constexpr (kIssue) {
-          if (2 * g < 18) issue_one(kt + 2, 2 * g);
-          if (2 * g + 1 < 18) issue_one(kt + 2, 2 * g + 1);
+          if (2 * g < kLoads) issue_one(kt + 2, 2 * g);
+          if (2 * g + 1 < kLoads) issue_one(kt + 2, 2 * g + 1);
         }
         if constexpr (kNext) {
           if (g == 0) read_s(nx);
-          else if (g - 1 < 4) b0[g - 1] = frag(nx + kOpBytes, t.brow + (g - 1) * 32 * 128, 0);
+          else if (g - 1 < 4) b0[g - 1] = frag_b(nx, g - 1, 0);
           else if (g - 5 < NI) a0[g - 5] = frag(nx, t.arow + (g - 5) * 32 * 128, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
@@ -180,13 +192,13 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
       // what did not fit beside the MFMAs
       if constexpr (kIssue) {
 #pragma unroll
-        for (int n = 2 * kMfma; n < 18; ++n) issue_one(kt + 2, n);
+        for (int n = 2 * kMfma; n < kLoads; ++n) issue_one(kt + 2, n);
       }
       if constexpr (kNext) {
 #pragma unroll
         for (int r = kMfma; r < 5 + NI; ++r) {
           if (r == 0) read_s(nx);
-          else if (r - 1 < 4) b0[r - 1] = frag(nx + kOpBytes, t.brow + (r - 1) * 32 * 128, 0);
+          else if (r - 1 < 4) b0[r - 1] = frag_b(nx, r - 1, 0);
           else a0[r - 5] = frag(nx, t.arow + (r - 5) * 32 * 128, 0);
         }
       }
@@ -217,12 +229,15 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
   stage(kt, no, no);
 }
 
-// acc = deq(A)[0:256, 0:K] deq(B)[rows(0:256), 0:K]^T. A / B: E4M3 code rows (lda / ldb bytes
-// apart, 16-byte aligned), As / Bs: E8M0 scale rows ([K / 32] bytes, lda_s / ldb_s apart,
-// 4-byte aligned). K a multiple of 128. B rows map through b_row_map (SwiGLU interleave).
-// Rows of A at or beyond a_rows read row a_rows - 1; a wave skips the MFMAs of 32-row blocks
-// past a_rows. Ends with a block barrier. Accumulator acc[i][j][q] is output
+// acc = deq(A)[0:256, 0:K] deq(B)[rows(0:256), 0:K]^T. A: E4M3 code rows (lda bytes apart,
+// 16-byte aligned); B: E4M3 code rows, or with BF4 E2M1 codes packed two per byte (low nibble
+// first, K / 2 bytes per row), ldb bytes apart, 16-byte aligned; As / Bs: E8M0 scale rows
+// ([K / 32] bytes, lda_s / ldb_s apart, 4-byte aligned). K a multiple of 128. B rows map
+// through b_row_map (SwiGLU interleave). Rows of A at or beyond a_rows read row a_rows - 1; a
+// wave skips the MFMAs of 32-row blocks past a_rows. Ends with a block barrier. Accumulator
+// acc[i][j][q] is output
 //   row wm*128 + 32 i + lane % 32, column wn*128 + 32 j + 8 (q / 4) + 4 (lane / 32) + q % 4.
+template <bool BF4 = false>
 __device__ __forceinline__ void gemm_mainloop_mx(const uint8_t* __restrict__ A, int64_t lda,
                                                  const uint8_t* __restrict__ As, int64_t lda_s,
                                                  int a_rows, const uint8_t* __restrict__ B,
@@ -238,6 +253,8 @@ __device__ __forceinline__ void gemm_mainloop_mx(const uint8_t* __restrict__ A, 
   t.sa = reinterpret_cast<const char*>(As);
   t.sb = reinterpret_cast<const char*>(Bs);
   t.w = w;
+  // fp8 rows: instruction i of wave w fills rows 32 i + 8 w .. + 7, lane -> (row lane / 8,
+  // physical piece lane % 8) holding logical piece (lane % 8) ^ ((row >> 1) & 7)
   const int lr = lane >> 3, lp = lane & 7;
   const int c16 = (lp ^ ((4 * w + (lr >> 1)) & 7)) * 16;
 #pragma unroll
@@ -245,13 +262,25 @@ __device__ __forceinline__ void gemm_mainloop_mx(const uint8_t* __restrict__ A, 
     const int r = 32 * i + 8 * w + lr;
     const int ar = r < a_rows ? r : a_rows - 1;
     t.oa[i] = static_cast<uint32_t>(ar * lda + c16);
-    t.ob[i] = static_cast<uint32_t>(b_row_map(r, b_n0, b_half, swiglu) * ldb + c16);
+    if constexpr (!BF4) t.ob[i] = static_cast<uint32_t>(b_row_map(r, b_n0, b_half, swiglu) * ldb + c16);
+  }
+  if constexpr (BF4) {
+    // fp4 rows (64 bytes): instruction i of wave w fills rows 16 (4 i + w) .. + 15, lane ->
+    // (row lane / 4, physical piece lane % 4) holding logical piece (lane % 4) ^ ((row >> 2) & 3)
+    const int c4 = ((lane & 3) ^ ((lane >> 4) & 3)) * 16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 16 * (4 * i + w) + (lane >> 2);
+      t.ob[i] = static_cast<uint32_t>(b_row_map(r, b_n0, b_half, swiglu) * ldb + c4);
+    }
   }
   const int rs = 64 * w + lane;            // the scale row this lane loads
   t.sao = static_cast<uint32_t>((rs < a_rows ? rs : a_rows - 1) * lda_s);
   t.sbo = static_cast<uint32_t>(b_row_map(rs, b_n0, b_half, swiglu) * ldb_s);
-  t.arow = (wm * 128 + (lane & 31)) * 128;
-  t.brow = (wn * 128 + (lane & 31)) * 128;
+  t.ar = wm * 128 + (lane & 31);
+  t.br = wn * 128 + (lane & 31);
+  t.arow = t.ar * 128;
+  t.brow = t.br * (BF4 ? 64 : 128);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -262,11 +291,11 @@ __device__ __forceinline__ void gemm_mainloop_mx(const uint8_t* __restrict__ A, 
   const int valid = a_rows - wm * 128;
   const int ni = valid >= 128 ? 4 : (valid <= 0 ? 0 : (valid + 31) >> 5);
   switch (__builtin_amdgcn_readfirstlane(ni)) {
-    case 4: mainloop_mx_ni<4>(t, nk, acc, lds); break;
-    case 3: mainloop_mx_ni<3>(t, nk, acc, lds); break;
-    case 2: mainloop_mx_ni<2>(t, nk, acc, lds); break;
-    case 1: mainloop_mx_ni<1>(t, nk, acc, lds); break;
-    default: mainloop_mx_ni<0>(t, nk, acc, lds); break;
+    case 4: mainloop_mx_ni<4, BF4>(t, nk, acc, lds); break;
+    case 3: mainloop_mx_ni<3, BF4>(t, nk, acc, lds); break;
+    case 2: mainloop_mx_ni<2, BF4>(t, nk, acc, lds); break;
+    case 1: mainloop_mx_ni<1, BF4>(t, nk, acc, lds); break;
+    default: mainloop_mx_ni<0, BF4>(t, nk, acc, lds); break;
   }
   __syncthreads();
 }

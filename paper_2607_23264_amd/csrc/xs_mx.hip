@@ -97,7 +97,9 @@ __global__ __launch_bounds__(256) void quantize_kernel(const uint16_t* __restric
   }
 }
 
-// Plain MXFP8 GEMM, persistent over 256 x 256 output tiles: C (bf16) = deq(A) deq(B)^T.
+// Plain MX GEMM, persistent over 256 x 256 output tiles: C (bf16) = deq(A) deq(B)^T; A E4M3,
+// B E4M3 or (BF4) packed E2M1.
+template <bool BF4>
 __global__ __launch_bounds__(kMxThreads, 1) void gemm_mx_kernel(
     const uint8_t* __restrict__ A, int64_t lda, const uint8_t* __restrict__ As, int64_t lda_s,
     const uint8_t* __restrict__ B, int64_t ldb, const uint8_t* __restrict__ Bs, int64_t ldb_s,
@@ -113,8 +115,8 @@ __global__ __launch_bounds__(kMxThreads, 1) void gemm_mx_kernel(
     const int rows = min(kBM, M - m0);
     const uint64_t t0 = tr.buf ? wall_ticks() : 0;
     AccMx acc;
-    gemm_mainloop_mx(A + static_cast<int64_t>(m0) * lda, lda, As + static_cast<int64_t>(m0) * lda_s, lda_s,
-                     rows, B, ldb, Bs, ldb_s, n0, 0, false, K, acc, lds);
+    gemm_mainloop_mx<BF4>(A + static_cast<int64_t>(m0) * lda, lda, As + static_cast<int64_t>(m0) * lda_s,
+                          lda_s, rows, B, ldb, Bs, ldb_s, n0, 0, false, K, acc, lds);
     const uint64_t t1 = tr.buf ? wall_ticks() : 0;
     if (tid < rows) rowptr[tid] = C + static_cast<int64_t>(m0 + tid) * ldc_bytes + static_cast<int64_t>(n0) * 2;
     stage_tile_mx(acc, lds);
@@ -177,8 +179,8 @@ extern "C" int xs_gemm_mx(const void* a, int64_t lda, const void* a_scales, int6
                           const xs_trace* trace, void* stream) {
   if (!a || !a_scales || !b || !b_scales || !c || M < 0 || N <= 0 || K <= 0) return XS_EINVAL;
   if (b_fmt != XS_FMT_E4M3 && b_fmt != XS_FMT_E2M1) return XS_EINVAL;
-  if (b_fmt != XS_FMT_E4M3) return XS_EUNSUPPORTED;
-  if (N % kBN || K % 128 || lda < K || ldb < K || lda % 16 || ldb % 16 || lda_s < K / 32 ||
+  const bool bf4 = b_fmt == XS_FMT_E2M1;
+  if (N % kBN || K % 128 || lda < K || ldb < (bf4 ? K / 2 : K) || lda % 16 || ldb % 16 || lda_s < K / 32 ||
       ldb_s < K / 32 || lda_s % 4 || ldb_s % 4 || ldc < N || ldc % 8)
     return XS_EUNSUPPORTED;
   if (!aligned(a, 16) || !aligned(b, 16) || !aligned(a_scales, 4) || !aligned(b_scales, 4) ||
@@ -189,9 +191,9 @@ extern "C" int xs_gemm_mx(const void* a, int64_t lda, const void* a_scales, int6
   if (trace && trace->buf && trace->count) tr = *trace;
   const int tiles = ((M + kBM - 1) / kBM) * (N / kBN);
   const int grid = std::min(tiles, xs_host::persistent_grid(0));
-  hipLaunchKernelGGL(mx::gemm_mx_kernel, dim3(grid), dim3(kMxThreads), 0, static_cast<hipStream_t>(stream),
-                     static_cast<const uint8_t*>(a), lda, static_cast<const uint8_t*>(a_scales), lda_s,
-                     static_cast<const uint8_t*>(b), ldb, static_cast<const uint8_t*>(b_scales), ldb_s,
-                     static_cast<char*>(c), ldc * 2, M, N, K, tr);
+  hipLaunchKernelGGL(bf4 ? mx::gemm_mx_kernel<true> : mx::gemm_mx_kernel<false>, dim3(grid), dim3(kMxThreads), 0,
+                     static_cast<hipStream_t>(stream), static_cast<const uint8_t*>(a), lda,
+                     static_cast<const uint8_t*>(a_scales), lda_s, static_cast<const uint8_t*>(b), ldb,
+                     static_cast<const uint8_t*>(b_scales), ldb_s, static_cast<char*>(c), ldc * 2, M, N, K, tr);
   return xs_host::launch_status();
 }

@@ -51,7 +51,11 @@ class EPLayer:
                  precision: int = X.XS_PREC_BF16):
         self.s = s
         self.precision = precision
-        mxp = precision == X.XS_PREC_MXFP8
+        mxp = precision in (X.XS_PREC_MXFP8, X.XS_PREC_W4A8)
+        self.mx = mxp
+        # weight code bytes per element: E4M3 one, packed E2M1 a half
+        self.w_fmt = X.XS_FMT_E2M1 if precision == X.XS_PREC_W4A8 else X.XS_FMT_E4M3
+        wdiv = 2 if precision == X.XS_PREC_W4A8 else 1
         # bytes per dispatched token row and per h row (MXFP8: codes, then one scale per 32)
         self.row_bytes = s.H + s.H // 32 if mxp else 2 * s.H
         self.h_bytes = s.I + s.I // 32 if mxp else 2 * s.I
@@ -93,9 +97,9 @@ class EPLayer:
         if mxp:
             self.h_ws = torch.zeros((h_rows, self.h_bytes), dtype=torch.uint8, device=d)
             E_, I_, H_ = s.n_experts, s.I, s.H
-            self.w1q = torch.zeros((E_, 2 * I_, H_), dtype=torch.uint8, device=d)
+            self.w1q = torch.zeros((E_, 2 * I_, H_ // wdiv), dtype=torch.uint8, device=d)
             self.w1s = torch.zeros((E_, 2 * I_, H_ // 32), dtype=torch.uint8, device=d)
-            self.w2q = torch.zeros((E_, H_, I_), dtype=torch.uint8, device=d)
+            self.w2q = torch.zeros((E_, H_, I_ // wdiv), dtype=torch.uint8, device=d)
             self.w2s = torch.zeros((E_, H_, I_ // 32), dtype=torch.uint8, device=d)
         else:
             self.h_ws = torch.zeros((h_rows, s.I if s.I else 1), dtype=torch.int16, device=d)
@@ -123,7 +127,7 @@ class EPLayer:
         L.logits = self.logits.data_ptr()
         L.x = self.x_all[s.src].data_ptr()
         L.precision = self.precision
-        if self.precision == X.XS_PREC_MXFP8:
+        if self.mx:
             L.w1, L.w2 = self.w1q.data_ptr(), self.w2q.data_ptr()
             L.w1_scale, L.w2_scale = self.w1s.data_ptr(), self.w2s.data_ptr()
         else:
@@ -153,18 +157,21 @@ class EPLayer:
             for i in range(w1_bits.shape[0]):   # expert by expert to bound host staging
                 self.w1[i].copy_(_dev_bits(w1_bits[i], "cpu"))
                 self.w2[i].copy_(_dev_bits(w2_bits[i], "cpu"))
-            if self.precision == X.XS_PREC_MXFP8:
+            if self.mx:
                 self.quantize_weights()
         torch.cuda.synchronize(self.dev)
 
     def quantize_weights(self):
-        """MXFP8 codes and scales of W1 (along H) and W2 (along I), on the GPU."""
+        """MX codes (E4M3, or packed E2M1 for W4A8) and scales of W1 (along H) and W2 (along I),
+        on the GPU."""
         s = self.s
         st = self.stream
-        X.check(X.xs_quantize_mx(self.w1.data_ptr(), s.n_experts * 2 * s.I, s.H, s.H, X.XS_FMT_E4M3,
-                                 self.w1q.data_ptr(), s.H, self.w1s.data_ptr(), s.H // 32, st), "quantize w1")
-        X.check(X.xs_quantize_mx(self.w2.data_ptr(), s.n_experts * s.H, s.I, s.I, X.XS_FMT_E4M3,
-                                 self.w2q.data_ptr(), s.I, self.w2s.data_ptr(), s.I // 32, st), "quantize w2")
+        X.check(X.xs_quantize_mx(self.w1.data_ptr(), s.n_experts * 2 * s.I, s.H, s.H, self.w_fmt,
+                                 self.w1q.data_ptr(), self.w1q.shape[2], self.w1s.data_ptr(), s.H // 32, st),
+                "quantize w1")
+        X.check(X.xs_quantize_mx(self.w2.data_ptr(), s.n_experts * s.H, s.I, s.I, self.w_fmt,
+                                 self.w2q.data_ptr(), self.w2q.shape[2], self.w2s.data_ptr(), s.I // 32, st),
+                "quantize w2")
 
     @property
     def stream(self):
@@ -188,7 +195,7 @@ class EPLayer:
 
     def dispatch(self, src: int):
         s = self.s
-        if self.precision == X.XS_PREC_MXFP8:
+        if self.mx:
             rb = self.row_bytes
             X.check(X.xs_quantize_mx(self.x_all[src].data_ptr(), s.T, s.H, s.H, X.XS_FMT_E4M3, self.xq.data_ptr(),
                                      rb, self.xq.data_ptr() + s.H, rb, self.stream), "quantize x")

@@ -29,7 +29,7 @@ XS_SCATTER_ROW_BLOCK, XS_SCATTER_HEAD_GROUP = 0, 1
 XS_MB_PERIODIC, XS_MB_COMPLETION = 0, 1
 XS_ATTN_LOCAL, XS_ATTN_WINDOWS, XS_ATTN_WINDOWS_COUPLED = 0, 1, 2
 XS_FMT_E4M3, XS_FMT_E2M1 = 0, 1
-XS_PREC_BF16, XS_PREC_MXFP8 = 0, 1
+XS_PREC_BF16, XS_PREC_MXFP8, XS_PREC_W4A8 = 0, 1, 2
 
 vp = C.c_void_p
 i32 = C.c_int32

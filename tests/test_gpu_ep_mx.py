@@ -1,6 +1,7 @@
-"""GPU parity of the MXFP8 (W8A8) expert-parallel layer against the CPU oracle, through the C
-ABI: dispatch windows of quantized token rows (bit-exact), the quantized h rows, the combine
-rows and the combined output; every pacing policy gives the same bits."""
+"""GPU parity of the quantized expert-parallel layer, W8A8 (MXFP8) and W4A8 (E2M1 weights),
+against the CPU oracle, through the C ABI: dispatch windows of quantized token rows
+(bit-exact), the quantized h rows, the combine rows and the combined output; every pacing
+policy gives the same bits."""
 import ctypes as C
 import dataclasses
 
@@ -23,13 +24,20 @@ def _gpu():
     torch.cuda.set_device(0)
 
 
-def _mx_layer(cfg, **kw):
+PRECISIONS = ["MXFP8", "W4A8"]
+
+
+def _wfmt(prec):
+    return omxf.E2M1 if prec == "W4A8" else omxf.E4M3
+
+
+def _mx_layer(cfg, prec="MXFP8", **kw):
     from paper_2607_23264_amd.layer import EPLayer, Shape
     X = xs()
     experts = synth.computed_experts(cfg)
     s = Shape(cfg.n_src, cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.W, experts[0], len(experts), src=cfg.rank,
               **kw)
-    return EPLayer(s, precision=X.XS_PREC_MXFP8)
+    return EPLayer(s, precision=getattr(X, f"XS_PREC_{prec}"))
 
 
 def _policies():
@@ -42,7 +50,7 @@ def _policies():
             "burst_w4_dyn": pacing(X.XS_POLICY_BURST, wave_tiles=4, claim=X.XS_CLAIM_DYNAMIC)}
 
 
-def _h_within_fp32_bound(got_codes, got_scales, xq, w1q, what):
+def _h_within_fp32_bound(got_codes, got_scales, xq, w1q, what, wfmt=omxf.E4M3):
     """The GPU's quantized h rows against the exact SwiGLU of the dequantized operands.
 
     The GPU accumulates Linear-1 in fp32 and evaluates SwiGLU in fp32, so its h differs from
@@ -54,7 +62,7 @@ def _h_within_fp32_bound(got_codes, got_scales, xq, w1q, what):
     where its value lies that close to a rounding midpoint (or a block maximum that close to a
     power-of-two threshold)."""
     X = omxf.dequantize_mx(*xq, omxf.E4M3)
-    W1 = omxf.dequantize_mx(*w1q, omxf.E4M3)
+    W1 = omxf.dequantize_mx(*w1q, wfmt)
     I = W1.shape[0] // 2
     K = X.shape[1]
     g, u = X @ W1[:I].T, X @ W1[I:].T
@@ -98,11 +106,13 @@ def _window_bases(lay):
     return out
 
 
-def test_tiny_layer_matches_oracle_for_every_policy():
+@pytest.mark.parametrize("prec", PRECISIONS)
+def test_tiny_layer_matches_oracle_for_every_policy(prec):
     cfg = synth.EP_TINY
     inp = synth.ep_inputs(cfg, 0)
-    ref = omx.ep_layer_mx(inp["x"], inp["logits"], inp["w1"], inp["w2"], cfg.k, cfg.E, cfg.W, cap=cfg.T * cfg.k)
-    lay = _mx_layer(cfg)
+    ref = omx.ep_layer_mx(inp["x"], inp["logits"], inp["w1"], inp["w2"], cfg.k, cfg.E, cfg.W, cap=cfg.T * cfg.k,
+                          wfmt=_wfmt(prec))
+    lay = _mx_layer(cfg, prec)
     lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
     outs = {}
     for name, p in _policies().items():
@@ -112,7 +122,7 @@ def test_tiny_layer_matches_oracle_for_every_policy():
         torch.cuda.synchronize()
         assert int(lay.status.item()) == 0, name
         outs[name] = host_bits(lay.out)
-        assert_close(outs[name], ref["out64"], f"tiny MXFP8 layer {name}")
+        assert_close(outs[name], ref["out64"], f"tiny {prec} layer {name}")
     first = next(iter(outs.values()))
     for name, o in outs.items():
         assert np.array_equal(o, first), f"policy {name} changed the output bits"
@@ -136,30 +146,32 @@ def test_tiny_layer_matches_oracle_for_every_policy():
         m = hc.shape[0]
         rows = h[bases[d] + r0:bases[d] + r0 + m]
         xq = (ref["win_codes"][d, r0:r0 + m], ref["win_scales"][d, r0:r0 + m])
-        flips += _h_within_fp32_bound(rows[:, :cfg.I], rows[:, cfg.I:], xq, omx.quantize_rows(inp["w1"][e]),
-                                      f"h of expert {e}")
+        flips += _h_within_fp32_bound(rows[:, :cfg.I], rows[:, cfg.I:], xq,
+                                      omx.quantize_rows(inp["w1"][e], _wfmt(prec)), f"h of expert {e}", _wfmt(prec))
     print(f"h codes that differ from the oracle's (all within the fp32 bound): {flips}")
     # combine rows (bf16 expert outputs) against the oracle's rounded rows
     comb = host_bits(lay.cwin)
     assert_close(comb[0], bits_f64(ref["combine"][0]), "combine rows")
 
 
-def test_multi_source_ragged_share():
+@pytest.mark.parametrize("prec", PRECISIONS)
+def test_multi_source_ragged_share(prec):
     # 3 sources, this GPU = rank 1 owning experts 4..7; T not a multiple of the 256-row tile
     cfg = synth.EPConfig("t", T=300, H=512, E=16, k=3, I=512, W=4, n_src=3, rank=1)
     inp = synth.ep_inputs(cfg, 7)
     experts = synth.computed_experts(cfg)
     fill = synth.normal_bf16(0, 200, (cfg.T * cfg.k, cfg.H))
     ref = omx.ep_layer_mx(inp["x"], inp["logits"], inp["w1"], inp["w2"], cfg.k, cfg.E, cfg.W,
-                          cap=cfg.n_src * cfg.T * cfg.k, experts=experts, combine_fill=fill, out_src=cfg.rank)
-    lay = _mx_layer(cfg)
+                          cap=cfg.n_src * cfg.T * cfg.k, experts=experts, combine_fill=fill, out_src=cfg.rank,
+                          wfmt=_wfmt(prec))
+    lay = _mx_layer(cfg, prec)
     lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
     lay.prefill_other_sources(fill)
     from paper_2607_23264_amd.layer import pacing
     lay.fused(pacing(xs().XS_POLICY_INTERLEAVE, lead=1))
     torch.cuda.synchronize()
     assert int(lay.status.item()) == 0
-    assert_close(host_bits(lay.out), ref["out64"], "ragged MXFP8 share output")
+    assert_close(host_bits(lay.out), ref["out64"], f"ragged {prec} share output")
     # the computed window holds every source's quantized rows bit for bit
     d = cfg.rank
     n = int(ref["layout"]["dest_counts"][d])
@@ -193,8 +205,8 @@ def _local_token_sample(idx_r, experts, T, n_tokens, max_experts, seed):
     return chosen
 
 
-@pytest.mark.parametrize("routing,claim", [("uniform", 0), ("zipf", 1)])
-def test_dsv3_share_full_size_sampled(routing, claim):
+@pytest.mark.parametrize("routing,claim,prec", [("uniform", 0, "MXFP8"), ("zipf", 1, "MXFP8"), ("zipf", 1, "W4A8")])
+def test_dsv3_share_full_size_sampled(routing, claim, prec):
     cfg = dataclasses.replace(synth.EP_DSV3_SHARE, routing=routing)
     if routing == "zipf":
         idx = np.stack([oep.route_topk_softmax(synth.zipf_logits(0, s, cfg.T, cfg.E), cfg.k)[0]
@@ -204,7 +216,7 @@ def test_dsv3_share_full_size_sampled(routing, claim):
     inp = synth.ep_inputs(cfg, 0)
     experts = synth.computed_experts(cfg)
     fill = synth.ep_remote_combine_fill(cfg, 0)
-    lay = _mx_layer(cfg)
+    lay = _mx_layer(cfg, prec)
     lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
     lay.prefill_other_sources(fill)
     from paper_2607_23264_amd.layer import pacing
@@ -232,13 +244,14 @@ def test_dsv3_share_full_size_sampled(routing, claim):
             if e in pos:
                 if e not in wq:
                     i = pos[e]
-                    wq[e] = (omx.quantize_rows(inp["w1"][i]), omx.quantize_rows(inp["w2"][i]))
-                _, _, _, yb = omx.expert_ffn_mx(xq, *wq[e])
+                    wq[e] = (omx.quantize_rows(inp["w1"][i], _wfmt(prec)),
+                             omx.quantize_rows(inp["w2"][i], _wfmt(prec)))
+                _, _, _, yb = omx.expert_ffn_mx(xq, *wq[e], _wfmt(prec))
                 row = bits_f64(yb[0])
             else:
                 row = bits_f64(fill[t * cfg.k + j])
             acc += np.float64(w[t, j]) * row
-        assert_close(out[t], acc, f"{routing} token {t}")
+        assert_close(out[t], acc, f"{prec} {routing} token {t}")
 
 
 def _fused_rc(L, lay):
@@ -260,7 +273,7 @@ def test_bad_arguments():
             setattr(L, k, v)
         return L
 
-    assert _fused_rc(variant(precision=2), lay) == X.XS_EINVAL
+    assert _fused_rc(variant(precision=3), lay) == X.XS_EINVAL
     assert _fused_rc(variant(reserved=1), lay) == X.XS_EINVAL
     assert _fused_rc(variant(w1_scale=None), lay) == X.XS_EINVAL
     assert _fused_rc(variant(w2_scale=None), lay) == X.XS_EINVAL
@@ -319,13 +332,16 @@ def test_dispatch_rows_bitexact():
     torch.cuda.synchronize()
 
 
-def test_weight_quantization_matches_oracle():
+@pytest.mark.parametrize("prec", PRECISIONS)
+def test_weight_quantization_matches_oracle(prec):
     cfg = synth.EP_TINY
     inp = synth.ep_inputs(cfg, 2)
-    lay = _mx_layer(cfg)
+    lay = _mx_layer(cfg, prec)
     lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
+    pack = omxf.pack_e2m1 if prec == "W4A8" else (lambda c: c)
     for i in (0, cfg.E - 1):
-        c1, s1 = omx.quantize_rows(inp["w1"][i])
-        c2, s2 = omx.quantize_rows(inp["w2"][i])
+        c1, s1 = omx.quantize_rows(inp["w1"][i], _wfmt(prec))
+        c2, s2 = omx.quantize_rows(inp["w2"][i], _wfmt(prec))
+        c1, c2 = pack(c1), pack(c2)
         assert np.array_equal(lay.w1q[i].cpu().numpy(), c1) and np.array_equal(lay.w1s[i].cpu().numpy(), s1)
         assert np.array_equal(lay.w2q[i].cpu().numpy(), c2) and np.array_equal(lay.w2s[i].cpu().numpy(), s2)

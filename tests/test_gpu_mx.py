@@ -1,6 +1,6 @@
 """GPU parity of the MX (microscaled) quantizer and GEMM against the CPU oracle, through the C
-ABI: codes and scales bit-exact, the GEMM within the fp32-accumulation tolerance of the fp64
-product of the dequantized operands."""
+ABI: codes and scales bit-exact, the GEMM (E4M3 x E4M3 and E4M3 x packed E2M1) within the
+fp32-accumulation tolerance of the fp64 product of the dequantized operands."""
 import numpy as np
 import pytest
 import torch
@@ -69,42 +69,52 @@ def test_quantize_bitexact(fmt_name, rows, cols):
     assert (codes[:, cb:] == 0x5A).all() and (scales[:, cols // 32:] == 0xA5).all()   # padding untouched
 
 
-def _gemm_mx(a_bits, b_bits):
-    """Quantize both operands on the GPU, multiply; returns (c bits, oracle fp64)."""
+def _gemm_mx(a_bits, b_bits, b_fmt="E4M3"):
+    """Quantize both operands on the GPU (B as E4M3 or packed E2M1), multiply; returns (c bits,
+    oracle fp64)."""
     X = xs()
     M, K = a_bits.shape
     N = b_bits.shape[0]
+    fmt = getattr(X, f"XS_FMT_{b_fmt}")
     ac, as_, _ = _quantize(a_bits, X.XS_FMT_E4M3)
-    bc, bs, _ = _quantize(b_bits, X.XS_FMT_E4M3)
+    bc, bs, ldb = _quantize(b_bits, fmt)
     da, das = torch.from_numpy(ac).cuda(), torch.from_numpy(as_).cuda()
     db, dbs = torch.from_numpy(bc).cuda(), torch.from_numpy(bs).cuda()
     c = torch.full((M, N), -1, dtype=torch.int16, device="cuda")
-    X.check(X.xs_gemm_mx(da.data_ptr(), K, das.data_ptr(), K // 32, db.data_ptr(), K, dbs.data_ptr(), K // 32,
-                         X.XS_FMT_E4M3, c.data_ptr(), N, M, N, K, None, _stream()))
+    X.check(X.xs_gemm_mx(da.data_ptr(), K, das.data_ptr(), K // 32, db.data_ptr(), ldb, dbs.data_ptr(), K // 32,
+                         fmt, c.data_ptr(), N, M, N, K, None, _stream()))
     torch.cuda.synchronize()
-    ref = mx.gemm_mx(ac, as_, mx.E4M3, bc, bs, mx.E4M3)
+    ofmt = getattr(mx, b_fmt)
+    ref = mx.gemm_mx(ac, as_, mx.E4M3, mx.unpack_e2m1(bc) if ofmt == mx.E2M1 else bc, bs, ofmt)
     return host_bits(c), ref
 
 
+@pytest.mark.parametrize("b_fmt", ["E4M3", "E2M1"])
 @pytest.mark.parametrize("M,N,K", [(256, 256, 128), (300, 512, 384), (1, 256, 256), (513, 768, 1024), (77, 256, 7168)])
-def test_gemm_mx_matches_oracle(M, N, K):
+def test_gemm_mx_matches_oracle(M, N, K, b_fmt):
     a = synth.normal_bf16(0, 20, (M, K))
     b = synth.normal_bf16(0, 21, (N, K), std=0.05)
-    c, ref = _gemm_mx(a, b)
-    assert_close(c, ref, f"gemm_mx {M}x{N}x{K}")
+    c, ref = _gemm_mx(a, b, b_fmt)
+    assert_close(c, ref, f"gemm_mx {M}x{N}x{K} B {b_fmt}")
 
 
-def test_gemm_mx_integer_operands_bitexact():
+@pytest.mark.parametrize("b_fmt", ["E4M3", "E2M1"])
+def test_gemm_mx_integer_operands_bitexact(b_fmt):
     # small integers are exact in E4M3 with scale 2^0 when every block holds a value of 256..448
-    # (scale exponent 0) - here blocks are integers in [-8, 8] plus one 256: scale 2^0, exact
-    # codes, and |sums| < 2^24, so fp32 accumulation is exact in any order
+    # (scale exponent 0) - here A blocks are integers in [-8, 8] plus one 256: scale 2^0, exact
+    # codes. B likewise, or for E2M1 integers that E2M1 holds ({0, 1, 2, 3, 4, 6} and negatives)
+    # with one 6 per block (scale 2^0). |sums| < 2^24, so fp32 accumulation is exact in any order
     g = np.random.default_rng(9)
     M, N, K = 300, 256, 512
     a = g.integers(-8, 9, (M, K)).astype(np.float32)
-    b = g.integers(-8, 9, (N, K)).astype(np.float32)
     a[:, ::32] = 256.0
-    b[:, ::32] = 256.0
-    c, ref = _gemm_mx(synth.to_bf16_bits(a), synth.to_bf16_bits(b))
+    if b_fmt == "E4M3":
+        b = g.integers(-8, 9, (N, K)).astype(np.float32)
+        b[:, ::32] = 256.0
+    else:
+        b = g.choice([0, 1, -1, 2, -2, 3, -3, 4, -4, 6, -6], (N, K)).astype(np.float32)
+        b[:, ::32] = 6.0
+    c, ref = _gemm_mx(synth.to_bf16_bits(a), synth.to_bf16_bits(b), b_fmt)
     from oracle.ep import f64_to_bf16_bits
     assert np.array_equal(c, f64_to_bf16_bits(a.astype(np.float64) @ b.astype(np.float64).T))
     assert np.array_equal(c, f64_to_bf16_bits(ref))
@@ -126,4 +136,7 @@ def test_mx_bad_arguments():
     assert X.xs_gemm_mx(*args(192, 256, X.XS_FMT_E4M3)) == X.XS_EUNSUPPORTED     # K % 128
     assert X.xs_gemm_mx(*args(256, 200, X.XS_FMT_E4M3)) == X.XS_EUNSUPPORTED     # N % 256
     assert X.xs_gemm_mx(*args(256, 256, 9)) == X.XS_EINVAL
+    # packed E2M1 rows need K / 2 bytes: 256 bytes cover K = 512 but not K = 640
+    assert X.xs_gemm_mx(a.data_ptr(), 640, sc.data_ptr(), 20, a.data_ptr(), 256, sc.data_ptr(), 20,
+                        X.XS_FMT_E2M1, o.data_ptr(), 256, 0, 256, 640, None, _stream()) == X.XS_EUNSUPPORTED
     torch.cuda.synchronize()
