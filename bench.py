@@ -52,7 +52,7 @@ def parse():
                    help="skip the attention + Ulysses exchange line (HBM and host-coherent windows)")
     p.add_argument("--policies", action="store_true",
                    help="also time the fused layer under every pacing policy (phases)")
-    p.add_argument("--no-mx", action="store_true", help="skip the MXFP8 (W8A8) layer line")
+    p.add_argument("--no-mx", action="store_true", help="skip the MXFP8 (W8A8) and W4A8 layer lines")
     p.add_argument("--seed", type=int, default=0)
     return p.parse_args()
 
@@ -232,13 +232,13 @@ def synth_rows(g, m, H):
     return synth.to_bf16_bits(g.standard_normal((m, H), dtype=np.float32))
 
 
-def mx_line(X, torch, cfg, inp, rank, experts, pol, steps, warmup, bf16_step_us):
-    """The same layer share at MXFP8 (W8A8): token rows quantized in the dispatch phase, both
-    expert GEMMs on the scaled MFMA. Step time, FFN kernel rate against the dense fp8 peak and
-    the in-step phases."""
+def mx_line(X, torch, cfg, inp, rank, experts, pol, steps, warmup, bf16_step_us, prec="MXFP8"):
+    """The same layer share at MXFP8 (W8A8) or W4A8 (E2M1 weights): token rows quantized in the
+    dispatch phase, both expert GEMMs on the scaled MFMA. Step time, FFN kernel rate against
+    the dense fp8 peak (an fp8 x fp4 MFMA issues at the fp8 rate) and the in-step phases."""
     from paper_2607_23264_amd.layer import EPLayer, Shape
     s = Shape(cfg.n_src, cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.W, experts[0], len(experts), src=rank)
-    lay = EPLayer(s, sentinel=False, precision=X.XS_PREC_MXFP8)
+    lay = EPLayer(s, sentinel=False, precision=getattr(X, f"XS_PREC_{prec}"))
     lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
     lay.prefill_other_sources(inp["fill"])
     for i in range(8):
@@ -274,26 +274,29 @@ def mx_line(X, torch, cfg, inp, rank, experts, pol, steps, warmup, bf16_step_us)
     del lay
     torch.cuda.empty_cache()
     if status:
-        raise RuntimeError(f"MXFP8 layer: device status {status}: {X.xs_strerror(status).decode()}")
+        raise RuntimeError(f"{prec} layer: device status {status}: {X.xs_strerror(status).decode()}")
     flops = 6.0 * cfg.H * cfg.I * rows
     tflops = flops / (ffn_us * 1e-6) / 1e12
-    # algorithmic HBM bytes of one launch: dispatched MXFP8 rows read once, codes and scales of
-    # both weight matrices of every local expert read once, MXFP8 h written and read back
-    # once, bf16 output rows stored once
+    # algorithmic HBM bytes of one launch: dispatched MXFP8 rows read once, codes (1 byte, or
+    # half a byte for E2M1) and scales of both weight matrices of every local expert read
+    # once, MXFP8 h written and read back once, bf16 output rows stored once
     hb = cfg.I + cfg.I // 32
-    alg_bytes = (rows * (cfg.H + cfg.H // 32) + len(experts) * 3 * cfg.H * cfg.I * 33 / 32 + 2 * rows * hb
+    wbytes = (0.5 if prec == "W4A8" else 1.0) + 1 / 32
+    alg_bytes = (rows * (cfg.H + cfg.H // 32) + len(experts) * 3 * cfg.H * cfg.I * wbytes + 2 * rows * hb
                  + rows * cfg.H * 2)
+    kname = "ep_ffn_w4a8_kernel" if prec == "W4A8" else "ep_ffn_mx_kernel"
     from paper_2607_23264_amd.profiling import read_traffic
-    tr = read_traffic(os.path.join(HERE, "profiles", "ep_ffn_mx_kernel_dsv3_share_traffic.md"))
+    tr = read_traffic(os.path.join(HERE, "profiles", f"{kname}_dsv3_share_traffic.md"))
     # dispatch phase: bf16 rows read, MXFP8 rows staged, then read and stored k times
     rb = cfg.H + cfg.H // 32
     disp_moved = cfg.T * cfg.H * 2 + cfg.T * rb * 2 + cfg.T * cfg.k * rb
-    return {"workload": f"{cfg.name} at MXFP8 (E4M3 codes, E8M0 scales per 32), rank {rank}",
-            "dtype": "mxfp8 (fp32 accumulation)", "us_per_step": step_us, "bf16_us_per_step": bf16_step_us,
+    fmt = "E2M1 weights, E4M3 activations" if prec == "W4A8" else "E4M3 codes"
+    return {"workload": f"{cfg.name} at {prec} ({fmt}, E8M0 scales per 32), rank {rank}",
+            "dtype": f"{prec.lower()} (fp32 accumulation)", "us_per_step": step_us, "bf16_us_per_step": bf16_step_us,
             "speedup_vs_bf16": bf16_step_us / step_us, "rows_computed": rows,
             "phases_in_step_us": in_step,
             "dispatch_moved_GBps": disp_moved / (in_step["dispatch"] * 1e-6) / 1e9,
-            "roofline": {"bound": "mfma", "kernel": "ep_ffn_mx_kernel<3> (persistent fused MX Linear-1 + Linear-2)",
+            "roofline": {"bound": "mfma", "kernel": f"{kname}<3> (persistent fused MX Linear-1 + Linear-2)",
                          "achieved": tflops, "peak": MFMA_PEAK_FP8 / 1e12, "unit": "TFLOP/s",
                          "frac": tflops * 1e12 / MFMA_PEAK_FP8, "traffic": tr["traffic_bytes"] if tr else None,
                          "flops_per_launch": flops, "algorithmic_bytes_per_launch": alg_bytes,
@@ -452,12 +455,12 @@ def main():
     del lay
     torch.cuda.empty_cache()
     if not a.no_mx:
-        log("[bench] the same layer share at MXFP8 (W8A8)")
-        res["ep_mxfp8"] = mx_line(X, torch, cfg, inp, rank, experts, pol[a.policy], a.steps, a.warmup,
-                                  ms_per_step * 1e3)
-        m = res["ep_mxfp8"]
-        log(f"[bench] MXFP8: {m['us_per_step']:.1f} us/step ({m['speedup_vs_bf16']:.2f}x bf16), FFN kernel "
-            f"{m['roofline']['avg_launch_us']:.1f} us ({m['roofline']['achieved']:.1f} TFLOP/s)")
+        for prec in ("MXFP8", "W4A8"):
+            log(f"[bench] the same layer share at {prec}")
+            res[f"ep_{prec.lower()}"] = m = mx_line(X, torch, cfg, inp, rank, experts, pol[a.policy], a.steps,
+                                                    a.warmup, ms_per_step * 1e3, prec)
+            log(f"[bench] {prec}: {m['us_per_step']:.1f} us/step ({m['speedup_vs_bf16']:.2f}x bf16), FFN kernel "
+                f"{m['roofline']['avg_launch_us']:.1f} us ({m['roofline']['achieved']:.1f} TFLOP/s)")
     if not a.no_phases:
         log("[bench] store ceiling")
         res["store_ceiling"] = store_ceiling(X, torch)
