@@ -30,6 +30,8 @@
 // number of valid 32-row blocks (0 to 4); every instantiation issues the same loads and
 // barriers, so the workgroup stays in step.
 #pragma once
+#include <type_traits>
+
 #include "xs_common.hpp"
 
 namespace xs {
@@ -161,8 +163,14 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
   if (nk > 1) issue_a(1);
   if (nk > 2) issue_b(2, 2);
   frags(lds, lds + kBBase, 0, 0);
-  int bs = 0;   // B slot of stage kt (kt mod 3)
-  for (int kt = 0; kt < nk; ++kt) {
+  // One stage. NEXT: a stage follows; IA: A(kt + 2) exists (then B(kt + 2) is the only newer
+  // load at the boundary: vmcnt(4)); IB: B(kt + 3) exists. Compile-time, so the steady loop
+  // body is one basic block: with the boundary's conditions inside the loop the register
+  // allocator split the accumulators' live ranges and copied all of them every stage.
+  auto stage = [&](int kt, int bs, auto next_c, auto ia_c, auto ib_c) {
+    constexpr bool kNext = decltype(next_c)::value;
+    constexpr bool kIA = decltype(ia_c)::value;
+    constexpr bool kIB = decltype(ib_c)::value;
     const char* ca = lds + (kt & 1) * kOpBytes;
     const char* cb = lds + kBBase + bs * kOpBytes;
     const int bs_next = bs == 2 ? 0 : bs + 1;
@@ -186,9 +194,9 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
     // sub-step 3 (fragments in buffer 1): most MFMAs, then the stage boundary
     mma(1, 0, kPre);
     if (NI > 0) __builtin_amdgcn_sched_group_barrier(0x008, 2 * kPre, 0);
-    if (kt + 1 < nk) {
+    if constexpr (kNext) {
       // this wave's loads of stage kt + 1 have landed ...
-      if (kt + 2 < nk)
+      if constexpr (kIA)
         __builtin_amdgcn_s_waitcnt(0x0F74);   // vmcnt(4)
       else
         wait_vm0();
@@ -198,12 +206,26 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
       // has waited for its own direct loads above, and LDS has no cache to flush.
       __builtin_amdgcn_s_barrier();
       frags(lds + ((kt + 1) & 1) * kOpBytes, lds + kBBase + bs_next * kOpBytes, 0, 0);
-      if (kt + 2 < nk) issue_a(kt + 2);      // into A buffer kt & 1
-      if (kt + 3 < nk) issue_b(kt + 3, bs);  // into B slot (kt + 3) mod 3 = kt mod 3
+      if constexpr (kIA) issue_a(kt + 2);      // into A buffer kt & 1
+      if constexpr (kIB) issue_b(kt + 3, bs);  // into B slot (kt + 3) mod 3 = kt mod 3
     }
     mma(1, kPre, NI);
-    bs = bs_next;
+  };
+  const std::true_type yes;
+  const std::false_type no;
+  int kt = 0, bs = 0;   // bs: B slot of stage kt (kt mod 3)
+  for (; kt + 3 < nk; ++kt, bs = bs == 2 ? 0 : bs + 1) stage(kt, bs, yes, yes, yes);
+  if (kt + 2 < nk) {
+    stage(kt, bs, yes, yes, no);
+    ++kt;
+    bs = bs == 2 ? 0 : bs + 1;
   }
+  if (kt + 1 < nk) {
+    stage(kt, bs, yes, no, no);
+    ++kt;
+    bs = bs == 2 ? 0 : bs + 1;
+  }
+  stage(kt, bs, no, no, no);
 }
 
 // acc = A[0:256, 0:K] * B[rows(0:256), 0:K]^T. Rows of A at or beyond a_rows read row
