@@ -33,12 +33,15 @@ KERNEL_SOURCES = {"ffn": FFN_KERNEL_SOURCES, "attn": ATTN_KERNEL_SOURCES}
 def sources_hash(paths=FFN_KERNEL_SOURCES) -> str:
     if os.path.dirname(HERE) not in sys.path:        # also when run as a script
         sys.path.insert(0, os.path.dirname(HERE))
-    from paper_2607_23264_amd.build import FLAGS, HIPCC
+    from paper_2607_23264_amd.build import FLAGS, HIPCC, ROOT
     h = hashlib.sha256()
     for p in paths:
         with open(os.path.join(HERE, p), "rb") as f:
             h.update(f.read())
-    h.update(" ".join([os.path.basename(HIPCC)] + FLAGS).encode())
+    # include paths relative to the repository, which sits at different absolute paths on
+    # different machines
+    flags = [f.replace(ROOT, "<root>") for f in FLAGS]
+    h.update(" ".join([os.path.basename(HIPCC)] + flags).encode())
     return h.hexdigest()[:16]
 
 
