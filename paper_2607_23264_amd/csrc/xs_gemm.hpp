@@ -97,12 +97,12 @@ struct TileAddr {
 // The software pipeline for a wave that multiplies NI of its four 32-row blocks.
 //
 // Fragments are double-buffered in registers: the reads of k sub-step kk + 1 are in flight
-// while the MFMAs of sub-step kk issue. sched_group_barrier pins the order (one MFMA, then
-// two fragment reads, three times, then the remaining MFMAs): left alone the scheduler reuses
-// one fragment register set and waits out every LDS read. At a stage boundary three quarters
-// of the last sub-step's MFMAs are issued before the vmcnt wait and the barrier, so the
-// matrix pipe keeps working while the workgroup synchronises; the next stage's first
-// fragments are read before the next loads are issued.
+// while the MFMAs of sub-step kk issue. The order is pinned one MFMA at a time between
+// scheduling fences (left alone, the scheduler reuses one fragment register set and waits out
+// every LDS read): in sub-steps 0-2 each MFMA is followed by one fragment read of the next
+// sub-step; the stage barrier comes before sub-step 3, whose MFMAs are each followed by one
+// fragment read of the next stage's sub-step 0 and one direct load, so the matrix pipe works
+// while the loads are issued and the next stage's first fragments arrive.
 template <int NI>
 __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc, char* lds) {
   const int lane = threadIdx.x & 63;
@@ -145,9 +145,6 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
   };
   // per sub-step: 2 NI MFMAs and NI + 2 fragment reads
   constexpr int kReads = NI + 2, kMfma = 2 * NI;
-  constexpr int kPairs = kReads / 2, kOdd = kReads % 2;
-  constexpr int kRest = kMfma - kPairs - kOdd;
-  constexpr int kPre = NI < 3 ? NI : 3;
   // Issue order: A(0), B(0), B(1) | A(1), B(2) | A(2), B(3) | ... At the boundary into
   // stage s + 1 the loads newer than A(s + 1) are only B(s + 2) (4 per wave), so waiting for
   // stage s + 1 is vmcnt(4), or vmcnt(0) when B(s + 2) does not exist.
@@ -167,6 +164,31 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
   // load at the boundary: vmcnt(4)); IB: B(kt + 3) exists. Compile-time, so the steady loop
   // body is one basic block: with the boundary's conditions inside the loop the register
   // allocator split the accumulators' live ranges and copied all of them every stage.
+  // one fragment read r of sub-step kk into buffer buf: 0, 1 = B blocks, 2.. = A blocks
+  auto read_one = [&](const char* ca, const char* cb, int kk, int buf, int r) {
+    const int piece = (((kk * 2 + khalf) ^ swz) << 4);
+    if (r < 2)
+      bfr[buf][r] = *reinterpret_cast<const bf16x8*>(cb + ta.brow + r * 32 * kBK * 2 + piece);
+    else
+      af[buf][r - 2] = *reinterpret_cast<const bf16x8*>(ca + ta.arow + (r - 2) * 32 * kBK * 2 + piece);
+  };
+  auto mma_one = [&](int buf, int g) {
+    const int i = g >> 1, j = g & 1;
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[buf][j], af[buf][i], acc[i][j], 0, 0, 0);
+  };
+  // one direct load n of stage kt + 2 (A, n < 4) or kt + 3 (B, n >= 4, into slot bs)
+  auto load_one = [&](int kt, int bs, int n) {
+    if (n < 4) {
+      char* st = lds + (kt & 1) * kOpBytes;
+      const char* a0 = ta.a + (kt + 2) * kBK * 2;
+      __builtin_amdgcn_global_load_lds((glob_void*)(a0 + ta.oa[n]), (lds_void*)(st + (8 * n + w) * 1024), 16, 0, 0);
+    } else {
+      char* st = lds + kBBase + bs * kOpBytes;
+      const char* b0 = ta.b + (kt + 3) * kBK * 2;
+      __builtin_amdgcn_global_load_lds((glob_void*)(b0 + ta.ob[n - 4]), (lds_void*)(st + (8 * (n - 4) + w) * 1024),
+                                       16, 0, 0);
+    }
+  };
   auto stage = [&](int kt, int bs, auto next_c, auto ia_c, auto ib_c) {
     constexpr bool kNext = decltype(next_c)::value;
     constexpr bool kIA = decltype(ia_c)::value;
@@ -174,42 +196,45 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
     const char* ca = lds + (kt & 1) * kOpBytes;
     const char* cb = lds + kBBase + bs * kOpBytes;
     const int bs_next = bs == 2 ? 0 : bs + 1;
+    const char* na = lds + ((kt + 1) & 1) * kOpBytes;
+    const char* nb = lds + kBBase + bs_next * kOpBytes;
 #pragma unroll
     for (int kk = 0; kk < 3; ++kk) {
-      frags(ca, cb, kk + 1, (kk + 1) & 1);
-      mma(kk & 1, 0, NI);
-      if (NI > 0) {
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int g = 0; g < kPairs; ++g) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
-          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // two ds_reads
-        }
-        if (kOdd) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        }
-        if (kRest > 0) __builtin_amdgcn_sched_group_barrier(0x008, kRest, 0);
+      for (int g = 0; g < kMfma; ++g) {
+        mma_one(kk & 1, g);
+        if (g < kReads) read_one(ca, cb, kk + 1, (kk + 1) & 1, g);
+        __builtin_amdgcn_sched_barrier(0);
       }
+#pragma unroll
+      for (int r = kMfma; r < kReads; ++r) read_one(ca, cb, kk + 1, (kk + 1) & 1, r);
     }
-    // sub-step 3 (fragments in buffer 1): most MFMAs, then the stage boundary
-    mma(1, 0, kPre);
-    if (NI > 0) __builtin_amdgcn_sched_group_barrier(0x008, 2 * kPre, 0);
+    __builtin_amdgcn_sched_barrier(0);
     if constexpr (kNext) {
-      // this wave's loads of stage kt + 1 have landed ...
-      if constexpr (kIA)
-        __builtin_amdgcn_s_waitcnt(0x0F74);   // vmcnt(4)
-      else
-        wait_vm0();
-      // ... and every wave's, and stage kt is no longer read. A bare s_barrier: the
-      // workgroup fence of __syncthreads would wait for every outstanding load (vmcnt(0)),
-      // including the weight loads meant to stay in flight. LDS needs no fence: each wave
-      // has waited for its own direct loads above, and LDS has no cache to flush.
+      // this wave's reads of stage kt are done and its loads of stage kt + 1 have landed (only
+      // B(kt + 2) may still be in flight) ... and every wave's (bare s_barrier, see above)
+      __builtin_amdgcn_s_waitcnt(kIA ? 0x0074 : 0x0070);   // vmcnt(4 or 0) lgkmcnt(0)
       __builtin_amdgcn_s_barrier();
-      frags(lds + ((kt + 1) & 1) * kOpBytes, lds + kBBase + bs_next * kOpBytes, 0, 0);
-      if constexpr (kIA) issue_a(kt + 2);      // into A buffer kt & 1
-      if constexpr (kIB) issue_b(kt + 3, bs);  // into B slot (kt + 3) mod 3 = kt mod 3
     }
-    mma(1, kPre, NI);
+    __builtin_amdgcn_sched_barrier(0);
+    constexpr int kLoads = (kIA ? 4 : 0) + (kIB ? 4 : 0);
+    // sub-step 3: each MFMA followed by one read of the next stage's sub-step 0 and one load
+#pragma unroll
+    for (int g = 0; g < kMfma; ++g) {
+      mma_one(1, g);
+      if constexpr (kNext) {
+        if (g < kReads) read_one(na, nb, 0, 0, g);
+      }
+      if (g < kLoads) load_one(kt, bs, kIA ? g : g + 4);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (kNext) {
+#pragma unroll
+      for (int r = kMfma; r < kReads; ++r) read_one(na, nb, 0, 0, r);
+    }
+#pragma unroll
+    for (int n = kMfma; n < kLoads; ++n) load_one(kt, bs, kIA ? n : n + 4);
   };
   const std::true_type yes;
   const std::false_type no;
