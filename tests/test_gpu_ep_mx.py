@@ -345,3 +345,134 @@ def test_weight_quantization_matches_oracle(prec):
         c1, c2 = pack(c1), pack(c2)
         assert np.array_equal(lay.w1q[i].cpu().numpy(), c1) and np.array_equal(lay.w1s[i].cpu().numpy(), s1)
         assert np.array_equal(lay.w2q[i].cpu().numpy(), c2) and np.array_equal(lay.w2s[i].cpu().numpy(), s2)
+
+
+def _records(buf, count):
+    n = min(int(count.item()), buf.shape[0])
+    r = buf[:n].cpu().numpy().astype(np.uint64)
+    kind = (r[:, 0] >> np.uint64(56)).astype(np.int64)
+    wg = ((r[:, 0] >> np.uint64(32)) & np.uint64(0xFFFFFF)).astype(np.int64)
+    tile = (r[:, 0] & np.uint64(0xFFFFFFFF)).astype(np.int64)
+    return kind, wg, tile, r
+
+
+@pytest.mark.parametrize("prec,policy", [("MXFP8", "interleave"), ("MXFP8", "burst"), ("W4A8", "chunk")])
+def test_dynamic_claim_takes_every_tile_once_after_its_dependencies(prec, policy):
+    from paper_2607_23264_amd.layer import pacing
+    X = xs()
+    cfg = synth.EP_TINY
+    inp = synth.ep_inputs(cfg, 0)
+    lay = _mx_layer(cfg, prec)
+    lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
+    G = 8
+    pol = {"interleave": pacing(X.XS_POLICY_INTERLEAVE, lead=1, max_producers=G, claim=X.XS_CLAIM_DYNAMIC),
+           "chunk": pacing(X.XS_POLICY_CHUNK, lead=1, chunk=1, max_producers=G, claim=X.XS_CLAIM_DYNAMIC),
+           "burst": pacing(X.XS_POLICY_BURST, max_producers=G, wave_tiles=16, claim=X.XS_CLAIM_DYNAMIC)}[policy]
+    buf = torch.zeros((4096, 4), dtype=torch.int64, device="cuda")
+    cnt = torch.zeros((1,), dtype=torch.int32, device="cuda")
+    lay.fused(pol, X.xs_trace(buf.data_ptr(), buf.shape[0], cnt.data_ptr()))
+    torch.cuda.synchronize()
+    assert int(lay.status.item()) == 0
+    kind, wg, tile, r = _records(buf, cnt)
+    idx = oep.route_topk_softmax(inp["logits"][0], cfg.k)[0][None]
+    counts = oep.dispatch_layout(idx, cfg.E, cfg.W)["expert_counts"].sum(0)
+    P = sum((int(c) + 255) // 256 for c in counts)
+    P1, P2 = cfg.I // 128, cfg.H // 256
+    # every tile exactly once, on producers 0..G-1
+    assert sorted(tile[kind == 1].tolist()) == list(range(P * P1))
+    assert sorted(tile[kind == 2].tolist()) == list(range(P * P2))
+    assert set(wg.tolist()) <= set(range(G))
+    # a Linear-2 tile's mainloop ends after every Linear-1 tile of its row has stored h
+    l1_end = {}
+    for t, e in zip(tile[kind == 1], r[kind == 1, 3].astype(np.int64)):
+        l1_end[int(t) // P1] = max(l1_end.get(int(t) // P1, 0), int(e))
+    for t, m in zip(tile[kind == 2], r[kind == 2, 2].astype(np.int64)):
+        assert int(m) >= l1_end[int(t) // P2], f"Linear-2 tile {int(t)} ran before its row"
+    # and the output equals the static order's, bit for bit
+    out_dyn = host_bits(lay.out)
+    lay.out.zero_()
+    lay.fused(pacing(X.XS_POLICY_INTERLEAVE, lead=1))
+    torch.cuda.synchronize()
+    assert np.array_equal(out_dyn, host_bits(lay.out))
+
+
+@pytest.mark.parametrize("claim", [0, 1])
+def test_withheld_dependency_times_out_and_kernel_exits(claim):
+    from paper_2607_23264_amd.layer import pacing
+    X = xs()
+    cfg = synth.EP_TINY
+    inp = synth.ep_inputs(cfg, 0)
+    lay = _mx_layer(cfg)
+    lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
+    lay.fused(pacing(X.XS_POLICY_INTERLEAVE, lead=1, withhold_row=0, spin_timeout_us=2000, claim=claim))
+    torch.cuda.synchronize()
+    assert int(lay.status.item()) == X.XS_ETIMEOUT
+    lay.status.zero_()
+    lay.fused(pacing(X.XS_POLICY_INTERLEAVE, lead=1))
+    torch.cuda.synchronize()
+    assert int(lay.status.item()) == 0
+
+
+@pytest.mark.parametrize("prec", PRECISIONS)
+def test_degenerate_token_rows(prec):
+    # all-zero rows (every block takes scale 2^0 and codes 0), rows scaled by 2^-40 and 2^20
+    # (block exponents far from 0), and sparse rows (eight nonzero elements 61 apart: most
+    # blocks all zero, the others with one nonzero code)
+    from paper_2607_23264_amd.layer import pacing
+    X = xs()
+    cfg = synth.EP_TINY
+    inp = synth.ep_inputs(cfg, 3)
+    xf = ((inp["x"][0].astype(np.uint32) << 16).view(np.float32)).copy()
+    xf[0:8] = 0.0
+    xf[8:16] *= 2.0 ** -40
+    xf[16:24] *= 2.0 ** 20
+    xf[24:32] = 0.0
+    xf[24:32, np.arange(8) * 61] = np.linspace(-3, 3, 8, dtype=np.float32)
+    x = synth.to_bf16_bits(xf)[None]
+    ref = omx.ep_layer_mx(x, inp["logits"], inp["w1"], inp["w2"], cfg.k, cfg.E, cfg.W, cap=cfg.T * cfg.k,
+                          wfmt=_wfmt(prec))
+    lay = _mx_layer(cfg, prec)
+    lay.upload(inp["logits"], x, inp["w1"], inp["w2"])
+    lay.fused(pacing(X.XS_POLICY_INTERLEAVE, lead=1))
+    torch.cuda.synchronize()
+    assert int(lay.status.item()) == 0
+    out = host_bits(lay.out)
+    assert np.all(out[0:8] & 0x7FFF == 0), "zero token rows must give zero outputs"
+    # y grows as x^2 through SwiGLU: the scaled rows are compared at their own magnitude
+    # (outputs times 2^80 and 2^-40, exact power-of-two rescalings), so reading 11's bound
+    # applies relative to the row scale rather than to 1
+    got, r = bits_f64(out), ref["out64"]
+    for rows, k in ((slice(8, 16), 2.0 ** 80), (slice(16, 24), 2.0 ** -40), (slice(24, 32), 1.0),
+                    (slice(32, None), 1.0)):
+        g_, r_ = got[rows] * k, r[rows] * k
+        err = np.abs(g_ - r_) / np.maximum(1.0, np.abs(r_))
+        assert np.all(np.isfinite(g_)) and err.max() <= 2e-2, (prec, rows, float(err.max()))
+        assert np.linalg.norm(g_ - r_) <= 1e-2 * np.linalg.norm(r_), (prec, rows)
+    win = lay.dwin.cpu().numpy()
+    for d in range(cfg.W):
+        n = int(ref["layout"]["dest_counts"][d])
+        assert np.array_equal(win[d, :n, :cfg.H], ref["win_codes"][d, :n])
+        assert np.array_equal(win[d, :n, cfg.H:cfg.H + cfg.H // 32], ref["win_scales"][d, :n])
+
+
+def test_share_without_local_rows():
+    # no token of any source routes to this rank's experts: the layer computes nothing and the
+    # output is the routing-weighted sum of the other ranks' combine rows
+    from paper_2607_23264_amd.layer import pacing
+    cfg = synth.EPConfig("t", T=300, H=512, E=16, k=3, I=512, W=4, n_src=3, rank=1)
+    inp = synth.ep_inputs(cfg, 5)
+    experts = synth.computed_experts(cfg)
+    logits = inp["logits"].copy()
+    logits[:, :, experts] = -1e4
+    fill = synth.normal_bf16(0, 201, (cfg.T * cfg.k, cfg.H))
+    ref = omx.ep_layer_mx(inp["x"], logits, inp["w1"], inp["w2"], cfg.k, cfg.E, cfg.W,
+                          cap=cfg.n_src * cfg.T * cfg.k, experts=experts, combine_fill=fill, out_src=cfg.rank)
+    assert not ref["h"]
+    lay = _mx_layer(cfg)
+    lay.upload(logits, inp["x"], inp["w1"], inp["w2"])
+    lay.prefill_other_sources(fill)
+    lay.fused(pacing(xs().XS_POLICY_INTERLEAVE, lead=1, claim=xs().XS_CLAIM_DYNAMIC))
+    torch.cuda.synchronize()
+    assert int(lay.status.item()) == 0
+    assert int(lay.dest_counts[cfg.rank].item()) == 0
+    assert_close(host_bits(lay.out), ref["out64"], "share without local rows")
