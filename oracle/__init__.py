@@ -18,7 +18,9 @@ Modules:
   xstage_model    Burst-Gap model (Eqs. 1-9), calibration fit, audit helpers
   schedule        tile orders: Expert-Wave, cross-wave interleave (Alg. 1), chunked
   attention       softmax attention and the post-attention Ulysses exchange
-  ep_mx           the EP layer with MXFP8 rows, weights and activations (W8A8)
+  ep_mx           the quantized EP layer (W8A8 MXFP8, W4A8 with E2M1 weights)
+  ring            dispatch through bounded destination rings, with optional per-destination
+                  token dedup
   mx              microscaled formats (E4M3 / E2M1 elements, E8M0 block scales) of the
                   quantized EP path: encode, decode, block quantizer, dequantized GEMM
 
@@ -26,4 +28,4 @@ Parity status: every function here is pinned by tests under ``tests/`` against
 closed forms, worked numbers the paper prints, brute force or library routines,
 except where a function's docstring says "parity unpinned".
 """
-from . import attention, ep, ep_mx, mx, scatter, xstage_model, schedule  # noqa: F401
+from . import attention, ep, ep_mx, mx, ring, scatter, xstage_model, schedule  # noqa: F401
