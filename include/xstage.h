@@ -127,6 +127,34 @@ int xs_dispatch_rows(const void* rows, int64_t row_stride, int32_t row_bytes, in
                      const int32_t* topk_idx, const int32_t* slot_row, int32_t k, int32_t E,
                      const xs_window* win, int32_t W, int32_t* dev_status, void* stream);
 
+/* Dispatch through bounded destination rings (Sec. 4.3: an eligible Linear-1 tile needs ready
+ * dispatch input and a free destination ring slot; App. A.2: ring-slot readiness is checked
+ * before a tile is emitted). Reading: destination d owns a ring of S slots (rings[d]: base,
+ * capacity_rows = S, equal for every d; row_stride_bytes >= xs_ring_slot_bytes(H, k), a
+ * multiple of 16; 16-byte aligned; device or host-coherent memory). An entry is one bf16
+ * token row of x [T][H] plus a header naming the rows of window d it is copied into: with
+ * dedup = 1 one entry per (token, destination) listing every k slot of the token there, with
+ * dedup = 0 one entry per (token, k) slot. Lifetime protocol: the producer of entry n
+ * (numbered per ring in claim order) fills slot n mod S only after entry n - S has been
+ * copied out and released; the consumer copies an entry into its window rows
+ * (slot_row[t][j] of win[d]) and then releases the slot. Workgroups produce their tokens'
+ * entries and consume entries, a stalled producer draining the entries it waits on, so the
+ * call completes for any S >= 1. The windows end equal to xs_dispatch's.
+ * max_producers: workgroups (0 = one per CU). spin_timeout_us: bound of every wait (0 = 2 s);
+ * on expiry XS_ETIMEOUT goes to dev_status and the kernel exits. workspace: device bytes from
+ * xs_dispatch_ring_workspace_bytes(W, S) (control words; cleared by the call). stats:
+ * optional device int32 [2W]: entries per destination, then productions that found their
+ * slot still occupied. Status words as xs_dispatch (XS_ECAPACITY for rows beyond a window,
+ * XS_EBADINPUT for bad experts). Argument errors: XS_EINVAL / XS_EUNSUPPORTED /
+ * XS_EWORKSPACE, nothing launched. */
+int xs_ring_slot_bytes(int32_t H, int32_t k, int64_t* bytes);
+int xs_dispatch_ring_workspace_bytes(int32_t W, int32_t slots, int64_t* bytes);
+int xs_dispatch_ring(const void* x, int32_t T, int32_t H, const int32_t* topk_idx,
+                     const int32_t* slot_row, int32_t k, int32_t E, const xs_window* win, int32_t W,
+                     const xs_window* rings, int32_t dedup, int32_t max_producers,
+                     int64_t spin_timeout_us, void* workspace, int64_t workspace_bytes,
+                     int32_t* stats, int32_t* dev_status, void* stream);
+
 /* ----------------------------------------------------------------------------- EP layer
  * One rank's share of an expert-parallel MoE layer (Sec. 4.3). Experts
  * [e_begin, e_begin + n_experts) are computed here; they must be whole windows

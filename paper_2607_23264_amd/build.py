@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libxstage.so")
 BUILD = os.path.join(ROOT, "_build")
 
-SOURCES = ["xs_runtime.hip", "xs_ep.hip", "xs_gemm.hip", "xs_ep_ffn.hip", "xs_attn.hip", "xs_mx.hip", "xs_microbench.hip",
+SOURCES = ["xs_runtime.hip", "xs_ep.hip", "xs_gemm.hip", "xs_ep_ffn.hip", "xs_attn.hip", "xs_mx.hip", "xs_ring.hip", "xs_microbench.hip",
            "xs_model.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
