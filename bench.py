@@ -53,6 +53,7 @@ def parse():
     p.add_argument("--policies", action="store_true",
                    help="also time the fused layer under every pacing policy (phases)")
     p.add_argument("--no-mx", action="store_true", help="skip the MXFP8 (W8A8) and W4A8 layer lines")
+    p.add_argument("--no-ring", action="store_true", help="skip the bounded-ring dispatch line")
     p.add_argument("--seed", type=int, default=0)
     return p.parse_args()
 
@@ -303,6 +304,100 @@ def mx_line(X, torch, cfg, inp, rank, experts, pol, steps, warmup, bf16_step_us,
                          "avg_launch_us": ffn_us, "hbm_GBps_algorithmic": alg_bytes / (ffn_us * 1e-6) / 1e9}}
 
 
+def gpu_route_layout(X, torch, logits, k, E, W):
+    """Top-k route and dispatch layout of one source on the GPU (the library's own calls).
+    Returns device (topk_idx [T][k], slot_row [T][k]) and the host dest_counts [W]."""
+    import ctypes as C
+    T = logits.shape[0]
+    stream = torch.cuda.current_stream().cuda_stream
+    lg = torch.from_numpy(np.ascontiguousarray(logits, dtype=np.float32)).cuda()
+    idx = torch.empty((T, k), dtype=torch.int32, device="cuda")
+    w = torch.empty((T, k), dtype=torch.float32, device="cuda")
+    X.check(X.xs_route_topk_softmax(lg.data_ptr(), T, E, k, 0, idx.data_ptr(), w.data_ptr(), stream))
+    cap = T * k
+    i32 = dict(dtype=torch.int32, device="cuda")
+    ec, sb, eo = torch.empty((1, E), **i32), torch.empty((1, E), **i32), torch.empty((E,), **i32)
+    dc, sr, rs = torch.empty((W,), **i32), torch.empty((T, k), **i32), torch.empty((W, cap), **i32)
+    st = torch.zeros((1,), **i32)
+    nb = C.c_int64()
+    X.check(X.xs_dispatch_layout_workspace_bytes(1, T, E, C.byref(nb)))
+    ws = torch.empty((max(1, nb.value),), dtype=torch.uint8, device="cuda")
+    X.check(X.xs_dispatch_layout(idx.data_ptr(), 1, T, k, E, W, cap, ec.data_ptr(), sb.data_ptr(), eo.data_ptr(),
+                                 dc.data_ptr(), sr.data_ptr(), rs.data_ptr(), ws.data_ptr(), ws.numel(),
+                                 st.data_ptr(), stream))
+    torch.cuda.synchronize()
+    if int(st.item()):
+        raise RuntimeError(f"layout status {int(st.item())}")
+    return idx, sr, dc.cpu().numpy()
+
+
+def ring_line(X, torch, synth, reps=5):
+    """Dispatch of one source of the share through bounded destination rings: time, entries,
+    producer stalls and ring bytes for ring sizes S and per-destination dedup, rings in HBM
+    and (a slow sink) in host-coherent memory, against the plain dispatch."""
+    import ctypes as C
+    from paper_2607_23264_amd.layer import HostCoherent
+    cfg = synth.EP_DSV3_SHARE
+    T, H, k, E, W = cfg.T, cfg.H, cfg.k, cfg.E, cfg.W
+    di, ds, dest_counts = gpu_route_layout(X, torch, synth.ep_logits(cfg, 0)[0], k, E, W)
+    cap = int(dest_counts.max())
+    dx = torch.from_numpy(np.ascontiguousarray(synth.ep_x(cfg, 0)[0]).view(np.int16)).cuda()
+    win = torch.empty((W, cap, H), dtype=torch.int16, device="cuda")
+    wins = X.windows([X.window(win[d]) for d in range(W)])
+    st = torch.zeros((1,), dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    nb = C.c_int64()
+    X.check(X.xs_ring_slot_bytes(H, k, C.byref(nb)))
+    slot_bytes = nb.value
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e3
+
+    plain_us = timed(lambda: X.check(X.xs_dispatch(dx.data_ptr(), T, H, di.data_ptr(), ds.data_ptr(), k, E, wins,
+                                                   W, st.data_ptr(), stream)))
+    window_bytes = T * k * H * 2
+    cells = []
+    for sink in ("hbm", "host"):
+        for S in ((4, 16, 64, 256, 4096) if sink == "hbm" else (16, 256)):
+            ring_mem = HostCoherent(W * S * slot_bytes) if sink == "host" else \
+                torch.empty((W * S * slot_bytes,), dtype=torch.uint8, device="cuda")
+            base = ring_mem.ptr if sink == "host" else ring_mem.data_ptr()
+            rings = X.windows([X.window((base + d * S * slot_bytes, S, slot_bytes)) for d in range(W)])
+            X.check(X.xs_dispatch_ring_workspace_bytes(T, k, W, S, C.byref(nb)))
+            ws = torch.zeros((nb.value,), dtype=torch.uint8, device="cuda")
+            stats = torch.zeros((2 * W,), dtype=torch.int32, device="cuda")
+            for dedup in (0, 1):
+                us = timed(lambda: X.check(X.xs_dispatch_ring(
+                    dx.data_ptr(), T, H, di.data_ptr(), ds.data_ptr(), k, E, wins, W, rings, dedup, 0, 0,
+                    ws.data_ptr(), ws.numel(), stats.data_ptr(), st.data_ptr(), stream)))
+                sv = stats.cpu().numpy()
+                entries = int(sv[:W].sum())
+                cells.append({"sink": sink, "slots": S, "dedup": dedup, "us": us, "entries": entries,
+                              "stalls": int(sv[W:].sum()), "ring_bytes": entries * slot_bytes,
+                              "window_GBps": window_bytes / (us * 1e-6) / 1e9})
+            torch.cuda.synchronize()
+            if sink == "host":
+                ring_mem.free()
+            else:
+                del ring_mem
+    status = int(st.item())
+    if status:
+        raise RuntimeError(f"ring dispatch: device status {status}: {X.xs_strerror(status).decode()}")
+    no_dd = next(c["entries"] for c in cells if c["dedup"] == 0)
+    dd = next(c["entries"] for c in cells if c["dedup"] == 1)
+    return {"workload": f"one source of {cfg.name}: {T} tokens, top-{k} of {E} experts, {W} destinations",
+            "plain_dispatch_us": plain_us, "slot_bytes": slot_bytes, "entries_without_dedup": no_dd,
+            "entries_with_dedup": dd, "dedup_ratio": no_dd / dd, "cells": cells}
+
+
 def main():
     a = parse()
     if a.gpus != 1:
@@ -322,11 +417,10 @@ def main():
     inp = {"logits": synth.ep_logits(cfg, a.seed), "x": synth.ep_x(cfg, a.seed)}
     rank = 0
     if a.routing == "zipf":
-        from oracle.ep import route_topk_softmax  # only to pick the most-loaded rank for the sample
+        # the most loaded destination, from the library's own routing of every source
         loads = np.zeros(cfg.W, np.int64)
         for s in range(cfg.n_src):
-            loads += np.bincount(route_topk_softmax(inp["logits"][s], cfg.k)[0].ravel() // cfg.E_local,
-                                 minlength=cfg.W)
+            loads += gpu_route_layout(X, torch, inp["logits"][s], cfg.k, cfg.E, cfg.W)[2]
         rank = int(loads.argmax())
     cfg = dataclasses.replace(cfg, rank=rank)
     experts = synth.computed_experts(cfg)
@@ -461,6 +555,12 @@ def main():
                                                     a.warmup, ms_per_step * 1e3, prec)
             log(f"[bench] {prec}: {m['us_per_step']:.1f} us/step ({m['speedup_vs_bf16']:.2f}x bf16), FFN kernel "
                 f"{m['roofline']['avg_launch_us']:.1f} us ({m['roofline']['achieved']:.1f} TFLOP/s)")
+    if not a.no_ring:
+        log("[bench] dispatch through bounded destination rings")
+        res["dispatch_ring"] = ring_line(X, torch, synth)
+        r = res["dispatch_ring"]
+        log(f"[bench] ring dispatch: plain {r['plain_dispatch_us']:.1f} us; dedup ratio {r['dedup_ratio']:.2f}; " +
+            ", ".join(f"{c['sink']} S={c['slots']} dd={c['dedup']}: {c['us']:.0f} us" for c in r["cells"]))
     if not a.no_phases:
         log("[bench] store ceiling")
         res["store_ceiling"] = store_ceiling(X, torch)

@@ -135,20 +135,21 @@ int xs_dispatch_rows(const void* rows, int64_t row_stride, int32_t row_bytes, in
  * token row of x [T][H] plus a header naming the rows of window d it is copied into: with
  * dedup = 1 one entry per (token, destination) listing every k slot of the token there, with
  * dedup = 0 one entry per (token, k) slot. Lifetime protocol: the producer of entry n
- * (numbered per ring in claim order) fills slot n mod S only after entry n - S has been
- * copied out and released; the consumer copies an entry into its window rows
+ * (numbered per ring in token order, then k slot order) fills slot n mod S only after entry
+ * n - S has been copied out and released; the consumer copies an entry into its window rows
  * (slot_row[t][j] of win[d]) and then releases the slot. Workgroups produce their tokens'
  * entries and consume entries, a stalled producer draining the entries it waits on, so the
  * call completes for any S >= 1. The windows end equal to xs_dispatch's.
  * max_producers: workgroups (0 = one per CU). spin_timeout_us: bound of every wait (0 = 2 s);
  * on expiry XS_ETIMEOUT goes to dev_status and the kernel exits. workspace: device bytes from
- * xs_dispatch_ring_workspace_bytes(W, S) (control words; cleared by the call). stats:
+ * xs_dispatch_ring_workspace_bytes(T, k, W, S) (control words and entry numbers; rewritten
+ * by every call). stats:
  * optional device int32 [2W]: entries per destination, then productions that found their
  * slot still occupied. Status words as xs_dispatch (XS_ECAPACITY for rows beyond a window,
  * XS_EBADINPUT for bad experts). Argument errors: XS_EINVAL / XS_EUNSUPPORTED /
  * XS_EWORKSPACE, nothing launched. */
 int xs_ring_slot_bytes(int32_t H, int32_t k, int64_t* bytes);
-int xs_dispatch_ring_workspace_bytes(int32_t W, int32_t slots, int64_t* bytes);
+int xs_dispatch_ring_workspace_bytes(int32_t T, int32_t k, int32_t W, int32_t slots, int64_t* bytes);
 int xs_dispatch_ring(const void* x, int32_t T, int32_t H, const int32_t* topk_idx,
                      const int32_t* slot_row, int32_t k, int32_t E, const xs_window* win, int32_t W,
                      const xs_window* rings, int32_t dedup, int32_t max_producers,

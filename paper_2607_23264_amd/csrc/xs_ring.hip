@@ -3,8 +3,8 @@
 //
 // Each destination d owns a ring of S slots. An entry is one token row plus a header listing
 // the rows of d's dispatch window it goes to: every (token, k) slot of that destination when
-// deduplicating, one slot otherwise. Entries of a ring are numbered by an atomic head counter
-// in the order producers claim them; entry n lives in slot n mod S.
+// deduplicating, one slot otherwise. Entries of a ring are numbered in token order (then k slot
+// order) by a prefix scan before the dispatch; entry n lives in slot n mod S.
 //
 // Lifetime protocol (per slot two words, counting completed uses):
 //   pub[s] = u + 1  entry n = u S + s is written (system-scope release by its producer);
@@ -14,13 +14,20 @@
 // counter, waits for pub == n / S + 1 (acquire), copies the row into every listed window row,
 // then releases the slot.
 //
+// Agents are waves: each produces its tokens' entries and consumes entries on its own, with no
+// workgroup barrier in the protocol, so about two thousand entries are in flight at once.
+// Each claim counter sits on a 128-byte line of its own (counters sharing a line serialise
+// every claim of every ring at one L2 atomic unit).
+//
 // Progress: a producer waiting for its slot helps: while the tail has not passed n - S it
 // claims and consumes the oldest entries itself, so the entry it waits for is always either
-// being consumed or consumable by it. Those entries were claimed by earlier producers, which
-// never wait on this one. A workgroup that has produced all its entries drains the rings
-// until every entry is consumed. Every wait is bounded: on time-out a workgroup reports
-// XS_ETIMEOUT and raises an abort word that makes every other wait give up, so the grid
-// always drains.
+// being consumed or consumable by it. Those entries belong to earlier tokens, whose producers
+// are behind this one in token order and so never wait on it. An agent that has produced all
+// its entries drains the rings until every entry is consumed. Every wait is bounded: on
+// time-out an agent reports XS_ETIMEOUT and raises an abort word that makes every other wait
+// give up, so the grid always drains. Same-address device-scope atomics are slow on this
+// GPU (measured: ~0.4 us each, serialised, when every entry took one): producers take no
+// atomic, and a draining agent claims eight entries per atomic.
 #include <algorithm>
 
 #include "xs_common.hpp"
@@ -28,8 +35,10 @@
 namespace xs {
 namespace ring {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 256;         // four waves; every wave is an independent agent
 constexpr int kMaxK = 32;
+constexpr int kLine = 32;             // ints per 128-byte line: one counter per line
+constexpr int kBatch = 8;             // entries a draining agent claims per atomic
 
 struct RingArgs {
   const char* x;               // token rows, x_stride bytes apart
@@ -41,63 +50,75 @@ struct RingArgs {
   WinSet win;                  // dispatch windows
   char* ring[XS_MAX_WINDOWS];  // ring memory per destination: S slots of slot_bytes
   int64_t slot_bytes;          // payload, then 1 + k header ints
-  int* head;                   // [W] producer claim counters
-  int* tail;                   // [W] consumer claim counters
-  int* total;                  // [W] entries per destination
+  int* entry_no;               // [T][k] entry number of each (token, k) slot in its ring
+  int* tail;                   // [W] consumer claim counters, one per line
+  int* total;                  // [W] entries per destination, one per line
   int* abort_word;
   int* pub;                    // [W][S]
-  int* rel;                        // [W][S]
+  int* rel;                    // [W][S]
   int* stats;                  // optional [2W]: entries, producer stalls
   int* status;
   int64_t timeout_ticks;
 };
 
-// Entries per destination and a clean control block (one workgroup).
+// Entry numbers, entries per destination and a clean control block (one workgroup of 1024).
+// Entries of ring d are numbered in token order (and k slot order within a token without
+// dedup): for each destination an exclusive scan over contiguous token chunks, one per thread.
 __global__ __launch_bounds__(1024) void ring_plan_kernel(RingArgs a) {
-  __shared__ int cnt[XS_MAX_WINDOWS];
+  __shared__ int scan[1024];
   const int W = a.win.n;
   const int epw = a.E / W;
-  for (int i = threadIdx.x; i < W; i += blockDim.x) {
-    cnt[i] = 0;
-    a.head[i] = 0;
-    a.tail[i] = 0;
-  }
-  if (threadIdx.x == 0) *a.abort_word = 0;
-  for (int64_t i = threadIdx.x; i < static_cast<int64_t>(W) * a.S; i += blockDim.x) {
+  const int tid = threadIdx.x;
+  for (int i = tid; i < W; i += blockDim.x) a.tail[i * kLine] = 0;
+  if (tid == 0) *a.abort_word = 0;
+  for (int64_t i = tid; i < static_cast<int64_t>(W) * a.S; i += blockDim.x) {
     a.pub[i] = 0;
     a.rel[i] = 0;
   }
-  __syncthreads();
-  for (int t = threadIdx.x; t < a.T; t += blockDim.x) {
-    uint64_t seen = 0;
-    for (int j = 0; j < a.k; ++j) {
-      const int e = a.idx[static_cast<int64_t>(t) * a.k + j];
-      if (e < 0 || e >= a.E) continue;
-      const int d = e / epw;
-      if (!a.dedup) {
-        atomicAdd(&cnt[d], 1);
-      } else if (!(seen >> d & 1ull)) {
-        seen |= 1ull << d;
-        atomicAdd(&cnt[d], 1);
+  const int chunk = (a.T + blockDim.x - 1) / blockDim.x;
+  const int t0 = min(a.T, tid * chunk), t1 = min(a.T, t0 + chunk);
+  for (int d = 0; d < W; ++d) {
+    int n = 0;
+    for (int t = t0; t < t1; ++t) {
+      bool any = false;
+      for (int j = 0; j < a.k; ++j) {
+        const int e = a.idx[static_cast<int64_t>(t) * a.k + j];
+        if (e < 0 || e >= a.E || e / epw != d) continue;
+        if (!a.dedup) ++n;
+        any = true;
+      }
+      if (a.dedup && any) ++n;
+    }
+    scan[tid] = n;
+    __syncthreads();
+    for (int off = 1; off < static_cast<int>(blockDim.x); off <<= 1) {   // inclusive scan
+      const int v = tid >= off ? scan[tid - off] : 0;
+      __syncthreads();
+      scan[tid] += v;
+      __syncthreads();
+    }
+    int next = scan[tid] - n;                                            // exclusive
+    for (int t = t0; t < t1; ++t) {
+      bool any = false;
+      for (int j = 0; j < a.k; ++j) {
+        const int64_t q = static_cast<int64_t>(t) * a.k + j;
+        const int e = a.idx[q];
+        if (e < 0 || e >= a.E || e / epw != d) continue;
+        a.entry_no[q] = a.dedup ? next : next++;
+        any = true;
+      }
+      if (a.dedup && any) ++next;
+    }
+    if (tid == blockDim.x - 1) {
+      a.total[d * kLine] = scan[tid];
+      if (a.stats) {
+        a.stats[d] = scan[tid];
+        a.stats[W + d] = 0;
       }
     }
-  }
-  __syncthreads();
-  for (int i = threadIdx.x; i < W; i += blockDim.x) {
-    a.total[i] = cnt[i];
-    if (a.stats) {
-      a.stats[i] = cnt[i];
-      a.stats[W + i] = 0;
-    }
+    __syncthreads();
   }
 }
-
-struct Shared {
-  int d[kMaxK], r[kMaxK];      // this token's (destination, window row) pairs, by destination
-  int nent, ent_first[kMaxK], ent_n[kMaxK];
-  int state, value;            // broadcast words
-  int hdr[kMaxK + 1];          // header of the entry being consumed
-};
 
 __device__ __forceinline__ bool aborted(const RingArgs& a) {
   return __hip_atomic_load(a.abort_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
@@ -108,184 +129,216 @@ __device__ __forceinline__ void give_up(const RingArgs& a) {
   __hip_atomic_store(a.abort_word, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// 16-byte copy of one payload by the whole workgroup.
-__device__ __forceinline__ void copy_row(char* dst, const char* src, int bytes) {
-  typedef __attribute__((address_space(1))) u32x4 gv;
-  for (int o = threadIdx.x * 16; o < bytes; o += kThreads * 16)
-    *(gv*)(dst + o) = *(const gv*)(src + o);
-}
+__device__ __forceinline__ int bcast(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
-// Consume entry m of ring d (already claimed by this workgroup). False on abort.
-__device__ bool consume(const RingArgs& a, int d, int m, Shared& sh) {
-  const int s = m % a.S;
-  const int u = m / a.S;
-  int* pub = a.pub + static_cast<int64_t>(d) * a.S + s;
-  int* rel = a.rel + static_cast<int64_t>(d) * a.S + s;
-  const char* slot = a.ring[d] + static_cast<int64_t>(s) * a.slot_bytes;
-  if (threadIdx.x == 0) {
-    int ok = 1;
-    if (__hip_atomic_load(pub, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != u + 1) {
-      const uint64_t t0 = wall_ticks();
-      while (__hip_atomic_load(pub, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != u + 1) {
-        if (aborted(a)) { ok = 0; break; }
-        if (wall_ticks() - t0 > static_cast<uint64_t>(a.timeout_ticks)) { give_up(a); ok = 0; break; }
-        __builtin_amdgcn_s_sleep(1);
+typedef __attribute__((address_space(1))) u32x4 gv4;
+
+// Consume entries [m0, m0 + nb) of ring d (claimed by this wave, nb <= min(64, S)): wait
+// until all are published, one acquire, one read of each ring row with one store per listed
+// window row, one release, then the nb slot releases. nb <= S, so no entry of the batch
+// waits on a slot the batch itself holds. False on abort. Wave-uniform control flow.
+__device__ bool consume(const RingArgs& a, int d, int m0, int nb, int lane) {
+  const int m = m0 + min(lane, nb - 1);
+  const int* pub_i = a.pub + static_cast<int64_t>(d) * a.S + m % a.S;
+  const int want = m / a.S + 1;
+  if (__ballot(lane < nb && __hip_atomic_load(pub_i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != want)) {
+    const uint64_t t0 = wall_ticks();
+    for (int it = 1;; ++it) {
+      const bool pending =
+          __ballot(lane < nb && __hip_atomic_load(pub_i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != want) != 0;
+      if (!pending) break;
+      int stop = 0;
+      if (lane == 0) {
+        if ((it & 15) == 0 && aborted(a)) stop = 1;
+        else if (wall_ticks() - t0 > static_cast<uint64_t>(a.timeout_ticks)) { give_up(a); stop = 1; }
+      }
+      if (bcast(stop)) return false;
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
+  const int pieces = a.row_bytes >> 4;
+  for (int b = 0; b < nb; ++b) {
+    const int mb = m0 + b;
+    const char* slot = a.ring[d] + static_cast<int64_t>(mb % a.S) * a.slot_bytes;
+    const int* h = reinterpret_cast<const int*>(slot + a.row_bytes);
+    int n = bcast(lane == 0 ? h[0] : 0);
+    if (n < 0 || n > a.k) {               // never written by a producer: report, copy nothing
+      if (lane == 0) set_status(a.status, XS_EBADINPUT);
+      n = 0;
+    }
+    const int my_row = lane < n ? h[1 + lane] : -1;
+    for (int p0 = 0; p0 < pieces; p0 += 64 * 8) {
+      u32x4 v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int p = p0 + q * 64 + lane;
+        if (p < pieces) v[q] = *(const gv4*)(slot + p * 16);
+      }
+      for (int i = 0; i < n; ++i) {
+        const int r = __shfl(my_row, i);
+        if (r < 0 || r >= a.win.cap[d]) {
+          if (lane == 0 && p0 == 0) set_status(a.status, XS_ECAPACITY);
+          continue;
+        }
+        char* dst = a.win.base[d] + static_cast<int64_t>(r) * a.win.stride[d];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int p = p0 + q * 64 + lane;
+          if (p < pieces) *(gv4*)(dst + p * 16) = v[q];
+        }
       }
     }
-    if (ok) {
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
-      const int* h = reinterpret_cast<const int*>(slot + a.row_bytes);
-      int n = h[0];
-      if (n < 0 || n > a.k) {                 // never written by a producer: report, copy nothing
-        set_status(a.status, XS_EBADINPUT);
-        n = 0;
-      }
-      sh.hdr[0] = n;
-      for (int i = 0; i < n; ++i) sh.hdr[1 + i] = h[1 + i];
-    }
-    sh.state = ok;
   }
-  __syncthreads();
-  const bool ok = sh.state != 0;
-  const int n = sh.hdr[0];
-  __syncthreads();
-  if (!ok) return false;
-  for (int i = 0; i < n; ++i) {
-    const int r = sh.hdr[1 + i];
-    if (r < 0 || r >= a.win.cap[d]) {
-      if (threadIdx.x == 0) set_status(a.status, XS_ECAPACITY);
-      continue;
-    }
-    copy_row(a.win.base[d] + static_cast<int64_t>(r) * a.win.stride[d], slot, a.row_bytes);
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_store(rel, u + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+  // every lane's reads of the slots are done before they are released
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
+  if (lane < nb)
+    __hip_atomic_store(a.rel + static_cast<int64_t>(d) * a.S + m % a.S, m / a.S + 1, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_SYSTEM);
   return true;
 }
 
-// Produce one entry of token t into ring d with window rows sh.r[first, first + n).
-__device__ bool produce(const RingArgs& a, int t, int d, int first, int n, Shared& sh) {
-  int* head = a.head + d;
-  if (threadIdx.x == 0) sh.value = atomicAdd(head, 1);
-  __syncthreads();
-  const int e = sh.value;
-  __syncthreads();
+// Entries a producer has written but not yet published: lane i < n holds the i-th flag and
+// its value. One release fence makes all of them visible; a producer publishes before it
+// ever waits, so no consumer waits on an entry whose producer is itself waiting.
+constexpr int kPend = 32;
+struct Pending {
+  int* flag;
+  int val;
+  int n;
+};
+
+__device__ __forceinline__ void publish(Pending& p, int lane) {
+  if (p.n == 0) return;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
+  if (lane < p.n) __hip_atomic_store(p.flag, p.val, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  p.n = 0;
+}
+
+// Produce entry e of token t into ring d: the window rows of the lanes in `mask` (each lane j
+// holds slot j's row in my_row). The entry is left pending. False on abort.
+__device__ bool produce(const RingArgs& a, int t, int d, int e, uint64_t mask, int my_row, int lane, Pending& pend) {
   const int s = e % a.S;
   const int u = e / a.S;
   int* rel = a.rel + static_cast<int64_t>(d) * a.S + s;
   int* pub = a.pub + static_cast<int64_t>(d) * a.S + s;
   bool stalled = false;
   const uint64_t t0 = wall_ticks();
-  for (;;) {
-    // state: 1 slot free, 0 abort, 2 help with entry value, 3 wait
-    if (threadIdx.x == 0) {
-      int st;
-      if (__hip_atomic_load(rel, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) == u) {
+  for (int it = 0;; ++it) {
+    // 1 slot free, 0 abort, 2 help with entry m, 3 wait
+    int st = 3, m = 0;
+    if (lane == 0) {
+      if (__hip_atomic_load(rel, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == u) {
         st = 1;
-      } else if (aborted(a)) {
+      } else if ((it & 15) == 15 && aborted(a)) {
         st = 0;
       } else if (wall_ticks() - t0 > static_cast<uint64_t>(a.timeout_ticks)) {
         give_up(a);
         st = 0;
       } else {
-        st = 3;
-        int m = __hip_atomic_load(a.tail + d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (m <= e - a.S && m < a.total[d] &&
-            __hip_atomic_compare_exchange_strong(a.tail + d, &m, m + 1, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_AGENT)) {
+        m = __hip_atomic_load(a.tail + d * kLine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (m <= e - a.S && m < a.total[d * kLine] &&
+            __hip_atomic_compare_exchange_strong(a.tail + d * kLine, &m, m + 1, __ATOMIC_RELAXED,
+                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
           st = 2;
-          sh.value = m;
-        } else {
+        else
           __builtin_amdgcn_s_sleep(1);
-        }
       }
-      sh.state = st;
     }
-    __syncthreads();
-    const int st = sh.state;
-    const int m = sh.value;
-    __syncthreads();
+    st = bcast(st);
+    m = bcast(m);
     if (st == 1) break;
     if (st == 0) return false;
+    if (!stalled) publish(pend, lane);     // never wait holding unpublished entries
     stalled = true;
-    if (st == 2 && !consume(a, d, m, sh)) return false;
+    if (st == 2 && !consume(a, d, m, 1, lane)) return false;
   }
-  if (threadIdx.x == 0) {
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");   // the slot's last reader is done
-    if (stalled && a.stats) atomicAdd(a.stats + a.win.n + d, 1);
-  }
-  __syncthreads();
+  // only orders this wave's stores below after the observation (a write after the last
+  // reader's reads): nothing is read here, so no cache maintenance
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  if (stalled && lane == 0 && a.stats) atomicAdd(a.stats + a.win.n + d, 1);
   char* slot = a.ring[d] + static_cast<int64_t>(s) * a.slot_bytes;
-  copy_row(slot, a.x + static_cast<int64_t>(t) * a.x_stride, a.row_bytes);
-  if (threadIdx.x == 0) {
-    int* h = reinterpret_cast<int*>(slot + a.row_bytes);
-    h[0] = n;
-    for (int i = 0; i < n; ++i) h[1 + i] = sh.r[first + i];
+  const char* src = a.x + static_cast<int64_t>(t) * a.x_stride;
+  const int pieces = a.row_bytes >> 4;
+  for (int p0 = 0; p0 < pieces; p0 += 64 * 8) {
+    u32x4 v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int p = p0 + q * 64 + lane;
+      if (p < pieces) v[q] = *(const gv4*)(src + p * 16);
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int p = p0 + q * 64 + lane;
+      if (p < pieces) *(gv4*)(slot + p * 16) = v[q];
+    }
   }
-  __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_store(pub, u + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+  // header: the number of rows, then the rows in ascending k slot order
+  int* hdr = reinterpret_cast<int*>(slot + a.row_bytes);
+  if ((mask >> lane) & 1ull) hdr[1 + __builtin_popcountll(mask & ((1ull << lane) - 1))] = my_row;
+  if (lane == 0) hdr[0] = __builtin_popcountll(mask);
+  if (lane == pend.n) {
+    pend.flag = pub;
+    pend.val = u + 1;
+  }
+  if (++pend.n == kPend) publish(pend, lane);
   return true;
 }
 
 __global__ __launch_bounds__(kThreads) void ring_dispatch_kernel(RingArgs a) {
-  __shared__ Shared sh;
+  const int lane = threadIdx.x & 63;
+  const int agents = gridDim.x * (kThreads / 64);
+  const int me = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
   const int W = a.win.n;
   const int epw = a.E / W;
-  for (int t = blockIdx.x; t < a.T; t += gridDim.x) {
-    if (threadIdx.x == 0) {
-      // (destination, window row) pairs of the valid slots, stably ordered by destination
-      int n = 0;
-      for (int j = 0; j < a.k; ++j) {
-        const int e = a.idx[static_cast<int64_t>(t) * a.k + j];
-        if (e < 0 || e >= a.E) {
-          set_status(a.status, XS_EBADINPUT);
-          continue;
-        }
-        const int d = e / epw, r = a.slot_row[static_cast<int64_t>(t) * a.k + j];
-        int p = n++;
-        if (a.dedup)
-          for (; p > 0 && sh.d[p - 1] > d; --p) {
-            sh.d[p] = sh.d[p - 1];
-            sh.r[p] = sh.r[p - 1];
-          }
-        sh.d[p] = d;
-        sh.r[p] = r;
+  // Odd waves consume from the start (the receivers), even waves produce in token order: a
+  // full ring then drains at the consumers' rate rather than through stalled producers'
+  // help. Both drain at the end.
+  const bool consumer = agents > 1 && (me & 1);
+  const int producers = agents > 1 ? agents / 2 : 1;
+  Pending pend{nullptr, 0, 0};
+  for (int t = consumer ? a.T : (agents > 1 ? me / 2 : me); t < a.T; t += producers) {
+    // lane j < k holds slot j's destination, window row and entry number
+    int d = -1, r = -1, en = 0;
+    if (lane < a.k) {
+      const int64_t q = static_cast<int64_t>(t) * a.k + lane;
+      const int e = a.idx[q];
+      if (e < 0 || e >= a.E) {
+        set_status(a.status, XS_EBADINPUT);
+      } else {
+        d = e / epw;
+        r = a.slot_row[q];
+        en = a.entry_no[q];
       }
-      int ne = 0;
-      for (int p = 0; p < n; ++p) {
-        if (a.dedup && ne > 0 && sh.d[sh.ent_first[ne - 1]] == sh.d[p]) {
-          ++sh.ent_n[ne - 1];
-        } else {
-          sh.ent_first[ne] = p;
-          sh.ent_n[ne] = 1;
-          ++ne;
-        }
-      }
-      sh.nent = ne;
     }
-    __syncthreads();
-    const int ne = sh.nent;
-    for (int i = 0; i < ne; ++i) {
-      const int first = sh.ent_first[i];
-      if (!produce(a, t, sh.d[first], first, sh.ent_n[i], sh)) return;
+    uint64_t todo = __ballot(d >= 0);
+    while (todo) {
+      const int lead = __builtin_ctzll(todo);
+      const int dd = __shfl(d, lead);
+      // the entry's lanes: this slot alone, or every slot of the token on destination dd
+      const uint64_t mask = a.dedup ? __ballot(d == dd) : (1ull << lead);
+      todo &= ~mask;
+      if (!produce(a, t, dd, __shfl(en, lead), mask, r, lane, pend)) return;
     }
   }
-  // drain: consume whatever is left, ring by ring
+  publish(pend, lane);
+  // drain: consume whatever is left, ring by ring, claiming up to kBatch entries per atomic
+  // (never more than S: see consume)
+  const int batch = min(kBatch, a.S);
   for (int i = 0; i < W; ++i) {
-    const int d = (blockIdx.x + i) % W;
+    const int d = (me + i) % W;
+    const int tot = a.total[d * kLine];
     for (;;) {
-      if (threadIdx.x == 0) {
-        const int m = __hip_atomic_load(a.tail + d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        sh.value = m < a.total[d] ? atomicAdd(a.tail + d, 1) : a.total[d];
-        sh.state = aborted(a) ? 0 : 1;
+      int m = 0, ok = 1;
+      if (lane == 0) {
+        ok = aborted(a) ? 0 : 1;
+        m = __hip_atomic_load(a.tail + d * kLine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        m = m < tot ? atomicAdd(a.tail + d * kLine, batch) : tot;
       }
-      __syncthreads();
-      const int m = sh.value;
-      const int ok = sh.state;
-      __syncthreads();
-      if (!ok) return;
-      if (m >= a.total[d]) break;
-      if (!consume(a, d, m, sh)) return;
+      if (!bcast(ok)) return;
+      m = bcast(m);
+      if (m >= tot) break;
+      if (!consume(a, d, m, min(batch, tot - m), lane)) return;
     }
   }
 }
@@ -303,9 +356,14 @@ namespace {
 
 int64_t align16(int64_t v) { return (v + 15) / 16 * 16; }
 
-// Control block in the workspace: head, tail, total [W] each, the abort word, then pub and rel
-// [W][S] each.
-int64_t ctrl_ints(int32_t W, int32_t S) { return 4 * static_cast<int64_t>(XS_MAX_WINDOWS) + 2 * static_cast<int64_t>(W) * S; }
+// Control block in the workspace: tail and total [W] each, one counter per 128-byte line, the
+// abort word on a line of its own, then pub and rel [W][S] each.
+constexpr int64_t kCtrlTail = 0, kCtrlTotal = XS_MAX_WINDOWS * 32, kCtrlAbort = 2 * XS_MAX_WINDOWS * 32,
+                  kCtrlPub = 2 * XS_MAX_WINDOWS * 32 + 32;
+// control words, then the entry numbers [T][k]
+int64_t ctrl_ints(int32_t T, int32_t k, int32_t W, int32_t S) {
+  return kCtrlPub + 2 * static_cast<int64_t>(W) * S + static_cast<int64_t>(T) * k;
+}
 
 }  // namespace
 
@@ -315,9 +373,9 @@ extern "C" int xs_ring_slot_bytes(int32_t H, int32_t k, int64_t* bytes) {
   return XS_OK;
 }
 
-extern "C" int xs_dispatch_ring_workspace_bytes(int32_t W, int32_t slots, int64_t* bytes) {
-  if (!bytes || W < 1 || W > XS_MAX_WINDOWS || slots < 1) return XS_EINVAL;
-  *bytes = ctrl_ints(W, slots) * 4;
+extern "C" int xs_dispatch_ring_workspace_bytes(int32_t T, int32_t k, int32_t W, int32_t slots, int64_t* bytes) {
+  if (!bytes || T < 0 || k < 1 || W < 1 || W > XS_MAX_WINDOWS || slots < 1) return XS_EINVAL;
+  *bytes = ctrl_ints(T, k, W, slots) * 4;
   return XS_OK;
 }
 
@@ -347,7 +405,7 @@ extern "C" int xs_dispatch_ring(const void* x, int32_t T, int32_t H, const int32
   for (int d = 0; d < W; ++d)
     if (rings[d].row_stride_bytes != rings[0].row_stride_bytes) return XS_EINVAL;
   int64_t need = 0;
-  xs_dispatch_ring_workspace_bytes(W, S, &need);
+  xs_dispatch_ring_workspace_bytes(T, k, W, S, &need);
   if (!workspace || workspace_bytes < need) return XS_EWORKSPACE;
   const int rc = xs_host::make_winset(win, W, static_cast<int64_t>(H) * 2, &a.win);
   if (rc) return rc;
@@ -363,12 +421,12 @@ extern "C" int xs_dispatch_ring(const void* x, int32_t T, int32_t H, const int32
   a.idx = topk_idx;
   a.slot_row = slot_row;
   a.slot_bytes = rings[0].row_stride_bytes;
-  a.head = ctrl;
-  a.tail = ctrl + XS_MAX_WINDOWS;
-  a.total = ctrl + 2 * XS_MAX_WINDOWS;
-  a.abort_word = ctrl + 3 * XS_MAX_WINDOWS;
-  a.pub = ctrl + 4 * XS_MAX_WINDOWS;
+  a.tail = ctrl + kCtrlTail;
+  a.total = ctrl + kCtrlTotal;
+  a.abort_word = ctrl + kCtrlAbort;
+  a.pub = ctrl + kCtrlPub;
   a.rel = a.pub + static_cast<int64_t>(W) * S;
+  a.entry_no = a.rel + static_cast<int64_t>(W) * S;
   a.stats = stats;
   a.status = dev_status;
   a.timeout_ticks = xs_host::ns_to_ticks((spin_timeout_us > 0 ? spin_timeout_us : 2000000) * 1000);
@@ -376,7 +434,8 @@ extern "C" int xs_dispatch_ring(const void* x, int32_t T, int32_t H, const int32
   hipLaunchKernelGGL(ring::ring_plan_kernel, dim3(1), dim3(1024), 0, st, a);
   if (xs_host::launch_status()) return XS_EHIP;
   if (T > 0) {
-    const int grid = std::min(T, xs_host::persistent_grid(max_producers));
+    // two workgroups (eight agent waves) per CU, all resident
+    const int grid = std::min((T + 3) / 4, 2 * xs_host::persistent_grid(max_producers));
     hipLaunchKernelGGL(ring::ring_dispatch_kernel, dim3(grid), dim3(ring::kThreads), 0, st, a);
     if (xs_host::launch_status()) return XS_EHIP;
   }

@@ -133,7 +133,7 @@ xs_ulysses_copy = _sig("xs_ulysses_copy", C.c_int, vp, i32, i32, i32, P(xs_windo
 xs_dispatch_rows = _sig("xs_dispatch_rows", C.c_int, vp, i64, i32, i32, vp, vp, i32, i32, P(xs_window), i32,
                         vp, vp)
 xs_ring_slot_bytes = _sig("xs_ring_slot_bytes", C.c_int, i32, i32, P(i64))
-xs_dispatch_ring_workspace_bytes = _sig("xs_dispatch_ring_workspace_bytes", C.c_int, i32, i32, P(i64))
+xs_dispatch_ring_workspace_bytes = _sig("xs_dispatch_ring_workspace_bytes", C.c_int, i32, i32, i32, i32, P(i64))
 xs_dispatch_ring = _sig("xs_dispatch_ring", C.c_int, vp, i32, i32, vp, vp, i32, i32, P(xs_window), i32,
                         P(xs_window), i32, i32, i64, vp, i64, vp, vp, vp)
 xs_quantize_mx = _sig("xs_quantize_mx", C.c_int, vp, i64, i32, i64, i32, vp, i64, vp, i64, vp)

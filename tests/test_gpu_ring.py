@@ -30,7 +30,7 @@ def _stream():
 class Rings:
     """W rings of S slots in device memory, or in host-coherent memory."""
 
-    def __init__(self, W, S, H, k, host=False):
+    def __init__(self, T, W, S, H, k, host=False):
         X = xs()
         nb = C.c_int64()
         X.check(X.xs_ring_slot_bytes(H, k, C.byref(nb)))
@@ -44,7 +44,7 @@ class Rings:
         else:
             self.mem = torch.zeros((W, S, self.slot_bytes), dtype=torch.uint8, device="cuda")
             self.arr = X.windows([X.window((self.mem[d].data_ptr(), S, self.slot_bytes)) for d in range(W)])
-        X.check(X.xs_dispatch_ring_workspace_bytes(W, S, C.byref(nb)))
+        X.check(X.xs_dispatch_ring_workspace_bytes(T, k, W, S, C.byref(nb)))
         self.ws = torch.zeros((nb.value,), dtype=torch.uint8, device="cuda")
 
     def free(self):
@@ -68,7 +68,7 @@ def _ring_dispatch(x, idx, sr, E, W, cap, S, dedup, host=False, max_producers=0,
     k = idx.shape[1]
     win = torch.full((W, cap, H), -1, dtype=torch.int16, device="cuda")
     wins = X.windows([X.window(win[d]) for d in range(W)])
-    rings = Rings(W, S, H, k, host)
+    rings = Rings(T, W, S, H, k, host)
     st = torch.zeros((1,), dtype=torch.int32, device="cuda")
     stats = torch.full((2 * W,), -1, dtype=torch.int32, device="cuda")
     dx, di, ds = dev_bits(x), torch.from_numpy(idx).cuda(), torch.from_numpy(np.ascontiguousarray(sr)).cuda()
@@ -166,7 +166,7 @@ def test_ring_bad_arguments():
     idx, sr, cap, x = _setup(T, H, E, k, W, 1)
     win = torch.zeros((W, cap, H), dtype=torch.int16, device="cuda")
     wins = X.windows([X.window(win[d]) for d in range(W)])
-    r = Rings(W, 4, H, k)
+    r = Rings(T, W, 4, H, k)
     st = torch.zeros((1,), dtype=torch.int32, device="cuda")
     dx, di, ds = dev_bits(x), torch.from_numpy(idx).cuda(), torch.from_numpy(np.ascontiguousarray(sr)).cuda()
 
