@@ -169,11 +169,14 @@ int xs_dispatch_ring(const void* x, int32_t T, int32_t H, const int32_t* topk_id
  *   XS_PREC_MXFP8  MX formats (see "MX formats" below). Token rows are quantized once, in
  *                  the dispatch phase, into workspace staging and dispatched as rows of H
  *                  E4M3 codes followed by H / 32 E8M0 scales (dispatch window rows >= H +
- *                  H / 32 bytes); w1 / w2 hold E4M3 codes ([n_experts][2I][H] and
+ *                  H / 32 bytes; a row stride that is a multiple of 128 bytes keeps every
+ *                  row on whole cache lines, which the Linear-1 loads run faster on);
+ *                  w1 / w2 hold E4M3 codes ([n_experts][2I][H] and
  *                  [n_experts][H][I] bytes) and w1_scale / w2_scale their scales
  *                  ([n_experts][2I][H / 32], [n_experts][H][I / 32]); Linear-1 runs on the
  *                  scaled MFMA, SwiGLU in fp32, and h is stored as MXFP8 rows of I codes and
- *                  I / 32 scales (h_ws: [h_rows][I + I / 32] bytes); Linear-2 likewise, its
+ *                  I / 32 scales (h_ws: [h_rows] rows of I + I / 32 bytes rounded up to a
+ *                  multiple of 128, the row pitch); Linear-2 likewise, its
  *                  output y rounded to bf16 for the unchanged combine. Requires H and I
  *                  multiples of 512. Only xs_fused_ep_layer takes it (the unfused phase calls
  *                  return XS_EUNSUPPORTED).

@@ -656,12 +656,15 @@ struct EpWorkspace {
 
 bool is_mx(const xs_ep_layer* L) { return L->precision == XS_PREC_MXFP8 || L->precision == XS_PREC_W4A8; }
 
-// Bytes of one dispatched token row and of one h row.
+// Bytes of one dispatched token row, and the pitch of h rows. MX h rows (I codes, then I / 32
+// scales) are padded to whole 128-byte lines: at a pitch of I + I / 32 bytes most rows would
+// start inside a line, and every 128-byte K step of a Linear-2 activation load would then
+// touch two lines instead of one.
 int64_t token_row_bytes(const xs_ep_layer* L) {
   return is_mx(L) ? static_cast<int64_t>(L->H) + L->H / 32 : static_cast<int64_t>(L->H) * 2;
 }
 int64_t h_row_bytes(const xs_ep_layer* L) {
-  return is_mx(L) ? static_cast<int64_t>(L->I) + L->I / 32 : static_cast<int64_t>(L->I) * 2;
+  return is_mx(L) ? (static_cast<int64_t>(L->I) + L->I / 32 + 127) / 128 * 128 : static_cast<int64_t>(L->I) * 2;
 }
 
 int n_cwin_of(const xs_ep_layer* L) { return L->n_experts / (L->E / L->W); }

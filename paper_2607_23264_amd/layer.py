@@ -56,9 +56,12 @@ class EPLayer:
         # weight code bytes per element: E4M3 one, packed E2M1 a half
         self.w_fmt = X.XS_FMT_E2M1 if precision == X.XS_PREC_W4A8 else X.XS_FMT_E4M3
         wdiv = 2 if precision == X.XS_PREC_W4A8 else 1
-        # bytes per dispatched token row and per h row (MXFP8: codes, then one scale per 32)
+        # bytes per dispatched token row and per h row (MXFP8: codes, then one scale per 32);
+        # MX rows sit at a pitch of whole 128-byte lines in the dispatch windows and in h, so
+        # that each 128-byte K step of a GEMM activation load reads one line, not two
         self.row_bytes = s.H + s.H // 32 if mxp else 2 * s.H
-        self.h_bytes = s.I + s.I // 32 if mxp else 2 * s.I
+        self.row_pitch = -(-self.row_bytes // 128) * 128 if mxp else self.row_bytes
+        self.h_bytes = -(-(s.I + s.I // 32) // 128) * 128 if mxp else 2 * s.I
         self.dev = torch.device(device)
         cap = s.cap if s.cap is not None else s.n_src * s.T * min(s.k, s.epw)
         self.cap = cap
@@ -80,7 +83,7 @@ class EPLayer:
         self.row_src = torch.full((s.W, cap), -1, dtype=i32, device=d)
         fill = -1 if sentinel else 0
         if mxp:
-            self.dwin = torch.full((s.W, cap, self.row_bytes), 0xFF if sentinel else 0, dtype=torch.uint8, device=d)
+            self.dwin = torch.full((s.W, cap, self.row_pitch), 0xFF if sentinel else 0, dtype=torch.uint8, device=d)
             self.xq = torch.zeros((s.T, self.row_bytes), dtype=torch.uint8, device=d)
         else:
             self.dwin = torch.full((s.W, cap, s.H), fill, dtype=torch.int16, device=d) if sentinel \
