@@ -214,8 +214,8 @@ typedef struct xs_ep_layer {
                                  recorded on `stream`; see XS_EV_* */
   int32_t precision;          /* XS_PREC_BF16 (0), XS_PREC_MXFP8 or XS_PREC_W4A8 */
   int32_t reserved;           /* 0 */
-  const void* w1_scale;       /* MX precisions: device E8M0 [n_experts][2I][H / 32] */
-  const void* w2_scale;       /* MX precisions: device E8M0 [n_experts][H][I / 32] */
+  const void* w1_scale;       /* MX precisions: device E8M0 [n_experts][2I][H / 32], 16-byte aligned */
+  const void* w2_scale;       /* MX precisions: device E8M0 [n_experts][H][I / 32], 16-byte aligned */
 } xs_ep_layer;
 
 /* Phase boundaries of the EP entry points: events[XS_EV_x] is recorded right before the
@@ -436,9 +436,9 @@ int xs_quantize_mx(const void* x, int64_t rows, int32_t cols, int64_t ldx, int32
  * bytes per row) and scales [M][K / 32] (lda_s bytes per row), b codes in b_fmt, [N][K]
  * bytes (E4M3) or [N][K / 2] packed (E2M1, ldb >= K / 2), ldb bytes per row, and scales
  * [N][K / 32] (ldb_s). fp32 accumulation on v_mfma_scale_f32_32x32x64_f8f6f4, one bf16
- * rounding at the end. N a multiple of 256, K of 128; code rows 16-byte aligned, scale rows
- * 4-byte aligned. XS_EINVAL / XS_EUNSUPPORTED on bad arguments (nothing launched), XS_EHIP
- * if the launch fails. */
+ * rounding at the end. N a multiple of 256, K of 512; code and scale rows 16-byte aligned
+ * (the kernel loads a row's scales for 512 K elements as one 16-byte piece). XS_EINVAL /
+ * XS_EUNSUPPORTED on bad arguments (nothing launched), XS_EHIP if the launch fails. */
 int xs_gemm_mx(const void* a, int64_t lda, const void* a_scales, int64_t lda_s, const void* b,
                int64_t ldb, const void* b_scales, int64_t ldb_s, int32_t b_fmt, void* c,
                int64_t ldc, int32_t M, int32_t N, int32_t K, const xs_trace* trace, void* stream);

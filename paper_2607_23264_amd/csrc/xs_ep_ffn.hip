@@ -717,13 +717,12 @@ int validate(const xs_ep_layer* L, bool need_out) {
   if (is_mx(L)) {
     if (L->expert_mode != XS_EXPERT_SWIGLU) return XS_EUNSUPPORTED;
     if (!L->w1_scale || !L->w2_scale) return XS_EINVAL;
-    // 16-byte code rows and 4-byte scale rows, whole 256 x 256 tiles along H, 128-column
-    // SwiGLU tiles and 128-deep K stages along I
+    // 16-byte code and scale rows (the GEMM core loads four K stages of scales at once), whole
+    // 256 x 256 tiles along H, 128-column SwiGLU tiles and 512-deep scale groups along I
     if (L->H % 512 || L->I % 512) return XS_EUNSUPPORTED;
     if ((reinterpret_cast<uintptr_t>(L->w1) | reinterpret_cast<uintptr_t>(L->w2) |
-         reinterpret_cast<uintptr_t>(L->h_ws)) & 15)
-      return XS_EINVAL;
-    if ((reinterpret_cast<uintptr_t>(L->w1_scale) | reinterpret_cast<uintptr_t>(L->w2_scale)) & 3)
+         reinterpret_cast<uintptr_t>(L->h_ws) | reinterpret_cast<uintptr_t>(L->w1_scale) |
+         reinterpret_cast<uintptr_t>(L->w2_scale)) & 15)
       return XS_EINVAL;
   }
   if (L->H % 8) return XS_EUNSUPPORTED;

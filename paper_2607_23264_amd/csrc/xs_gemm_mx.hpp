@@ -7,13 +7,19 @@
 // bytes per MFMA.
 //
 // LDS: two stages, each with an A and a B operand tile of 256 rows x 128 bytes (here 128 K
-// elements; logical piece c of row r at c ^ ((r >> 1) & 7), as in the bf16 core) and the
-// 256 + 256 rows' scale words of the stage (one 32-bit word per row: its four 32-element
-// blocks), 132 KiB in all. Everything arrives by direct global -> LDS loads, the swizzle
-// applied on the global side (instruction i of wave w fills operand rows 32 i + 8 w .. + 7;
-// one dword load per lane fills the scale words of rows 64 w + lane). A stage is 32 MFMAs of
-// 64 cycles per wave (one wave per SIMD), so loading it one stage ahead gives the loads about
-// as long to land as the bf16 core's three-deep weight pipeline does.
+// elements; logical piece c of row r at c ^ ((r >> 1) & 7), as in the bf16 core), 128 KiB,
+// and two scale groups at the top of the LDS. A group holds, per A and per B row, the 16
+// bytes of block scales of four stages (K elements [512 g, 512 g + 512): stage kt reads the
+// 32-bit word kt % 4 of group kt / 4). Everything arrives by direct global -> LDS loads, the
+// swizzle applied on the global side (instruction i of wave w fills operand rows 32 i + 8 w
+// .. + 7). A row's scale bytes are contiguous in memory, so loading one 4-byte word per row
+// and stage would touch a different cache line in every lane (64 lines per instruction, as
+// many as all of the stage's code loads together). Instead each stage loads one quarter of
+// the next group: wave w's scale instruction covers rows 64 w + 16 q .. + 15 of quarter q,
+// four lanes per row reading its 16 contiguous bytes, which divides those line touches by
+// four with every lane active (no branch in the K loop). A stage is 32
+// MFMAs of 64 cycles per wave (one wave per SIMD), so loading it one stage ahead gives the
+// loads about as long to land as the bf16 core's three-deep weight pipeline does.
 //
 // Operand layout of the scaled MFMA (measured on gfx950): lane 32 h + i holds row i's K
 // elements [16 h, 16 h + 16) in bytes 0..15 and [32 + 16 h, 48 + 16 h) in bytes 16..31 of its
@@ -35,10 +41,12 @@
 namespace xs {
 
 constexpr int kMxThreads = 256;
-constexpr int kMxStage = 2 * kOpBytes + 2048;    // A tile, B tile, A and B scale words: 66 KiB
-constexpr int kMxScaleOff = 2 * kOpBytes;
-constexpr int kMxLds = 2 * kMxStage;             // 132 KiB
-static_assert(kMxLds <= kLdsBytes, "the MX stages fit the LDS the kernels declare");
+constexpr int kMxStage = 2 * kOpBytes;             // A tile and B tile of one stage: 64 KiB
+constexpr int kMxScaleBuf = 2 * kBM * 16;          // one scale group: 16 bytes per A and B row
+constexpr int kMxScaleOff = kLdsBytes - 2 * kMxScaleBuf;
+static_assert(2 * kMxStage <= kMxScaleOff, "the MX stages and scale groups fit the LDS");
+// the epilogue's row pointers and the scheduler scratch (touched between mainloops) lie below
+static_assert(kLdsMiscOff + 64 <= kMxScaleOff, "scale groups clear of the scheduler scratch");
 typedef int v8i_t __attribute__((ext_vector_type(8)));
 typedef int v4i_t __attribute__((ext_vector_type(4)));
 typedef f32x16 AccMx[4][4];
@@ -49,7 +57,10 @@ struct MxTile {
   const char* sa;         // A scale base (tile row 0)
   const char* sb;         // B scale base
   uint32_t oa[8], ob[8];  // per-lane byte offsets of the eight direct loads of each operand
-  uint32_t sao, sbo;      // per-lane byte offsets of the scale rows this lane loads
+  // scale word this lane loads in quarter q: A at min(sa0 + q * sa16, samax), B at sb0 +
+  // (q % 2) * sbq1 + (q / 2) * sbq2 (row offsets are linear in q; uniform strides)
+  uint32_t sa0, samax, sb0;
+  uint32_t sa16, sbq1, sbq2;
   int ar, br;             // this lane's fragment rows in the A and B tiles
   int arow, brow;         // their LDS byte offsets within an operand tile
   int w;
@@ -66,43 +77,49 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
   // B as E2M1 (BF4): 64-byte tile rows per stage (four direct loads per wave instead of
   // eight), one 16-byte fragment read per sub-step, and the MFMA told its first operand is fp4
   constexpr int kBLoads = BF4 ? 4 : 8;
-  constexpr int kLoads = 10 + kBLoads;                 // direct loads per wave and stage
+  constexpr int kLoads = 8 + kBLoads;                  // operand loads per wave and stage
   constexpr uint32_t kBStep = BF4 ? 64u : 128u;        // B bytes per row and stage
   constexpr int kBRow = BF4 ? 64 : 128;                // B tile row pitch in LDS
   constexpr int kFmtB = BF4 ? 4 : 0;
   // Addresses are the uniform base plus a 32-bit per-lane offset that includes the stage
   // (a 32-bit sum that may wrap is not folded into loop-invariant 64-bit per-lane pointers,
   // which would cost two registers per load): the loads keep the scalar-base + vector-offset
-  // form. Direct load n of stage kt: 0..7 A pieces, 8 / 9 A / B scale words, 10.. B pieces.
+  // form. Direct load n of stage kt: 0..7 A pieces, 8.. B pieces; then, in a stage that issues
+  // loads, the two scale loads (A rows, B rows) of one quarter of a group.
   auto issue_one = [&](int kt, int n) {
     char* st = lds + (kt & 1) * kMxStage;
-    const uint32_t k0 = static_cast<uint32_t>(kt) * 128u, k4 = static_cast<uint32_t>(kt) * 4u;
     if (n < 8)
-      __builtin_amdgcn_global_load_lds((glob_void*)(t.a + (t.oa[n] + k0)), (lds_void*)(st + (4 * n + w) * 1024),
-                                       16, 0, 0);
-    else if (n == 8)
-      __builtin_amdgcn_global_load_lds((glob_void*)(t.sa + (t.sao + k4)), (lds_void*)(st + kMxScaleOff + w * 256),
-                                       4, 0, 0);
-    else if (n == 9)
-      __builtin_amdgcn_global_load_lds((glob_void*)(t.sb + (t.sbo + k4)),
-                                       (lds_void*)(st + kMxScaleOff + 1024 + w * 256), 4, 0, 0);
+      __builtin_amdgcn_global_load_lds((glob_void*)(t.a + (t.oa[n] + static_cast<uint32_t>(kt) * 128u)),
+                                       (lds_void*)(st + (4 * n + w) * 1024), 16, 0, 0);
     else
-      __builtin_amdgcn_global_load_lds((glob_void*)(t.b + (t.ob[n - 10] + static_cast<uint32_t>(kt) * kBStep)),
-                                       (lds_void*)(st + kOpBytes + (4 * (n - 10) + w) * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((glob_void*)(t.b + (t.ob[n - 8] + static_cast<uint32_t>(kt) * kBStep)),
+                                       (lds_void*)(st + kOpBytes + (4 * (n - 8) + w) * 1024), 16, 0, 0);
   };
   auto issue = [&](int kt) {
 #pragma unroll
     for (int n = 0; n < kLoads; ++n) issue_one(kt, n);
   };
+  // scale load n (0: A rows, 1: B rows) of quarter q of group g, into group buffer g % 2 (row
+  // r's 16 bytes at r * 16, so the lanes' words land in order). A group past the last one
+  // reads the last group's bytes (in bounds; that buffer is no longer read).
+  const int last_group = (nk >> 2) - 1;
+  auto issue_scale = [&](int g, int n, int q) {
+    char* sb = lds + kMxScaleOff + (g & 1) * kMxScaleBuf + n * (kBM * 16) + (64 * w + 16 * q) * 16;
+    const uint32_t uq = static_cast<uint32_t>(q);
+    const uint32_t oq = n ? t.sb0 + (uq & 1u) * t.sbq1 + (uq >> 1) * t.sbq2 : min(t.sa0 + uq * t.sa16, t.samax);
+    const char* base = (n ? t.sb : t.sa) + min(g, last_group) * 16;
+    __builtin_amdgcn_global_load_lds((glob_void*)(base + oq), (lds_void*)sb, 4, 0, 0);
+  };
   uint32_t sw[8];         // a stage's scale words as read: A blocks 0..3, B blocks 0..3
   int sc[8];              // the same, byte kk = scale of K block 2 kk + h (the MFMA's op_sel)
-  auto read_s = [&](const char* st) {
+  auto read_s = [&](int ks) {   // the scale words of stage ks
+    const char* sg = lds + kMxScaleOff + ((ks >> 2) & 1) * kMxScaleBuf + (ks & 3) * 4;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      sw[i] = *reinterpret_cast<const uint32_t*>(st + kMxScaleOff + t.ar * 4 + i * 128);
+      sw[i] = *reinterpret_cast<const uint32_t*>(sg + (t.ar + 32 * i) * 16);
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      sw[4 + j] = *reinterpret_cast<const uint32_t*>(st + kMxScaleOff + 1024 + t.br * 4 + j * 128);
+      sw[4 + j] = *reinterpret_cast<const uint32_t*>(sg + kBM * 16 + (t.br + 32 * j) * 16);
   };
   auto perm_s = [&]() {
 #pragma unroll
@@ -141,7 +158,12 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
   //     wave's share;
   //   B: sub-step 1's MFMAs, each followed by two global loads of the stage after next (into
   //     this stage's buffers, which no wave reads any more) and one read of the next stage's
-  //     scale words or sub-step-0 fragments.
+  //     scale words or sub-step-0 fragments. Among the loads are the scale loads of quarter
+  //     (kt + 1) % 4 of group (kt + 1) / 4 + 1: its buffer last held group (kt + 1) / 4 - 1,
+  //     whose final words were read in stage 4 ((kt + 1) / 4) - 2 or earlier, before this
+  //     stage's barrier; its last quarter lands by the barrier of stage 4 ((kt + 1) / 4) + 3,
+  //     before the group's first words are read. Past the last group the loads repeat the
+  //     last group into the other buffer, which is no longer read (no branch).
   // NEXT: a stage follows; ISSUE: the stage after next exists. Compile-time, so the steady
   // loop body has no branches.
   auto stage = [&](int kt, auto next_c, auto issue_c) {
@@ -149,6 +171,15 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
     constexpr bool kIssue = decltype(issue_c)::value;
     const char* st = lds + (kt & 1) * kMxStage;
     const char* nx = lds + ((kt + 1) & 1) * kMxStage;
+    const int sg = ((kt + 1) >> 2) + 1;
+    const int sq = (kt + 1) & 3;
+    // load n of this stage's issue: 0..7 A pieces, 8 / 9 scale quarter (A / B rows), 10.. B
+    auto load_n = [&](int n) {
+      if (n < 8) issue_one(kt + 2, n);
+      else if (n < 10) issue_scale(sg, n - 8, sq);
+      else issue_one(kt + 2, n - 2);
+    };
+    constexpr int kAll = kLoads + 2;
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (NI > 0) {
 #pragma unroll
@@ -179,11 +210,11 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
         acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b1[j], a1[i], acc[i][j], kFmtB, 0, 1,
                                                                     sc[4 + j], 1, sc[i]);
         if constexpr (kIssue) {
-          if (2 * g < kLoads) issue_one(kt + 2, 2 * g);
-          if (2 * g + 1 < kLoads) issue_one(kt + 2, 2 * g + 1);
+          if (2 * g < kAll) load_n(2 * g);
+          if (2 * g + 1 < kAll) load_n(2 * g + 1);
         }
         if constexpr (kNext) {
-          if (g == 0) read_s(nx);
+          if (g == 0) read_s(kt + 1);
           else if (g - 1 < 4) b0[g - 1] = frag_b(nx, g - 1, 0);
           else if (g - 5 < NI) a0[g - 5] = frag(nx, t.arow + (g - 5) * 32 * 128, 0);
         }
@@ -192,29 +223,38 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
       // what did not fit beside the MFMAs
       if constexpr (kIssue) {
 #pragma unroll
-        for (int n = 2 * kMfma; n < kLoads; ++n) issue_one(kt + 2, n);
+        for (int n = 2 * kMfma; n < kAll; ++n) load_n(n);
       }
       if constexpr (kNext) {
 #pragma unroll
         for (int r = kMfma; r < 5 + NI; ++r) {
-          if (r == 0) read_s(nx);
+          if (r == 0) read_s(kt + 1);
           else if (r - 1 < 4) b0[r - 1] = frag_b(nx, r - 1, 0);
           else a0[r - 5] = frag(nx, t.arow + (r - 5) * 32 * 128, 0);
         }
       }
     } else if constexpr (kIssue) {
-      issue(kt + 2);
+#pragma unroll
+      for (int n = 0; n < kAll; ++n) load_n(n);
     }
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (kNext && NI > 0) perm_s();
   };
-  // prologue: stage 0 resident, stage 1 in flight, stage 0's sub-step-0 operands in registers
+  // prologue: stage 0 and scale group 0 resident, stage 1 and the first quarter of group 1
+  // in flight, stage 0's sub-step-0 operands in registers
   issue(0);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    issue_scale(0, 0, q);
+    issue_scale(0, 1, q);
+  }
   wait_vm0();
   __builtin_amdgcn_s_barrier();
   if (nk > 1) issue(1);
+  issue_scale(1, 0, 0);   // group 1, or (K = 512) group 0 again into the unused buffer
+  issue_scale(1, 1, 0);
   if constexpr (NI > 0) {
-    read_s(lds);
+    read_s(0);
     read_frags(lds, 0, a0, b0);
     perm_s();
   }
@@ -232,7 +272,7 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
 // acc = deq(A)[0:256, 0:K] deq(B)[rows(0:256), 0:K]^T. A: E4M3 code rows (lda bytes apart,
 // 16-byte aligned); B: E4M3 code rows, or with BF4 E2M1 codes packed two per byte (low nibble
 // first, K / 2 bytes per row), ldb bytes apart, 16-byte aligned; As / Bs: E8M0 scale rows
-// ([K / 32] bytes, lda_s / ldb_s apart, 4-byte aligned). K a multiple of 128. B rows map
+// ([K / 32] bytes, lda_s / ldb_s apart, 16-byte aligned). K a multiple of 512. B rows map
 // through b_row_map (SwiGLU interleave). Rows of A at or beyond a_rows read row a_rows - 1; a
 // wave skips the MFMAs of 32-row blocks past a_rows. Ends with a block barrier. Accumulator
 // acc[i][j][q] is output
@@ -274,9 +314,16 @@ __device__ __forceinline__ void gemm_mainloop_mx(const uint8_t* __restrict__ A, 
       t.ob[i] = static_cast<uint32_t>(b_row_map(r, b_n0, b_half, swiglu) * ldb + c4);
     }
   }
-  const int rs = 64 * w + lane;            // the scale row this lane loads
-  t.sao = static_cast<uint32_t>((rs < a_rows ? rs : a_rows - 1) * lda_s);
-  t.sbo = static_cast<uint32_t>(b_row_map(rs, b_n0, b_half, swiglu) * ldb_s);
+  // scale words: quarter q covers wave w's rows 64 w + 16 q + lane / 4, four lanes per row.
+  // B rows through b_row_map move by 16 rows from q = 0 to 1 and by b_half (SwiGLU) or 32
+  // rows from q = 0 to 2.
+  const int rs = 64 * w + (lane >> 2);
+  t.sa0 = static_cast<uint32_t>(rs * lda_s + (lane & 3) * 4);
+  t.samax = static_cast<uint32_t>((a_rows - 1) * lda_s + (lane & 3) * 4);
+  t.sa16 = static_cast<uint32_t>(16 * lda_s);
+  t.sb0 = static_cast<uint32_t>(b_row_map(rs, b_n0, b_half, swiglu) * ldb_s + (lane & 3) * 4);
+  t.sbq1 = static_cast<uint32_t>(16 * ldb_s);
+  t.sbq2 = static_cast<uint32_t>((swiglu ? b_half : 32) * ldb_s);
   t.ar = wm * 128 + (lane & 31);
   t.br = wn * 128 + (lane & 31);
   t.arow = t.ar * 128;

@@ -180,10 +180,10 @@ extern "C" int xs_gemm_mx(const void* a, int64_t lda, const void* a_scales, int6
   if (!a || !a_scales || !b || !b_scales || !c || M < 0 || N <= 0 || K <= 0) return XS_EINVAL;
   if (b_fmt != XS_FMT_E4M3 && b_fmt != XS_FMT_E2M1) return XS_EINVAL;
   const bool bf4 = b_fmt == XS_FMT_E2M1;
-  if (N % kBN || K % 128 || lda < K || ldb < (bf4 ? K / 2 : K) || lda % 16 || ldb % 16 || lda_s < K / 32 ||
-      ldb_s < K / 32 || lda_s % 4 || ldb_s % 4 || ldc < N || ldc % 8)
+  if (N % kBN || K % 512 || lda < K || ldb < (bf4 ? K / 2 : K) || lda % 16 || ldb % 16 || lda_s < K / 32 ||
+      ldb_s < K / 32 || lda_s % 16 || ldb_s % 16 || ldc < N || ldc % 8)
     return XS_EUNSUPPORTED;
-  if (!aligned(a, 16) || !aligned(b, 16) || !aligned(a_scales, 4) || !aligned(b_scales, 4) ||
+  if (!aligned(a, 16) || !aligned(b, 16) || !aligned(a_scales, 16) || !aligned(b_scales, 16) ||
       !aligned(c, 16))
     return XS_EINVAL;
   if (M == 0) return XS_OK;

@@ -90,7 +90,8 @@ def _gemm_mx(a_bits, b_bits, b_fmt="E4M3"):
 
 
 @pytest.mark.parametrize("b_fmt", ["E4M3", "E2M1"])
-@pytest.mark.parametrize("M,N,K", [(256, 256, 128), (300, 512, 384), (1, 256, 256), (513, 768, 1024), (77, 256, 7168)])
+@pytest.mark.parametrize("M,N,K", [(256, 256, 512), (300, 512, 1536), (1, 256, 512), (513, 768, 1024), (77, 256, 7168),
+                                   (260, 256, 2560)])
 def test_gemm_mx_matches_oracle(M, N, K, b_fmt):
     a = synth.normal_bf16(0, 20, (M, K))
     b = synth.normal_bf16(0, 21, (N, K), std=0.05)
@@ -128,15 +129,20 @@ def test_mx_bad_arguments():
     assert X.xs_quantize_mx(x.data_ptr(), 4, 48, 64, X.XS_FMT_E4M3, c.data_ptr(), 64, s.data_ptr(), 2, _stream()) == X.XS_EINVAL
     assert X.xs_quantize_mx(x.data_ptr(), 4, 64, 64, 7, c.data_ptr(), 64, s.data_ptr(), 2, _stream()) == X.XS_EINVAL
     assert X.xs_quantize_mx(x.data_ptr(), 4, 64, 64, X.XS_FMT_E4M3, c.data_ptr(), 32, s.data_ptr(), 2, _stream()) == X.XS_EINVAL
-    a = torch.zeros((256, 256), dtype=torch.uint8, device="cuda")
-    sc = torch.zeros((256, 8), dtype=torch.uint8, device="cuda")
+    a = torch.zeros((256, 1024), dtype=torch.uint8, device="cuda")
+    sc = torch.zeros((256, 32), dtype=torch.uint8, device="cuda")
     o = torch.zeros((256, 256), dtype=torch.int16, device="cuda")
-    args = lambda K, N, fmt: (a.data_ptr(), 256, sc.data_ptr(), 8, a.data_ptr(), 256, sc.data_ptr(), 8, fmt,
-                              o.data_ptr(), 256, 256, N, K, None, _stream())
-    assert X.xs_gemm_mx(*args(192, 256, X.XS_FMT_E4M3)) == X.XS_EUNSUPPORTED     # K % 128
-    assert X.xs_gemm_mx(*args(256, 200, X.XS_FMT_E4M3)) == X.XS_EUNSUPPORTED     # N % 256
-    assert X.xs_gemm_mx(*args(256, 256, 9)) == X.XS_EINVAL
-    # packed E2M1 rows need K / 2 bytes: 256 bytes cover K = 512 but not K = 640
-    assert X.xs_gemm_mx(a.data_ptr(), 640, sc.data_ptr(), 20, a.data_ptr(), 256, sc.data_ptr(), 20,
-                        X.XS_FMT_E2M1, o.data_ptr(), 256, 0, 256, 640, None, _stream()) == X.XS_EUNSUPPORTED
+
+    def gemm(K=512, N=256, fmt=X.XS_FMT_E4M3, lda=1024, ldb=1024, lds=32, sa=0, M=256):
+        return X.xs_gemm_mx(a.data_ptr(), lda, sc.data_ptr() + sa, lds, a.data_ptr(), ldb, sc.data_ptr(), lds, fmt,
+                            o.data_ptr(), 256, M, N, K, None, _stream())
+
+    assert gemm(K=384) == X.XS_EUNSUPPORTED            # K % 512
+    assert gemm(N=200) == X.XS_EUNSUPPORTED            # N % 256
+    assert gemm(fmt=9) == X.XS_EINVAL
+    assert gemm(lds=20) == X.XS_EUNSUPPORTED           # scale rows of 16-byte pieces
+    assert gemm(sa=4) == X.XS_EINVAL                   # scale base 16-byte aligned
+    # packed E2M1 rows need K / 2 bytes: 256 bytes cover K = 512 but not K = 1024
+    assert gemm(K=1024, fmt=X.XS_FMT_E2M1, ldb=256, M=0) == X.XS_EUNSUPPORTED
+    assert gemm(K=512, fmt=X.XS_FMT_E2M1, ldb=256, M=0) == X.XS_OK
     torch.cuda.synchronize()
