@@ -11,6 +11,11 @@
       Per-dispatch HBM bytes of one kernel from two counter passes, each scaled by what the
       same counter reads for the copy; writes a markdown summary whose `traffic-json:` line
       the benchmark reads, keyed by the hash of the kernel's sources.
+  python -m paper_2607_23264_amd.profiling mfma --csv C.csv --kernel NAME=FLOPS [...]
+      --command CMD --out F.md
+      MFMA busy fraction, shader clock and executed MFMA flops per dispatch from one counter
+      pass (SQ_VALU_MFMA_BUSY_CYCLES, GRBM_GUI_ACTIVE, SQ_INSTS_VALU_MFMA_MOPS_*), beside
+      each kernel's algorithmic flops.
 """
 from __future__ import annotations
 
@@ -27,7 +32,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 # measurement (a change to either makes it stale)
 FFN_KERNEL_SOURCES = ("csrc/xs_ep_ffn.hip", "csrc/xs_gemm.hpp", "csrc/xs_gemm_mx.hpp", "csrc/xs_common.hpp")
 ATTN_KERNEL_SOURCES = ("csrc/xs_attn.hip", "csrc/xs_common.hpp")
-KERNEL_SOURCES = {"ffn": FFN_KERNEL_SOURCES, "attn": ATTN_KERNEL_SOURCES}
+EP_KERNEL_SOURCES = ("csrc/xs_ep.hip", "csrc/xs_common.hpp")
+KERNEL_SOURCES = {"ffn": FFN_KERNEL_SOURCES, "attn": ATTN_KERNEL_SOURCES, "ep": EP_KERNEL_SOURCES}
 
 
 def sources_hash(paths=FFN_KERNEL_SOURCES) -> str:
@@ -147,6 +153,53 @@ def cmd_traffic(a):
     print("\n".join(out))
 
 
+MOPS_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_INSTS_VALU_MFMA_MOPS_F8", "SQ_INSTS_VALU_MFMA_MOPS_F6F4")
+
+
+def cmd_mfma(a):
+    """Per kernel, averaged over its dispatches in one counter pass:
+    busy = SQ_VALU_MFMA_BUSY_CYCLES (summed over every SIMD), active = GRBM_GUI_ACTIVE (summed
+    over the XCDs; per XCD it counts the cycles the GPU was busy), duration from the dispatch's
+    timestamps. MFMA busy fraction = busy / (active per XCD x SIMDs), the definition of the
+    profiler's MfmaUtil; shader clock = active per XCD / duration; executed MFMA flops = MOPS x
+    512 (the counters count 512-flop units)."""
+    by = {}
+    for r in _rows(a.csv):
+        by.setdefault(_short(r["Kernel_Name"]), {}).setdefault(int(r["Dispatch_Id"]), {})[r["Counter_Name"]] = r
+    out = ["# MFMA utilisation per dispatch (rocprofv3 counters)", "", "Command (run from the repository root):",
+           "", "```", a.command, "```", "",
+           f"Busy fraction = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE per XCD x {a.simds} SIMDs); "
+           f"clock = GRBM_GUI_ACTIVE per XCD / dispatch duration; executed flops = MFMA MOPS x 512. "
+           f"Durations are those of the counter run (kernels serialized by the profiler).", "",
+           "| kernel | dispatches | µs | MFMA busy | clock GHz | executed TFLOP | algorithmic TFLOP | "
+           "executed / algorithmic | algorithmic TFLOP/s |", "|---|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    recs = []
+    for spec in a.kernel:
+        name, flops = spec.rsplit("=", 1)
+        flops = float(flops)
+        ds = [d for k, v in by.items() if k.startswith(name) for d in v.values()]
+        ds = [d for d in ds if "SQ_VALU_MFMA_BUSY_CYCLES" in d and "GRBM_GUI_ACTIVE" in d]
+        if not ds:
+            sys.exit(f"no {name} dispatches with the MFMA counters in {a.csv}")
+        mean = lambda f: sum(f(d) for d in ds) / len(ds)
+        val = lambda d, c: float(d[c]["Counter_Value"]) if c in d else 0.0
+        dur = mean(lambda d: (int(d["GRBM_GUI_ACTIVE"]["End_Timestamp"]) - int(d["GRBM_GUI_ACTIVE"]["Start_Timestamp"])) * 1e-9)
+        act = mean(lambda d: val(d, "GRBM_GUI_ACTIVE")) / a.xcds
+        busy = mean(lambda d: val(d, "SQ_VALU_MFMA_BUSY_CYCLES"))
+        ex = mean(lambda d: sum(val(d, c) for c in MOPS_COUNTERS)) * 512.0
+        util = busy / (act * a.simds)
+        clk = act / dur / 1e9
+        rec = {"kernel": name, "dispatches": len(ds), "us": dur * 1e6, "mfma_busy": util, "clock_GHz": clk,
+               "executed_flops": ex, "algorithmic_flops": flops, "algorithmic_TFLOPs": flops / dur / 1e12}
+        recs.append(rec)
+        out.append(f"| `{name}` | {len(ds)} | {dur * 1e6:.1f} | {util:.3f} | {clk:.2f} | {ex / 1e12:.3f} | "
+                   f"{flops / 1e12:.3f} | {ex / flops:.3f} | {flops / dur / 1e12:.0f} |")
+    out += ["", "mfma-json: " + json.dumps(recs)]
+    with open(a.out, "w") as f:
+        f.write("\n".join(out) + "\n")
+    print("\n".join(out))
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -171,8 +224,15 @@ def main():
                    help="which kernel's sources key the record")
     t.add_argument("--commands", required=True, help="the counter commands, separated by ';;'")
     t.add_argument("--out", required=True)
+    m = sub.add_parser("mfma")
+    m.add_argument("--csv", required=True)
+    m.add_argument("--kernel", action="append", required=True, help="NAME=ALGORITHMIC_FLOPS, repeatable")
+    m.add_argument("--simds", type=int, default=1024)
+    m.add_argument("--xcds", type=int, default=8)
+    m.add_argument("--command", required=True)
+    m.add_argument("--out", required=True)
     a = ap.parse_args()
-    {"copy": cmd_copy, "stats": cmd_stats, "traffic": cmd_traffic}[a.cmd](a)
+    {"copy": cmd_copy, "stats": cmd_stats, "traffic": cmd_traffic, "mfma": cmd_mfma}[a.cmd](a)
 
 
 if __name__ == "__main__":
