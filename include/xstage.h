@@ -172,11 +172,13 @@ int xs_dispatch_ring(const void* x, int32_t T, int32_t H, const int32_t* topk_id
  *                  H / 32 bytes; a row stride that is a multiple of 128 bytes keeps every
  *                  row on whole cache lines, which the Linear-1 loads run faster on);
  *                  w1 / w2 hold E4M3 codes ([n_experts][2I][H] and
- *                  [n_experts][H][I] bytes) and w1_scale / w2_scale their scales
- *                  ([n_experts][2I][H / 32], [n_experts][H][I / 32]); Linear-1 runs on the
- *                  scaled MFMA, SwiGLU in fp32, and h is stored as MXFP8 rows of I codes and
- *                  I / 32 scales (h_ws: [h_rows] rows of I + I / 32 bytes rounded up to a
- *                  multiple of 128, the row pitch); Linear-2 likewise, its
+ *                  [n_experts][H][I] bytes) and w1_scale / w2_scale their scales grouped
+ *                  by 512 K elements, as xs_quantize_mx_grouped writes them over all of
+ *                  the weight rows: [H / 512][n_experts * 2I][16] and
+ *                  [I / 512][n_experts * H][16] bytes. Linear-1 runs on the scaled MFMA,
+ *                  SwiGLU in fp32, and h is stored as MXFP8: h_ws holds h_rows code rows of
+ *                  I bytes, then the scales in groups [I / 512][h_rows][16] (h_rows * (I +
+ *                  I / 32) bytes in all); Linear-2 likewise, its
  *                  output y rounded to bf16 for the unchanged combine. Requires H and I
  *                  multiples of 512. Only xs_fused_ep_layer takes it (the unfused phase calls
  *                  return XS_EUNSUPPORTED).
@@ -214,8 +216,8 @@ typedef struct xs_ep_layer {
                                  recorded on `stream`; see XS_EV_* */
   int32_t precision;          /* XS_PREC_BF16 (0), XS_PREC_MXFP8 or XS_PREC_W4A8 */
   int32_t reserved;           /* 0 */
-  const void* w1_scale;       /* MX precisions: device E8M0 [n_experts][2I][H / 32], 16-byte aligned */
-  const void* w2_scale;       /* MX precisions: device E8M0 [n_experts][H][I / 32], 16-byte aligned */
+  const void* w1_scale;       /* MX precisions: device E8M0 [H / 512][n_experts * 2I][16], 16-byte aligned */
+  const void* w2_scale;       /* MX precisions: device E8M0 [I / 512][n_experts * H][16], 16-byte aligned */
 } xs_ep_layer;
 
 /* Phase boundaries of the EP entry points: events[XS_EV_x] is recorded right before the
@@ -431,6 +433,14 @@ enum { XS_FMT_E4M3 = 0, XS_FMT_E2M1 = 1 };
  * arguments (nothing launched), XS_EHIP if the launch fails. */
 int xs_quantize_mx(const void* x, int64_t rows, int32_t cols, int64_t ldx, int32_t fmt,
                    void* codes, int64_t ld_codes, void* scales, int64_t ld_scales, void* stream);
+
+/* The same quantizer with the scales grouped by 512 columns, the layout the MX GEMM core of
+ * the EP layer loads a run of rows from at once: the scale of row r, block j (columns
+ * [32 j, 32 j + 32)) at byte ((j / 16) * rows + r) * 16 + j % 16, i.e. [cols / 512][rows][16].
+ * cols a multiple of 512, scales 16-byte aligned; otherwise as xs_quantize_mx (the static
+ * weights of an MX EP layer are quantized with it once, at upload). */
+int xs_quantize_mx_grouped(const void* x, int64_t rows, int32_t cols, int64_t ldx, int32_t fmt,
+                           void* codes, int64_t ld_codes, void* scales, void* stream);
 
 /* MX GEMM: c (bf16 [M][N], ldc elements) = deq(a) deq(b)^T with a E4M3 codes [M][K] (lda
  * bytes per row) and scales [M][K / 32] (lda_s bytes per row), b codes in b_fmt, [N][K]

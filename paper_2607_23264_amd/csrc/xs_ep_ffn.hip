@@ -46,9 +46,11 @@ struct EpArgs {
   const uint16_t* w2;
   uint16_t* h;
   uint16_t* y;
-  const uint8_t* w1s;          // MXFP8: weight scales (w1 / w2 then hold E4M3 codes)
-  const uint8_t* w2s;
-  int64_t h_stride;            // MXFP8: bytes per h row (I codes, then I / 32 scales)
+  const uint8_t* w1s;          // MX: weight scales in groups of 512 K elements (w1 / w2 then
+  const uint8_t* w2s;          //     hold E4M3 or packed E2M1 codes)
+  int64_t h_stride;            // MX: bytes per h code row (I)
+  uint8_t* hs;                 // MX: h scales, groups [I / 512][h_rows][16 bytes]
+  int64_t h_rows;
   const int* meta;             // [0] rows P, [1] waves, [2] wave-list length, [3] computed rows
   const int* row_expert;
   const int* exp_m;
@@ -283,9 +285,11 @@ __device__ __forceinline__ int xcd_instance_ep(int b, int G) {
 }
 
 // MX tiles (256 threads, the MX core); BF4: the weights are packed E2M1 (W4A8), else E4M3.
-// Linear-1: the dispatch window rows hold H codes then H / 32 scales; the SwiGLU output is
-// quantized in the epilogue into h rows of I codes then I / 32 scales (this tile's 128
-// columns: codes at 128 nt, scales at I + 4 nt).
+// Weight scales are grouped by 512 K elements ([K / 512][n_experts * rows][16 bytes]), so a
+// quarter of a scale group is one contiguous run of rows. Linear-1: the dispatch window rows
+// hold H codes then H / 32 scales; the SwiGLU output is quantized in the epilogue into h code
+// rows of I bytes (this tile's 128 columns at 128 nt) and one scale word per row into the h
+// scale groups (group nt / 4, word nt % 4).
 template <bool BF4>
 __device__ __forceinline__ void ep_l1_tile_mx(const EpArgs& a, int p, int nt, bool fused, char* lds,
                                               char** rowptr) {
@@ -302,13 +306,13 @@ __device__ __forceinline__ void ep_l1_tile_mx(const EpArgs& a, int p, int nt, bo
   const int64_t wrows = static_cast<int64_t>(x) * 2 * a.I;
   const int64_t ldb = BF4 ? a.H / 2 : a.H;
   const uint8_t* B = reinterpret_cast<const uint8_t*>(a.w1) + wrows * ldb;
-  const uint8_t* Bs = a.w1s + wrows * (a.H / 32);
+  const uint8_t* Bs = a.w1s + wrows * 16;
   AccMx acc;
-  gemm_mainloop_mx<BF4>(A, ws, A + a.H, ws, rows, B, ldb, Bs, a.H / 32, nt * (kBN / 2), a.I, true, a.H, acc,
-                        lds);
+  gemm_mainloop_mx<BF4>(A, ws, A + a.H, ws, 16, rows, B, ldb, Bs, 16, static_cast<int64_t>(a.n_experts) * 2 * a.I * 16,
+                        nt * (kBN / 2), a.I, true, a.H, acc, lds);
   const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
-  if (tid < rows)
-    rowptr[tid] = reinterpret_cast<char*>(a.h) + static_cast<int64_t>(a.exp_hrow[x] + m0 + tid) * a.h_stride;
+  const int64_t hrow0 = static_cast<int64_t>(a.exp_hrow[x] + m0);
+  if (tid < rows) rowptr[tid] = reinterpret_cast<char*>(a.h) + (hrow0 + tid) * a.h_stride;
   stage_swiglu_mxq(acc, lds);
   __syncthreads();
   typedef __attribute__((address_space(1))) u32x4 global_u32x4;
@@ -318,7 +322,7 @@ __device__ __forceinline__ void ep_l1_tile_mx(const EpArgs& a, int p, int nt, bo
     *(global_u32x4*)(rowptr[r] + nt * 128 + pc * 16) = *reinterpret_cast<const u32x4*>(lds + r * kHqPitch + pc * 16);
   }
   if (tid < rows)
-    *(__attribute__((address_space(1))) uint32_t*)(rowptr[tid] + a.I + nt * 4) =
+    *(__attribute__((address_space(1))) uint32_t*)(a.hs + ((nt >> 2) * a.h_rows + hrow0 + tid) * 16 + (nt & 3) * 4) =
         *reinterpret_cast<const uint32_t*>(lds + kHqScaleOff + tid * 4);
   if (fused) {
     __syncthreads();
@@ -350,18 +354,20 @@ __device__ __forceinline__ void ep_l2_tile_mx(const EpArgs& a, int p, int nt, bo
   const int e = a.e_begin + x;
   int m0, rows;
   expert_block(a, x, p, false, m0, rows);
-  const uint8_t* A = reinterpret_cast<const uint8_t*>(a.h) + static_cast<int64_t>(a.exp_hrow[x] + m0) * a.h_stride;
+  const int64_t hrow0 = static_cast<int64_t>(a.exp_hrow[x] + m0);
+  const uint8_t* A = reinterpret_cast<const uint8_t*>(a.h) + hrow0 * a.h_stride;
+  const uint8_t* As = a.hs + hrow0 * 16;
   const int64_t wrows = static_cast<int64_t>(x) * a.H;
   const int64_t ldb = BF4 ? a.I / 2 : a.I;
   const uint8_t* B = reinterpret_cast<const uint8_t*>(a.w2) + wrows * ldb;
-  const uint8_t* Bs = a.w2s + wrows * (a.I / 32);
+  const uint8_t* Bs = a.w2s + wrows * 16;
   const int n0 = nt * kBN;
   int code = -1;
   if (a.l2_combine && tid < rows)
     code = a.row_src[static_cast<int64_t>(e / a.epw) * a.cap + a.expert_offsets[e] + m0 + tid];
   AccMx acc;
-  gemm_mainloop_mx<BF4>(A, a.h_stride, A + a.I, a.h_stride, rows, B, ldb, Bs, a.I / 32, n0, 0, false, a.I, acc,
-                        lds);
+  gemm_mainloop_mx<BF4>(A, a.h_stride, As, 16, a.h_rows * 16, rows, B, ldb, Bs, 16,
+                        static_cast<int64_t>(a.n_experts) * a.H * 16, n0, 0, false, a.I, acc, lds);
   const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
   if (tid < rows) {
     char* ptr = nullptr;
@@ -656,15 +662,13 @@ struct EpWorkspace {
 
 bool is_mx(const xs_ep_layer* L) { return L->precision == XS_PREC_MXFP8 || L->precision == XS_PREC_W4A8; }
 
-// Bytes of one dispatched token row, and the pitch of h rows. MX h rows (I codes, then I / 32
-// scales) are padded to whole 128-byte lines: at a pitch of I + I / 32 bytes most rows would
-// start inside a line, and every 128-byte K step of a Linear-2 activation load would then
-// touch two lines instead of one.
+// Bytes of one dispatched token row, and of one h code row. MX h holds I-byte code rows
+// (whole 128-byte lines, as I is a multiple of 512) followed by the scale groups.
 int64_t token_row_bytes(const xs_ep_layer* L) {
   return is_mx(L) ? static_cast<int64_t>(L->H) + L->H / 32 : static_cast<int64_t>(L->H) * 2;
 }
 int64_t h_row_bytes(const xs_ep_layer* L) {
-  return is_mx(L) ? (static_cast<int64_t>(L->I) + L->I / 32 + 127) / 128 * 128 : static_cast<int64_t>(L->I) * 2;
+  return is_mx(L) ? static_cast<int64_t>(L->I) : static_cast<int64_t>(L->I) * 2;
 }
 
 int n_cwin_of(const xs_ep_layer* L) { return L->n_experts / (L->E / L->W); }
@@ -775,6 +779,8 @@ int fill_args(const xs_ep_layer* L, void* workspace, EpArgs* a, WinSet* dws, Win
   a->w1s = static_cast<const uint8_t*>(L->w1_scale);
   a->w2s = static_cast<const uint8_t*>(L->w2_scale);
   a->h_stride = h_row_bytes(L);
+  a->h_rows = L->h_rows;
+  a->hs = is_mx(L) ? static_cast<uint8_t*>(L->h_ws) + L->h_rows * static_cast<int64_t>(L->I) : nullptr;
   int* meta = reinterpret_cast<int*>(ws + w.meta_off);
   int* exp = reinterpret_cast<int*>(ws + w.exp_off);
   a->meta = meta;

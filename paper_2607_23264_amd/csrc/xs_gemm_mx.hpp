@@ -58,9 +58,11 @@ struct MxTile {
   const char* sb;         // B scale base
   uint32_t oa[8], ob[8];  // per-lane byte offsets of the eight direct loads of each operand
   // scale word this lane loads in quarter q: A at min(sa0 + q * sa16, samax), B at sb0 +
-  // (q % 2) * sbq1 + (q / 2) * sbq2 (row offsets are linear in q; uniform strides)
+  // (q % 2) * sbq1 + (q / 2) * sbq2 (row offsets are linear in q; uniform strides); group g
+  // of either operand starts g * sa_grp / sb_grp bytes further
   uint32_t sa0, samax, sb0;
   uint32_t sa16, sbq1, sbq2;
+  int64_t sa_grp, sb_grp;
   int ar, br;             // this lane's fragment rows in the A and B tiles
   int arow, brow;         // their LDS byte offsets within an operand tile
   int w;
@@ -107,7 +109,7 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
     char* sb = lds + kMxScaleOff + (g & 1) * kMxScaleBuf + n * (kBM * 16) + (64 * w + 16 * q) * 16;
     const uint32_t uq = static_cast<uint32_t>(q);
     const uint32_t oq = n ? t.sb0 + (uq & 1u) * t.sbq1 + (uq >> 1) * t.sbq2 : min(t.sa0 + uq * t.sa16, t.samax);
-    const char* base = (n ? t.sb : t.sa) + min(g, last_group) * 16;
+    const char* base = (n ? t.sb : t.sa) + min(g, last_group) * (n ? t.sb_grp : t.sa_grp);
     __builtin_amdgcn_global_load_lds((glob_void*)(base + oq), (lds_void*)sb, 4, 0, 0);
   };
   uint32_t sw[8];         // a stage's scale words as read: A blocks 0..3, B blocks 0..3
@@ -271,18 +273,21 @@ __device__ __forceinline__ void mainloop_mx_ni(const MxTile& t, int nk, AccMx& a
 
 // acc = deq(A)[0:256, 0:K] deq(B)[rows(0:256), 0:K]^T. A: E4M3 code rows (lda bytes apart,
 // 16-byte aligned); B: E4M3 code rows, or with BF4 E2M1 codes packed two per byte (low nibble
-// first, K / 2 bytes per row), ldb bytes apart, 16-byte aligned; As / Bs: E8M0 scale rows
-// ([K / 32] bytes, lda_s / ldb_s apart, 16-byte aligned). K a multiple of 512. B rows map
+// first, K / 2 bytes per row), ldb bytes apart, 16-byte aligned; As / Bs: E8M0 scales, the 16
+// bytes of row r's blocks [16 g, 16 g + 16) (K elements [512 g, 512 g + 512)) at r * srow + g
+// * sgrp: row-major scale rows are (srow = row bytes, sgrp = 16), the grouped layout [K / 512]
+// [rows][16] is (16, 16 * rows). 16-byte aligned. K a multiple of 512. B rows map
 // through b_row_map (SwiGLU interleave). Rows of A at or beyond a_rows read row a_rows - 1; a
 // wave skips the MFMAs of 32-row blocks past a_rows. Ends with a block barrier. Accumulator
 // acc[i][j][q] is output
 //   row wm*128 + 32 i + lane % 32, column wn*128 + 32 j + 8 (q / 4) + 4 (lane / 32) + q % 4.
 template <bool BF4 = false>
 __device__ __forceinline__ void gemm_mainloop_mx(const uint8_t* __restrict__ A, int64_t lda,
-                                                 const uint8_t* __restrict__ As, int64_t lda_s,
-                                                 int a_rows, const uint8_t* __restrict__ B,
-                                                 int64_t ldb, const uint8_t* __restrict__ Bs,
-                                                 int64_t ldb_s, int b_n0, int b_half, bool swiglu,
+                                                 const uint8_t* __restrict__ As, int64_t a_srow,
+                                                 int64_t a_sgrp, int a_rows,
+                                                 const uint8_t* __restrict__ B, int64_t ldb,
+                                                 const uint8_t* __restrict__ Bs, int64_t b_srow,
+                                                 int64_t b_sgrp, int b_n0, int b_half, bool swiglu,
                                                  int K, AccMx& acc, char* lds) {
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -318,12 +323,14 @@ __device__ __forceinline__ void gemm_mainloop_mx(const uint8_t* __restrict__ A, 
   // B rows through b_row_map move by 16 rows from q = 0 to 1 and by b_half (SwiGLU) or 32
   // rows from q = 0 to 2.
   const int rs = 64 * w + (lane >> 2);
-  t.sa0 = static_cast<uint32_t>(rs * lda_s + (lane & 3) * 4);
-  t.samax = static_cast<uint32_t>((a_rows - 1) * lda_s + (lane & 3) * 4);
-  t.sa16 = static_cast<uint32_t>(16 * lda_s);
-  t.sb0 = static_cast<uint32_t>(b_row_map(rs, b_n0, b_half, swiglu) * ldb_s + (lane & 3) * 4);
-  t.sbq1 = static_cast<uint32_t>(16 * ldb_s);
-  t.sbq2 = static_cast<uint32_t>((swiglu ? b_half : 32) * ldb_s);
+  t.sa0 = static_cast<uint32_t>(rs * a_srow + (lane & 3) * 4);
+  t.samax = static_cast<uint32_t>((a_rows - 1) * a_srow + (lane & 3) * 4);
+  t.sa16 = static_cast<uint32_t>(16 * a_srow);
+  t.sb0 = static_cast<uint32_t>(b_row_map(rs, b_n0, b_half, swiglu) * b_srow + (lane & 3) * 4);
+  t.sbq1 = static_cast<uint32_t>(16 * b_srow);
+  t.sbq2 = static_cast<uint32_t>((swiglu ? b_half : 32) * b_srow);
+  t.sa_grp = a_sgrp;
+  t.sb_grp = b_sgrp;
   t.ar = wm * 128 + (lane & 31);
   t.br = wn * 128 + (lane & 31);
   t.arow = t.ar * 128;

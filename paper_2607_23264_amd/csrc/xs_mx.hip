@@ -50,12 +50,15 @@ __device__ __forceinline__ uint32_t e2m1_code(float v) {
 }
 
 // One lane per 8 consecutive elements; four lanes per 32-element block. Codes: E4M3 one byte
-// per element, E2M1 two per byte (element 2 i in the low nibble).
+// per element, E2M1 two per byte (element 2 i in the low nibble). The scale of row r, block j
+// goes to byte r * s_row + (j / 16) * s_grp + j % 16: row-major rows with s_grp = 16, or
+// groups of 16 blocks (512 columns) [cols / 512][rows][16] with s_row = 16, s_grp = 16 rows.
 template <int FMT>
 __global__ __launch_bounds__(256) void quantize_kernel(const uint16_t* __restrict__ x, int64_t ldx,
                                                        int64_t rows, int cols,
                                                        uint8_t* __restrict__ codes, int64_t ldc,
-                                                       uint8_t* __restrict__ scales, int64_t lds) {
+                                                       uint8_t* __restrict__ scales, int64_t s_row,
+                                                       int64_t s_grp) {
   const int per_row = cols / 8;
   const int64_t total = rows * per_row;
   for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < total;
@@ -93,7 +96,10 @@ __global__ __launch_bounds__(256) void quantize_kernel(const uint16_t* __restric
       for (int q = 0; q < 8; ++q) p |= e2m1_code(v[q]) << (4 * q);
       *reinterpret_cast<uint32_t*>(codes + r * ldc + pc * 4) = p;
     }
-    if ((pc & 3) == 0) scales[r * lds + pc / 4] = static_cast<uint8_t>(e + 127);
+    if ((pc & 3) == 0) {
+      const int j = pc / 4;
+      scales[r * s_row + (j >> 4) * s_grp + (j & 15)] = static_cast<uint8_t>(e + 127);
+    }
   }
 }
 
@@ -116,7 +122,7 @@ __global__ __launch_bounds__(kMxThreads, 1) void gemm_mx_kernel(
     const uint64_t t0 = tr.buf ? wall_ticks() : 0;
     AccMx acc;
     gemm_mainloop_mx<BF4>(A + static_cast<int64_t>(m0) * lda, lda, As + static_cast<int64_t>(m0) * lda_s,
-                          lda_s, rows, B, ldb, Bs, ldb_s, n0, 0, false, K, acc, lds);
+                          lda_s, 16, rows, B, ldb, Bs, ldb_s, 16, n0, 0, false, K, acc, lds);
     const uint64_t t1 = tr.buf ? wall_ticks() : 0;
     if (tid < rows) rowptr[tid] = C + static_cast<int64_t>(m0 + tid) * ldc_bytes + static_cast<int64_t>(n0) * 2;
     stage_tile_mx(acc, lds);
@@ -147,30 +153,54 @@ int persistent_grid(int max_producers);
 
 static bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
-extern "C" int xs_quantize_mx(const void* x, int64_t rows, int32_t cols, int64_t ldx, int32_t fmt,
-                              void* codes, int64_t ld_codes, void* scales, int64_t ld_scales,
-                              void* stream) {
-  if (!x || !codes || !scales || rows < 0 || cols <= 0) return XS_EINVAL;
-  if (fmt != XS_FMT_E4M3 && fmt != XS_FMT_E2M1) return XS_EINVAL;
-  const int64_t code_bytes = fmt == XS_FMT_E4M3 ? cols : cols / 2;
-  if (cols % 32 || ldx < cols || ldx % 8 || ld_codes < code_bytes || ld_scales < cols / 32)
-    return XS_EINVAL;
-  if (!aligned(x, 16) || ld_codes % (fmt == XS_FMT_E4M3 ? 8 : 4) ||
-      !aligned(codes, fmt == XS_FMT_E4M3 ? 8 : 4))
-    return XS_EINVAL;
-  if (rows == 0) return XS_OK;
+namespace {
+
+int quantize_mx(const void* x, int64_t rows, int32_t cols, int64_t ldx, int32_t fmt, void* codes,
+                int64_t ld_codes, void* scales, int64_t s_row, int64_t s_grp, void* stream) {
   const int64_t pieces = rows * (cols / 8);
   const int grid = static_cast<int>(std::min<int64_t>((pieces + 255) / 256, 16384));
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (fmt == XS_FMT_E4M3)
     hipLaunchKernelGGL(mx::quantize_kernel<XS_FMT_E4M3>, dim3(grid), dim3(256), 0, st,
                        static_cast<const uint16_t*>(x), ldx, rows, cols, static_cast<uint8_t*>(codes),
-                       ld_codes, static_cast<uint8_t*>(scales), ld_scales);
+                       ld_codes, static_cast<uint8_t*>(scales), s_row, s_grp);
   else
     hipLaunchKernelGGL(mx::quantize_kernel<XS_FMT_E2M1>, dim3(grid), dim3(256), 0, st,
                        static_cast<const uint16_t*>(x), ldx, rows, cols, static_cast<uint8_t*>(codes),
-                       ld_codes, static_cast<uint8_t*>(scales), ld_scales);
+                       ld_codes, static_cast<uint8_t*>(scales), s_row, s_grp);
   return xs_host::launch_status();
+}
+
+int quantize_args_ok(const void* x, int64_t rows, int32_t cols, int64_t ldx, int32_t fmt, const void* codes,
+                     int64_t ld_codes, const void* scales) {
+  if (!x || !codes || !scales || rows < 0 || cols <= 0) return XS_EINVAL;
+  if (fmt != XS_FMT_E4M3 && fmt != XS_FMT_E2M1) return XS_EINVAL;
+  const int64_t code_bytes = fmt == XS_FMT_E4M3 ? cols : cols / 2;
+  if (cols % 32 || ldx < cols || ldx % 8 || ld_codes < code_bytes) return XS_EINVAL;
+  if (!aligned(x, 16) || ld_codes % (fmt == XS_FMT_E4M3 ? 8 : 4) || !aligned(codes, fmt == XS_FMT_E4M3 ? 8 : 4))
+    return XS_EINVAL;
+  return XS_OK;
+}
+
+}  // namespace
+
+extern "C" int xs_quantize_mx(const void* x, int64_t rows, int32_t cols, int64_t ldx, int32_t fmt,
+                              void* codes, int64_t ld_codes, void* scales, int64_t ld_scales,
+                              void* stream) {
+  int rc = quantize_args_ok(x, rows, cols, ldx, fmt, codes, ld_codes, scales);
+  if (rc) return rc;
+  if (ld_scales < cols / 32) return XS_EINVAL;
+  if (rows == 0) return XS_OK;
+  return quantize_mx(x, rows, cols, ldx, fmt, codes, ld_codes, scales, ld_scales, 16, stream);
+}
+
+extern "C" int xs_quantize_mx_grouped(const void* x, int64_t rows, int32_t cols, int64_t ldx, int32_t fmt,
+                                      void* codes, int64_t ld_codes, void* scales, void* stream) {
+  int rc = quantize_args_ok(x, rows, cols, ldx, fmt, codes, ld_codes, scales);
+  if (rc) return rc;
+  if (cols % 512 || !aligned(scales, 16)) return XS_EINVAL;
+  if (rows == 0) return XS_OK;
+  return quantize_mx(x, rows, cols, ldx, fmt, codes, ld_codes, scales, 16, rows * 16, stream);
 }
 
 extern "C" int xs_gemm_mx(const void* a, int64_t lda, const void* a_scales, int64_t lda_s,

@@ -56,12 +56,13 @@ class EPLayer:
         # weight code bytes per element: E4M3 one, packed E2M1 a half
         self.w_fmt = X.XS_FMT_E2M1 if precision == X.XS_PREC_W4A8 else X.XS_FMT_E4M3
         wdiv = 2 if precision == X.XS_PREC_W4A8 else 1
-        # bytes per dispatched token row and per h row (MXFP8: codes, then one scale per 32);
-        # MX rows sit at a pitch of whole 128-byte lines in the dispatch windows and in h, so
-        # that each 128-byte K step of a GEMM activation load reads one line, not two
+        # bytes per dispatched token row (MXFP8: codes, then one scale per 32) and per h row;
+        # MX token rows sit at a pitch of whole 128-byte lines in the dispatch windows, so that
+        # each 128-byte K step of a GEMM activation load reads one line, not two (MX h is
+        # h_rows code rows of I bytes followed by the scale groups)
         self.row_bytes = s.H + s.H // 32 if mxp else 2 * s.H
         self.row_pitch = -(-self.row_bytes // 128) * 128 if mxp else self.row_bytes
-        self.h_bytes = -(-(s.I + s.I // 32) // 128) * 128 if mxp else 2 * s.I
+        self.h_bytes = s.I + s.I // 32 if mxp else 2 * s.I
         self.dev = torch.device(device)
         cap = s.cap if s.cap is not None else s.n_src * s.T * min(s.k, s.epw)
         self.cap = cap
@@ -101,9 +102,9 @@ class EPLayer:
             self.h_ws = torch.zeros((h_rows, self.h_bytes), dtype=torch.uint8, device=d)
             E_, I_, H_ = s.n_experts, s.I, s.H
             self.w1q = torch.zeros((E_, 2 * I_, H_ // wdiv), dtype=torch.uint8, device=d)
-            self.w1s = torch.zeros((E_, 2 * I_, H_ // 32), dtype=torch.uint8, device=d)
+            self.w1s = torch.zeros((H_ // 512, E_ * 2 * I_, 16), dtype=torch.uint8, device=d)   # scale groups
             self.w2q = torch.zeros((E_, H_, I_ // wdiv), dtype=torch.uint8, device=d)
-            self.w2s = torch.zeros((E_, H_, I_ // 32), dtype=torch.uint8, device=d)
+            self.w2s = torch.zeros((I_ // 512, E_ * H_, 16), dtype=torch.uint8, device=d)
         else:
             self.h_ws = torch.zeros((h_rows, s.I if s.I else 1), dtype=torch.int16, device=d)
         self.y_ws = torch.zeros((h_rows, s.H), dtype=torch.int16, device=d)
@@ -166,14 +167,14 @@ class EPLayer:
 
     def quantize_weights(self):
         """MX codes (E4M3, or packed E2M1 for W4A8) and scales of W1 (along H) and W2 (along I),
-        on the GPU."""
+        on the GPU; the scales grouped by 512 K elements over all weight rows."""
         s = self.s
         st = self.stream
-        X.check(X.xs_quantize_mx(self.w1.data_ptr(), s.n_experts * 2 * s.I, s.H, s.H, self.w_fmt,
-                                 self.w1q.data_ptr(), self.w1q.shape[2], self.w1s.data_ptr(), s.H // 32, st),
+        X.check(X.xs_quantize_mx_grouped(self.w1.data_ptr(), s.n_experts * 2 * s.I, s.H, s.H, self.w_fmt,
+                                         self.w1q.data_ptr(), self.w1q.shape[2], self.w1s.data_ptr(), st),
                 "quantize w1")
-        X.check(X.xs_quantize_mx(self.w2.data_ptr(), s.n_experts * s.H, s.I, s.I, self.w_fmt,
-                                 self.w2q.data_ptr(), self.w2q.shape[2], self.w2s.data_ptr(), s.I // 32, st),
+        X.check(X.xs_quantize_mx_grouped(self.w2.data_ptr(), s.n_experts * s.H, s.I, s.I, self.w_fmt,
+                                         self.w2q.data_ptr(), self.w2q.shape[2], self.w2s.data_ptr(), st),
                 "quantize w2")
 
     @property

@@ -137,6 +137,7 @@ xs_dispatch_ring_workspace_bytes = _sig("xs_dispatch_ring_workspace_bytes", C.c_
 xs_dispatch_ring = _sig("xs_dispatch_ring", C.c_int, vp, i32, i32, vp, vp, i32, i32, P(xs_window), i32,
                         P(xs_window), i32, i32, i64, vp, i64, vp, vp, vp)
 xs_quantize_mx = _sig("xs_quantize_mx", C.c_int, vp, i64, i32, i64, i32, vp, i64, vp, i64, vp)
+xs_quantize_mx_grouped = _sig("xs_quantize_mx_grouped", C.c_int, vp, i64, i32, i64, i32, vp, i64, vp, vp)
 xs_gemm_mx = _sig("xs_gemm_mx", C.c_int, vp, i64, vp, i64, vp, i64, vp, i64, i32, vp, i64, i32, i32, i32,
                   P(xs_trace), vp)
 xs_model_predict = _sig("xs_model_predict", C.c_int, P(xs_model), P(xs_burst), i32, f64, P(xs_burst_pred))
@@ -147,7 +148,7 @@ xs_clock_rate_hz = _sig("xs_clock_rate_hz", C.c_double)
 EXPORTED = ["xs_strerror", "xs_version", "xs_route_topk_softmax", "xs_dispatch_layout_workspace_bytes",
             "xs_dispatch_layout", "xs_dispatch", "xs_ep_layer_workspace_bytes", "xs_expert_ffn",
             "xs_combine_send", "xs_combine_reduce", "xs_fused_ep_layer", "xs_gemm", "xs_gemm_scatter",
-            "xs_scatter_copy", "xs_attention", "xs_ulysses_copy", "xs_quantize_mx", "xs_gemm_mx", "xs_dispatch_rows",
+            "xs_scatter_copy", "xs_attention", "xs_ulysses_copy", "xs_quantize_mx", "xs_quantize_mx_grouped", "xs_gemm_mx", "xs_dispatch_rows",
             "xs_ring_slot_bytes", "xs_dispatch_ring_workspace_bytes", "xs_dispatch_ring",
             "xs_model_predict", "xs_model_fit",
             "xs_xstage_microbench", "xs_clock_rate_hz"]

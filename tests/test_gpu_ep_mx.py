@@ -136,17 +136,17 @@ def test_tiny_layer_matches_oracle_for_every_policy(prec):
         assert np.array_equal(win[d, :n, :H], ref["win_codes"][d, :n]), f"window {d} codes"
         assert np.array_equal(win[d, :n, H:H + H // 32], ref["win_scales"][d, :n]), f"window {d} scales"
         assert (win[d, n:] == 0xFF).all(), f"window {d} rows past the count were written"
-    # h rows of every expert: I codes then I / 32 scales
-    h = lay.h_ws.cpu().numpy()
+    # h rows of every expert: I codes and I / 32 scales (code rows, then the scale groups)
+    hcodes, hscales = _h_codes_scales(lay, cfg.I)
     bases = _window_bases(lay)
     epw = cfg.E // cfg.W
     flips = 0
     for e, (hc, hs) in ref["h"].items():
         d, r0 = e // epw, int(ref["layout"]["expert_offsets"][e])
         m = hc.shape[0]
-        rows = h[bases[d] + r0:bases[d] + r0 + m]
+        sl = slice(bases[d] + r0, bases[d] + r0 + m)
         xq = (ref["win_codes"][d, r0:r0 + m], ref["win_scales"][d, r0:r0 + m])
-        flips += _h_within_fp32_bound(rows[:, :cfg.I], rows[:, cfg.I:cfg.I + cfg.I // 32], xq,
+        flips += _h_within_fp32_bound(hcodes[sl], hscales[sl], xq,
                                       omx.quantize_rows(inp["w1"][e], _wfmt(prec)), f"h of expert {e}", _wfmt(prec))
     print(f"h codes that differ from the oracle's (all within the fp32 bound): {flips}")
     # combine rows (bf16 expert outputs) against the oracle's rounded rows
@@ -332,6 +332,23 @@ def test_dispatch_rows_bitexact():
     torch.cuda.synchronize()
 
 
+def _ungroup(groups, expert, rows):
+    """Row-major scales [rows][K / 32] of one expert from the grouped layout [K / 512][experts *
+    rows][16] (group g of row r holds the scales of blocks 16 g .. 16 g + 15)."""
+    g = groups.cpu().numpy()[:, expert * rows:(expert + 1) * rows, :]
+    return np.ascontiguousarray(g.transpose(1, 0, 2)).reshape(rows, -1)
+
+
+def _h_codes_scales(lay, I):
+    """h code rows [h_rows][I] and row-major h scales [h_rows][I / 32] from h_ws (code rows,
+    then the scale groups [I / 512][h_rows][16])."""
+    flat = lay.h_ws.cpu().numpy().reshape(-1)
+    hr = flat.size // (I + I // 32)
+    codes = flat[:hr * I].reshape(hr, I)
+    sc = flat[hr * I:hr * (I + I // 32)].reshape(I // 512, hr, 16).transpose(1, 0, 2).reshape(hr, I // 32)
+    return codes, sc
+
+
 @pytest.mark.parametrize("prec", PRECISIONS)
 def test_weight_quantization_matches_oracle(prec):
     cfg = synth.EP_TINY
@@ -343,8 +360,8 @@ def test_weight_quantization_matches_oracle(prec):
         c1, s1 = omx.quantize_rows(inp["w1"][i], _wfmt(prec))
         c2, s2 = omx.quantize_rows(inp["w2"][i], _wfmt(prec))
         c1, c2 = pack(c1), pack(c2)
-        assert np.array_equal(lay.w1q[i].cpu().numpy(), c1) and np.array_equal(lay.w1s[i].cpu().numpy(), s1)
-        assert np.array_equal(lay.w2q[i].cpu().numpy(), c2) and np.array_equal(lay.w2s[i].cpu().numpy(), s2)
+        assert np.array_equal(lay.w1q[i].cpu().numpy(), c1) and np.array_equal(_ungroup(lay.w1s, i, 2 * cfg.I), s1)
+        assert np.array_equal(lay.w2q[i].cpu().numpy(), c2) and np.array_equal(_ungroup(lay.w2s, i, cfg.H), s2)
 
 
 def _records(buf, count):

@@ -39,6 +39,36 @@ def _quantize(x_bits, fmt, pad_codes=0, pad_scales=0):
     return codes.cpu().numpy(), scales.cpu().numpy(), cb
 
 
+@pytest.mark.parametrize("fmt_name", ["E4M3", "E2M1"])
+@pytest.mark.parametrize("rows,cols", [(1, 512), (37, 1536), (300, 7168)])
+def test_quantize_grouped_is_the_oracle_regrouped(fmt_name, rows, cols):
+    # the grouped quantizer writes the oracle's codes bit for bit and its scales regrouped as
+    # [cols / 512][rows][16]: scale (r, j) at ((j / 16) * rows + r) * 16 + j % 16
+    X = xs()
+    fmt = getattr(X, f"XS_FMT_{fmt_name}")
+    g = np.random.default_rng(rows * 7 + cols)
+    x = synth.to_bf16_bits((g.standard_normal((rows, cols)) * np.exp(g.uniform(-6, 6, (rows, 1)))).astype(np.float32))
+    want_c, want_s = mx.quantize_mx(_bits_f64(x), getattr(mx, fmt_name))
+    if fmt_name == "E2M1":
+        want_c = mx.pack_e2m1(want_c)
+    cb = want_c.shape[1]
+    codes = torch.full((rows, cb), 0x5A, dtype=torch.uint8, device="cuda")
+    scales = torch.full((cols // 512, rows, 16), 0xA5, dtype=torch.uint8, device="cuda")
+    dx = dev_bits(x)
+    X.check(X.xs_quantize_mx_grouped(dx.data_ptr(), rows, cols, cols, fmt, codes.data_ptr(), cb,
+                                     scales.data_ptr(), _stream()))
+    torch.cuda.synchronize()
+    assert np.array_equal(codes.cpu().numpy(), want_c)
+    got_s = scales.cpu().numpy().transpose(1, 0, 2).reshape(rows, cols // 32)
+    assert np.array_equal(got_s, want_s)
+    # arguments: columns not a multiple of 512, a misaligned scale base
+    assert X.xs_quantize_mx_grouped(dx.data_ptr(), rows, 480, 480, fmt, codes.data_ptr(), cb, scales.data_ptr(),
+                                    _stream()) == X.XS_EINVAL
+    assert X.xs_quantize_mx_grouped(dx.data_ptr(), rows, cols, cols, fmt, codes.data_ptr(), cb,
+                                    scales.data_ptr() + 4, _stream()) == X.XS_EINVAL
+    torch.cuda.synchronize()
+
+
 def _special_rows(cols):
     """Rows that hit the exponent rule's edges and the encoder's ties."""
     t = mx.fmt_values(mx.E4M3)
