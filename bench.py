@@ -443,16 +443,18 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] warmup done; timing {a.steps} steps ({a.policy})")
     stream = torch.cuda.current_stream().cuda_stream
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # one event per step boundary (the first and last bracket the timed region)
+    bounds = [torch.cuda.Event(enable_timing=True) for _ in range(a.steps + 1)]
     torch.cuda.synchronize()
-    start.record()
+    bounds[0].record()
     for i in range(a.steps):
         lay.L.events[X.XS_EV_FFN] = ev.ev[2 * i]
         lay.L.events[X.XS_EV_FFN_END] = ev.ev[2 * i + 1]
         lay.fused(pol[a.policy])
-    stop.record()
+        bounds[i + 1].record()
     torch.cuda.synchronize()
-    total_ms = start.elapsed_time(stop)
+    total_ms = bounds[0].elapsed_time(bounds[-1])
+    step_us = [bounds[i].elapsed_time(bounds[i + 1]) * 1e3 for i in range(a.steps)]
     ffn_ms = [ev.elapsed_ms(2 * i, 2 * i + 1) for i in range(a.steps)]
     lay.L.events[X.XS_EV_FFN] = None
     lay.L.events[X.XS_EV_FFN_END] = None
@@ -494,6 +496,11 @@ def main():
     tr = read_traffic(os.path.join(HERE, "profiles", "ep_ffn_kernel_dsv3_share_traffic.md"))
     disp_bytes = cfg.T * cfg.k * cfg.H * 2          # stored rows (plus T * H * 2 read)
     red_bytes = cfg.T * cfg.k * cfg.H * 2 + cfg.T * cfg.H * 2
+    res["step_us_dist"] = {"median": float(np.median(step_us)), "p10": float(np.percentile(step_us, 10)),
+                           "p90": float(np.percentile(step_us, 90)), "min": float(np.min(step_us)),
+                           "max": float(np.max(step_us))}
+    res["ffn_us_dist"] = {"median": float(np.median(ffn_ms)) * 1e3, "p10": float(np.percentile(ffn_ms, 10)) * 1e3,
+                          "p90": float(np.percentile(ffn_ms, 90)) * 1e3}
     res["phases_in_step_us"] = in_step
     res["store_GBps"] = {
         "dispatch_stored": disp_bytes / (in_step["dispatch"] * 1e-6) / 1e9,
