@@ -61,62 +61,98 @@ struct RingArgs {
   int64_t timeout_ticks;
 };
 
+// Exclusive prefix sum of v over the block's threads in order (1024 threads, 16 waves): a
+// shuffle scan inside each wave, then each thread adds the totals of the waves before it.
+// `total` receives the block's sum. Two barriers; wsum is 16 ints of LDS.
+__device__ __forceinline__ int block_exclusive_scan(int v, int* wsum, int& total) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wsum[wv] = x;
+  __syncthreads();
+  int before = 0, all = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int w = wsum[i];
+    before += i < wv ? w : 0;
+    all += w;
+  }
+  total = all;
+  __syncthreads();
+  return before + x - v;
+}
+
+constexpr int kPlanInts = 32768;   // expert indices staged in LDS per round (128 KiB)
+
 // Entry numbers, entries per destination and a clean control block (one workgroup of 1024).
 // Entries of ring d are numbered in token order (and k slot order within a token without
 // dedup): for each destination an exclusive scan over contiguous token chunks, one per thread.
 __global__ __launch_bounds__(1024) void ring_plan_kernel(RingArgs a) {
-  __shared__ int scan[1024];
+  __shared__ int sidx[kPlanInts];
+  __shared__ int wsum[16];
+  __shared__ int base[XS_MAX_WINDOWS];
   const int W = a.win.n;
   const int epw = a.E / W;
   const int tid = threadIdx.x;
-  for (int i = tid; i < W; i += blockDim.x) a.tail[i * kLine] = 0;
+  for (int i = tid; i < W; i += blockDim.x) {
+    a.tail[i * kLine] = 0;
+    base[i] = 0;
+  }
   if (tid == 0) *a.abort_word = 0;
   for (int64_t i = tid; i < static_cast<int64_t>(W) * a.S; i += blockDim.x) {
     a.pub[i] = 0;
     a.rel[i] = 0;
   }
-  const int chunk = (a.T + blockDim.x - 1) / blockDim.x;
-  const int t0 = min(a.T, tid * chunk), t1 = min(a.T, t0 + chunk);
-  for (int d = 0; d < W; ++d) {
-    int n = 0;
-    for (int t = t0; t < t1; ++t) {
-      bool any = false;
-      for (int j = 0; j < a.k; ++j) {
-        const int e = a.idx[static_cast<int64_t>(t) * a.k + j];
-        if (e < 0 || e >= a.E || e / epw != d) continue;
-        if (!a.dedup) ++n;
-        any = true;
-      }
-      if (a.dedup && any) ++n;
-    }
-    scan[tid] = n;
+  // Rounds of R tokens: their k indices are staged in LDS by coalesced loads, then each thread
+  // numbers a contiguous run of the round's tokens per destination (entries in token order,
+  // k slots ascending), continuing from the destination's count of earlier rounds.
+  const int R = kPlanInts / a.k;
+  for (int r0 = 0; r0 < a.T; r0 += R) {
+    const int nr = min(R, a.T - r0);
+    __syncthreads();   // the previous round's reads of sidx and base are done
+    for (int i = tid; i < nr * a.k; i += blockDim.x) sidx[i] = a.idx[static_cast<int64_t>(r0) * a.k + i];
     __syncthreads();
-    for (int off = 1; off < static_cast<int>(blockDim.x); off <<= 1) {   // inclusive scan
-      const int v = tid >= off ? scan[tid - off] : 0;
-      __syncthreads();
-      scan[tid] += v;
-      __syncthreads();
-    }
-    int next = scan[tid] - n;                                            // exclusive
-    for (int t = t0; t < t1; ++t) {
-      bool any = false;
-      for (int j = 0; j < a.k; ++j) {
-        const int64_t q = static_cast<int64_t>(t) * a.k + j;
-        const int e = a.idx[q];
-        if (e < 0 || e >= a.E || e / epw != d) continue;
-        a.entry_no[q] = a.dedup ? next : next++;
-        any = true;
+    const int chunk = (nr + blockDim.x - 1) / blockDim.x;
+    const int t0 = min(nr, tid * chunk), t1 = min(nr, t0 + chunk);
+    for (int d = 0; d < W; ++d) {
+      const int lo = d * epw, hi = lo + epw;   // destination d's experts
+      int n = 0;
+      for (int t = t0; t < t1; ++t) {
+        int c = 0;
+        for (int j = 0; j < a.k; ++j) {
+          const int e = sidx[t * a.k + j];
+          c += e >= lo && e < hi;
+        }
+        n += a.dedup ? (c > 0) : c;
       }
-      if (a.dedup && any) ++next;
-    }
-    if (tid == blockDim.x - 1) {
-      a.total[d * kLine] = scan[tid];
-      if (a.stats) {
-        a.stats[d] = scan[tid];
-        a.stats[W + d] = 0;
+      int round_total;
+      const int b = base[d];   // read before the scan's barriers; thread 0 advances it after them
+      int next = b + block_exclusive_scan(n, wsum, round_total);
+      for (int t = t0; t < t1; ++t) {
+        bool any = false;
+        for (int j = 0; j < a.k; ++j) {
+          const int e = sidx[t * a.k + j];
+          if (e >= lo && e < hi) {
+            a.entry_no[static_cast<int64_t>(r0 + t) * a.k + j] = a.dedup ? next : next++;
+            any = true;
+          }
+        }
+        if (a.dedup && any) ++next;
       }
+      if (tid == 0) base[d] = b + round_total;
     }
-    __syncthreads();
+  }
+  __syncthreads();
+  for (int d = tid; d < W; d += blockDim.x) {
+    a.total[d * kLine] = base[d];
+    if (a.stats) {
+      a.stats[d] = base[d];
+      a.stats[W + d] = 0;
+    }
   }
 }
 
