@@ -401,7 +401,7 @@ def ring_line(X, torch, synth, reps=5):
 def main():
     a = parse()
     if a.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {a.gpus}); this build has no multi-GPU path",
+        print(f"bench.py runs on one GPU only (got --gpus {a.gpus}); the library has no multi-GPU path",
               file=sys.stderr)
         sys.exit(2)
     import dataclasses
