@@ -270,6 +270,7 @@ def mx_line(X, torch, cfg, inp, rank, experts, pol, steps, warmup, bf16_step_us,
     names = ["route", "layout", "dispatch", "plan", "expert_ffn", "signal", "combine_reduce"]
     in_step = {n: float(np.median([pev.elapsed_ms(8 * i + j, 8 * i + j + 1) * 1e3 for i in range(n_ph)]))
                for j, n in enumerate(names)}
+    graph = graph_steps(torch, lay, pol[a.policy], a.steps)
     status = int(lay.status.item())
     rows = int(lay.dest_counts[rank].item())
     del lay
@@ -398,6 +399,35 @@ def ring_line(X, torch, synth, reps=5):
             "entries_with_dedup": dd, "dedup_ratio": no_dd / dd, "cells": cells}
 
 
+def graph_steps(torch, lay, pol, steps):
+    """The same step captured once in a HIP graph (torch's graph API over the library's launches
+    on the capture stream) and replayed `steps` times: the launch gaps between the step's
+    kernels go away, the work is identical (the layer's kernels only; no memset, copy or host
+    synchronisation inside a step). Reported beside the eager step, not instead of it."""
+    try:
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            lay.fused(pol)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            lay.fused(pol)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return {"us_per_step": e0.elapsed_time(e1) * 1e3 / steps, "steps": steps}
+    except RuntimeError as err:   # capture refused: report it, keep the eager figures
+        torch.cuda.synchronize()
+        return {"us_per_step": None, "error": str(err)[:200]}
+
+
 def main():
     a = parse()
     if a.gpus != 1:
@@ -471,6 +501,7 @@ def main():
     names = ["route", "layout", "dispatch", "plan", "expert_ffn", "signal", "combine_reduce"]
     in_step = {n: float(np.median([pev.elapsed_ms(8 * i + j, 8 * i + j + 1) * 1e3 for i in range(n_ph)]))
                for j, n in enumerate(names)}
+    graph = graph_steps(torch, lay, pol[a.policy], a.steps)
     status = int(lay.status.item())
     if status:
         log(f"[bench] device status {status}: {X.xs_strerror(status).decode()}")
@@ -496,6 +527,7 @@ def main():
     tr = read_traffic(os.path.join(HERE, "profiles", "ep_ffn_kernel_dsv3_share_traffic.md"))
     disp_bytes = cfg.T * cfg.k * cfg.H * 2          # stored rows (plus T * H * 2 read)
     red_bytes = cfg.T * cfg.k * cfg.H * 2 + cfg.T * cfg.H * 2
+    res["graph_replay"] = graph
     res["step_us_dist"] = {"median": float(np.median(step_us)), "p10": float(np.percentile(step_us, 10)),
                            "p90": float(np.percentile(step_us, 90)), "min": float(np.min(step_us)),
                            "max": float(np.max(step_us))}
