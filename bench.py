@@ -270,7 +270,6 @@ def mx_line(X, torch, cfg, inp, rank, experts, pol, steps, warmup, bf16_step_us,
     names = ["route", "layout", "dispatch", "plan", "expert_ffn", "signal", "combine_reduce"]
     in_step = {n: float(np.median([pev.elapsed_ms(8 * i + j, 8 * i + j + 1) * 1e3 for i in range(n_ph)]))
                for j, n in enumerate(names)}
-    graph = graph_steps(torch, lay, pol[a.policy], a.steps)
     status = int(lay.status.item())
     rows = int(lay.dest_counts[rank].item())
     del lay
