@@ -26,6 +26,7 @@ import numpy as np
 
 STATUS_OK = 0
 STATUS_CAPACITY = 5      # a window received more rows than its capacity
+STATUS_BADINPUT = 7      # a token lists one expert twice
 SENTINEL_BF16 = np.uint16(0xFFFF)  # a NaN pattern no correct kernel ever writes
 
 __all__ = [
@@ -110,7 +111,8 @@ def dispatch_layout(idx: np.ndarray, E: int, W: int, cap: int | None = None):
       dest_counts    [W]         rows in each window
       slot_row       [n_src, T, k] row of the slot inside its window
       row_src        list of W int64 arrays, the inverse map (src << 24 | t*k + j)
-      status         STATUS_CAPACITY if some window exceeds ``cap`` rows
+      status         STATUS_CAPACITY if some window exceeds ``cap`` rows, STATUS_BADINPUT
+                     if a token lists one expert twice
     """
     idx = np.asarray(idx, dtype=np.int64)
     if idx.ndim == 2:
@@ -151,6 +153,10 @@ def dispatch_layout(idx: np.ndarray, E: int, W: int, cap: int | None = None):
     status = STATUS_OK
     if cap is not None and dest_counts.size and dest_counts.max() > cap:
         status = STATUS_CAPACITY
+    # the k experts of a token must be distinct: a repeated one is invalid input (the rows are
+    # still assigned one per slot here, but callers must not rely on them)
+    if k > 1 and np.any(np.sort(idx, axis=2)[:, :, 1:] == np.sort(idx, axis=2)[:, :, :-1]):
+        status = STATUS_BADINPUT
     return {
         "expert_counts": counts.astype(np.int32),
         "src_base": src_base.astype(np.int32),

@@ -21,7 +21,9 @@ dequantized operands.
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
 import math
+import os
 
 import numpy as np
 
@@ -96,17 +98,35 @@ def shared_exponent(amax, fmt):
     return np.clip(e, -127, 127).astype(np.int64)
 
 
+def _quantize_block_rows(x, fmt, group):
+    g = x.reshape(*x.shape[:-1], x.shape[-1] // group, group)
+    e = shared_exponent(np.abs(g).max(axis=-1), fmt)
+    codes = encode(g / np.ldexp(1.0, e)[..., None], fmt)
+    return codes.reshape(x.shape), (e + 127).astype(np.uint8)
+
+
 def quantize_mx(x, fmt, group=GROUP):
     """x: fp64 values [..., K] with K % group == 0. Returns (codes uint8 [..., K], scale codes
-    uint8 [..., K / group] = e + 127)."""
+    uint8 [..., K / group] = e + 127).
+
+    Every block is quantized on its own, so large inputs are split into row chunks handled on
+    a thread pool (numpy releases the interpreter lock in these element-wise steps); the
+    arithmetic of each element is the same either way."""
     x = np.asarray(x, dtype=np.float64)
     K = x.shape[-1]
     if K % group:
         raise ValueError("reduction length must be a multiple of the group")
-    g = x.reshape(*x.shape[:-1], K // group, group)
-    e = shared_exponent(np.abs(g).max(axis=-1), fmt)
-    codes = encode(g / np.ldexp(1.0, e)[..., None], fmt)
-    return codes.reshape(x.shape), (e + 127).astype(np.uint8)
+    rows = x.reshape(-1, K)
+    if rows.size <= 1 << 20:
+        c, s = _quantize_block_rows(rows, fmt, group)
+    else:
+        step = max(1, (1 << 16) // K)
+        with cf.ThreadPoolExecutor(max(1, len(os.sched_getaffinity(0)))) as ex:
+            parts = list(ex.map(lambda r0: _quantize_block_rows(rows[r0:r0 + step], fmt, group),
+                                range(0, rows.shape[0], step)))
+        c = np.concatenate([p[0] for p in parts])
+        s = np.concatenate([p[1] for p in parts])
+    return c.reshape(x.shape), s.reshape(*x.shape[:-1], K // group)
 
 
 def dequantize_mx(codes, scales, fmt, group=GROUP):

@@ -8,13 +8,12 @@ whole Linear-1 output row, so it depends on all P1 Linear-1 tiles of row p.
 * Expert-Wave (Sec. 4.3): rows are grouped into waves of consecutive experts; the
   global order is [L1 tiles of wave 0, L2 tiles of wave 0, L1 of wave 1, ...] and
   scheduler instance g of G takes every G-th entry starting at g.
-* Cross-wave interleaving (App. A.2, Alg. 1): instance g keeps one cursor per tile
-  stream, both starting at g and advancing by G. It emits the next Linear-2 tile
-  when one remains and its row trails the Linear-1 cursor's row by at least the
-  lead D (the Linear-1 row counts as infinitely far ahead once Linear-1 is done);
-  otherwise it emits the next Linear-1 tile. The paired-CTA role r of the paper
-  has no counterpart here and is dropped. "P P_1" in the paper is read as the
-  product rows x tiles-per-row.
+* Cross-wave interleaving (App. A.2, Alg. 1): instance g of G owns every G-th entry
+  of each tile stream, starting at its own index, and a Linear-2 entry may run before
+  the instance's next Linear-1 entry only when Linear-1 leads it by at least D rows
+  (``interleave_stream`` writes this as a merge of the two owned lists). The
+  paired-CTA role r of the paper has no counterpart here and is dropped. "P P_1" in
+  the paper is read as the product rows x tiles-per-row.
 * Chunked pacing (a generalisation, not in the paper): the interleave rule, but
   after ``chunk`` consecutive Linear-2 tiles a Linear-1 tile is forced if any is
   left.
@@ -34,24 +33,33 @@ Tile = Tuple[int, int, int]
 
 def interleave_stream(g: int, G: int, P: int, P1: int, P2: int, D: int,
                       chunk: int | None = None) -> List[Tile]:
-    n1, n2 = P * P1, P * P2
-    k1 = k2 = g
-    run = 0   # consecutive Linear-2 tiles since the last Linear-1 tile
+    """The tiles scheduler instance g runs, in order, under cross-wave interleaving.
+
+    Instance g owns every G-th entry of each stream starting at g: Linear-1 entries
+    g, g + G, ... and Linear-2 entries g, g + G, ... It runs its own entries in stream
+    order. A Linear-2 entry of row r may run ahead of the instance's next Linear-1 entry
+    only when that Linear-1 entry is at least D rows further on (row >= r + D); the lead
+    is what keeps a Linear-2 tile from reaching a row whose Linear-1 tiles may not all be
+    done. So the order is a merge of the two owned lists: before each owned Linear-1 entry
+    come the not yet run Linear-2 entries that this entry's row already releases (at most
+    ``chunk`` of them when a cap is given; the rest wait for the next Linear-1 entry, whose
+    row releases at least as much), and once the Linear-1 entries are used up every
+    remaining Linear-2 entry follows.
+    """
+    own1 = list(range(g, P * P1, G))
+    own2 = list(range(g, P * P2, G))
     out: List[Tile] = []
-    while k1 < n1 or k2 < n2:
-        p1 = k1 // P1 if k1 < n1 else math.inf
-        p2 = k2 // P2
-        take_l2 = k2 < n2 and p2 + D <= p1
-        if take_l2 and chunk is not None and run >= chunk and k1 < n1:
-            take_l2 = False
-        if take_l2:
-            out.append((2, p2, k2))
-            k2 += G
-            run += 1
-        else:
-            out.append((1, int(p1), k1))
-            k1 += G
-            run = 0
+    nxt = 0   # first owned Linear-2 entry not yet placed
+    for e1 in own1:
+        r1 = e1 // P1
+        placed = 0
+        while (nxt < len(own2) and own2[nxt] // P2 + D <= r1
+               and (chunk is None or placed < chunk)):
+            out.append((2, own2[nxt] // P2, own2[nxt]))
+            nxt += 1
+            placed += 1
+        out.append((1, r1, e1))
+    out.extend((2, e2 // P2, e2) for e2 in own2[nxt:])
     return out
 
 

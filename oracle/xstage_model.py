@@ -23,8 +23,9 @@ Functions follow the equations in order:
 stretch until enough volume drains, Sec. 3.5). The reading used here: a fluid
 queue capped at Q drains at R, so a burst whose guard fails is issued in
 max(T0, (q + V - Q) / R) and leaves the queue at Q; with the guard holding this is
-exactly Eq. 5, and its homogeneous steady state is Eq. 1 ("parity pinned" by the
-recurrence tests, the stalled branch itself is a reading).
+exactly Eq. 5, and its homogeneous steady state is Eq. 1. The stalled branch is pinned
+against a brute-force time-stepped fluid-queue simulation (tests), which derives the same
+issue time and backlog from the queue's rules rather than from this formula.
 
 ``fit`` reads the calibration procedure of Sec. 3.3/3.5: T0 from recovered
 (large-gap) points, R from the zero-gap steady state T_period = V / R, Q from the
@@ -145,7 +146,8 @@ def predict(V, T0, G, R: float, Q: float, q0: float = 0.0):
 
 def completion_coupled_period(T0, G, V, R):
     """Counterfactual of Sec. 3.2: an issuer blocked until remote visibility adds the
-    gap to the communication time, period = max(T0, V/R) + G (a reading)."""
+    gap to the communication time, period = max(T0, V/R) + G (a reading; pinned against
+    a simulated issuer that waits for its queue to empty before the gap)."""
     return np.maximum(T0, np.divide(V, R)) + G
 
 
@@ -207,12 +209,18 @@ def average_rate_feasible(V, T0, T_L2, T_L1, n1, n2, R) -> bool:
 
 
 def d_knee(b_n, K_sm, h_inter):
-    """App. A.2 anti-starvation lead: ceil(b_n K_SM / (2 h_inter))."""
+    """App. A.2 anti-starvation lead: ceil(b_n K_SM / (2 h_inter)), the rows spanned by one
+    round of Linear-1 tiles over all K_SM producers (P1 = 2 h_inter / b_n tiles per row).
+    The rows-per-round reading is pinned by counting; the paper calls the knee approximate,
+    and a lock-step simulation shows the wait-free lead varies around it with the tile mix,
+    so its scheduling meaning is parity unpinned."""
     return int(math.ceil(b_n * K_sm / (2.0 * h_inter)))
 
 
 def mma_stall(T_RS, T_cover):
-    """App. A.2: [T_RS - T_cover]_+."""
+    """App. A.2: [T_RS - T_cover]_+, the part of a tile's remote-store span that the mainloop
+    before its staging slot's reuse does not cover (pinned against a discrete-event
+    simulation of a producer and an epilogue sharing two staging slots)."""
     return pos(np.subtract(T_RS, T_cover))
 
 

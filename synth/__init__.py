@@ -16,6 +16,8 @@ permutation, 101+s per-source Gumbel noise, 200 pre-filled remote combine rows,
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
+import os
 from dataclasses import dataclass, field
 from typing import Optional
 
@@ -168,8 +170,12 @@ def ep_x(cfg: EPConfig, seed: int = 0) -> np.ndarray:
     if cfg.n_src == 1:
         return normal_bf16(seed, 1, (cfg.T, cfg.H))[None]
     out = np.empty((cfg.n_src, cfg.T, cfg.H), dtype=np.uint16)
-    for s in range(cfg.n_src):
+
+    def one(s):
         out[s] = normal_bf16(seed, 10 + s, (cfg.T, cfg.H))
+
+    with cf.ThreadPoolExecutor(max(1, min(16, len(os.sched_getaffinity(0))))) as ex:
+        list(ex.map(one, range(cfg.n_src)))
     return out
 
 
@@ -182,9 +188,14 @@ def ep_weights(cfg: EPConfig, experts, seed: int = 0):
     experts = list(experts)
     w1 = np.empty((len(experts), 2 * cfg.I, cfg.H), dtype=np.uint16)
     w2 = np.empty((len(experts), cfg.H, cfg.I), dtype=np.uint16)
-    for i, e in enumerate(experts):
+
+    def one(i):   # every expert has its own streams, so experts are drawn concurrently
+        e = experts[i]
         w1[i] = normal_bf16(seed, 300 + e, (2 * cfg.I, cfg.H), std=cfg.w_std)
         w2[i] = normal_bf16(seed, 600 + e, (cfg.H, cfg.I), std=cfg.w_std)
+
+    with cf.ThreadPoolExecutor(max(1, min(16, len(os.sched_getaffinity(0))))) as ex:
+        list(ex.map(one, range(len(experts))))
     return w1, w2
 
 

@@ -143,6 +143,27 @@ def test_layout_invariants_multi_source():
         assert np.array_equal(r, np.arange(lay["dest_counts"][d]))
 
 
+def test_route_masked_experts_rank_last_in_index_order():
+    # -inf logits (masked experts) come after every finite one, ties to the lower index,
+    # with zero weight; checked against the selection brute force
+    lg = np.full((4, 10), -np.inf, np.float32)
+    lg[0, [2, 7]] = [0.5, 1.5]
+    lg[1, :] = 0.0
+    lg[1, 3:6] = -np.inf
+    lg[2, 9] = 2.0
+    lg[3, [0, 4, 8]] = [1.0, 1.0, 3.0]
+    idx, w = ep.route_topk_softmax(lg, 5)
+    assert np.array_equal(idx, _route_by_selection(lg, 5))
+    assert idx[0].tolist() == [7, 2, 0, 1, 3] and idx[2].tolist() == [9, 0, 1, 2, 3]
+    assert np.all(w[np.isneginf(np.take_along_axis(lg, idx.astype(np.int64), 1))] == 0)
+
+
+def test_layout_repeated_expert_is_bad_input():
+    idx = np.array([[[0, 1], [2, 2], [1, 3]]])
+    assert ep.dispatch_layout(idx, 4, 2)["status"] == ep.STATUS_BADINPUT
+    assert ep.dispatch_layout(idx[:, [0, 2]], 4, 2)["status"] == ep.STATUS_OK
+
+
 def test_layout_capacity_status():
     idx = np.array([[[0, 1], [0, 1], [0, 1]]])
     assert ep.dispatch_layout(idx, 4, 2, cap=3)["status"] == ep.STATUS_CAPACITY
