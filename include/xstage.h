@@ -49,7 +49,7 @@ enum {
   XS_EWORKSPACE = 4,    /* workspace missing or too small */
   XS_ECAPACITY = 5,     /* device: a window received more rows than capacity_rows */
   XS_ETIMEOUT = 6,      /* device: a bounded dependency wait expired */
-  XS_EBADINPUT = 7      /* device: an expert id outside [0, E) */
+  XS_EBADINPUT = 7      /* device: an expert id outside [0, E), or listed twice by one token */
 };
 
 /* Text for a status code (static storage; never NULL). */
@@ -76,7 +76,8 @@ typedef struct xs_window {
 /* ----------------------------------------------------------------------------- routing
  * Top-k softmax gating (routing is fixed by the model and unchanged by the method:
  * Related Work, "MoE communication").
- *   logits   device fp32 [T][E], finite.
+ *   logits   device fp32 [T][E], finite or -inf (a masked expert), at least one finite
+ *            value per row.
  *   topk_idx device int32 [T][k] out: the k largest logits in descending order, ties to
  *            the lower expert index (selection is exact on the fp32 logits).
  *   topk_w   device fp32 [T][k] out: softmax over all E experts taken at topk_idx; with
@@ -90,7 +91,9 @@ int xs_route_topk_softmax(const float* logits, int32_t T, int32_t E, int32_t k,
  * Sec. 2.2 and Sec. 4.3: expert-parallel tokens go to the ranks owning their experts).
  * Expert e lives in window d(e) = e / (E / W). Rows of window d are the slots routed to
  * its experts ordered by (expert, source, token), unpadded, one row per slot.
- *   topk_idx       device int32 [n_src][T][k]
+ *   topk_idx       device int32 [n_src][T][k]; the k experts of a token are distinct (an id
+ *                  outside [0, E) or listed twice by one token sets XS_EBADINPUT, and the
+ *                  rows of that token are then unspecified)
  *   expert_counts  device int32 [n_src][E] out: slots of source s routed to expert e
  *   src_base       device int32 [n_src][E] out: rows of expert e from sources < s
  *   expert_offsets device int32 [E] out: first row of expert e inside window d(e)

@@ -147,7 +147,8 @@ __global__ __launch_bounds__(256) void route_topk16_kernel(const float* __restri
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         const int e = 64 * q + 4 * sub + c;
-        if (e < E && !((taken >> (4 * q + c)) & 1u) && v[4 * q + c] > bv) {
+        // ties (equal values, or only -inf left) go to the lower expert index
+        if (e < E && !((taken >> (4 * q + c)) & 1u) && (v[4 * q + c] > bv || (v[4 * q + c] == bv && e < bi))) {
           bv = v[4 * q + c];
           bi = e;
         }
@@ -210,6 +211,9 @@ __global__ __launch_bounds__(256) void layout_chunk_kernel(const int* __restrict
       int e = idx[base + j];
       if (e >= 0 && e < E) atomicOr(&masks[w * E + e], bit);
       else set_status(status, XS_EBADINPUT);
+      // a token that lists one expert twice would give both slots one row
+      for (int j2 = 0; j2 < j; ++j2)
+        if (idx[base + j2] == e) set_status(status, XS_EBADINPUT);
     }
   }
   __syncthreads();

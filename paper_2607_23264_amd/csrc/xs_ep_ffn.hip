@@ -12,13 +12,13 @@
 // Tile order per persistent workgroup ("scheduler instance" g of G):
 //   BURST       Expert-Wave: global list [L1 of wave 0, L2 of wave 0, L1 of wave 1, ...],
 //               instance g takes entries g, g + G, ...
-//   INTERLEAVE  Alg. 1: one cursor per tile stream, both starting at g and stepping by G; the
-//               next Linear-2 tile is taken when its row trails the Linear-1 cursor's row by
-//               at least D rows, otherwise the next Linear-1 tile.
-//   CHUNK       Alg. 1 with at most c consecutive Linear-2 tiles before a Linear-1 tile.
-// With dynamic claiming the per-instance cursors become two shared counters: a workgroup
-// that finishes a tile takes the next Linear-2 entry if its row trails the first untaken
-// Linear-1 row by at least D rows (and the chunk cap allows), else the next Linear-1 entry.
+//   INTERLEAVE  cross-wave interleaving (Alg. 1): a Linear-2 entry is taken only while the
+//               first Linear-1 entry not yet taken is at least D rows ahead of it, otherwise
+//               the next Linear-1 entry (l2_may_run).
+//   CHUNK       the same with at most c consecutive Linear-2 tiles before a Linear-1 tile.
+// The entries a workgroup sees are either its own share of each stream (static claiming:
+// entries g, g + G, ...) or the next entries of two shared counters (dynamic claiming); the
+// rule is the same.
 // Deadlock freedom needs every workgroup resident (grid <= CUs, one workgroup per CU by
 // LDS) and D >= 1: an instance only waits on a row strictly behind its own Linear-1 cursor,
 // so the lowest row anyone waits on always has its Linear-1 owners running.
@@ -412,6 +412,16 @@ __device__ __forceinline__ void l2_tile(const EpArgs& a, int p, int nt, bool fus
   else ep_l2_tile(a, p, nt, fused, lds, rowptr, flag);
 }
 
+// The rule every claim mode applies (App. A.2): Linear-2 entry e2 may run next when the first
+// Linear-1 entry not yet taken, e1, is at least the lead D rows past e2's row (or no Linear-1
+// entry is left), and the chunk cap, if set, still allows another Linear-2 tile before a
+// Linear-1 one ("run" Linear-2 tiles have run since the last Linear-1 tile).
+__device__ __forceinline__ bool l2_may_run(const EpArgs& a, int e2, int e1, int n1, int run) {
+  const bool l1_left = e1 < n1;
+  if (a.chunk > 0 && run >= a.chunk && l1_left) return false;
+  return !l1_left || e2 / a.P2 + a.lead <= e1 / a.P1;
+}
+
 // Dynamic claiming. Thread 0 takes the next tile and broadcasts it through LDS:
 //   > 0: Linear-1 entry (value - 1), < -1: Linear-2 entry (-value - 2), -1: no work left.
 // Linear-2 entries are taken as tickets (one fetch_add, no retry loop): a producer holds at
@@ -425,25 +435,22 @@ __device__ __forceinline__ int ep_claim(const EpArgs& a, int n1, int n2, int& ru
   int* c2p = a.claim_ctr + 1;
   for (;;) {
     const int c1 = __hip_atomic_load(c1p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const bool l1_left = c1 < n1;
-    const int p1 = l1_left ? c1 / a.P1 : 0x3fffffff;
-    const bool chunk_ok = !(a.chunk > 0 && run >= a.chunk && l1_left);
-    if (ticket == -1 && chunk_ok) {
+    if (ticket == -1) {
       const int c2 = __hip_atomic_load(c2p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (c2 >= n2) {
         ticket = -2;   // Linear-2 entries exhausted
-      } else if (c2 / a.P2 + a.lead <= p1) {
+      } else if (l2_may_run(a, c2, c1, n1, run)) {
         const int k = __hip_atomic_fetch_add(c2p, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         ticket = k < n2 ? k : -2;
       }
     }
-    if (ticket >= 0 && chunk_ok && ticket / a.P2 + a.lead <= p1) {
+    if (ticket >= 0 && l2_may_run(a, ticket, c1, n1, run)) {
       const int k = ticket;
       ticket = -1;
       ++run;
       return -k - 2;
     }
-    if (l1_left) {
+    if (c1 < n1) {
       const int k = __hip_atomic_fetch_add(c1p, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (k < n1) {
         run = 0;
@@ -533,21 +540,23 @@ __device__ __forceinline__ void ep_ffn_body(const EpArgs& a, char* smem) {
     ep_dynamic<MODE, PREC>(a, n1, n2, lds, rowptr, flag);
     return;
   }
-  const int D = a.lead, c = a.chunk;
-  int k1 = g, k2 = g, run = 0;
-  while (k1 < n1 || k2 < n2) {
-    const int p1 = k1 < n1 ? k1 / a.P1 : 0x3fffffff;
-    const int p2 = k2 / a.P2;
-    bool take2 = k2 < n2 && p2 + D <= p1;
-    if (take2 && c > 0 && run >= c && k1 < n1) take2 = false;
-    if (take2) {
-      l2_tile<PREC>(a, p2, k2 % a.P2, fused, lds, rowptr, flag);
-      k2 += G;
+  // Static claiming: this instance owns entries g, g + G, ... of each stream and applies the
+  // claim rule to its own next entries (its own Linear-1 entries play the part of the shared
+  // frontier). An owned Linear-2 entry then only waits on rows whose Linear-1 tiles every
+  // instance has already passed, so with D >= 1 the lowest waited-on row always has running
+  // owners.
+  int e1 = g, e2 = g, run = 0;
+  for (;;) {
+    if (e2 < n2 && l2_may_run(a, e2, e1, n1, run)) {
+      l2_tile<PREC>(a, e2 / a.P2, e2 % a.P2, fused, lds, rowptr, flag);
+      e2 += G;
       ++run;
-    } else {
-      l1_tile<PREC>(a, p1, k1 % a.P1, fused, lds, rowptr);
-      k1 += G;
+    } else if (e1 < n1) {
+      l1_tile<PREC>(a, e1 / a.P1, e1 % a.P1, fused, lds, rowptr);
+      e1 += G;
       run = 0;
+    } else {
+      break;
     }
   }
 }

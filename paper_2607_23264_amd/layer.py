@@ -48,7 +48,8 @@ class EPLayer:
     """Owns every device buffer of one EP layer call (inputs, layout, windows, outputs)."""
 
     def __init__(self, s: Shape, device="cuda", combine_host: bool = False, sentinel: bool = True,
-                 precision: int = X.XS_PREC_BF16):
+                 precision: int = X.XS_PREC_BF16, ready_flags: bool = False,
+                 host_combine_sources=None):
         self.s = s
         self.precision = precision
         mxp = precision in (X.XS_PREC_MXFP8, X.XS_PREC_W4A8)
@@ -90,13 +91,27 @@ class EPLayer:
             self.dwin = torch.full((s.W, cap, s.H), fill, dtype=torch.int16, device=d) if sentinel \
                 else torch.empty((s.W, cap, s.H), dtype=torch.int16, device=d)
         self.combine_host = combine_host
-        if combine_host:
+        # combine windows of the sources listed in host_combine_sources (all of them with
+        # combine_host) live in host-coherent memory: slow sinks beside HBM windows
+        host_src = list(range(s.n_src)) if combine_host else list(host_combine_sources or [])
+        self.host_sources = host_src
+        if host_src and len(host_src) == s.n_src:
             self._host = HostCoherent(s.n_src * s.T * s.k * s.H * 2)
             self.cwin = self._host.view.view(s.n_src, s.T * s.k, s.H)
             self.cwin.fill_(fill)
+            self._cw = [self.cwin[i] for i in range(s.n_src)]
         else:
             self.cwin = torch.full((s.n_src, s.T * s.k, s.H), fill, dtype=torch.int16, device=d) if sentinel \
                 else torch.empty((s.n_src, s.T * s.k, s.H), dtype=torch.int16, device=d)
+            self._cw = [self.cwin[i] for i in range(s.n_src)]
+            self._hosts = {}
+            for i in host_src:
+                h = HostCoherent(s.T * s.k * s.H * 2)
+                self._hosts[i] = h
+                self._cw[i] = h.view.view(s.T * s.k, s.H)
+                self._cw[i].fill_(fill)
+        # readiness words: dispatch windows [0, W), combine windows [W, W + n_src)
+        self.flags = torch.zeros((s.W + s.n_src,), dtype=i32, device=d) if ready_flags else None
         h_rows = s.n_cwin * cap
         if mxp:
             self.h_ws = torch.zeros((h_rows, self.h_bytes), dtype=torch.uint8, device=d)
@@ -110,16 +125,28 @@ class EPLayer:
         self.y_ws = torch.zeros((h_rows, s.H), dtype=torch.int16, device=d)
         self.out = torch.zeros((s.T, s.H), dtype=torch.int16, device=d)
         self.status = torch.zeros((1,), dtype=i32, device=d)
-        self._dwins = X.windows([X.window(self.dwin[w]) for w in range(s.W)])
+        fl = (lambda i: self.flags[i].data_ptr()) if ready_flags else (lambda i: None)
+        self._dwins = X.windows([X.window(self.dwin[w], flag=fl(w)) for w in range(s.W)])
+        self._cflag = [fl(s.W + i) for i in range(s.n_src)]
         self._cwins = X.windows([self._cwin_desc(i) for i in range(s.n_src)])
         self.L = self._layer_struct()
         nb = C.c_int64()
         X.check(X.xs_ep_layer_workspace_bytes(C.byref(self.L), C.byref(nb)), "workspace")
         self.workspace = torch.zeros((max(1, nb.value),), dtype=torch.uint8, device=d)
 
+    def close(self):
+        """Releases the host-coherent sinks (device buffers go with the object)."""
+        torch.cuda.synchronize(self.dev)
+        for h in list(getattr(self, "_hosts", {}).values()) + ([self._host] if hasattr(self, "_host") else []):
+            h.free()
+
     def _cwin_desc(self, i):
-        t = self.cwin[i]
-        return X.xs_window(t.data_ptr(), t.shape[0], t.stride(0) * 2, None)
+        t = self._cw[i]
+        return X.xs_window(t.data_ptr(), t.shape[0], t.stride(0) * 2, self._cflag[i])
+
+    def combine_rows(self, src: int) -> torch.Tensor:
+        """Combine window of source src ([T * k][H] int16; a CPU view for host-coherent ones)."""
+        return self._cw[src]
 
     def _layer_struct(self) -> X.xs_ep_layer:
         s = self.s
@@ -221,7 +248,7 @@ class EPLayer:
 
     def combine_reduce(self):
         s = self.s
-        c = self.cwin[s.src]
+        c = self._cw[s.src]
         X.check(X.xs_combine_reduce(c.data_ptr(), c.stride(0) * 2, self.topk_w[s.src].data_ptr(), s.T, s.k,
                                     s.H, self.out.data_ptr(), self.stream), "combine_reduce")
 
@@ -235,7 +262,7 @@ class EPLayer:
             if s != self.s.src:
                 self.dispatch(s)
         if remote_combine_bits is not None:
-            self.cwin[self.s.src].copy_(_dev_bits(remote_combine_bits, "cpu"))
+            self._cw[self.s.src].copy_(_dev_bits(remote_combine_bits, "cpu"))
         torch.cuda.synchronize(self.dev)
 
     def fused(self, pacing: X.xs_pacing | None = None, trace: X.xs_trace | None = None):
