@@ -37,7 +37,8 @@ def _route_gpu(logits, k, renorm=0):
 
 
 @pytest.mark.parametrize("case", ["tiny", "dsv3_uniform", "dsv3_zipf", "ties_E1000_k32", "one_token",
-                                  "k_equals_E", "renorm", "ties_E200_k16", "E100_k3_T17"])
+                                  "k_equals_E", "renorm", "ties_E200_k16", "E100_k3_T17",
+                                  "masked_E256_k8", "masked_E300_k8"])
 def test_route_matches_oracle(case):
     g = np.random.default_rng(11)
     renorm = 0
@@ -60,6 +61,13 @@ def test_route_matches_oracle(case):
         lg[7, 150:] = 9.0
     elif case == "E100_k3_T17":     # sixteen-lane kernel with 8 logits per lane, T not a multiple of 16
         lg, k = g.standard_normal((17, 100)).astype(np.float32), 3
+    elif case.startswith("masked"):   # -inf logits (masked experts), fewer finite ones than k
+        E = 256 if case == "masked_E256_k8" else 300
+        lg, k = g.standard_normal((33, E)).astype(np.float32), 8
+        lg[g.random((33, E)) < 0.9] = -np.inf
+        lg[:, 5] = 0.25                 # at least one finite logit per row
+        lg[4, :] = -np.inf
+        lg[4, [17, 200]] = [1.0, 1.0]   # two finite ones: six slots take -inf experts
     else:
         lg, k, renorm = synth.uniform_logits(0, 2, 200, 64), 6, 1
     idx, w = _route_gpu(lg, k, renorm)
@@ -131,6 +139,10 @@ def test_layout_capacity_and_bad_expert_status():
     bad = idx.copy()
     bad[0, 5, 1] = 9
     assert _layout_gpu(bad, 4, 2, cap=128)["status"] == xs().XS_EBADINPUT
+    dup = idx.copy()
+    dup[0, 7, 1] = dup[0, 7, 0]         # one token lists an expert twice
+    assert oep.dispatch_layout(dup, 4, 2, cap=128)["status"] == xs().XS_EBADINPUT
+    assert _layout_gpu(dup, 4, 2, cap=128)["status"] == xs().XS_EBADINPUT
 
 
 def _ep_layer(cfg, seed=0, **kw):
@@ -290,58 +302,6 @@ def test_multi_source_ragged_share():
                     assert_close(row, ref["y"][d][0][r], "combine row")
                 elif s != cfg.rank:
                     assert np.all(row == 0xFFFF)
-
-
-def _full_share(routing):
-    import dataclasses
-    cfg = dataclasses.replace(synth.EP_DSV3_SHARE, routing=routing)
-    if routing == "zipf":
-        # "this GPU" is the most loaded destination (the max across ranks)
-        idx = np.stack([oep.route_topk_softmax(synth.zipf_logits(0, s, cfg.T, cfg.E), cfg.k)[0]
-                        for s in range(cfg.n_src)])
-        loads = np.bincount((idx // cfg.E_local).ravel(), minlength=cfg.W)
-        cfg = dataclasses.replace(cfg, rank=int(loads.argmax()))
-    return cfg
-
-
-@pytest.mark.parametrize("routing,claim", [("uniform", 0), ("zipf", 1)])
-def test_dsv3_share_full_size_sampled(routing, claim):
-    cfg = _full_share(routing)
-    inp = synth.ep_inputs(cfg, 0)
-    experts = synth.computed_experts(cfg)
-    fill = synth.ep_remote_combine_fill(cfg, 0)
-    lay = _ep_layer(cfg)
-    lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
-    lay.prefill_other_sources(fill)
-    from paper_2607_23264_amd.layer import pacing
-    lay.fused(pacing(xs().XS_POLICY_INTERLEAVE, lead=0, claim=claim))
-    torch.cuda.synchronize()
-    assert int(lay.status.item()) == 0
-    # layout of all sources is bit-exact
-    idx = np.stack([oep.route_topk_softmax(inp["logits"][s], cfg.k)[0] for s in range(cfg.n_src)])
-    w = np.stack([oep.route_topk_softmax(inp["logits"][s], cfg.k)[1] for s in range(cfg.n_src)])
-    assert np.array_equal(lay.topk_idx.cpu().numpy(), idx)
-    lref = oep.dispatch_layout(idx, cfg.E, cfg.W)
-    assert np.array_equal(lay.slot_row.cpu().numpy(), lref["slot_row"])
-    assert np.array_equal(lay.dest_counts.cpu().numpy(), lref["dest_counts"])
-    # sampled output tokens, each computed one by one by the oracle
-    out = host_bits(lay.out)
-    g = np.random.default_rng(1)
-    toks = np.concatenate([[0, cfg.T - 1], g.choice(cfg.T, 10, replace=False)])
-    r = cfg.rank
-    pos = {e: i for i, e in enumerate(experts)}
-    for t in toks:
-        acc = np.zeros(cfg.H)
-        for j in range(cfg.k):
-            e = int(idx[r, t, j])
-            if e in pos:
-                i = pos[e]
-                _, _, yb = oep.expert_ffn(inp["x"][r, t:t + 1], inp["w1"][i], inp["w2"][i])
-                row = bits_f64(yb[0])
-            else:
-                row = bits_f64(fill[t * cfg.k + j])
-            acc += np.float64(w[r, t, j]) * row
-        assert_close(out[t], acc, f"{routing} token {t}")
 
 
 def _records(buf, count):

@@ -188,72 +188,6 @@ def test_multi_source_ragged_share(prec):
             assert (comb[s][~own[s]] == 0xFFFF).all()
 
 
-def _local_token_sample(idx_r, experts, T, n_tokens, max_experts, seed):
-    """Tokens 0 and T - 1 and random others whose locally computed experts stay within a set
-    of at most max_experts (bounds the oracle's weight quantization)."""
-    g = np.random.default_rng(seed)
-    local = set(experts)
-    chosen, used = [], set()
-    for t in [0, T - 1] + list(g.permutation(T)):
-        mine = {int(e) for e in idx_r[t] if int(e) in local}
-        if len(used | mine) > max_experts or t in chosen:
-            continue
-        chosen.append(int(t))
-        used |= mine
-        if len(chosen) == n_tokens:
-            break
-    return chosen
-
-
-@pytest.mark.parametrize("routing,claim,prec", [("uniform", 0, "MXFP8"), ("zipf", 1, "MXFP8"), ("zipf", 1, "W4A8")])
-def test_dsv3_share_full_size_sampled(routing, claim, prec):
-    cfg = dataclasses.replace(synth.EP_DSV3_SHARE, routing=routing)
-    if routing == "zipf":
-        idx = np.stack([oep.route_topk_softmax(synth.zipf_logits(0, s, cfg.T, cfg.E), cfg.k)[0]
-                        for s in range(cfg.n_src)])
-        loads = np.bincount((idx // cfg.E_local).ravel(), minlength=cfg.W)
-        cfg = dataclasses.replace(cfg, rank=int(loads.argmax()))
-    inp = synth.ep_inputs(cfg, 0)
-    experts = synth.computed_experts(cfg)
-    fill = synth.ep_remote_combine_fill(cfg, 0)
-    lay = _mx_layer(cfg, prec)
-    lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
-    lay.prefill_other_sources(fill)
-    from paper_2607_23264_amd.layer import pacing
-    lay.fused(pacing(xs().XS_POLICY_INTERLEAVE, lead=0, claim=claim))
-    torch.cuda.synchronize()
-    assert int(lay.status.item()) == 0
-    r = cfg.rank
-    idx, w = oep.route_topk_softmax(inp["logits"][r], cfg.k)
-    assert np.array_equal(lay.topk_idx[r].cpu().numpy(), idx)
-    slot_row = lay.slot_row[r].cpu().numpy()
-    toks = _local_token_sample(idx, experts, cfg.T, 10, 4, seed=1)
-    out = host_bits(lay.out)
-    win = lay.dwin.cpu().numpy()
-    pos = {e: i for i, e in enumerate(experts)}
-    wq = {}
-    for t in toks:
-        xq = omx.quantize_rows(inp["x"][r, t:t + 1])
-        acc = np.zeros(cfg.H)
-        for j in range(cfg.k):
-            e = int(idx[t, j])
-            d = e // cfg.E_local
-            # this source's token row in its destination window, codes and scales
-            assert np.array_equal(win[d, slot_row[t, j], :cfg.H], xq[0][0]), (t, j)
-            assert np.array_equal(win[d, slot_row[t, j], cfg.H:cfg.H + cfg.H // 32], xq[1][0]), (t, j)
-            if e in pos:
-                if e not in wq:
-                    i = pos[e]
-                    wq[e] = (omx.quantize_rows(inp["w1"][i], _wfmt(prec)),
-                             omx.quantize_rows(inp["w2"][i], _wfmt(prec)))
-                _, _, _, yb = omx.expert_ffn_mx(xq, *wq[e], _wfmt(prec))
-                row = bits_f64(yb[0])
-            else:
-                row = bits_f64(fill[t * cfg.k + j])
-            acc += np.float64(w[t, j]) * row
-        assert_close(out[t], acc, f"{prec} {routing} token {t}")
-
-
 def _fused_rc(L, lay):
     X = xs()
     ws = lay.workspace
