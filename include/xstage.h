@@ -277,9 +277,17 @@ typedef struct xs_pacing {
                                      completion, so its Linear-2 waits expire (-1 = none) */
   int32_t claim;                  /* XS_CLAIM_STATIC or XS_CLAIM_DYNAMIC */
   int32_t reserved;               /* must be 0 */
-  double t_l1_us, t_l2_us;        /* AUTO: mainloop time of one Linear-1 / Linear-2 tile;
-                                     0 = estimate from the tile FLOPs */
-  const struct xs_model* model;   /* host, for XS_POLICY_AUTO; may be NULL */
+  double t_l1_us, t_l2_us;        /* mainloop time of one Linear-1 / Linear-2 tile for the
+                                     model audit (xs_trace_tile_times gives them from a traced
+                                     run); 0 = an estimate from the tile FLOPs at 40 % of one
+                                     CU's share of the dense peak */
+  const struct xs_model* model;   /* host, for XS_POLICY_AUTO and xs_pacing_audit; may be NULL */
+  const int32_t* expert_rows;     /* host int32 [n_experts] or NULL: rows each local expert is
+                                     expected to compute (for instance the last step's counts);
+                                     NULL = the uniform expectation n_src T k / E */
+  double sink_share;              /* share of each Linear-2 tile's stored bytes that reach the
+                                     sink `model` describes (e.g. 2 / 8 with two of eight combine
+                                     windows in host memory); 0 = all of them */
 } xs_pacing;
 
 /* Optional device trace of the persistent kernels: one 32-byte record per tile,
@@ -290,11 +298,18 @@ typedef struct xs_pacing {
  *   rec[3] = wall clock after the last store of the epilogue was issued (sender-visible
  *            issue end: the stores are accepted, not necessarily visible)
  * records are appended at atomicAdd(count, 1); records past `capacity` are dropped but
- * still counted. buf and count are device memory; the caller zeroes *count. */
+ * still counted. buf and count are device memory; the caller zeroes *count.
+ * ext (nullable, device, 4 x uint64 per record, same index; EP kernels only):
+ *   ext[0] = wall clock when the tile's dependency wait ended (= rec[1] for Linear-1 tiles)
+ *   ext[1] = staging wait in ticks: how long the workgroup's first wave waited, before this
+ *            tile's mainloop, for the stores of its previous epilogue to leave the wave (the
+ *            local staging reuse point of App. A.2; taking it adds that wait to the wave)
+ *   ext[2] = bytes the tile's epilogue stored, ext[3] = rows of the tile */
 typedef struct xs_trace {
   uint64_t* buf;
   int64_t capacity;
   uint32_t* count;
+  uint64_t* ext;
 } xs_trace;
 
 /* Workspace of the EP calls below (layout scratch, tile tables, readiness counters). */
@@ -470,14 +485,18 @@ typedef struct xs_model {
   int32_t _pad;
 } xs_model;
 
-typedef struct xs_burst { double V_bytes, T0_us, G_us; } xs_burst;
+/* One burst of a sequence (Sec. 4.1): aggregate volume, recovered issue floor, the compute
+ * gap before the next burst and, for App. A.2's MMA-side stall, the mainloop time T_cover
+ * that runs before the burst's local staging must be reused (0 = none). */
+typedef struct xs_burst { double V_bytes, T0_us, G_us, cover_us; } xs_burst;
 
 /* Per-burst audit: rho and delta_b (Eqs. 3-4), backlog before the burst, b_iso and the
  * capacity guard (Eq. 6), and the predicted issue time: T0 while the guard holds, else
  * (q + V - Q) / R (a fluid queue capped at Q); the backlog then follows
- * q' = [q + V - R (T_iss + G)]_+, which is Eq. 5 whenever the guard holds. */
+ * q' = [q + V - R (T_iss + G)]_+, which is Eq. 5 whenever the guard holds. stall_us =
+ * T_iss - T0; mma_stall_us = [T_iss - cover]_+ (App. A.2, with T_RS = T_iss). */
 typedef struct xs_burst_pred {
-  double rho, delta_b, q_before, b_iso, T_iss_us, stall_us;
+  double rho, delta_b, q_before, b_iso, T_iss_us, stall_us, mma_stall_us;
   int32_t guard_ok;
   int32_t _pad;
 } xs_burst_pred;
@@ -500,6 +519,95 @@ typedef struct xs_calib {
 } xs_calib;
 
 int xs_model_fit(const xs_calib* c, xs_model* out);
+
+/* The calibration procedure around xs_model_fit (Sec. 3.1, 3.3, 3.5), host-only:
+ *   xs_drain_rate   R = sum V^2 / sum V T over zero-gap periodic runs (T = V / R through the
+ *                   origin), the estimate used to size the recovery gaps of later runs;
+ *   xs_calib_knee   the isolated-burst knee: the first index i >= 2 whose issue time exceeds
+ *                   (1 + knee_excess) times the line through bursts 0 and i - 1 (n if none);
+ *                   iso_V ascending;
+ *   xs_model_calibrate  xs_model_fit on c, plus the knee of c's isolated bursts and the capacity
+ *                   bracket it gives: Q between V - R T0(V) at the last isolated burst on the
+ *                   floor and at the first one off it (lo = hi = +inf without a knee). A sharp
+ *                   knee whose stalled bursts issue at about V / R makes the fluid Q of
+ *                   xs_model_fit come out <= 0; the bracket's lower end is then the capacity to
+ *                   use (the largest volume seen absorbed without stalling). */
+typedef struct xs_calib_summary {
+  xs_model model;                 /* xs_model_fit's T0, R and fluid Q */
+  int32_t knee;                   /* index of the first isolated burst past the knee, n_iso if none */
+  int32_t _pad;
+  double Q_bracket_lo, Q_bracket_hi;
+} xs_calib_summary;
+
+int xs_drain_rate(const double* zg_V, const double* zg_T, int32_t n, double* R_bytes_per_us);
+int xs_calib_knee(const double* iso_V, const double* iso_T, int32_t n, double knee_excess, int32_t* knee);
+int xs_model_calibrate(const xs_calib* c, xs_calib_summary* out);
+
+/* Eq. 1 for periodic bursts of aggregate volume V separated by a non-injecting gap G:
+ * T_period = max(T0(V) + G, V / R) and T_iss = max(T0(V), V / R - G), with T0(V) from m.
+ * Host-only. */
+int xs_burst_gap(const xs_model* m, double V_bytes, double G_us, double* T_period_us, double* T_iss_us);
+
+/* Recovery audit of a producer's output bursts (App. B, App. C): n_bursts aligned bursts of V
+ * bytes, each followed by the gap G (the next Q-loop); the recurrence of xs_model_predict over
+ * them; G* = [V / R - T0(V)]_+ (Eq. 2); with sigma_us the compute per K/V tile of b_n keys, the
+ * smallest sequence length whose Q-loop covers G*, M_ub* = b_n ceil(G* / sigma) (App. C.2); the
+ * drain left after the last burst, [(q_last + V) / R - T0]_+ (no compute follows it); and the
+ * completion-coupled issuer's extra time, n_bursts max(T0, V / R) (Sec. 3.2). Host-only. */
+typedef struct xs_recovery {
+  double T0_us, G_star_us, rho, delta_b, b_iso, stall_us, tail_us, coupled_us;
+  int32_t guard_ok;               /* the capacity guard held at every burst */
+  int32_t M_ub_star;              /* 0 when sigma_us <= 0 */
+} xs_recovery;
+
+int xs_recovery_audit(const xs_model* m, double V_bytes, int32_t n_bursts, double G_us, double sigma_us,
+                      int32_t b_n, xs_recovery* out);
+
+/* ----------------------------------------------------------------------------- pacing audit
+ * The audit of Sec. 4.1 applied to the persistent EP kernel's tile orders, and the choice
+ * XS_POLICY_AUTO makes with it (App. A.1: the average-rate bound of Eq. 9 is necessary but
+ * not sufficient; the concrete order must pass the backlog recurrence and capacity guard).
+ * For one order the burst sequence is rebuilt from the schedule (Sec. 4.2): producer 0's own
+ * tile stream (static claiming, the grid's G producers), each of its Linear-2 epilogues one
+ * burst of the fully aligned producers, V = K_act V_t with K_act = G and V_t the tile's
+ * stored bytes times sink_share; G_n = the mainloops that follow before the next burst (T_L1
+ * per Linear-1 tile, T_L2 for the next Linear-2 tile); cover = T0 (a workgroup issues its own
+ * epilogue stores, so only the floor issue is covered). Rows per local expert come from
+ * pacing->expert_rows (else the uniform expectation), split into blocks as the kernel does.
+ * Candidates: the given policy alone, or for XS_POLICY_AUTO: BURST (Expert-Wave), INTERLEAVE
+ * at the given lead, and CHUNK c = 1, 2, 4, ..., 32. AUTO takes the least predicted stall;
+ * among the candidates within 1 % of BURST's mainloop time of it, BURST first (it keeps each
+ * expert's weights together, the working-set side of the choice, Sec. 5.3), then INTERLEAVE,
+ * then the largest chunk.
+ * Host-only and synchronous; needs the current device only for the grid size. */
+#define XS_AUDIT_MAX 16
+typedef struct xs_pacing_audit {
+  int32_t policy;                 /* chosen policy: XS_POLICY_BURST, _INTERLEAVE or _CHUNK */
+  int32_t chunk;                  /* chosen chunk (CHUNK), else 0 */
+  int32_t lead_rows;              /* lead D the order uses */
+  int32_t producers;              /* G = K_act */
+  int32_t rows;                   /* scheduler rows P (expert row blocks) */
+  int32_t rate_feasible;          /* Eq. 9 at the whole share's tile mix */
+  int32_t n_cand;
+  int32_t _pad;
+  double t_l1_us, t_l2_us;        /* mainloop times used */
+  double V_full_bytes;            /* V of a burst of full tiles */
+  int32_t cand_policy[XS_AUDIT_MAX], cand_chunk[XS_AUDIT_MAX];
+  int32_t cand_bursts[XS_AUDIT_MAX], cand_guard_fail[XS_AUDIT_MAX];
+  double cand_stall_us[XS_AUDIT_MAX];       /* sum of predicted issue stall over the bursts */
+  double cand_mma_stall_us[XS_AUDIT_MAX];   /* sum of App. A.2's MMA-side stall */
+  double cand_compute_us[XS_AUDIT_MAX];     /* producer 0's mainloop time */
+} xs_pacing_audit;
+
+int xs_pacing_audit_run(const xs_ep_layer* L, const xs_pacing* pacing, xs_pacing_audit* out);
+
+/* Mainloop times from a device trace copied to the host (records as xs_trace, n of them, with
+ * their ext records, or ext = NULL): medians over Linear-1 tiles of (mainloop end - start) and
+ * over Linear-2 tiles of (mainloop end - dependency-wait end), in microseconds, and the
+ * median epilogue issue span of Linear-2 tiles (rec[3] - rec[2]). Tiles with fewer than
+ * min_rows rows are left out when ext is given (partial tiles run shorter). Host-only. */
+int xs_trace_tile_times(const uint64_t* recs, const uint64_t* ext, int64_t n, int32_t min_rows,
+                        double* t_l1_us, double* t_l2_us, double* l2_issue_us);
 
 /* Remote-store microbenchmark (Sec. 3.1): K producer workgroups each store B bytes per
  * burst into `target` (HBM window or host-coherent sink), separated by a non-injecting

@@ -133,3 +133,79 @@ def simulate(streams: Sequence[Sequence[Tile]], P: int, P1: int) -> int:
         remaining -= len(finished)
         rounds += 1
     return rounds
+
+
+# ----------------------------------------------------------------------------- pacing audit
+def expert_blocks(rows_per_expert: Sequence[int], equal: bool) -> Tuple[List[int], List[int]]:
+    """Row blocks of the persistent kernel's scheduler rows, expert by expert: an expert's m
+    rows give ceil(m / 256) blocks; equal blocks hold ceil(m / blocks) rows rounded up to a
+    multiple of 32 (at most 256), the last block what is left; otherwise 256 rows each with
+    a ragged last block. Returns (rows of each block, expert of each block)."""
+    sizes, owner = [], []
+    for x, m in enumerate(rows_per_expert):
+        nb = -(-int(m) // 256)
+        if nb == 0:
+            continue
+        bm = min(256, -(-(-(-int(m) // nb)) // 32) * 32) if equal else 256
+        left = int(m)
+        for _ in range(nb):
+            sizes.append(min(bm, left))
+            owner.append(x)
+            left -= bm
+    return sizes, owner
+
+
+def audit_bursts(tiles: Sequence[Tile], block_rows: Sequence[int], G: int, sink_share: float,
+                 T_L1: float, T_L2: float):
+    """The burst sequence a tile stream gives under full alignment (Sec. 4.2): every
+    Linear-2 tile of the stream is one burst of the G aligned producers, V = G * V_t with
+    V_t = its rows x 256 columns x 2 bytes x sink_share; the gap after it is the mainloop
+    time of the tiles that follow up to and including the next Linear-2 tile (T_L1 or T_L2
+    each). Returns (V list, gap list, producer mainloop time)."""
+    V, gaps = [], []
+    compute = sum(T_L1 if kind == 1 else T_L2 for kind, _, _ in tiles)
+    l2_at = [i for i, t in enumerate(tiles) if t[0] == 2]
+    for n, i in enumerate(l2_at):
+        V.append(G * block_rows[tiles[i][1]] * 256 * 2 * sink_share)
+        stop = l2_at[n + 1] + 1 if n + 1 < len(l2_at) else len(tiles)
+        gaps.append(sum(T_L1 if tiles[j][0] == 1 else T_L2 for j in range(i + 1, stop)))
+    return V, gaps, compute
+
+
+def pacing_audit(rows_per_expert, equal_blocks: bool, P1: int, P2: int, G: int, D: int,
+                 wave_tiles: int, sink_share: float, T_L1: float, T_L2: float,
+                 t0_a: float, t0_b: float, R: float, Q: float, policy: str = "auto",
+                 chunk: int | None = None):
+    """Audit of producer 0's tile order (Sec. 4.1 with Eqs. 3-6 via xstage_model.predict) and
+    the automatic choice among "wave" (Expert-Wave), "interleave" and "chunk" c in 1, 2, 4,
+    ..., 32: the least predicted stall, and among the candidates within 1 % of the Expert-Wave
+    order's mainloop time of it, Expert-Wave first (it keeps an expert's weights together),
+    then the plain interleave, then the larger chunk (a reading: the paper asks to pick the
+    order from X-Stage pressure and working-set size, Sec. 5.3). Returns (choice (policy,
+    chunk), {candidate: (stall, bursts, guard failures, mainloop time)})."""
+    from . import xstage_model as xm
+    sizes, owner = expert_blocks(rows_per_expert, equal_blocks)
+    P = len(sizes)
+    if policy == "auto":
+        cands = [("wave", None), ("interleave", None)] + [("chunk", c) for c in (1, 2, 4, 8, 16, 32)]
+    else:
+        cands = [(policy, chunk)]
+    res = {}
+    for pol, c in cands:
+        if pol == "wave":
+            tiles = expert_wave_stream(0, G, P, P1, P2, waves_by_tiles(owner, P1, wave_tiles))
+        else:
+            tiles = interleave_stream(0, G, P, P1, P2, D, chunk=c)
+        V, gaps, compute = audit_bursts(tiles, sizes, G, sink_share, T_L1, T_L2)
+        T0 = [t0_a + t0_b * v for v in V]
+        pred = xm.predict(V, T0, gaps, R, Q)
+        res[(pol, c)] = (sum(p.stall for p in pred), len(pred), sum(not p.guard_ok for p in pred), compute)
+    if policy != "auto":
+        return cands[0], res
+    tol = 0.01 * res[("wave", None)][3]
+    best = min(v[0] for v in res.values())
+    near = [key for key in cands if res[key][0] <= best + tol]
+    for pref in (("wave", None), ("interleave", None)):
+        if pref in near:
+            return pref, res
+    return max(near, key=lambda key: key[1]), res

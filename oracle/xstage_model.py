@@ -44,7 +44,7 @@ __all__ = [
     "capacity_guard", "capacity_from_knee", "predict", "BurstPrediction", "fit", "Model",
     "interleaved_gap", "interleaved_overhead", "average_rate_feasible", "d_knee",
     "mma_stall", "fa_work", "fa_qloop_lower_bound", "fa_recovery_threshold",
-    "completion_coupled_period", "residual", "speedup",
+    "completion_coupled_period", "residual", "speedup", "knee_index", "capacity_bracket",
 ]
 
 
@@ -190,6 +190,28 @@ def fit(recovered_V, recovered_Tiss, zero_gap_V, zero_gap_period, isolated_V, is
     stalled = it > (a + b * iv) * (1.0 + knee_excess)
     Q = float(np.median(iv[stalled] - R * it[stalled])) if stalled.any() else math.inf
     return Model(t0_a=float(a), t0_b=float(b), R=R, Q=Q, K=int(K))
+
+
+def knee_index(iso_V, iso_T, knee_excess: float) -> int:
+    """Sec. 3.5's isolated-burst knee (a reading of how to locate it): the first burst, from
+    the third on, whose issue time exceeds (1 + knee_excess) times the straight line through
+    the first burst and the one before it; len(iso_V) when none does. iso_V ascending."""
+    for i in range(2, len(iso_V)):
+        v0, t0, v1, t1 = iso_V[0], iso_T[0], iso_V[i - 1], iso_T[i - 1]
+        slope = (t1 - t0) / (v1 - v0) if v1 > v0 else 0.0
+        if iso_T[i] > (1.0 + knee_excess) * (t0 + slope * (iso_V[i] - v0)):
+            return i
+    return len(iso_V)
+
+
+def capacity_bracket(iso_V, knee: int, model: Model):
+    """Q lies between V - R T0(V) at the last isolated burst on the floor and at the first one
+    past the knee (Sec. 3.5: the knee is where the floor meets the stalled branch); (inf, inf)
+    without a knee."""
+    if not (0 < knee < len(iso_V)):
+        return math.inf, math.inf
+    q = lambda V: V - model.R * float(model.T0(V))
+    return q(iso_V[knee - 1]), q(iso_V[knee])
 
 
 # ----------------------------------------------------------------------------- App. A

@@ -129,30 +129,26 @@ def measure(share: Share, base_ptr: int, reps: int, rate: float, max_producers=0
 
 
 def audit(model: X.xs_model, cell: dict) -> dict:
-    """App. B recovery audit of one cell with a calibrated sink model."""
+    """App. B recovery audit of one cell with a calibrated sink model (xs_recovery_audit): every
+    producer's output bursts of one 128 x 128 bf16 tile, all K producers aligned, the median
+    Q-loop as the gap."""
     K = cell["grid"]
     Bt = B_M * HEAD_DIM * 2
     V = K * Bt
-    R = model.R_bytes_per_us
-    T0 = model.t0_a_us + model.t0_b_us_per_byte * V
-    g_star = max(0.0, V / R - T0)
     boundaries = math.ceil(cell["tiles"] / K)          # output bursts per producer
     G = cell["qloop_us_median"]
-    bursts = (X.xs_burst * boundaries)(*[X.xs_burst(V, T0, G) for _ in range(boundaries)])
-    pred = (X.xs_burst_pred * boundaries)()
-    X.check(X.xs_model_predict(C.byref(model), bursts, boundaries, 0.0, pred), "model_predict")
     sigma = cell["sigma_us_per_kv_tile"]
-    return {"B_t_bytes": Bt, "K": K, "V_bytes": V, "T0_us": T0, "R_GBps": R / 1e3,
+    rec = X.xs_recovery()
+    X.check(X.xs_recovery_audit(C.byref(model), V, boundaries, G, sigma, B_N, C.byref(rec)), "recovery_audit")
+    return {"B_t_bytes": Bt, "K": K, "V_bytes": V, "T0_us": rec.T0_us, "R_GBps": model.R_bytes_per_us / 1e3,
             "Q_bytes": model.Q_bytes if math.isfinite(model.Q_bytes) else None,
-            "G_star_us": g_star, "qloop_gap_us": G, "rho": pred[0].rho, "delta_b_bytes": pred[0].delta_b,
-            "guard_ok": bool(pred[0].guard_ok), "b_iso_bytes": pred[0].b_iso,
+            "G_star_us": rec.G_star_us, "qloop_gap_us": G, "rho": rec.rho, "delta_b_bytes": rec.delta_b,
+            "guard_ok": bool(rec.guard_ok), "b_iso_bytes": rec.b_iso,
             # the last burst has no Q-loop after it: with every producer aligned, what it and any
             # carried backlog leave undrained shows up after the compute (a conservative bound)
-            "E_res_bound_us": max(0.0, (pred[boundaries - 1].q_before + V) / R - T0),
-            "predicted_stall_us": float(sum(p.stall_us for p in pred)),
-            "M_ub_star": B_N * math.ceil(g_star / sigma) if sigma > 0 else None,
-            "output_boundaries_per_producer": boundaries,
-            "coupled_residual_predicted_us": boundaries * max(T0, V / R)}
+            "E_res_bound_us": rec.tail_us, "predicted_stall_us": rec.stall_us,
+            "M_ub_star": rec.M_ub_star if sigma > 0 else None,
+            "output_boundaries_per_producer": boundaries, "coupled_residual_predicted_us": rec.coupled_us}
 
 
 def run(Ms=(8192, 16384, 32768), sinks=("hbm", "host"), reps=None, calibrate_models=True, seed=0):

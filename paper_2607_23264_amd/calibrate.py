@@ -12,8 +12,9 @@ per-burst wall-clock records into sender-visible issue times and periods, and fi
 A burst's aggregate volume is V = K * B. Issue times and periods are taken per producer
 (producers drift apart over many bursts); an isolated burst, which every producer starts
 at the launch, is timed from the first start to the last issued store. This module only
-marshals calls and computes statistics of the timestamps; every store is issued by the
-library's kernel.
+marshals calls and takes medians of the timestamps: every store is issued by the library's
+kernel, and the model arithmetic (drain rate, knee, fit, capacity bracket, Eq. 1, G*) runs in
+the library's host calls.
 """
 from __future__ import annotations
 
@@ -68,6 +69,10 @@ def run_bursts(target_ptr: int, target_bytes: int, K: int, B: int, n_bursts: int
                     span)
 
 
+def _f64(v):
+    return np.ascontiguousarray(np.asarray(v, dtype=np.float64))
+
+
 @dataclass
 class Calibration:
     sink: str
@@ -108,17 +113,14 @@ def calibrate(target_ptr: int, target_bytes: int, sink: str, K: int, Bs, knee_ex
             continue
         run = run_bursts(target_ptr, target_bytes, K, B, n, 0, store_waves=store_waves)
         zg.append((K * B, run.total_span_us / n))
-    R_est = sum(v * v for v, _ in zg) / max(sum(v * t for v, t in zg), 1e-30)   # bytes per us
-    # knee: compare each isolated burst with the line through the bursts before it
-    knee = len(iso)
-    for i in range(2, len(iso)):
-        v0, t0 = iso[0]
-        v1, t1 = iso[i - 1]
-        slope = (t1 - t0) / (v1 - v0) if v1 > v0 else 0.0
-        line = t0 + slope * (iso[i][0] - v0)
-        if iso[i][1] > (1.0 + knee_excess) * line:
-            knee = i
-            break
+    zv, zt = _f64([v for v, _ in zg]), _f64([t for _, t in zg])
+    R_est = C.c_double()
+    X.check(X.xs_drain_rate(zv.ctypes.data, zt.ctypes.data, len(zg), C.byref(R_est)), "drain_rate")
+    R_est = R_est.value                                      # bytes per us
+    iv, it = _f64([v for v, _ in iso]), _f64([t for _, t in iso])
+    knee = C.c_int32()
+    X.check(X.xs_calib_knee(iv.ctypes.data, it.ctypes.data, len(iso), knee_excess, C.byref(knee)), "knee")
+    knee = knee.value
     # recovered floor: large-gap bursts below the knee that actually returned to the floor
     # (issue within 3x of the isolated burst of the same volume)
     rec = []
@@ -138,15 +140,12 @@ def calibrate(target_ptr: int, target_bytes: int, sink: str, K: int, Bs, knee_ex
     c = X.xs_calib(keep[0].ctypes.data_as(P), keep[1].ctypes.data_as(P), len(rec),
                    keep[2].ctypes.data_as(P), keep[3].ctypes.data_as(P), len(zg),
                    keep[4].ctypes.data_as(P), keep[5].ctypes.data_as(P), len(iso), K, knee_excess)
-    m = X.xs_model()
-    X.check(X.xs_model_fit(C.byref(c), C.byref(m)), "model_fit")
-    # Q two ways: the fluid fit (stalled isolated bursts on T = (V - Q) / R, xs_model_fit) and
-    # the knee bracket: between the last isolated burst on the floor and the first one off it
-    t0v = lambda v: m.t0_a_us + m.t0_b_us_per_byte * v
-    bracket = None
-    if 0 < knee < len(iso):
-        lo, hi = iso[knee - 1][0], iso[knee][0]
-        bracket = [lo - m.R_bytes_per_us * t0v(lo), hi - m.R_bytes_per_us * t0v(hi)]
+    sm = X.xs_calib_summary()
+    X.check(X.xs_model_calibrate(C.byref(c), C.byref(sm)), "model_calibrate")
+    m = sm.model
+    # Q two ways: the fluid fit (stalled isolated bursts on T = (V - Q) / R) and the knee
+    # bracket between the last isolated burst on the floor and the first one off it
+    bracket = [sm.Q_bracket_lo, sm.Q_bracket_hi] if math.isfinite(sm.Q_bracket_lo) else None
     model = {"t0_a_us": m.t0_a_us, "t0_b_us_per_byte": m.t0_b_us_per_byte, "R_bytes_per_us": m.R_bytes_per_us,
              "Q_bytes": m.Q_bytes if math.isfinite(m.Q_bytes) else None, "K": m.K,
              "knee_V_bytes": iso[knee][0] if knee < len(iso) else None, "Q_knee_bracket_bytes": bracket}
@@ -154,16 +153,17 @@ def calibrate(target_ptr: int, target_bytes: int, sink: str, K: int, Bs, knee_ex
     sweep = []
     B = gap_sweep_B or Bs[len(Bs) // 2]
     V = K * B
-    T0 = m.t0_a_us + m.t0_b_us_per_byte * V
-    g_star = max(0.0, V / m.R_bytes_per_us - T0)
+    rec1 = X.xs_recovery()
+    X.check(X.xs_recovery_audit(C.byref(m), V, 1, 0.0, 0.0, 1, C.byref(rec1)), "recovery_audit")
+    g_star = rec1.G_star_us
     n = n_fit(B, 32)
     for frac in (0.0, 0.25, 0.5, 0.75, 1.0, 1.5, 2.0, 3.0):
         gap_us = frac * max(g_star, 1.0)
         run = run_bursts(target_ptr, target_bytes, K, B, n, int(gap_us * 1e3), store_waves=store_waves)
+        tp, ti = C.c_double(), C.c_double()
+        X.check(X.xs_burst_gap(C.byref(m), V, gap_us, C.byref(tp), C.byref(ti)), "burst_gap")
         sweep.append({"V": V, "G_us": gap_us, "T_iss_us": run.steady(run.iss_us),
-                      "period_us": run.total_span_us / n,
-                      "pred_T_iss_us": max(T0, V / m.R_bytes_per_us - gap_us),
-                      "pred_period_us": max(T0 + gap_us, V / m.R_bytes_per_us)})
+                      "period_us": run.total_span_us / n, "pred_T_iss_us": ti.value, "pred_period_us": tp.value})
     log(f"[calibrate] {sink} K={K}: T0 = {m.t0_a_us:.3f} us + {m.t0_b_us_per_byte * 1e6:.3f} us/MB, "
         f"R = {m.R_bytes_per_us / 1e3:.1f} GB/s, Q = {model['Q_bytes']}, knee V = {model['knee_V_bytes']}")
     return Calibration(sink, K, model, rec, zg, iso, sweep)

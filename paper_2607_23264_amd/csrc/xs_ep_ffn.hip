@@ -149,6 +149,42 @@ __device__ __forceinline__ void expert_block(const EpArgs& a, int x, int p, bool
   rows = min(bm, m - m0);
 }
 
+// Tracing with ext records only: the first wave waits until the stores of its previous
+// epilogue have left it (vmcnt(0)), the point where this design reuses its local staging
+// (App. A.2), and returns how many ticks that took. Without ext records nothing waits.
+__device__ __forceinline__ uint64_t staging_wait(const EpArgs& a) {
+  if (!a.tr.ext || threadIdx.x >= 64) return 0;
+  __builtin_amdgcn_sched_barrier(0);
+  const uint64_t t = wall_ticks();
+  __builtin_amdgcn_sched_barrier(0);
+  wait_vm0();
+  __builtin_amdgcn_sched_barrier(0);
+  const uint64_t d = wall_ticks() - t;
+  __builtin_amdgcn_sched_barrier(0);
+  return d;
+}
+
+// One trace record (thread 0): kind 1 / 2, tile index, start, mainloop end, issue end; with
+// ext records also the dependency-wait end, the staging wait, the bytes stored and the rows.
+__device__ __forceinline__ void trace_tile(const EpArgs& a, uint64_t kind, uint32_t tile, uint64_t t0,
+                                           uint64_t t1, uint64_t t2, uint64_t t_dep, uint64_t stage,
+                                           uint64_t bytes, int rows) {
+  const uint32_t i = atomicAdd(a.tr.count, 1u);
+  if (static_cast<int64_t>(i) >= a.tr.capacity) return;
+  uint64_t* r = a.tr.buf + static_cast<int64_t>(i) * 4;
+  r[0] = (kind << 56) | (static_cast<uint64_t>(blockIdx.x) << 32) | tile;
+  r[1] = t0;
+  r[2] = t1;
+  r[3] = t2;
+  if (a.tr.ext) {
+    uint64_t* x = a.tr.ext + static_cast<int64_t>(i) * 4;
+    x[0] = t_dep;
+    x[1] = stage;
+    x[2] = bytes;
+    x[3] = static_cast<uint64_t>(rows);
+  }
+}
+
 __device__ __forceinline__ void ep_l1_tile(const EpArgs& a, int p, int nt, bool fused,
                                            char* lds, char** rowptr) {
   const int tid = threadIdx.x;
@@ -158,6 +194,7 @@ __device__ __forceinline__ void ep_l1_tile(const EpArgs& a, int p, int nt, bool 
   int m0, rows;
   expert_block(a, x, p, true, m0, rows);
   const uint64_t t0 = a.tr.buf ? wall_ticks() : 0;
+  const uint64_t stw = staging_wait(a);
   const int64_t lda = a.dwin.stride[dl] / 2;
   const uint16_t* A = reinterpret_cast<const uint16_t*>(
       a.dwin.base[dl] + static_cast<int64_t>(a.expert_offsets[e] + m0) * a.dwin.stride[dl]);
@@ -180,17 +217,9 @@ __device__ __forceinline__ void ep_l1_tile(const EpArgs& a, int p, int nt, bool 
   } else {
     lds_barrier();   // the unfused h rows are read by a later launch
   }
-  if (a.tr.buf && tid == 0) {
-    uint32_t i = atomicAdd(a.tr.count, 1u);
-    if (static_cast<int64_t>(i) < a.tr.capacity) {
-      uint64_t* r = a.tr.buf + static_cast<int64_t>(i) * 4;
-      r[0] = (1ull << 56) | (static_cast<uint64_t>(blockIdx.x) << 32) |
-             static_cast<uint32_t>(p * a.P1 + nt);
-      r[1] = t0;
-      r[2] = t1;
-      r[3] = wall_ticks();
-    }
-  }
+  if (a.tr.buf && tid == 0)
+    trace_tile(a, 1, static_cast<uint32_t>(p * a.P1 + nt), t0, t1, wall_ticks(), t0, stw,
+               static_cast<uint64_t>(rows) * (kBN / 2) * 2, rows);
 }
 
 // Returns false if the wait for row p's Linear-1 tiles expired (the tile is then skipped).
@@ -225,6 +254,8 @@ __device__ __forceinline__ void ep_l2_tile(const EpArgs& a, int p, int nt, bool 
   const int tid = threadIdx.x;
   const uint64_t t0 = a.tr.buf ? wall_ticks() : 0;
   if (fused && !ep_wait_row(a, p, flag)) return;
+  const uint64_t t_dep = a.tr.buf ? wall_ticks() : 0;
+  const uint64_t stw = staging_wait(a);
   const int x = a.row_expert[p];
   const int e = a.e_begin + x;
   int m0, rows;
@@ -263,18 +294,9 @@ __device__ __forceinline__ void ep_l2_tile(const EpArgs& a, int p, int nt, bool 
   // stores drain while the next tile runs.
   lds_barrier();
   if (tid == 0) {
-    const uint64_t t2 = a.tr.buf ? wall_ticks() : 0;
-    if (a.tr.buf) {
-      uint32_t i = atomicAdd(a.tr.count, 1u);
-      if (static_cast<int64_t>(i) < a.tr.capacity) {
-        uint64_t* r = a.tr.buf + static_cast<int64_t>(i) * 4;
-        r[0] = (2ull << 56) | (static_cast<uint64_t>(blockIdx.x) << 32) |
-               static_cast<uint32_t>(p * a.P2 + nt);
-        r[1] = t0;
-        r[2] = t1;
-        r[3] = t2;
-      }
-    }
+    if (a.tr.buf)
+      trace_tile(a, 2, static_cast<uint32_t>(p * a.P2 + nt), t0, t1, wall_ticks(), t_dep, stw,
+                 static_cast<uint64_t>(rows) * kBN * 2, rows);
     spin_ticks(static_cast<uint64_t>(a.gap_ticks));   // non-injecting gap after the burst
   }
   if (a.gap_ticks) __syncthreads();
@@ -300,6 +322,7 @@ __device__ __forceinline__ void ep_l1_tile_mx(const EpArgs& a, int p, int nt, bo
   int m0, rows;
   expert_block(a, x, p, false, m0, rows);
   const uint64_t t0 = a.tr.buf ? wall_ticks() : 0;
+  const uint64_t stw = staging_wait(a);
   const int64_t ws = a.dwin.stride[dl];
   const uint8_t* A = reinterpret_cast<const uint8_t*>(a.dwin.base[dl] +
                                                       static_cast<int64_t>(a.expert_offsets[e] + m0) * ws);
@@ -331,16 +354,9 @@ __device__ __forceinline__ void ep_l1_tile_mx(const EpArgs& a, int p, int nt, bo
   } else {
     lds_barrier();
   }
-  if (a.tr.buf && tid == 0) {
-    uint32_t i = atomicAdd(a.tr.count, 1u);
-    if (static_cast<int64_t>(i) < a.tr.capacity) {
-      uint64_t* r = a.tr.buf + static_cast<int64_t>(i) * 4;
-      r[0] = (1ull << 56) | (static_cast<uint64_t>(blockIdx.x) << 32) | static_cast<uint32_t>(p * a.P1 + nt);
-      r[1] = t0;
-      r[2] = t1;
-      r[3] = wall_ticks();
-    }
-  }
+  if (a.tr.buf && tid == 0)
+    trace_tile(a, 1, static_cast<uint32_t>(p * a.P1 + nt), t0, t1, wall_ticks(), t0, stw,
+               static_cast<uint64_t>(rows) * (128 + 4), rows);
 }
 
 // Linear-2 on MXFP8 h rows; bf16 output rows into the combine windows as in the bf16 tile.
@@ -350,6 +366,8 @@ __device__ __forceinline__ void ep_l2_tile_mx(const EpArgs& a, int p, int nt, bo
   const int tid = threadIdx.x;
   const uint64_t t0 = a.tr.buf ? wall_ticks() : 0;
   if (fused && !ep_wait_row(a, p, flag)) return;
+  const uint64_t t_dep = a.tr.buf ? wall_ticks() : 0;
+  const uint64_t stw = staging_wait(a);
   const int x = a.row_expert[p];
   const int e = a.e_begin + x;
   int m0, rows;
@@ -383,17 +401,9 @@ __device__ __forceinline__ void ep_l2_tile_mx(const EpArgs& a, int p, int nt, bo
   store_rows_n<kMxThreads>(lds, kEpiPitch * 2, kBN * 2 / 16, rows, rowptr);
   lds_barrier();
   if (tid == 0) {
-    const uint64_t t2 = a.tr.buf ? wall_ticks() : 0;
-    if (a.tr.buf) {
-      uint32_t i = atomicAdd(a.tr.count, 1u);
-      if (static_cast<int64_t>(i) < a.tr.capacity) {
-        uint64_t* r = a.tr.buf + static_cast<int64_t>(i) * 4;
-        r[0] = (2ull << 56) | (static_cast<uint64_t>(blockIdx.x) << 32) | static_cast<uint32_t>(p * a.P2 + nt);
-        r[1] = t0;
-        r[2] = t1;
-        r[3] = t2;
-      }
-    }
+    if (a.tr.buf)
+      trace_tile(a, 2, static_cast<uint32_t>(p * a.P2 + nt), t0, t1, wall_ticks(), t_dep, stw,
+                 static_cast<uint64_t>(rows) * kBN * 2, rows);
     spin_ticks(static_cast<uint64_t>(a.gap_ticks));
   }
   if (a.gap_ticks) __syncthreads();
@@ -816,23 +826,6 @@ int launch_plan(const xs_ep_layer* L, const EpArgs& a, int wave_tiles, hipStream
   return xs_host::launch_status();
 }
 
-// Chunk length for AUTO from the average-rate bound (Eq. 9) with n1 = 1 Linear-1 tile per
-// cycle and n2 = c aligned Linear-2 bursts of V = K * tile bytes each:
-//   c V / (c (T0 + T_L2) + T_L1) <= R  <=>  c (V/R - T0 - T_L2) <= T_L1.
-int auto_chunk(const xs_pacing* pc, const xs_ep_layer* L, int K) {
-  if (!pc->model) return 0;
-  const xs_model* m = pc->model;
-  const double V = static_cast<double>(K) * kBM * kBN * 2;
-  const double T0 = m->t0_a_us + m->t0_b_us_per_byte * V;
-  // fallback mainloop estimates: tile FLOPs at 40 % of one CU's share of 2.5 PFLOP/s
-  const double cu_flops_us = 2.5e15 / 256.0 * 0.4 * 1e-6;
-  const double tl1 = pc->t_l1_us > 0 ? pc->t_l1_us : 2.0 * kBM * kBN * L->H / cu_flops_us;
-  const double tl2 = pc->t_l2_us > 0 ? pc->t_l2_us : 2.0 * kBM * kBN * L->I / cu_flops_us;
-  const double excess = V / m->R_bytes_per_us - T0 - tl2;
-  if (!(m->R_bytes_per_us > 0) || excess <= 0) return 0;   // drain keeps up: plain interleave
-  return std::max(1, static_cast<int>(std::floor(tl1 / excess)));
-}
-
 }  // namespace
 
 // Records the phase event `i` of the layer descriptor, if the caller set one.
@@ -864,8 +857,15 @@ static int run_ffn(const xs_ep_layer* L, const EpArgs& base, int mode, int l2_co
   a.chunk = pc ? pc->chunk_tiles : 0;
   if (a.policy == XS_POLICY_INTERLEAVE) a.chunk = 0;
   if (a.policy == XS_POLICY_AUTO) {
-    a.chunk = auto_chunk(pc, L, grid);
-    a.policy = a.chunk > 0 ? XS_POLICY_CHUNK : XS_POLICY_INTERLEAVE;
+    // the audited choice (xs_pacing_audit_run); plain interleave without a model
+    xs_pacing_audit au;
+    if (pc->model && xs_pacing_audit_run(L, pc, &au) == XS_OK) {
+      a.policy = au.policy;
+      a.chunk = au.chunk;
+    } else {
+      a.policy = XS_POLICY_INTERLEAVE;
+      a.chunk = 0;
+    }
   }
   a.withhold_row = pc ? pc->withhold_row : -1;
   a.claim = pc ? pc->claim : XS_CLAIM_STATIC;

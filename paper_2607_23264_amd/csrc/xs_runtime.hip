@@ -12,7 +12,7 @@ extern "C" const char* xs_strerror(int code) {
     case XS_EWORKSPACE: return "workspace missing or too small";
     case XS_ECAPACITY: return "a destination window exceeded its capacity";
     case XS_ETIMEOUT: return "a bounded dependency wait timed out";
-    case XS_EBADINPUT: return "expert id out of range";
+    case XS_EBADINPUT: return "expert id out of range, or listed twice by one token";
     default: return "unknown status";
   }
 }

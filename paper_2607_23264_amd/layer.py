@@ -282,12 +282,16 @@ class EPLayer:
 
 def pacing(policy=X.XS_POLICY_INTERLEAVE, lead=1, chunk=0, max_producers=0, wave_tiles=0, gap_ns=0,
            spin_timeout_us=0, withhold_row=-1, t_l1_us=0.0, t_l2_us=0.0, model=None,
-           claim=0) -> X.xs_pacing:
+           claim=0, expert_rows=None, sink_share=0.0) -> X.xs_pacing:
     p = X.xs_pacing(policy, lead, chunk, max_producers, wave_tiles, gap_ns, spin_timeout_us, withhold_row,
-                    claim, 0, t_l1_us, t_l2_us, None)
+                    claim, 0, t_l1_us, t_l2_us, None, None, sink_share)
     if model is not None:
         p._model_ref = model
         p.model = C.pointer(model)
+    if expert_rows is not None:
+        arr = (C.c_int32 * len(expert_rows))(*[int(v) for v in expert_rows])
+        p._rows_ref = arr
+        p.expert_rows = C.cast(arr, C.POINTER(C.c_int32))
     return p
 
 

@@ -51,11 +51,12 @@ class xs_pacing(C.Structure):
     _fields_ = [("policy", i32), ("lead_rows", i32), ("chunk_tiles", i32), ("max_producers", i32),
                 ("wave_tiles", i32), ("gap_ns", i32), ("spin_timeout_us", i32), ("withhold_row", i32),
                 ("claim", i32), ("reserved", i32),
-                ("t_l1_us", f64), ("t_l2_us", f64), ("model", C.POINTER(xs_model))]
+                ("t_l1_us", f64), ("t_l2_us", f64), ("model", C.POINTER(xs_model)),
+                ("expert_rows", C.POINTER(i32)), ("sink_share", f64)]
 
 
 class xs_trace(C.Structure):
-    _fields_ = [("buf", vp), ("capacity", i64), ("count", vp)]
+    _fields_ = [("buf", vp), ("capacity", i64), ("count", vp), ("ext", vp)]
 
 
 class xs_ep_layer(C.Structure):
@@ -82,12 +83,33 @@ class xs_scatter_desc(C.Structure):
 
 
 class xs_burst(C.Structure):
-    _fields_ = [("V_bytes", f64), ("T0_us", f64), ("G_us", f64)]
+    _fields_ = [("V_bytes", f64), ("T0_us", f64), ("G_us", f64), ("cover_us", f64)]
 
 
 class xs_burst_pred(C.Structure):
     _fields_ = [("rho", f64), ("delta_b", f64), ("q_before", f64), ("b_iso", f64), ("T_iss_us", f64),
-                ("stall_us", f64), ("guard_ok", i32), ("_pad", i32)]
+                ("stall_us", f64), ("mma_stall_us", f64), ("guard_ok", i32), ("_pad", i32)]
+
+
+class xs_calib_summary(C.Structure):
+    _fields_ = [("model", xs_model), ("knee", i32), ("_pad", i32), ("Q_bracket_lo", f64), ("Q_bracket_hi", f64)]
+
+
+class xs_recovery(C.Structure):
+    _fields_ = [("T0_us", f64), ("G_star_us", f64), ("rho", f64), ("delta_b", f64), ("b_iso", f64),
+                ("stall_us", f64), ("tail_us", f64), ("coupled_us", f64), ("guard_ok", i32), ("M_ub_star", i32)]
+
+
+XS_AUDIT_MAX = 16
+
+
+class xs_pacing_audit(C.Structure):
+    _fields_ = [("policy", i32), ("chunk", i32), ("lead_rows", i32), ("producers", i32), ("rows", i32),
+                ("rate_feasible", i32), ("n_cand", i32), ("_pad", i32), ("t_l1_us", f64), ("t_l2_us", f64),
+                ("V_full_bytes", f64), ("cand_policy", i32 * XS_AUDIT_MAX), ("cand_chunk", i32 * XS_AUDIT_MAX),
+                ("cand_bursts", i32 * XS_AUDIT_MAX), ("cand_guard_fail", i32 * XS_AUDIT_MAX),
+                ("cand_stall_us", f64 * XS_AUDIT_MAX), ("cand_mma_stall_us", f64 * XS_AUDIT_MAX),
+                ("cand_compute_us", f64 * XS_AUDIT_MAX)]
 
 
 class xs_calib(C.Structure):
@@ -144,13 +166,21 @@ xs_model_predict = _sig("xs_model_predict", C.c_int, P(xs_model), P(xs_burst), i
 xs_model_fit = _sig("xs_model_fit", C.c_int, P(xs_calib), P(xs_model))
 xs_xstage_microbench = _sig("xs_xstage_microbench", C.c_int, P(xs_microbench_args), P(xs_trace), vp)
 xs_clock_rate_hz = _sig("xs_clock_rate_hz", C.c_double)
+xs_drain_rate = _sig("xs_drain_rate", C.c_int, vp, vp, i32, P(f64))
+xs_calib_knee = _sig("xs_calib_knee", C.c_int, vp, vp, i32, f64, P(i32))
+xs_model_calibrate = _sig("xs_model_calibrate", C.c_int, P(xs_calib), P(xs_calib_summary))
+xs_burst_gap = _sig("xs_burst_gap", C.c_int, P(xs_model), f64, f64, P(f64), P(f64))
+xs_recovery_audit = _sig("xs_recovery_audit", C.c_int, P(xs_model), f64, i32, f64, f64, i32, P(xs_recovery))
+xs_pacing_audit_run = _sig("xs_pacing_audit_run", C.c_int, P(xs_ep_layer), P(xs_pacing), P(xs_pacing_audit))
+xs_trace_tile_times = _sig("xs_trace_tile_times", C.c_int, vp, vp, i64, i32, P(f64), P(f64), P(f64))
 
 EXPORTED = ["xs_strerror", "xs_version", "xs_route_topk_softmax", "xs_dispatch_layout_workspace_bytes",
             "xs_dispatch_layout", "xs_dispatch", "xs_ep_layer_workspace_bytes", "xs_expert_ffn",
             "xs_combine_send", "xs_combine_reduce", "xs_fused_ep_layer", "xs_gemm", "xs_gemm_scatter",
             "xs_scatter_copy", "xs_attention", "xs_ulysses_copy", "xs_quantize_mx", "xs_quantize_mx_grouped", "xs_gemm_mx", "xs_dispatch_rows",
             "xs_ring_slot_bytes", "xs_dispatch_ring_workspace_bytes", "xs_dispatch_ring",
-            "xs_model_predict", "xs_model_fit",
+            "xs_model_predict", "xs_model_fit", "xs_pacing_audit_run", "xs_trace_tile_times",
+            "xs_drain_rate", "xs_calib_knee", "xs_model_calibrate", "xs_burst_gap", "xs_recovery_audit",
             "xs_xstage_microbench", "xs_clock_rate_hz"]
 
 

@@ -425,3 +425,92 @@ def test_bad_arguments_rejected_synchronously():
                                lay.status.data_ptr(), None) == X.XS_EWORKSPACE
     assert X.xs_route_topk_softmax(lay.logits.data_ptr(), 4, 8, 9, 0, lay.topk_idx.data_ptr(),
                                    lay.topk_w.data_ptr(), None) == X.XS_EINVAL
+
+
+SKEWED = synth.EPConfig("skewed_T2048_H2048_E8_k2_I512_W4", T=2048, H=2048, E=8, k=2, I=512, W=4, n_src=1,
+                        rank=0, compute_all=True, routing="zipf")
+
+
+@pytest.mark.parametrize("Q,want", [(1e6, "interleave"), (float("inf"), "wave")])
+def test_auto_follows_the_audited_choice(Q, want):
+    """AUTO with a model: the library audits every candidate order and runs the one with the least
+    predicted stall; the traced tile order of every workgroup equals the schedule oracle's stream
+    of the order the oracle's own audit picks."""
+    from paper_2607_23264_amd.layer import pacing
+    X = xs()
+    cfg = SKEWED
+    inp = synth.ep_inputs(cfg, 0)
+    lay = _ep_layer(cfg)
+    lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
+    idx = oep.route_topk_softmax(inp["logits"][0], cfg.k)[0]
+    counts = [int(c) for c in np.bincount(idx.ravel(), minlength=cfg.E)]
+    G, D, tl1, tl2 = 8, 1, 20.0, 10.0
+    a, b, R = 1.0, 1e-7, 30000.0
+    P1, P2 = cfg.I // 128, cfg.H // 256
+    choice, _ = osc.pacing_audit(counts, True, P1, P2, G, D, G, 1.0, tl1, tl2, a, b, R, Q)
+    assert choice[0] == want
+    m = X.xs_model(a, b, R, Q, G, 0)
+    pol = pacing(X.XS_POLICY_AUTO, lead=D, max_producers=G, model=m, t_l1_us=tl1, t_l2_us=tl2,
+                 expert_rows=counts)
+    buf = torch.zeros((8192, 4), dtype=torch.int64, device="cuda")
+    cnt = torch.zeros((1,), dtype=torch.int32, device="cuda")
+    lay.fused(pol, X.xs_trace(buf.data_ptr(), buf.shape[0], cnt.data_ptr()))
+    torch.cuda.synchronize()
+    assert int(lay.status.item()) == 0
+    kind, wg, tile, _ = _records(buf, cnt)
+    sizes, owner = osc.expert_blocks(counts, True)
+    P = len(sizes)
+    if want == "wave":
+        streams = osc.all_streams("wave", G, P, P1, P2, waves=osc.waves_by_tiles(owner, P1, G))
+    else:
+        streams = osc.all_streams("interleave", G, P, P1, P2, D=D)
+    for g in range(G):
+        got = [(int(kk), int(tt)) for kk, ww, tt in zip(kind, wg, tile) if ww == g]
+        assert got == [(kk, tt) for kk, _, tt in streams[g]], f"workgroup {g}"
+    ref = oep.ep_layer(inp["x"], inp["logits"], inp["w1"], inp["w2"], cfg.k, cfg.E, cfg.W, cap=cfg.T * cfg.k)
+    assert_close(host_bits(lay.out), ref["out64"], f"skewed layer under AUTO ({want})")
+
+
+def test_trace_ext_records_and_tile_times():
+    """The ext trace records: dependency-wait end, staging wait, stored bytes and rows of every
+    tile, consistent with the main records; and the library's tile-time medians of that trace."""
+    from paper_2607_23264_amd.layer import pacing
+    X = xs()
+    cfg = SKEWED
+    inp = synth.ep_inputs(cfg, 0)
+    lay = _ep_layer(cfg)
+    lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
+    buf = torch.zeros((8192, 4), dtype=torch.int64, device="cuda")
+    ext = torch.zeros((8192, 4), dtype=torch.int64, device="cuda")
+    cnt = torch.zeros((1,), dtype=torch.int32, device="cuda")
+    lay.fused(pacing(X.XS_POLICY_INTERLEAVE, lead=1, claim=X.XS_CLAIM_DYNAMIC),
+              X.xs_trace(buf.data_ptr(), buf.shape[0], cnt.data_ptr(), ext.data_ptr()))
+    torch.cuda.synchronize()
+    assert int(lay.status.item()) == 0
+    n = int(cnt.item())
+    r = buf[:n].cpu().numpy().astype(np.uint64)
+    x = ext[:n].cpu().numpy().astype(np.uint64)
+    kind = (r[:, 0] >> np.uint64(56)).astype(np.int64)
+    idx = oep.route_topk_softmax(inp["logits"][0], cfg.k)[0]
+    sizes, _ = osc.expert_blocks(np.bincount(idx.ravel(), minlength=cfg.E), True)
+    P1, P2 = cfg.I // 128, cfg.H // 256
+    assert (kind == 1).sum() == len(sizes) * P1 and (kind == 2).sum() == len(sizes) * P2
+    tile = (r[:, 0] & np.uint64(0xFFFFFFFF)).astype(np.int64)
+    sz = np.array(sizes)
+    rows = np.empty(n, np.int64)
+    rows[kind == 1] = sz[tile[kind == 1] // P1]
+    rows[kind == 2] = sz[tile[kind == 2] // P2]
+    assert np.array_equal(x[:, 3].astype(np.int64), rows)
+    assert np.array_equal(x[kind == 2, 2].astype(np.int64), rows[kind == 2] * 256 * 2)
+    assert np.array_equal(x[kind == 1, 2].astype(np.int64), rows[kind == 1] * 128 * 2)
+    assert np.all(x[kind == 1, 0] == r[kind == 1, 1])
+    assert np.all((x[kind == 2, 0] >= r[kind == 2, 1]) & (x[kind == 2, 0] <= r[kind == 2, 2]))
+    assert np.all(x[:, 1] <= r[:, 2] - r[:, 1])       # the staging wait lies inside the tile
+    t1, t2, t3 = C.c_double(), C.c_double(), C.c_double()
+    rc = np.ascontiguousarray(r)
+    xc = np.ascontiguousarray(x)
+    X.check(X.xs_trace_tile_times(rc.ctypes.data, xc.ctypes.data, n, 0, C.byref(t1), C.byref(t2), C.byref(t3)))
+    us = 1e6 / X.xs_clock_rate_hz()
+    assert t1.value == pytest.approx(np.median((r[kind == 1, 2] - r[kind == 1, 1]).astype(np.float64)) * us)
+    assert t2.value == pytest.approx(np.median((r[kind == 2, 2] - x[kind == 2, 0]).astype(np.float64)) * us)
+    assert t1.value > 0 and t2.value > 0 and t3.value > 0

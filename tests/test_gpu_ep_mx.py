@@ -13,7 +13,7 @@ import synth
 from oracle import ep as oep
 from oracle import ep_mx as omx
 from oracle import mx as omxf
-from gpu_helpers import assert_close, bits_f64, host_bits, require_gpu, xs
+from gpu_helpers import assert_close, bits_f64, check_h_admissible, host_bits, mx_h_admissible, require_gpu, xs
 
 pytestmark = pytest.mark.gpu
 
@@ -48,50 +48,6 @@ def _policies():
             "auto_nomodel": pacing(X.XS_POLICY_AUTO),
             "interleave_dyn": pacing(X.XS_POLICY_INTERLEAVE, lead=1, claim=X.XS_CLAIM_DYNAMIC),
             "burst_w4_dyn": pacing(X.XS_POLICY_BURST, wave_tiles=4, claim=X.XS_CLAIM_DYNAMIC)}
-
-
-def _h_within_fp32_bound(got_codes, got_scales, xq, w1q, what, wfmt=omxf.E4M3):
-    """The GPU's quantized h rows against the exact SwiGLU of the dequantized operands.
-
-    The GPU accumulates Linear-1 in fp32 and evaluates SwiGLU in fp32, so its h differs from
-    the exact value by at most bh = |dh/dg| bg + |dh/du| bu + (8 + 2|g|) 2^-24 |h|, where
-    bg, bu = 2 K 2^-24 sum_k |x_k w_k| bound the accumulation error of the gate and up
-    sums (K terms) and the last term covers the exp, reciprocal and products. Each block's
-    scale must be the shared exponent of some values within that bound, and each code the
-    round-to-nearest-even of some value within it: codes may differ from the oracle's only
-    where its value lies that close to a rounding midpoint (or a block maximum that close to a
-    power-of-two threshold)."""
-    X = omxf.dequantize_mx(*xq, omxf.E4M3)
-    W1 = omxf.dequantize_mx(*w1q, wfmt)
-    I = W1.shape[0] // 2
-    K = X.shape[1]
-    g, u = X @ W1[:I].T, X @ W1[I:].T
-    u_eps = 2.0 ** -24
-    bg = 2 * K * u_eps * (np.abs(X) @ np.abs(W1[:I]).T)
-    bu = 2 * K * u_eps * (np.abs(X) @ np.abs(W1[I:]).T)
-    with np.errstate(over="ignore"):
-        sig = 1.0 / (1.0 + np.exp(-g))
-    h = g * sig * u
-    dh_dg = np.abs(u * sig * (1 + g * (1 - sig)))
-    bh = dh_dg * bg + np.abs(g * sig) * bu + (8 + 2 * np.abs(g)) * u_eps * np.abs(h)
-    lo, hi = h - bh, h + bh
-    m = h.shape[0]
-    es = got_scales.astype(np.int64) - 127                       # [m][I / 32]
-    # admissible scales: the exponent of some block maximum in [max|lo..hi|]
-    amax_lo = np.where((lo > 0) | (hi < 0), np.minimum(np.abs(lo), np.abs(hi)), 0.0)
-    amax_hi = np.maximum(np.abs(lo), np.abs(hi))
-    e_lo = omxf.shared_exponent(amax_lo.reshape(m, -1, 32).max(-1), omxf.E4M3)
-    e_hi = omxf.shared_exponent(amax_hi.reshape(m, -1, 32).max(-1), omxf.E4M3)
-    bad_scale = (es < e_lo) | (es > e_hi)
-    assert not bad_scale.any(), f"{what}: {bad_scale.sum()} block scales outside the fp32 bound"
-    sc = np.repeat(np.ldexp(1.0, es), 32, axis=1)
-    vals = omxf.decode(got_codes, omxf.E4M3)
-    c_lo = omxf.decode(omxf.encode(lo / sc, omxf.E4M3), omxf.E4M3)
-    c_hi = omxf.decode(omxf.encode(hi / sc, omxf.E4M3), omxf.E4M3)
-    bad = (vals < c_lo) | (vals > c_hi)
-    assert not bad.any(), f"{what}: {bad.sum()} codes outside the fp32 bound, first at {np.argwhere(bad)[0]}"
-    want, _ = omxf.quantize_mx(h, omxf.E4M3)
-    return int((got_codes != want).sum())
 
 
 def _window_bases(lay):
@@ -146,8 +102,8 @@ def test_tiny_layer_matches_oracle_for_every_policy(prec):
         m = hc.shape[0]
         sl = slice(bases[d] + r0, bases[d] + r0 + m)
         xq = (ref["win_codes"][d, r0:r0 + m], ref["win_scales"][d, r0:r0 + m])
-        flips += _h_within_fp32_bound(hcodes[sl], hscales[sl], xq,
-                                      omx.quantize_rows(inp["w1"][e], _wfmt(prec)), f"h of expert {e}", _wfmt(prec))
+        adm = mx_h_admissible(xq, omx.quantize_rows(inp["w1"][e], _wfmt(prec)), _wfmt(prec))
+        flips += check_h_admissible(hcodes[sl], hscales[sl], adm, f"h of expert {e}")
     print(f"h codes that differ from the oracle's (all within the fp32 bound): {flips}")
     # combine rows (bf16 expert outputs) against the oracle's rounded rows
     comb = host_bits(lay.cwin)

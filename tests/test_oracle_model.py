@@ -254,3 +254,21 @@ def test_fit_recovers_generating_parameters():
     assert m.Q == pytest.approx(Q, rel=1e-9)
     # a path with no knee reports unbounded capacity
     assert math.isinf(xm.fit(Vr, Tr, Vz, Tz, Vi, a + b * Vi, K=64).Q)
+
+
+def test_knee_bracket_contains_the_generating_capacity():
+    # isolated bursts on the fluid law T = max(T0(V), (V - Q) / R): the knee bracket holds Q
+    a, b, R = 1.0, 2e-7, 56000.0
+    for Q in (3e6, 16.7e6, 40e6):
+        V = np.array([2 ** k * 65536.0 for k in range(12)])
+        T = np.maximum(a + b * V, (V - Q) / R)
+        m = xm.fit(V[:3], a + b * V[:3], V, V / R, V, T, K=256, knee_excess=0.5)
+        k = xm.knee_index(V, T, 0.5)
+        assert 0 < k < len(V)
+        lo, hi = xm.capacity_bracket(V, k, m)
+        assert lo <= Q < hi
+        # every burst before the knee is on the floor, the knee burst is off it
+        assert np.all(T[:k] <= (1.5) * (a + b * V[:k])) and T[k] > a + b * V[k]
+    # no stall anywhere: no knee, unbounded bracket
+    V = np.linspace(1e5, 1e7, 8)
+    assert xm.knee_index(V, 1.0 + 2e-7 * V, 0.5) == len(V)

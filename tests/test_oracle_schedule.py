@@ -78,3 +78,41 @@ def test_zero_lead_can_deadlock():
 def test_waves_by_tiles_whole_experts():
     row_expert = [0, 0, 1, 2, 2, 2, 3]
     assert sc.waves_by_tiles(row_expert, P1=2, min_tiles=4) == [(0, 2), (2, 6), (6, 7)]
+
+
+def test_expert_blocks_hand_counted():
+    # 600 rows: 3 equal blocks of ceil(600 / 3) = 200 -> 224 rows (multiple of 32), the last 152
+    assert sc.expert_blocks([600, 0, 1, 256], True) == ([224, 224, 152, 1, 256], [0, 0, 0, 2, 3])
+    assert sc.expert_blocks([600, 257], False) == ([256, 256, 88, 256, 1], [0, 0, 0, 1, 1])
+
+
+def test_audit_bursts_hand_traced():
+    # G = 1, two rows, P1 = 1, P2 = 2, D = 1: row 1's Linear-1 tile releases row 0's two
+    # Linear-2 tiles, and row 1's follow once Linear-1 is used up: L1 L2 L2 L1 L2 L2
+    tiles = sc.interleave_stream(0, 1, P=2, P1=1, P2=2, D=1)
+    assert [t[0] for t in tiles] == [1, 2, 2, 1, 2, 2]
+    V, gaps, comp = sc.audit_bursts(tiles, [100, 50], G=1, sink_share=0.5, T_L1=10.0, T_L2=3.0)
+    assert V == [100 * 256 * 2 * 0.5, 100 * 256 * 2 * 0.5, 50 * 256 * 2 * 0.5, 50 * 256 * 2 * 0.5]
+    # after burst 0: the next Linear-2 mainloop; after burst 1: L1 + L2; then L2; last: nothing
+    assert gaps == [3.0, 13.0, 3.0, 0.0]
+    assert comp == 2 * 10.0 + 4 * 3.0
+
+
+def test_audit_unbounded_capacity_and_fast_drain_predict_no_stall():
+    for rows in ([1039] * 32, [30466, 128, 175, 9344] + [200] * 28):
+        ch, res = sc.pacing_audit(rows, True, 16, 28, 256, 16, 256, 1.0, 210.0, 64.0, 1.0, 1e-8, 5.6e6, np.inf)
+        assert ch == ("wave", None)
+        assert all(v[0] == 0 and v[2] == 0 for v in res.values())
+
+
+def test_audit_rate_infeasible_stalls_every_order():
+    # offered rate far above R (Eq. 9 fails): no order can recover, every candidate stalls
+    ch, res = sc.pacing_audit([1039] * 32, True, 16, 28, 256, 16, 256, 1.0, 210.0, 64.0, 1.0, 1e-8, 1000.0, 1e6)
+    assert all(v[0] > 0 for v in res.values())
+    # and the stall is at least the drain time the compute cannot cover, V_total / R - compute,
+    # for producer 0's bursts (issue alone cannot drain faster than R)
+    sizes, owner = sc.expert_blocks([1039] * 32, True)
+    tiles = sc.interleave_stream(0, 256, len(sizes), 16, 28, 16)
+    V, gaps, comp = sc.audit_bursts(tiles, sizes, 256, 1.0, 210.0, 64.0)
+    stall = res[("interleave", None)][0]
+    assert stall >= sum(V) / 1000.0 - comp - 1e-6 - (1e6 / 1000.0)
