@@ -151,7 +151,7 @@ def scatter_lines(X, torch, synth, reps=20):
     desc = X.xs_scatter_desc(X.XS_SCATTER_ROW_BLOCK, rpd, 0, 0, 0, 0)
     c = torch.empty((tp.M, tp.N), dtype=torch.int16, device="cuda")
     M, N, K = tp.M, tp.N, tp.K
-    f = lambda: X.check(X.xs_gemm_scatter(a.data_ptr(), K, bt.data_ptr(), K, M, N, K, desc, wins, tp.W, None, st))
+    f = lambda: X.check(X.xs_gemm_scatter(a.data_ptr(), K, bt.data_ptr(), K, M, N, K, desc, wins, tp.W, None, None, st))
     g = lambda: X.check(X.xs_gemm(a.data_ptr(), K, bt.data_ptr(), K, c.data_ptr(), N, M, N, K, None, st))
     sc = lambda: X.check(X.xs_scatter_copy(c.data_ptr(), N, M, N, desc, wins, tp.W, st))
     out["tp_rowblock"] = _scatter_result(tp.name, 2.0 * M * N * K, 2.0 * M * N,
@@ -168,7 +168,7 @@ def scatter_lines(X, torch, synth, reps=20):
                       for q in range(G)])
     desc = X.xs_scatter_desc(X.XS_SCATTER_HEAD_GROUP, 0, 3, sp.n_heads, sp.head_dim, sp.heads_per_group)
     c = torch.empty((S, N), dtype=torch.int16, device="cuda")
-    f = lambda: X.check(X.xs_gemm_scatter(x.data_ptr(), Dm, wt.data_ptr(), Dm, S, N, Dm, desc, wins, G, None, st))
+    f = lambda: X.check(X.xs_gemm_scatter(x.data_ptr(), Dm, wt.data_ptr(), Dm, S, N, Dm, desc, wins, G, None, None, st))
     g = lambda: X.check(X.xs_gemm(x.data_ptr(), Dm, wt.data_ptr(), Dm, c.data_ptr(), N, S, N, Dm, None, st))
     sc = lambda: X.check(X.xs_scatter_copy(c.data_ptr(), N, S, N, desc, wins, G, st))
     out["sp_qkv"] = _scatter_result(sp.name, 2.0 * S * N * Dm, 2.0 * S * N, *timed(f, g, lambda: (g(), sc())))

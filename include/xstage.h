@@ -323,8 +323,12 @@ int xs_expert_ffn(const xs_ep_layer* L, void* workspace, int64_t workspace_bytes
 
 /* Combine-send (the Combine exchange, Sec. 4.3): computed row r of window d goes to
  * combine window s at row t*k+j where row_src[d][r] = (s << 24) | (t*k+j). Unfused form of
- * the Linear-2 epilogue stores; reads y_ws. */
-int xs_combine_send(const xs_ep_layer* L, int32_t* dev_status, void* stream);
+ * the Linear-2 epilogue stores; reads y_ws. pacing (nullable) shapes the bursts the combine
+ * windows see: max_producers workgroups (0 = eight per CU) each store bursts of chunk_tiles
+ * blocks of 256 consecutive computed rows (0 = 64 rows), burst b of producer g being block
+ * g + b * producers, with a non-injecting gap of gap_ns after each burst; the other fields
+ * are ignored. Every setting stores the same bytes. */
+int xs_combine_send(const xs_ep_layer* L, const xs_pacing* pacing, int32_t* dev_status, void* stream);
 
 /* Combine-reduce: out[t] = bf16(sum_{j<k} w[t][j] * C[t*k + j]), fp32 sum in ascending j.
  *   cbuf device bf16 [T*k][H] (row stride cbuf_stride_bytes), topk_w device fp32 [T][k],
@@ -349,6 +353,27 @@ int xs_fused_ep_layer(const xs_ep_layer* L, const xs_pacing* pacing, const xs_tr
 int xs_gemm(const void* a, int64_t lda, const void* b, int64_t ldb, void* c, int64_t ldc,
             int32_t M, int32_t N, int32_t K, const xs_trace* trace, void* stream);
 
+/* Grouped GEMM over row segments (the local-expert grouped GEMM of Sec. 4.3 as a library
+ * call, with the Linear-1 SwiGLU epilogue of the expert FFN): for every segment s, rows
+ * [seg_offsets[s], seg_offsets[s] + seg_rows[s]) of a times B_s^T, B_s = b + s N K elements, into
+ * the same rows of c, fp32 accumulation, bf16 output:
+ *   XS_EPI_STORE   c bf16 [M][N] (row stride ldc elements): c = bf16(a B_s^T)
+ *   XS_EPI_SWIGLU  B_s holds the gate rows [0, N / 2) then the up rows [N / 2, N); c bf16
+ *                  [M][N / 2]: c = bf16(silu(a Wg^T) * (a Wu^T))
+ *   a         device bf16 [M][K], row stride lda elements
+ *   seg_offsets, seg_rows  device int32 [n_seg] (n_seg <= 1024): a segment may be empty; one
+ *             that does not lie inside [0, M) sets XS_EBADINPUT in dev_status and is skipped;
+ *             overlapping segments race on their common rows
+ *   b         device bf16 [n_seg][N][K] (output-major, K-contiguous)
+ * Rows outside every segment are not written. Requires K % 64 == 0, N % 256 == 0 (STORE) or
+ * N % 256 == 0 (SWIGLU: 128 output columns per tile), lda and ldc multiples of 8. Returns
+ * XS_EINVAL / XS_EUNSUPPORTED on bad arguments (nothing launched), XS_EHIP if the launch fails.
+ * The caller owns every buffer; nothing is allocated. */
+enum { XS_EPI_STORE = 0, XS_EPI_SWIGLU = 1 };
+int xs_grouped_gemm(const void* a, int64_t lda, int32_t M, const int32_t* seg_offsets, const int32_t* seg_rows,
+                    int32_t n_seg, const void* b, int32_t N, int32_t K, void* c, int64_t ldc, int32_t epilogue,
+                    int32_t* dev_status, void* stream);
+
 /* GEMM with a scatter epilogue: every output tile is stored on completion into the
  * destination windows (no separate permutation pass).
  *   XS_SCATTER_ROW_BLOCK  (Sec. 4.5, row-parallel TP): output row m goes to window
@@ -370,9 +395,21 @@ typedef struct xs_scatter_desc {
   int32_t n_proj, n_heads, head_dim, heads_per_group;
 } xs_scatter_desc;
 
+/* pacing (nullable) sets the order in which the persistent producers take tiles, and so the
+ * bursts the windows see (Sec. 4.5: aligned producers push V_n = K_act B_c, with B_c one
+ * 256 x 256 bf16 tile of 128 KiB; chunking makes bursts smaller but more frequent):
+ *   NULL                  tiles in groups of 4 M-tiles (the L2-friendly order)
+ *   XS_POLICY_BURST       destination-major: every tile of window 0, then of window 1, ...
+ *   XS_POLICY_INTERLEAVE  round robin over the windows, one tile each
+ *   XS_POLICY_CHUNK       chunk_tiles consecutive tiles of one window, then the next window
+ *                         (the tiles per window must be a multiple of chunk_tiles)
+ * plus max_producers (grid cap, 0 = one workgroup per CU) and gap_ns (a non-injecting wait
+ * after every tile's stores); the other fields are ignored. With a pacing order, HEAD_GROUP
+ * needs tile-aligned groups ((n_heads head_dim) % 256 == 0, (heads_per_group head_dim) % 256
+ * == 0, 256 % head_dim == 0), else XS_EUNSUPPORTED. Every order stores the same bytes. */
 int xs_gemm_scatter(const void* a, int64_t lda, const void* b, int64_t ldb, int32_t M, int32_t N,
                     int32_t K, const xs_scatter_desc* desc, const xs_window* win, int32_t W,
-                    const xs_trace* trace, void* stream);
+                    const xs_pacing* pacing, const xs_trace* trace, void* stream);
 
 /* Serial counterpart of xs_gemm_scatter: a separate permutation pass that copies a plain
  * GEMM output c [M][N] into the windows with the same mapping (the "permutation before the

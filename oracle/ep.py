@@ -31,7 +31,7 @@ SENTINEL_BF16 = np.uint16(0xFFFF)  # a NaN pattern no correct kernel ever writes
 
 __all__ = [
     "bf16_bits_to_f64", "round_bf16", "f64_to_bf16_bits", "route_topk_softmax",
-    "dispatch_layout", "dispatch", "expert_ffn", "grouped_ffn", "combine_send",
+    "dispatch_layout", "dispatch", "expert_ffn", "grouped_gemm", "grouped_ffn", "combine_send",
     "combine_reduce", "ep_layer", "ep_layer_dense", "encode_row_src", "decode_row_src",
 ]
 
@@ -219,6 +219,36 @@ def expert_ffn(x_bits: np.ndarray, w1_bits: np.ndarray, w2_bits: np.ndarray):
     h = round_bf16(silu * u)
     y64 = h @ W2.T
     return f64_to_bf16_bits(h), y64, f64_to_bf16_bits(y64)
+
+
+def grouped_gemm(a_bits: np.ndarray, seg_offsets, seg_rows, b_bits: np.ndarray, swiglu: bool = False):
+    """Grouped GEMM over row segments (the local-expert grouped GEMM of Sec. 4.3): rows
+    [seg_offsets[s], seg_offsets[s] + seg_rows[s]) of A times segment s's own B_s^T
+    (b_bits [n_seg][N][K]). Plain: C = A B_s^T. SwiGLU: B_s's rows [0, N/2) are the gate and
+    [N/2, N) the up projection, C = silu(A Wg^T) * (A Wu^T). In fp64 from the bf16 operands.
+    Returns (c64 [M][N or N/2] with NaN in rows outside every segment, c bits with the sentinel
+    there)."""
+    A = bf16_bits_to_f64(a_bits)
+    M = A.shape[0]
+    n_out = b_bits.shape[1] // 2 if swiglu else b_bits.shape[1]
+    c64 = np.full((M, n_out), np.nan)
+    for s, (o, r) in enumerate(zip(seg_offsets, seg_rows)):
+        o, r = int(o), int(r)
+        if r == 0:
+            continue
+        B = bf16_bits_to_f64(b_bits[s])
+        X = A[o:o + r]
+        if swiglu:
+            g = X @ B[:n_out].T
+            u = X @ B[n_out:].T
+            with np.errstate(over="ignore"):
+                c64[o:o + r] = g / (1.0 + np.exp(-g)) * u
+        else:
+            c64[o:o + r] = X @ B.T
+    bits = np.full(c64.shape, SENTINEL_BF16, dtype=np.uint16)
+    inside = ~np.isnan(c64[:, 0]) if n_out else np.zeros(M, bool)
+    bits[inside] = f64_to_bf16_bits(c64[inside])
+    return c64, bits
 
 
 def grouped_ffn(windows: np.ndarray, layout: dict, w1_bits: np.ndarray, w2_bits: np.ndarray,

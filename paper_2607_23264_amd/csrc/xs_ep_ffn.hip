@@ -631,20 +631,44 @@ __global__ __launch_bounds__(256) void ep_identity_kernel(EpArgs a, const int* _
   }
 }
 
-// Unfused combine-send: computed row -> combine window of its source.
+// Unfused combine-send: computed row -> combine window of its source. Each workgroup is one
+// producer issuing bursts of `burst_rows` consecutive computed rows (burst b of producer g is
+// rows [(g + b G) burst_rows, ... + burst_rows)), optionally followed by a non-injecting gap.
+// A wave copies one row at a time with up to 8 16-byte loads in flight per lane before their
+// stores.
 __global__ __launch_bounds__(256) void ep_combine_send_kernel(EpArgs a, const int* __restrict__ dest_counts,
-                                                              int n_cwin) {
+                                                              int n_cwin, int burst_rows) {
   __shared__ int base[XS_MAX_WINDOWS + 1];
-  const int lane = threadIdx.x & 63;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int total = window_prefix(a, dest_counts, n_cwin, base);
-  for (int gr = blockIdx.x * 4 + (threadIdx.x >> 6); gr < total; gr += gridDim.x * 4) {
-    int dl = 0;
-    while (base[dl + 1] <= gr) ++dl;
-    const int r = gr - base[dl];
-    u32x4* dst = reinterpret_cast<u32x4*>(combine_row(a, dl, r));
-    if (!dst) continue;
-    const u32x4* src = reinterpret_cast<const u32x4*>(a.y + static_cast<int64_t>(gr) * a.H);
-    for (int pc = lane; pc < a.H / 8; pc += 64) dst[pc] = src[pc];
+  const int npc = a.H / 8;   // 16-byte pieces per row
+  for (int b0 = blockIdx.x * burst_rows; b0 < total; b0 += gridDim.x * burst_rows) {
+    const int b1 = min(total, b0 + burst_rows);
+    for (int gr = b0 + wv; gr < b1; gr += 4) {
+      int dl = 0;
+      while (base[dl + 1] <= gr) ++dl;
+      u32x4* dst = reinterpret_cast<u32x4*>(combine_row(a, dl, gr - base[dl]));
+      if (!dst) continue;
+      const u32x4* src = reinterpret_cast<const u32x4*>(a.y + static_cast<int64_t>(gr) * a.H);
+      for (int p0 = 0; p0 < npc; p0 += 8 * 64) {
+        u32x4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int pc = p0 + u * 64 + lane;
+          if (pc < npc) v[u] = __builtin_nontemporal_load(src + pc);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int pc = p0 + u * 64 + lane;
+          if (pc < npc) dst[pc] = v[u];
+        }
+      }
+    }
+    if (a.gap_ticks) {
+      __syncthreads();
+      if (threadIdx.x == 0) spin_ticks(static_cast<uint64_t>(a.gap_ticks));
+      __syncthreads();
+    }
   }
 }
 
@@ -914,11 +938,15 @@ extern "C" int xs_expert_ffn(const xs_ep_layer* L, void* workspace, int64_t work
   return record_event(L, XS_EV_FFN_END, st);
 }
 
-extern "C" int xs_combine_send(const xs_ep_layer* L, int32_t* dev_status, void* stream) {
+extern "C" int xs_combine_send(const xs_ep_layer* L, const xs_pacing* pacing, int32_t* dev_status,
+                               void* stream) {
   int rc = validate(L, false);
   if (rc) return rc;
   if (is_mx(L)) return XS_EUNSUPPORTED;
   if (!L->y_ws) return XS_EINVAL;
+  if (pacing && (pacing->max_producers < 0 || pacing->chunk_tiles < 0 || pacing->gap_ns < 0 ||
+                 pacing->reserved != 0))
+    return XS_EINVAL;
   hipStream_t st = static_cast<hipStream_t>(stream);
   EpArgs a;
   WinSet dws, cws;
@@ -926,8 +954,13 @@ extern "C" int xs_combine_send(const xs_ep_layer* L, int32_t* dev_status, void* 
   rc = fill_args(L, dummy, &a, &dws, &cws);
   if (rc) return rc;
   a.status = dev_status;
-  hipLaunchKernelGGL(ep_combine_send_kernel, dim3(2048), dim3(256), 0, st, a, L->dest_counts,
-                     n_cwin_of(L));
+  // producers: max_producers workgroups (default eight per CU); a burst is chunk_tiles blocks of
+  // 256 rows (default 64 rows)
+  const int grid = pacing && pacing->max_producers > 0 ? pacing->max_producers : 8 * xs_host::persistent_grid(0);
+  const int burst_rows = pacing && pacing->chunk_tiles > 0 ? pacing->chunk_tiles * kBM : 64;
+  a.gap_ticks = pacing ? xs_host::ns_to_ticks(pacing->gap_ns) : 0;
+  hipLaunchKernelGGL(ep_combine_send_kernel, dim3(grid), dim3(256), 0, st, a, L->dest_counts,
+                     n_cwin_of(L), burst_rows);
   if (xs_host::launch_status()) return XS_EHIP;
   return xs_host::signal_windows(cws, st);
 }

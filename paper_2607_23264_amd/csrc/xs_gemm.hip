@@ -14,7 +14,45 @@ struct ScatterArgs {
   int rpd;
   int n_proj, n_heads, head_dim, hpg;
   int group_aligned;   // every 256-column tile lies inside one projection and one head group
+  // store pacing: order 0 = the L2-grouped order; 1 = destination-major (Expert-Wave-like
+  // bursts: every tile of window 0, then window 1, ...); 2 = `chunk` consecutive tiles of one
+  // window, then the next window (chunk 1 = round robin over the windows)
+  int order, chunk, n_dest;
+  int64_t gap_ticks;   // non-injecting wait after every tile's stores
 };
+
+// Tile j of destination d's tiles: a row block's M-tiles walked down then across (ROW_BLOCK),
+// or every M-tile of each of the group's column tiles, projection by projection (HEAD_GROUP).
+__device__ __forceinline__ void dest_tile(const ScatterArgs& sa, int kind_head, int tm, int d, int j, int* mb,
+                                          int* nb) {
+  if (!kind_head) {
+    const int mpd = sa.rpd / kBM;
+    *mb = d * mpd + j % mpd;
+    *nb = j / mpd;
+  } else {
+    const int cpg = sa.hpg * sa.head_dim / kBN;          // column tiles of one group per projection
+    const int per_proj = sa.n_heads * sa.head_dim / kBN;
+    *mb = j % tm;
+    const int rest = j / tm;
+    *nb = (rest / cpg) * per_proj + d * cpg + rest % cpg;
+  }
+}
+
+// Work index -> tile under the pacing order (order 0 handled by grouped_tile).
+__device__ __forceinline__ void paced_tile(const ScatterArgs& sa, int kind_head, int w, int tm, int ntiles,
+                                           int* mb, int* nb) {
+  const int W = sa.n_dest, td = ntiles / W;
+  int d, j;
+  if (sa.order == 1) {
+    d = w / td;
+    j = w - d * td;
+  } else {
+    const int c = sa.chunk, blk = w / (W * c), r = w - blk * W * c;
+    d = r / c;
+    j = blk * c + (r - d * c);
+  }
+  dest_tile(sa, kind_head, tm, d, j, mb, nb);
+}
 
 // Instance id with consecutive ids on one XCD: workgroups are dealt to the 8 XCDs round
 // robin, so block b runs on XCD b % 8.
@@ -76,7 +114,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tiles_kernel(
   const int G = gridDim.x;
   for (int t = xcd_instance(blockIdx.x, G); t < ntiles; t += G) {
     int mb, nb;
-    grouped_tile(t, tm, tn, &mb, &nb);
+    if (KIND != KIND_PLAIN && sa.order)
+      paced_tile(sa, KIND == KIND_HEAD_GROUP, t, tm, ntiles, &mb, &nb);
+    else
+      grouped_tile(t, tm, tn, &mb, &nb);
     const int m0 = mb * kBM, n0 = nb * kBN;
     const int rows = min(kBM, M - m0);
     const uint64_t t0 = tr.buf ? wall_ticks() : 0;
@@ -130,6 +171,101 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tiles_kernel(
     }
     lds_barrier();   // output tiles are read only after the kernel
     if (tr.buf && tid == 0) trace_tile(tr, 3, t, t0, t1, wall_ticks());
+    if (KIND != KIND_PLAIN && sa.gap_ticks) {
+      if (tid == 0) spin_ticks(static_cast<uint64_t>(sa.gap_ticks));   // non-injecting gap
+      __syncthreads();
+    }
+  }
+}
+
+// Grouped GEMM over row segments: segment s multiplies rows [seg_off[s], seg_off[s] + rows) of A
+// by its own weight B_s ([N][K], K-contiguous) into the same rows of C. Tiles are numbered
+// segment by segment (ceil(rows / 256) row blocks x nt column tiles each); a workgroup maps its
+// tile number to (segment, block, column) with a wave scan over the segment counts, 64
+// segments at a time, so no plan or workspace is needed. SWIGLU: B_s holds the gate rows
+// [0, N / 2) and the up rows [N / 2, N); a column tile computes 128 gate and 128 up columns
+// and stores 128 columns of silu(g) u.
+__device__ __forceinline__ bool grouped_tile_of(int t, const int* __restrict__ seg_off,
+                                                const int* __restrict__ seg_rows, int n_seg, int M,
+                                                int nt, int* status, int* out) {
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    int base = 0, found = 0;
+    for (int s0 = 0; s0 < n_seg; s0 += 64) {
+      const int sg = s0 + lane;
+      int tiles = 0;
+      if (sg < n_seg) {
+        int r = seg_rows[sg];
+        const int o = seg_off[sg];
+        if (r < 0 || o < 0 || static_cast<int64_t>(o) + r > M) {
+          if (r != 0) set_status(status, XS_EBADINPUT);
+          r = 0;
+        }
+        tiles = ((r + kBM - 1) / kBM) * nt;
+      }
+      int incl = tiles;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const int v = __shfl_up(incl, off);
+        if (lane >= off) incl += v;
+      }
+      const int total = __shfl(incl, 63);
+      if (t < base + total) {
+        const bool mine = t >= base + incl - tiles && t < base + incl;
+        const unsigned long long m = __ballot(mine);
+        if (lane == __ffsll(static_cast<long long>(m)) - 1) {
+          out[0] = sg;
+          out[1] = t - (base + incl - tiles);
+        }
+        found = 1;
+        break;
+      }
+      base += total;
+    }
+    if (lane == 0 && !found) out[0] = -1;
+  }
+  __syncthreads();
+  const bool ok = out[0] >= 0;
+  return ok;
+}
+
+template <bool SWIGLU>
+__global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(
+    const uint16_t* __restrict__ A, int64_t lda, int M, const int* __restrict__ seg_off,
+    const int* __restrict__ seg_rows, int n_seg, const uint16_t* __restrict__ B, int N, int K,
+    char* __restrict__ C, int64_t ldc_bytes, int* status) {
+  __shared__ __attribute__((aligned(16))) char smem[kLdsBytes];
+  char* lds = smem;
+  char** rowptr = reinterpret_cast<char**>(smem + kLdsRowPtrOff);
+  int* misc = reinterpret_cast<int*>(smem + kLdsMiscOff);
+  const int tid = threadIdx.x;
+  const int nt = SWIGLU ? (N / 2) / (kBN / 2) : N / kBN;
+  for (int t = blockIdx.x;; t += gridDim.x) {
+    const bool more = grouped_tile_of(t, seg_off, seg_rows, n_seg, M, nt, status, misc);
+    const int sg = misc[0], local = misc[1];
+    __syncthreads();   // every thread has read the mapping before the mainloop reuses the LDS
+    if (!more) break;
+    const int mb = local / nt, nb = local - mb * nt;
+    const int m0 = seg_off[sg] + mb * kBM;
+    const int rows = min(kBM, seg_rows[sg] - mb * kBM);
+    const uint16_t* Bs = B + static_cast<int64_t>(sg) * N * K;
+    Acc acc;
+    if (SWIGLU) {
+      gemm_mainloop(A + static_cast<int64_t>(m0) * lda, lda, rows, Bs, K, nb * (kBN / 2), N / 2, true, K, acc, lds);
+      if (tid < rows)
+        rowptr[tid] = C + static_cast<int64_t>(m0 + tid) * ldc_bytes + static_cast<int64_t>(nb) * (kBN / 2) * 2;
+      stage_swiglu(acc, lds);
+      __syncthreads();
+      store_rows(lds, kEpiPitchH, kBN / 2, rows, rowptr);
+    } else {
+      gemm_mainloop(A + static_cast<int64_t>(m0) * lda, lda, rows, Bs, K, nb * kBN, 0, false, K, acc, lds);
+      if (tid < rows)
+        rowptr[tid] = C + static_cast<int64_t>(m0 + tid) * ldc_bytes + static_cast<int64_t>(nb) * kBN * 2;
+      stage_tile(acc, lds);
+      __syncthreads();
+      store_rows(lds, kEpiPitch, kBN, rows, rowptr);
+    }
+    lds_barrier();   // the output rows are read only after the kernel
   }
 }
 
@@ -239,8 +375,8 @@ static int scatter_setup(const xs_scatter_desc* desc, int32_t M, int32_t N, cons
 
 extern "C" int xs_gemm_scatter(const void* a, int64_t lda, const void* b, int64_t ldb, int32_t M,
                                int32_t N, int32_t K, const xs_scatter_desc* desc,
-                               const xs_window* win, int32_t W, const xs_trace* trace,
-                               void* stream) {
+                               const xs_window* win, int32_t W, const xs_pacing* pacing,
+                               const xs_trace* trace, void* stream) {
   if (!a || !b) return XS_EINVAL;
   if (!gemm_shape_ok(lda, ldb, M, N, K)) return XS_EUNSUPPORTED;
   ScatterArgs sa;
@@ -248,10 +384,31 @@ extern "C" int xs_gemm_scatter(const void* a, int64_t lda, const void* b, int64_
   int kind = 0;
   int rc = scatter_setup(desc, M, N, win, W, &sa, &ws, &kind);
   if (rc) return rc;
+  int max_producers = 0;
+  if (pacing) {
+    if (pacing->max_producers < 0 || pacing->gap_ns < 0 || pacing->chunk_tiles < 0 || pacing->reserved != 0)
+      return XS_EINVAL;
+    max_producers = pacing->max_producers;
+    sa.gap_ticks = xs_host::ns_to_ticks(pacing->gap_ns);
+    sa.n_dest = W;
+    const int ntiles = ((M + kBM - 1) / kBM) * (N / kBN);
+    const int pol = pacing->policy;
+    if (pol == XS_POLICY_BURST) {
+      sa.order = 1;
+    } else if (pol == XS_POLICY_INTERLEAVE || pol == XS_POLICY_CHUNK) {
+      sa.order = 2;
+      sa.chunk = pol == XS_POLICY_CHUNK && pacing->chunk_tiles > 0 ? pacing->chunk_tiles : 1;
+      if ((ntiles / W) % sa.chunk) return XS_EINVAL;   // a chunk never spans two windows' lists
+    } else {
+      return XS_EINVAL;
+    }
+    // orders over destinations need each tile inside one window (head groups tile-aligned)
+    if (kind == KIND_HEAD_GROUP && !sa.group_aligned) return XS_EUNSUPPORTED;
+  }
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (M > 0) {
     const int tiles = ((M + kBM - 1) / kBM) * (N / kBN);
-    const int grid = std::min(tiles, xs_host::persistent_grid(0));
+    const int grid = std::min(tiles, xs_host::persistent_grid(max_producers));
     if (kind == KIND_ROW_BLOCK)
       hipLaunchKernelGGL(gemm_tiles_kernel<KIND_ROW_BLOCK>, dim3(grid), dim3(kThreads), 0, st,
                          static_cast<const uint16_t*>(a), lda, static_cast<const uint16_t*>(b), ldb,
@@ -263,6 +420,29 @@ extern "C" int xs_gemm_scatter(const void* a, int64_t lda, const void* b, int64_
     if (xs_host::launch_status()) return XS_EHIP;
   }
   return xs_host::signal_windows(ws, st);
+}
+
+extern "C" int xs_grouped_gemm(const void* a, int64_t lda, int32_t M, const int32_t* seg_offsets,
+                               const int32_t* seg_rows, int32_t n_seg, const void* b, int32_t N,
+                               int32_t K, void* c, int64_t ldc, int32_t epilogue, int32_t* dev_status,
+                               void* stream) {
+  if (!a || !b || !c || !seg_offsets || !seg_rows || M < 0 || n_seg < 0 || n_seg > 1024) return XS_EINVAL;
+  if (epilogue != XS_EPI_STORE && epilogue != XS_EPI_SWIGLU) return XS_EINVAL;
+  const int n_out = epilogue == XS_EPI_SWIGLU ? N / 2 : N;
+  if (N <= 0 || K <= 0 || K % kBK || lda < K || lda % 8 || ldc < n_out || ldc % 8) return XS_EUNSUPPORTED;
+  if (epilogue == XS_EPI_STORE ? N % kBN : (N % 2 || (N / 2) % (kBN / 2))) return XS_EUNSUPPORTED;
+  if (M == 0 || n_seg == 0) return XS_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int grid = xs_host::persistent_grid(0);
+  if (epilogue == XS_EPI_SWIGLU)
+    hipLaunchKernelGGL(grouped_gemm_kernel<true>, dim3(grid), dim3(kThreads), 0, st,
+                       static_cast<const uint16_t*>(a), lda, M, seg_offsets, seg_rows, n_seg,
+                       static_cast<const uint16_t*>(b), N, K, static_cast<char*>(c), ldc * 2, dev_status);
+  else
+    hipLaunchKernelGGL(grouped_gemm_kernel<false>, dim3(grid), dim3(kThreads), 0, st,
+                       static_cast<const uint16_t*>(a), lda, M, seg_offsets, seg_rows, n_seg,
+                       static_cast<const uint16_t*>(b), N, K, static_cast<char*>(c), ldc * 2, dev_status);
+  return xs_host::launch_status();
 }
 
 extern "C" int xs_scatter_copy(const void* c, int64_t ldc, int32_t M, int32_t N,

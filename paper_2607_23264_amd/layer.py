@@ -243,8 +243,9 @@ class EPLayer:
         X.check(X.xs_expert_ffn(C.byref(self.L), ws.data_ptr(), ws.numel(), self.status.data_ptr(),
                                 self.stream), "expert_ffn")
 
-    def combine_send(self):
-        X.check(X.xs_combine_send(C.byref(self.L), self.status.data_ptr(), self.stream), "combine_send")
+    def combine_send(self, pacing: X.xs_pacing | None = None):
+        X.check(X.xs_combine_send(C.byref(self.L), C.byref(pacing) if pacing is not None else None,
+                                  self.status.data_ptr(), self.stream), "combine_send")
 
     def combine_reduce(self):
         s = self.s

@@ -1,24 +1,27 @@
-"""Slow-sink pacing sweep (post-issue backpressure on a real slow path).
+"""Store pacing against a slow sink: the EP layer with combine windows in host-coherent memory.
 
-The EP layer's combine windows are placed in fine-grained host-coherent memory
-(hipHostMalloc coherent), so the Linear-2 epilogue stores (the bursts of Sec. 4.3) drain
-across the host link; the same layer with HBM combine windows is the local-memory control
-(Sec. 3.1). Layers:
-  * tiny: T=256, H=512, 8 experts, top-2, I=1024, 4 windows (512 KiB of combine stores);
-  * tiny_T32768: the same dimensions at 32768 tokens (64 MiB of combine stores), enough to
-    exceed the sink's post-issue capacity.
-First both sinks are calibrated with the remote-store microbenchmark (calibrate.py). Then, for
-each policy (Expert-Wave burst issue, Alg. 1 interleave at the anti-starvation lead,
-chunked bursts, the model-driven AUTO) and producer cap, the fused layer is timed with HIP
-events around the persistent kernel and its device trace gives every Linear-2 tile's issue
-span (mainloop end -> last store issued):
-  (interleave_dyn: the same rule with tiles claimed from shared counters, XS_CLAIM_DYNAMIC)
-  * measured stall = sum over tiles of [span - median span of the HBM control]_+, and its
-    share of the producers' time (stall / (producers x kernel time));
-  * predicted stall = xs_model_predict (Eqs. 3-6) on the burst sequence reconstructed from
-    the trace (epilogues with overlapping issue intervals form one burst of their bytes; G
-    is the gap to the next burst) with the calibrated host-sink (T0, R) and the capacity at
-    the lower end of the measured knee bracket, weighted by the tiles in each burst.
+The Linear-2 epilogue stores (the bursts of Sec. 4.3) of the combine windows placed in
+fine-grained host-coherent memory (hipHostMalloc coherent) drain across the host link; the same
+layer with every window in HBM is the local-memory control (Sec. 3.1). Two layers:
+  * tiny (the c1 dimensions: T=256, H=512, 8 experts, top-2, I=1024, 4 windows), every combine
+    window on the sink: 512 KiB of combine stores per layer, swept over chunk sizes and producer
+    caps;
+  * the DeepSeek-V3-like share with two of its eight source windows on the sink (a quarter of
+    the combine bytes), uniform and Zipf(1.2) routing: Eq. 9 holds at the sink's drain rate, and
+    the skewed routing gives the long runs of aligned Linear-2 epilogues the paper describes.
+Per policy (Expert-Wave burst, cross-wave interleave at the anti-starvation lead, chunked, and
+AUTO with the calibrated model):
+  * kernel time (HIP events around the persistent kernel, median of repetitions), on the sink
+    and on the HBM control;
+  * measured issue stall: from one traced run (ext records), the sum over Linear-2 tiles of the
+    epilogue issue span beyond the HBM control's median span, per producer; the staging wait
+    (App. A.2's MMA-side wait on this design: the first wave's wait before the next mainloop for
+    its previous stores); the dependency waits and the mainloop time against the control;
+  * predicted stall: the library's audit of the same order (xs_pacing_audit_run: the schedule's
+    aligned bursts through the backlog recurrence and capacity guard) with the calibrated sink
+    model and the mainloop times of the HBM control's trace (xs_trace_tile_times).
+This module only allocates, launches and takes sums and medians of trace timestamps; the model
+arithmetic runs in the library.
 Usage: python -m paper_2607_23264_amd.slow_sink [--out FILE] [--quick]
 """
 from __future__ import annotations
@@ -41,46 +44,6 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def trace_l2(buf, cnt, rate):
-    n = min(int(cnt.item()), buf.shape[0])
-    r = buf[:n].cpu().numpy().astype(np.int64)
-    l2 = r[(r[:, 0] >> 56) == 2]
-    us = 1e6 / rate
-    t_origin = r[:, 1].min()
-    return (l2[:, 2] - t_origin) * us, (l2[:, 3] - l2[:, 2]) * us, (r[:, 3].max() - t_origin) * us
-
-
-def bursts_from_trace(start, span, bytes_per_tile):
-    """Epilogues whose issue intervals overlap form one burst: (V, issue span, gap after)."""
-    order = np.argsort(start)
-    s, e = start[order], start[order] + span[order]
-    groups = []
-    g0, gend, n = s[0], e[0], 1
-    for i in range(1, len(s)):
-        if s[i] <= gend:
-            gend = max(gend, e[i])
-            n += 1
-        else:
-            groups.append((g0, gend, n))
-            g0, gend, n = s[i], e[i], 1
-    groups.append((g0, gend, n))
-    out = []
-    for i, (a, b, n) in enumerate(groups):
-        nxt = groups[i + 1][0] if i + 1 < len(groups) else b
-        out.append((n * bytes_per_tile, b - a, max(0.0, nxt - b)))
-    return out
-
-
-def predicted_stall(model: X.xs_model, bursts, bytes_per_tile) -> float:
-    """Producer-time stall: each burst's predicted excess issue time (Eqs. 3-6 and the stalled
-    reading) times the number of tiles (producers) that issued it."""
-    n = len(bursts)
-    arr = (X.xs_burst * n)(*[X.xs_burst(V, model.t0_a_us + model.t0_b_us_per_byte * V, G) for V, _, G in bursts])
-    out = (X.xs_burst_pred * n)()
-    X.check(X.xs_model_predict(C.byref(model), arr, n, 0.0, out), "model_predict")
-    return float(sum(o.stall_us * (b[0] / bytes_per_tile) for o, b in zip(out, bursts)))
-
-
 def calibrate_sinks(K, Bs, store_waves, target_bytes=1 << 30):
     host = HostCoherent(target_bytes)
     hbm = torch.empty(target_bytes // 2, dtype=torch.int16, device="cuda")
@@ -92,60 +55,240 @@ def calibrate_sinks(K, Bs, store_waves, target_bytes=1 << 30):
     return ch, cd
 
 
-def sweep_layer(cfg, host_model, caps, chunks, reps, rate):
-    import synth
-    inp = synth.ep_inputs(cfg, 0)
-    s = Shape(cfg.n_src, cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.W, 0, cfg.E)
-    tile_bytes = (cfg.T * cfg.k // cfg.E) * 256 * 2   # rows of an expert's M-block x 256 columns
-    tile_bytes = min(tile_bytes, 256 * 256 * 2)
-    P1 = cfg.I // 128
-    configs = [("burst", X.XS_POLICY_BURST, 0, 0, 0)]
-    configs += [(f"chunk{c}", X.XS_POLICY_CHUNK, c, 0, 0) for c in chunks]
-    configs += [("interleave", X.XS_POLICY_INTERLEAVE, 0, 0, 0), ("interleave_4xlead", X.XS_POLICY_INTERLEAVE, 0, 4, 0),
-                ("auto", X.XS_POLICY_AUTO, 0, 0, 0), ("interleave_dyn", X.XS_POLICY_INTERLEAVE, 0, 0, 1)]
-    results, control = [], {}
-    for where in ("hbm", "host"):
-        lay = EPLayer(s, combine_host=(where == "host"))
-        lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
-        buf = torch.zeros((16384, 4), dtype=torch.int64, device="cuda")
+class Traced:
+    """A traced run's records (with ext records) on the host."""
+
+    def __init__(self, lay: EPLayer, pol: X.xs_pacing, cap_records: int = 65536):
+        buf = torch.zeros((cap_records, 4), dtype=torch.int64, device="cuda")
+        ext = torch.zeros((cap_records, 4), dtype=torch.int64, device="cuda")
         cnt = torch.zeros((1,), dtype=torch.int32, device="cuda")
-        e0, e1 = X.HipEvents(1), X.HipEvents(1)
-        for cap in caps:
-            for name, pol, chunk, lead_mult, claim in configs:
-                knee = -(-(cap or 256) // P1)          # App. A.2 anti-starvation lead
-                p = pacing(pol, lead=lead_mult * knee, chunk=chunk, max_producers=cap,
-                           model=host_model if pol == X.XS_POLICY_AUTO else None, claim=claim)
-                times = []
-                for _ in range(reps):
-                    cnt.zero_()
-                    lay.L.events[X.XS_EV_FFN], lay.L.events[X.XS_EV_FFN_END] = e0.ev[0], e1.ev[0]
-                    lay.fused(p, X.xs_trace(buf.data_ptr(), buf.shape[0], cnt.data_ptr()))
-                    torch.cuda.synchronize()
-                    times.append(X.HipEvents.elapsed_ms_pair(e0.ev[0], e1.ev[0]) * 1e3)
-                lay.L.events[X.XS_EV_FFN], lay.L.events[X.XS_EV_FFN_END] = None, None
-                if int(lay.status.item()):
-                    raise RuntimeError(f"device status {int(lay.status.item())}")
-                start, span, kern_us = trace_l2(buf, cnt, rate)
-                if where == "hbm":
-                    control[(cap, name)] = float(np.median(span))
-                meas = float(np.maximum(0.0, span - control[(cap, name)]).sum())
-                pred = predicted_stall(host_model, bursts_from_trace(start, span, tile_bytes), tile_bytes) \
-                    if where == "host" else None
-                row = {"layer": cfg.name, "sink": where, "policy": name, "chunk": chunk,
-                       "max_producers": cap or 256, "kernel_us_median": float(np.median(times)),
-                       "kernel_us_p10": float(np.percentile(times, 10)),
-                       "kernel_us_p90": float(np.percentile(times, 90)),
-                       "l2_span_us_median": float(np.median(span)), "l2_span_us_p90": float(np.percentile(span, 90)),
-                       # share of the producers' kernel time spent in issue beyond the control
-                       "stall_measured_us": meas, "stall_fraction": meas / max((cap or 256) * kern_us, 1e-9),
-                       "stall_predicted_us": pred}
-                results.append(row)
-                log(f"[slow-sink] {cfg.name} {where} cap={cap or 256} {name}: {row['kernel_us_median']:.1f} us, "
-                    f"span med {row['l2_span_us_median']:.2f} p90 {row['l2_span_us_p90']:.2f} us, "
-                    f"stall {meas:.1f} us, pred {pred}")
+        lay.fused(pol, X.xs_trace(buf.data_ptr(), buf.shape[0], cnt.data_ptr(), ext.data_ptr()))
+        torch.cuda.synchronize()
+        n = min(int(cnt.item()), cap_records)
+        self.r = np.ascontiguousarray(buf[:n].cpu().numpy().astype(np.uint64))
+        self.x = np.ascontiguousarray(ext[:n].cpu().numpy().astype(np.uint64))
+        self.n = n
+        us = 1e6 / X.xs_clock_rate_hz()
+        r = self.r.astype(np.int64)
+        x = self.x.astype(np.int64)
+        self.kind = r[:, 0] >> 56
+        self.issue_us = (r[:, 3] - r[:, 2]) * us
+        self.stage_us = x[:, 1] * us
+        self.dep_us = (x[:, 0] - r[:, 1]) * us
+        self.main_us = (r[:, 2] - x[:, 0]) * us
+
+    def tile_times(self, min_rows: int = 0):
+        t1, t2, t3 = C.c_double(), C.c_double(), C.c_double()
+        X.check(X.xs_trace_tile_times(self.r.ctypes.data, self.x.ctypes.data, self.n, min_rows, C.byref(t1),
+                                      C.byref(t2), C.byref(t3)), "trace_tile_times")
+        return t1.value, t2.value, t3.value
+
+
+def kernel_us(lay: EPLayer, pol: X.xs_pacing, reps: int) -> list:
+    ev = X.HipEvents(2)
+    lay.L.events[X.XS_EV_FFN], lay.L.events[X.XS_EV_FFN_END] = ev.ev[0], ev.ev[1]
+    out = []
+    for _ in range(reps):
+        lay.fused(pol)
+        torch.cuda.synchronize()
+        out.append(X.HipEvents.elapsed_ms_pair(ev.ev[0], ev.ev[1]) * 1e3)
+    lay.L.events[X.XS_EV_FFN], lay.L.events[X.XS_EV_FFN_END] = None, None
+    if int(lay.status.item()):
+        raise RuntimeError(f"device status {int(lay.status.item())}: {X.xs_strerror(int(lay.status.item())).decode()}")
+    return out
+
+
+def audit(lay: EPLayer, pol: X.xs_pacing) -> X.xs_pacing_audit:
+    au = X.xs_pacing_audit()
+    X.check(X.xs_pacing_audit_run(C.byref(lay.L), C.byref(pol), C.byref(au)), "pacing_audit")
+    return au
+
+
+POLICY_NAMES = {X.XS_POLICY_BURST: "burst", X.XS_POLICY_INTERLEAVE: "interleave", X.XS_POLICY_CHUNK: "chunk"}
+
+
+def evaluate(name: str, make_layer, policies: dict, model: X.xs_model, sink_share: float, reps: int,
+             claim: int = X.XS_CLAIM_DYNAMIC) -> dict:
+    """Every policy on the HBM control and on the sink layer: kernel time, measured and predicted
+    stall. make_layer(on_sink) returns an uploaded EPLayer; policies maps a name to
+    (policy, lead, chunk, max_producers)."""
+    out = {"layer": name, "sink_share": sink_share, "policies": {}}
+    control = {}                 # (policy, lead, chunk, producers) -> kernel time and trace
+    ctrl = make_layer(False)
+    counts = None
+    try:
+        s = ctrl.s
+        c = ctrl.expert_counts.sum(0).cpu().numpy()
+        counts = [int(v) for v in c[s.e_begin:s.e_begin + s.n_experts]]   # the layout's rows per local expert
+        for pname, (pol, lead, chunk, cap) in policies.items():
+            p = pacing(pol, lead=lead, chunk=chunk, max_producers=cap, claim=claim)
+            if pol == X.XS_POLICY_AUTO:
+                continue
+            times = kernel_us(ctrl, p, reps)
+            control[(pol, lead, chunk, cap)] = {"kernel_us": float(np.median(times)), "trace": Traced(ctrl, p)}
+        ref = next(v for k, v in control.items() if k[0] == X.XS_POLICY_INTERLEAVE)
+        tl1, tl2, _ = ref["trace"].tile_times(min_rows=0)
+        out["control_tile_times_us"] = {"T_L1": tl1, "T_L2": tl2}
+    finally:
+        ctrl.close()
+        del ctrl
+        torch.cuda.empty_cache()
+    lay = make_layer(True)
+    try:
+        for pname, (pol, lead, chunk, cap) in policies.items():
+            p = pacing(pol, lead=lead, chunk=chunk, max_producers=cap, claim=claim, model=model, t_l1_us=tl1,
+                       t_l2_us=tl2, expert_rows=counts, sink_share=sink_share)
+            au = audit(lay, p)
+            chosen = au.policy
+            times = kernel_us(lay, p, reps)
+            tr = Traced(lay, p)
+            G = au.producers
+            base = control.get((chosen, lead, au.chunk, cap))
+            ctr = base["trace"] if base else None
+            l2 = tr.kind == 2
+            if ctr is not None:
+                excess = np.maximum(0.0, tr.issue_us[l2] - float(np.median(ctr.issue_us[ctr.kind == 2])))
+                stage = np.maximum(0.0, tr.stage_us - float(np.median(ctr.stage_us)))
+                main_excess = float(tr.main_us.sum() - ctr.main_us.sum()) / G
+                dep_excess = float(tr.dep_us.sum() - ctr.dep_us.sum()) / G
+            else:
+                excess, stage, main_excess, dep_excess = tr.issue_us[l2] * 0, tr.stage_us * 0, 0.0, 0.0
+            k_us = float(np.median(times))
+            i = next(j for j in range(au.n_cand) if au.cand_policy[j] == chosen and au.cand_chunk[j] == au.chunk)
+            row = {"policy": POLICY_NAMES[chosen], "chunk": au.chunk, "lead_rows": au.lead_rows, "producers": G,
+                   "kernel_us": k_us, "kernel_us_p10": float(np.percentile(times, 10)),
+                   "kernel_us_p90": float(np.percentile(times, 90)),
+                   "control_kernel_us": base["kernel_us"] if base else None,
+                   "stall_measured_us_per_producer": float(excess.sum()) / G,
+                   "stall_predicted_us_per_producer": au.cand_stall_us[i],
+                   "mma_stall_predicted_us_per_producer": au.cand_mma_stall_us[i],
+                   "staging_wait_measured_us_per_producer": float(stage.sum()) / G,
+                   "stall_fraction_measured": float(excess.sum()) / G / k_us,
+                   "stall_fraction_predicted": au.cand_stall_us[i] / k_us,
+                   "l2_issue_us_median": float(np.median(tr.issue_us[l2])),
+                   "l2_issue_us_p90": float(np.percentile(tr.issue_us[l2], 90)),
+                   "mainloop_excess_us_per_producer": main_excess,
+                   "dependency_wait_excess_us_per_producer": dep_excess,
+                   "guard_failures_predicted": au.cand_guard_fail[i], "bursts_predicted": au.cand_bursts[i],
+                   "rate_feasible_eq9": bool(au.rate_feasible)}
+            if pol == X.XS_POLICY_AUTO:
+                row["auto_candidates"] = [{"policy": POLICY_NAMES[au.cand_policy[j]], "chunk": au.cand_chunk[j],
+                                           "stall_predicted_us": au.cand_stall_us[j]} for j in range(au.n_cand)]
+            out["policies"][pname] = row
+            log(f"[slow-sink] {name} {pname}: {k_us:.1f} us (control {row['control_kernel_us']}), stall measured "
+                f"{row['stall_measured_us_per_producer']:.1f} / predicted {row['stall_predicted_us_per_producer']:.1f} "
+                f"us per producer, staging {row['staging_wait_measured_us_per_producer']:.1f}")
+    finally:
+        lay.close()
         del lay
         torch.cuda.empty_cache()
-    return results
+    burst = out["policies"].get("burst")
+    if burst:
+        for row in out["policies"].values():
+            row["speedup_over_burst"] = burst["kernel_us"] / row["kernel_us"]
+    return out
+
+
+def tiny_layer(cfg, inp):
+    def make(on_sink: bool) -> EPLayer:
+        s = Shape(cfg.n_src, cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.W, 0, cfg.E)
+        lay = EPLayer(s, combine_host=on_sink)
+        lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
+        lay.route()
+        lay.layout()
+        torch.cuda.synchronize()
+        return lay
+    return make
+
+
+def share_layer(cfg, inp, host_sources):
+    def make(on_sink: bool) -> EPLayer:
+        experts = list(range(cfg.rank * cfg.E_local, (cfg.rank + 1) * cfg.E_local))
+        s = Shape(cfg.n_src, cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.W, experts[0], len(experts), src=cfg.rank)
+        lay = EPLayer(s, sentinel=False, host_combine_sources=host_sources if on_sink else None)
+        lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
+        lay.prefill_other_sources(inp["fill"])
+        return lay
+    return make
+
+
+def tiny_policies(caps, chunks):
+    pol = {}
+    for cap in caps:
+        suffix = f"_p{cap}" if cap else ""
+        pol[f"burst{suffix}"] = (X.XS_POLICY_BURST, 0, 0, cap)
+        pol[f"interleave{suffix}"] = (X.XS_POLICY_INTERLEAVE, 0, 0, cap)
+        for c in chunks:
+            pol[f"chunk{c}{suffix}"] = (X.XS_POLICY_CHUNK, 0, c, cap)
+        pol[f"auto{suffix}"] = (X.XS_POLICY_AUTO, 0, 0, cap)
+    return pol
+
+
+SHARE_POLICIES = {"burst": (X.XS_POLICY_BURST, 0, 0, 0), "interleave": (X.XS_POLICY_INTERLEAVE, 0, 0, 0),
+                  "chunk2": (X.XS_POLICY_CHUNK, 0, 2, 0), "auto": (X.XS_POLICY_AUTO, 0, 0, 0)}
+
+
+def most_loaded_rank(logits: np.ndarray, k: int, E: int, W: int) -> int:
+    """The destination window receiving the most rows, from the library's routing and layout of
+    every source (n_src x T tokens)."""
+    n_src, T, _ = logits.shape
+    st = torch.cuda.current_stream().cuda_stream
+    i32 = dict(dtype=torch.int32, device="cuda")
+    lg = torch.from_numpy(np.ascontiguousarray(logits, dtype=np.float32)).cuda()
+    idx = torch.empty((n_src, T, k), **i32)
+    w = torch.empty((n_src, T, k), dtype=torch.float32, device="cuda")
+    X.check(X.xs_route_topk_softmax(lg.data_ptr(), n_src * T, E, k, 0, idx.data_ptr(), w.data_ptr(), st), "route")
+    cap = 1                     # only the counts are wanted: rows past capacity are not recorded
+    ec, sb, eo = torch.empty((n_src, E), **i32), torch.empty((n_src, E), **i32), torch.empty((E,), **i32)
+    dc, sr, rs = torch.empty((W,), **i32), torch.empty((n_src, T, k), **i32), torch.empty((W, cap), **i32)
+    status = torch.zeros((1,), **i32)
+    nb = C.c_int64()
+    X.check(X.xs_dispatch_layout_workspace_bytes(n_src, T, E, C.byref(nb)), "layout workspace")
+    ws = torch.empty((max(1, nb.value),), dtype=torch.uint8, device="cuda")
+    X.check(X.xs_dispatch_layout(idx.data_ptr(), n_src, T, k, E, W, cap, ec.data_ptr(), sb.data_ptr(), eo.data_ptr(),
+                                 dc.data_ptr(), sr.data_ptr(), rs.data_ptr(), ws.data_ptr(), ws.numel(),
+                                 status.data_ptr(), st), "layout")
+    torch.cuda.synchronize()
+    return int(dc.cpu().numpy().argmax())
+
+
+def share_inputs(routing: str, seed: int = 0):
+    """Inputs of the DeepSeek-V3-like share; Zipf routing puts this GPU on the most loaded rank,
+    taken from the library's own routing and layout of every source."""
+    import synth
+    cfg = dataclasses.replace(synth.EP_DSV3_SHARE, routing=routing)
+    inp = {"logits": synth.ep_logits(cfg, seed), "x": synth.ep_x(cfg, seed)}
+    rank = most_loaded_rank(inp["logits"], cfg.k, cfg.E, cfg.W) if routing == "zipf" else 0
+    cfg = dataclasses.replace(cfg, rank=rank)
+    experts = list(range(rank * cfg.E_local, (rank + 1) * cfg.E_local))
+    inp["w1"], inp["w2"] = synth.ep_weights(cfg, experts, seed)
+    inp["fill"] = synth.ep_remote_combine_fill(cfg, seed)
+    return cfg, inp
+
+
+def run(quick=False, reps=5, routings=("zipf", "uniform"), seed=0):
+    import synth
+    torch.cuda.set_device(0)
+    ch, cd = calibrate_sinks(256, [16384, 65536, 262144] if quick else [4096, 16384, 65536, 131072, 262144],
+                             store_waves=8, target_bytes=256 << 20)
+    model = to_model(ch, capacity="knee")
+    report = {"sink_model": {k: ch.model[k] for k in ("t0_a_us", "t0_b_us_per_byte", "R_bytes_per_us",
+                                                        "Q_knee_bracket_bytes", "Q_bytes")},
+              "hbm_R_bytes_per_us": cd.model["R_bytes_per_us"], "layers": []}
+    cfg = synth.EP_TINY
+    inp = synth.ep_inputs(cfg, seed)
+    caps = [16, 0] if quick else [16, 64, 0]
+    chunks = [1, 8] if quick else [1, 2, 4, 8, 16, 32, 64]
+    report["layers"].append(evaluate(cfg.name + " (every combine window on the sink)", tiny_layer(cfg, inp),
+                                     tiny_policies(caps, chunks), model, 1.0, reps))
+    for routing in routings:
+        scfg, sinp = share_inputs(routing, seed)
+        hosts = [q for q in range(scfg.n_src) if q != scfg.rank][:2]
+        report["layers"].append(evaluate(f"{scfg.name} ({routing}, rank {scfg.rank}; combine windows of sources "
+                                         f"{hosts} on the sink)", share_layer(scfg, sinp, hosts), SHARE_POLICIES,
+                                         model, len(hosts) / scfg.n_src, reps))
+        del sinp
+    return report
 
 
 def main():
@@ -154,36 +297,12 @@ def main():
     ap.add_argument("--quick", action="store_true")
     ap.add_argument("--reps", type=int, default=5)
     a = ap.parse_args()
-    import synth
-    torch.cuda.set_device(0)
-    rate = X.xs_clock_rate_hz()
-    K = 256
-    Bs = [4096, 8192, 16384, 32768, 65536, 131072, 262144]
-    ch, cd = calibrate_sinks(K, Bs, store_waves=8)
-    host_model = to_model(ch, capacity="knee")
-    report = {"calibration": [dataclasses.asdict(ch), dataclasses.asdict(cd)], "sweeps": []}
-    layers = [synth.EP_TINY, dataclasses.replace(synth.EP_TINY, name="ep_tiny_dims_T32768", T=32768)]
-    caps = [16, 0] if a.quick else [16, 64, 0]
-    chunks = [1, 8] if a.quick else [1, 2, 4, 8, 16, 32, 64]
-    for cfg in layers:
-        report["sweeps"] += sweep_layer(cfg, host_model, caps, chunks, a.reps, rate)
-    speed = {}
-    for cfg in layers:
-        for cap in caps:
-            rows = [r for r in report["sweeps"] if r["layer"] == cfg.name and r["sink"] == "host"
-                    and r["max_producers"] == (cap or 256)]
-            burst = next(r for r in rows if r["policy"] == "burst")
-            best = min((r for r in rows if r["policy"] != "burst"), key=lambda r: r["kernel_us_median"])
-            speed[f"{cfg.name}/cap{cap or 256}"] = {
-                "burst_us": burst["kernel_us_median"], "best_policy": best["policy"],
-                "best_us": best["kernel_us_median"], "speedup_over_burst": burst["kernel_us_median"] / best["kernel_us_median"],
-                "burst_stall_measured_us": burst["stall_measured_us"], "burst_stall_predicted_us": burst["stall_predicted_us"],
-                "best_stall_measured_us": best["stall_measured_us"], "best_stall_predicted_us": best["stall_predicted_us"]}
-    report["pacing_speedup_host"] = speed
+    rep = run(quick=a.quick, reps=a.reps)
     if a.out:
         with open(a.out, "w") as f:
-            json.dump(report, f, indent=1, default=float)
-    print(json.dumps(speed), flush=True)
+            json.dump(rep, f, indent=1, default=float)
+    print(json.dumps({L["layer"]: {k: (v["kernel_us"], v.get("speedup_over_burst")) for k, v in L["policies"].items()}
+                      for L in rep["layers"]}), flush=True)
 
 
 if __name__ == "__main__":

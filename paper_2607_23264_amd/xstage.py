@@ -30,6 +30,7 @@ XS_MB_PERIODIC, XS_MB_COMPLETION = 0, 1
 XS_ATTN_LOCAL, XS_ATTN_WINDOWS, XS_ATTN_WINDOWS_COUPLED = 0, 1, 2
 XS_FMT_E4M3, XS_FMT_E2M1 = 0, 1
 XS_PREC_BF16, XS_PREC_MXFP8, XS_PREC_W4A8 = 0, 1, 2
+XS_EPI_STORE, XS_EPI_SWIGLU = 0, 1
 
 vp = C.c_void_p
 i32 = C.c_int32
@@ -141,13 +142,13 @@ xs_dispatch_layout = _sig("xs_dispatch_layout", C.c_int, vp, i32, i32, i32, i32,
 xs_dispatch = _sig("xs_dispatch", C.c_int, vp, i32, i32, vp, vp, i32, i32, P(xs_window), i32, vp, vp)
 xs_ep_layer_workspace_bytes = _sig("xs_ep_layer_workspace_bytes", C.c_int, P(xs_ep_layer), P(i64))
 xs_expert_ffn = _sig("xs_expert_ffn", C.c_int, P(xs_ep_layer), vp, i64, vp, vp)
-xs_combine_send = _sig("xs_combine_send", C.c_int, P(xs_ep_layer), vp, vp)
+xs_combine_send = _sig("xs_combine_send", C.c_int, P(xs_ep_layer), P(xs_pacing), vp, vp)
 xs_combine_reduce = _sig("xs_combine_reduce", C.c_int, vp, i64, vp, i32, i32, i32, vp, vp)
 xs_fused_ep_layer = _sig("xs_fused_ep_layer", C.c_int, P(xs_ep_layer), P(xs_pacing), P(xs_trace), vp, i64,
                          vp, vp)
 xs_gemm = _sig("xs_gemm", C.c_int, vp, i64, vp, i64, vp, i64, i32, i32, i32, P(xs_trace), vp)
 xs_gemm_scatter = _sig("xs_gemm_scatter", C.c_int, vp, i64, vp, i64, i32, i32, i32, P(xs_scatter_desc),
-                       P(xs_window), i32, P(xs_trace), vp)
+                       P(xs_window), i32, P(xs_pacing), P(xs_trace), vp)
 xs_scatter_copy = _sig("xs_scatter_copy", C.c_int, vp, i64, i32, i32, P(xs_scatter_desc), P(xs_window),
                        i32, vp)
 xs_attention = _sig("xs_attention", C.c_int, P(xs_attn), i32, P(xs_trace), vp)
@@ -166,6 +167,7 @@ xs_model_predict = _sig("xs_model_predict", C.c_int, P(xs_model), P(xs_burst), i
 xs_model_fit = _sig("xs_model_fit", C.c_int, P(xs_calib), P(xs_model))
 xs_xstage_microbench = _sig("xs_xstage_microbench", C.c_int, P(xs_microbench_args), P(xs_trace), vp)
 xs_clock_rate_hz = _sig("xs_clock_rate_hz", C.c_double)
+xs_grouped_gemm = _sig("xs_grouped_gemm", C.c_int, vp, i64, i32, vp, vp, i32, vp, i32, i32, vp, i64, i32, vp, vp)
 xs_drain_rate = _sig("xs_drain_rate", C.c_int, vp, vp, i32, P(f64))
 xs_calib_knee = _sig("xs_calib_knee", C.c_int, vp, vp, i32, f64, P(i32))
 xs_model_calibrate = _sig("xs_model_calibrate", C.c_int, P(xs_calib), P(xs_calib_summary))
@@ -180,7 +182,7 @@ EXPORTED = ["xs_strerror", "xs_version", "xs_route_topk_softmax", "xs_dispatch_l
             "xs_scatter_copy", "xs_attention", "xs_ulysses_copy", "xs_quantize_mx", "xs_quantize_mx_grouped", "xs_gemm_mx", "xs_dispatch_rows",
             "xs_ring_slot_bytes", "xs_dispatch_ring_workspace_bytes", "xs_dispatch_ring",
             "xs_model_predict", "xs_model_fit", "xs_pacing_audit_run", "xs_trace_tile_times",
-            "xs_drain_rate", "xs_calib_knee", "xs_model_calibrate", "xs_burst_gap", "xs_recovery_audit",
+            "xs_grouped_gemm", "xs_drain_rate", "xs_calib_knee", "xs_model_calibrate", "xs_burst_gap", "xs_recovery_audit",
             "xs_xstage_microbench", "xs_clock_rate_hz"]
 
 

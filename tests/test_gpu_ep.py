@@ -514,3 +514,33 @@ def test_trace_ext_records_and_tile_times():
     assert t1.value == pytest.approx(np.median((r[kind == 1, 2] - r[kind == 1, 1]).astype(np.float64)) * us)
     assert t2.value == pytest.approx(np.median((r[kind == 2, 2] - x[kind == 2, 0]).astype(np.float64)) * us)
     assert t1.value > 0 and t2.value > 0 and t3.value > 0
+
+
+def test_combine_send_pacing_stores_the_same_rows():
+    """The unfused combine-send under pacing settings (producer caps, bursts of row blocks, gaps)
+    writes the same combine windows as the fused layer, whose rows match the oracle."""
+    from paper_2607_23264_amd.layer import pacing
+    X = xs()
+    cfg = synth.EPConfig("t", T=300, H=256, E=16, k=3, I=256, W=4, n_src=3, rank=1)
+    inp = synth.ep_inputs(cfg, 7)
+    experts = synth.computed_experts(cfg)
+    ref = oep.ep_layer(inp["x"], inp["logits"], inp["w1"], inp["w2"], cfg.k, cfg.E, cfg.W,
+                       cap=cfg.n_src * cfg.T * cfg.k, experts=experts, out_src=cfg.rank)
+    lay = _ep_layer(cfg)
+    lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
+    lay.prefill_other_sources()
+    lay.fused(pacing(X.XS_POLICY_INTERLEAVE, lead=1))
+    torch.cuda.synchronize()
+    fused = host_bits(lay.cwin)
+    own = (ref["idx"] // (cfg.E // cfg.W) == cfg.rank).reshape(cfg.n_src, -1)
+    assert_close(fused[own], bits_f64(ref["combine"][own]), "fused combine rows")
+    lay.expert_ffn()
+    for p in (None, pacing(X.XS_POLICY_BURST, max_producers=3, chunk=1),
+              pacing(X.XS_POLICY_BURST, max_producers=1, gap_ns=2000), pacing(X.XS_POLICY_BURST, chunk=2)):
+        lay.cwin.fill_(-1)
+        lay.combine_send(p)
+        torch.cuda.synchronize()
+        assert int(lay.status.item()) == 0
+        assert np.array_equal(host_bits(lay.cwin), np.where(own[..., None], fused, np.uint16(0xFFFF)))
+    bad = pacing(X.XS_POLICY_BURST, gap_ns=-5)
+    assert X.xs_combine_send(C.byref(lay.L), C.byref(bad), lay.status.data_ptr(), lay.stream) == X.XS_EINVAL

@@ -174,7 +174,7 @@ def test_bad_arguments():
     # the unfused phase calls take bf16 only
     assert X.xs_expert_ffn(C.byref(lay.L), ws.data_ptr(), ws.numel(), lay.status.data_ptr(),
                            lay.stream) == X.XS_EUNSUPPORTED
-    assert X.xs_combine_send(C.byref(lay.L), lay.status.data_ptr(), lay.stream) == X.XS_EUNSUPPORTED
+    assert X.xs_combine_send(C.byref(lay.L), None, lay.status.data_ptr(), lay.stream) == X.XS_EUNSUPPORTED
     # a workspace sized for bf16 is too small: the quantized rows are staged in it
     nb = C.c_int64()
     X.check(X.xs_ep_layer_workspace_bytes(C.byref(variant(precision=X.XS_PREC_BF16)), C.byref(nb)))

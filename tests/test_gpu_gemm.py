@@ -55,7 +55,7 @@ def _windows_rowblock(W, rpd, N):
     return win, X.windows([X.window(win[d]) for d in range(W)])
 
 
-def _tp(a_bits, b_bits, rpd, serial=False):
+def _tp(a_bits, b_bits, rpd, serial=False, pacing=None):
     X = xs()
     M, K = a_bits.shape
     N = b_bits.shape[1]
@@ -68,7 +68,7 @@ def _tp(a_bits, b_bits, rpd, serial=False):
         X.check(X.xs_gemm(a.data_ptr(), K, bt.data_ptr(), K, c.data_ptr(), N, M, N, K, None, _stream()))
         X.check(X.xs_scatter_copy(c.data_ptr(), N, M, N, desc, wins, W, _stream()))
     else:
-        X.check(X.xs_gemm_scatter(a.data_ptr(), K, bt.data_ptr(), K, M, N, K, desc, wins, W, None, _stream()))
+        X.check(X.xs_gemm_scatter(a.data_ptr(), K, bt.data_ptr(), K, M, N, K, desc, wins, W, pacing, None, _stream()))
     torch.cuda.synchronize()
     return host_bits(win)
 
@@ -93,7 +93,7 @@ def test_tp_full_size_every_element_and_fused_equals_serial():
     assert np.mean(fused == win_ref) > 0.99      # nearly every element rounds like the oracle's
 
 
-def _sp(x_bits, w_bits, nh, hd, hpg, serial=False):
+def _sp(x_bits, w_bits, nh, hd, hpg, serial=False, pacing=None):
     X = xs()
     S, Dm = x_bits.shape
     N = w_bits.shape[1]
@@ -107,7 +107,7 @@ def _sp(x_bits, w_bits, nh, hd, hpg, serial=False):
         X.check(X.xs_gemm(x.data_ptr(), Dm, wt.data_ptr(), Dm, c.data_ptr(), N, S, N, Dm, None, _stream()))
         X.check(X.xs_scatter_copy(c.data_ptr(), N, S, N, desc, wins, G, _stream()))
     else:
-        X.check(X.xs_gemm_scatter(x.data_ptr(), Dm, wt.data_ptr(), Dm, S, N, Dm, desc, wins, G, None, _stream()))
+        X.check(X.xs_gemm_scatter(x.data_ptr(), Dm, wt.data_ptr(), Dm, S, N, Dm, desc, wins, G, pacing, None, _stream()))
     torch.cuda.synchronize()
     return host_bits(win)
 
@@ -146,7 +146,118 @@ def test_scatter_rejects_bad_descriptors():
     b = torch.zeros((256, 64), dtype=torch.int16, device="cuda")
     win, wins = _windows_rowblock(2, 256, 256)
     bad = X.xs_scatter_desc(X.XS_SCATTER_ROW_BLOCK, 200, 0, 0, 0, 0)
-    assert X.xs_gemm_scatter(a.data_ptr(), 64, b.data_ptr(), 64, 512, 256, 64, bad, wins, 2, None,
+    assert X.xs_gemm_scatter(a.data_ptr(), 64, b.data_ptr(), 64, 512, 256, 64, bad, wins, 2, None, None,
                              None) != X.XS_OK
     assert X.xs_gemm(a.data_ptr(), 64, b.data_ptr(), 64, a.data_ptr(), 64, 512, 100, 64, None,
                      None) == X.XS_EUNSUPPORTED
+
+
+def _grouped(a_bits, offs, rows, b_bits, swiglu, M=None):
+    X = xs()
+    M = a_bits.shape[0] if M is None else M
+    K = a_bits.shape[1]
+    n_seg, N = b_bits.shape[0], b_bits.shape[1]
+    n_out = N // 2 if swiglu else N
+    a, b = dev_bits(a_bits), dev_bits(b_bits)
+    c = torch.full((M, n_out), -1, dtype=torch.int16, device="cuda")
+    so = torch.tensor(offs, dtype=torch.int32, device="cuda")
+    sr = torch.tensor(rows, dtype=torch.int32, device="cuda")
+    st = torch.zeros((1,), dtype=torch.int32, device="cuda")
+    X.check(X.xs_grouped_gemm(a.data_ptr(), K, M, so.data_ptr(), sr.data_ptr(), n_seg, b.data_ptr(), N, K,
+                              c.data_ptr(), n_out, X.XS_EPI_SWIGLU if swiglu else X.XS_EPI_STORE, st.data_ptr(),
+                              _stream()))
+    torch.cuda.synchronize()
+    return host_bits(c), int(st.item())
+
+
+@pytest.mark.parametrize("swiglu", [False, True])
+def test_grouped_gemm_matches_oracle(swiglu):
+    # ragged segments with gaps, an empty one and one of a single row; K = 7168 as the expert FFN
+    M, K, N = 1500, 7168, 512
+    offs = [0, 300, 301, 700, 1200, 1499]
+    rows = [257, 0, 399, 480, 299, 1]
+    a = synth.normal_bf16(0, 20, (M, K))
+    b = synth.normal_bf16(0, 21, (len(offs), N, K), std=0.02)
+    got, st = _grouped(a, offs, rows, b, swiglu)
+    assert st == 0
+    c64, bits = oep.grouped_gemm(a, offs, rows, b, swiglu=swiglu)
+    inside = ~np.isnan(c64[:, 0])
+    assert_close(got[inside], c64[inside], f"grouped gemm swiglu={swiglu}")
+    assert (got[~inside] == 0xFFFF).all()
+
+
+def test_grouped_gemm_integer_operands_bitexact_and_bad_segment():
+    X = xs()
+    M, K, N = 600, 512, 256
+    offs, rows = [0, 256, 512], [256, 256, 88]
+    a = synth.int_valued_bf16(0, 22, (M, K))
+    b = synth.int_valued_bf16(0, 23, (3, N, K))
+    got, st = _grouped(a, offs, rows, b, False)
+    _, bits = oep.grouped_gemm(a, offs, rows, b)
+    assert st == 0 and np.array_equal(got, bits)
+    # a segment past the rows is skipped and reported; the others are still computed
+    got, st = _grouped(a, [0, 500], [256, 200], b[:2], False)
+    assert st == X.XS_EBADINPUT
+    _, bits = oep.grouped_gemm(a, [0], [256], b[:1])
+    assert np.array_equal(got[:256], bits[:256]) and (got[256:] == 0xFFFF).all()
+    # argument errors: nothing launched
+    z = torch.zeros((16,), dtype=torch.int32, device="cuda")
+    assert X.xs_grouped_gemm(z.data_ptr(), 64, 4, z.data_ptr(), z.data_ptr(), 1, z.data_ptr(), 100, 64, z.data_ptr(),
+                             100, X.XS_EPI_STORE, None, None) == X.XS_EUNSUPPORTED
+    assert X.xs_grouped_gemm(z.data_ptr(), 64, 4, z.data_ptr(), z.data_ptr(), 1, z.data_ptr(), 256, 64, z.data_ptr(),
+                             256, 7, None, None) == X.XS_EINVAL
+
+
+def _pacing(policy, chunk=0, max_producers=0, gap_ns=0):
+    from paper_2607_23264_amd.layer import pacing
+    return pacing(policy, lead=0, chunk=chunk, max_producers=max_producers, gap_ns=gap_ns)
+
+
+def test_scatter_pacing_orders_store_the_same_windows():
+    """Every pacing order of the scatter GEMM (destination-major bursts, round robin, chunks of
+    tiles, a producer cap and a gap) fills the windows with the oracle's values, bit for bit equal
+    to the default order."""
+    X = xs()
+    a = synth.normal_bf16(0, 30, (2048, 512))
+    b = synth.normal_bf16(0, 31, (512, 1024), std=0.05)
+    rpd = 512
+    base = _tp(a, b, rpd)
+    c64, _ = osc.tp_row_block_scatter(a, b, rpd)
+    assert_close(base.reshape(2048, 1024), c64, "tp small")
+    for pol in (_pacing(X.XS_POLICY_BURST), _pacing(X.XS_POLICY_INTERLEAVE, max_producers=7),
+                _pacing(X.XS_POLICY_CHUNK, chunk=4, max_producers=16, gap_ns=3000)):
+        assert np.array_equal(_tp(a, b, rpd, pacing=pol), base), pol.policy
+    cfg = synth.SP_QKV
+    x = synth.normal_bf16(0, 32, (512, 1024))
+    w = synth.normal_bf16(0, 33, (1024, 3 * 16 * 64), std=0.05)
+    base = _sp(x, w, 16, 64, 4)
+    qkv64, _ = osc.sp_head_group_scatter(x, w, 16, 64, 4)
+    ref64 = qkv64.reshape(512, 3, 4, 4, 64).transpose(2, 1, 3, 0, 4)
+    assert_close(base, ref64, "sp small")
+    for pol in (_pacing(X.XS_POLICY_BURST), _pacing(X.XS_POLICY_CHUNK, chunk=2, max_producers=5)):
+        assert np.array_equal(_sp(x, w, 16, 64, 4, pacing=pol), base), pol.policy
+
+
+def test_scatter_pacing_full_size_tp_equals_default():
+    X = xs()
+    cfg = synth.TP_ROWBLOCK
+    inp = synth.tp_inputs(cfg, 0)
+    rpd = cfg.M // cfg.W
+    base = _tp(inp["a"], inp["b"], rpd)
+    for pol in (_pacing(X.XS_POLICY_BURST), _pacing(X.XS_POLICY_INTERLEAVE), _pacing(X.XS_POLICY_CHUNK, chunk=8)):
+        assert np.array_equal(_tp(inp["a"], inp["b"], rpd, pacing=pol), base), pol.policy
+
+
+def test_scatter_pacing_rejects_bad_orders():
+    X = xs()
+    a = torch.zeros((1024, 64), dtype=torch.int16, device="cuda")
+    b = torch.zeros((256, 64), dtype=torch.int16, device="cuda")
+    win, wins = _windows_rowblock(2, 512, 256)
+    desc = X.xs_scatter_desc(X.XS_SCATTER_ROW_BLOCK, 512, 0, 0, 0, 0)
+    bad_chunk = _pacing(X.XS_POLICY_CHUNK, chunk=3)          # 2 tiles per window: 3 does not divide
+    assert X.xs_gemm_scatter(a.data_ptr(), 64, b.data_ptr(), 64, 1024, 256, 64, desc, wins, 2, bad_chunk, None,
+                             None) == X.XS_EINVAL
+    neg = _pacing(X.XS_POLICY_BURST, gap_ns=-1)
+    assert X.xs_gemm_scatter(a.data_ptr(), 64, b.data_ptr(), 64, 1024, 256, 64, desc, wins, 2, neg, None,
+                             None) == X.XS_EINVAL
+    torch.cuda.synchronize()

@@ -308,3 +308,27 @@ def test_multi_source_layer_combine_targets():
                     assert np.array_equal(row, inp["x"][s, t])
                 else:
                     assert np.all(row == ep.SENTINEL_BF16)
+
+
+def test_grouped_gemm_integer_exact_and_swiglu_matches_expert_ffn():
+    g = np.random.default_rng(12)
+    M, K, N = 40, 64, 32
+    a = synth.int_valued_bf16(0, 7, (M, K))
+    b = synth.int_valued_bf16(0, 8, (3, N, K))
+    offs, rows = [0, 10, 30], [7, 0, 10]
+    c64, bits = ep.grouped_gemm(a, offs, rows, b)
+    A, B = ep.bf16_bits_to_f64(a), ep.bf16_bits_to_f64(b)
+    for s, (o, r) in enumerate(zip(offs, rows)):
+        for i in range(o, o + r):                 # explicit dot products of integers: exact
+            for n in range(N):
+                assert c64[i, n] == sum(A[i, kk] * B[s, n, kk] for kk in range(K))
+    outside = np.ones(M, bool)
+    outside[0:7] = outside[30:40] = False
+    assert np.isnan(c64[outside]).all() and (bits[outside] == ep.SENTINEL_BF16).all()
+    # the SwiGLU epilogue is the expert FFN's Linear-1 + activation, h before rounding
+    x = synth.normal_bf16(0, 9, (12, 64))
+    w1 = synth.normal_bf16(0, 10, (2, 2 * 16, 64), std=0.1)
+    c64, bits = ep.grouped_gemm(x, [0, 5], [5, 7], w1, swiglu=True)
+    for s, (o, r) in enumerate([(0, 5), (5, 7)]):
+        h_bits, _, _ = ep.expert_ffn(x[o:o + r], w1[s], np.zeros((64, 16), np.uint16))
+        assert np.array_equal(bits[o:o + r], h_bits)
