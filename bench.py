@@ -45,9 +45,11 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-phases", action="store_true")
     p.add_argument("--no-scatter", action="store_true", help="skip the TP / SP scatter GEMM lines")
-    p.add_argument("--slow-sink", action="store_true",
-                   help="also run the host-coherent sink line (the tiny layer: it launches the same "
-                        "fused kernel, so it stays out of the default run and its kernel statistics)")
+    p.add_argument("--no-slow-sink", action="store_true",
+                   help="skip the store-pacing lines against the host-coherent sink (the tiny layer with "
+                        "every combine window on the sink; the DeepSeek-V3 share with two of eight)")
+    p.add_argument("--no-zipf", action="store_true", help="skip the Zipf(1.2)-routed share line")
+    p.add_argument("--no-tiny", action="store_true", help="skip the tiny-layer line (eager and HIP graph)")
     p.add_argument("--no-attn", action="store_true",
                    help="skip the attention + Ulysses exchange line (HBM and host-coherent windows)")
     p.add_argument("--policies", action="store_true",
@@ -109,9 +111,90 @@ def cpu_baseline(cfg, inp, rank, seed, ffn_budget_s=12.0, comb_budget_s=3.0):
                        f"{cfg.T} tokens in full; SwiGLU FFN of {n_exp} of {cfg.E_local} local experts "
                        f"({rows_done} of {rows_all} rows, synthetic rows) scaled by rows; combine-reduce "
                        f"of {tok} of {cfg.T} tokens scaled by tokens; {wall:.1f} s of CPU time"),
-            "cpu": platform.processor() or platform.machine(),
+            "cpu": cpu_model(),
             "phases_us": {"route_layout": t_route_layout * 1e6, "dispatch": t_disp * 1e6,
                           "expert_ffn": t_ffn * 1e6, "combine_reduce": t_comb * 1e6}}
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo), else the machine type."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
+def tiny_line(X, torch, synth, steps=20, warmup=3):
+    """The tiny layer (c1: T=256, H=512, 8 experts, top-2, I=1024, 4 windows, one source): one
+    step = the whole fused layer, timed eagerly and as a HIP graph replay (the step captured
+    once), since it is launch-bound."""
+    from paper_2607_23264_amd.layer import EPLayer, Shape, pacing
+    cfg = synth.EP_TINY
+    inp = synth.ep_inputs(cfg, 0)
+    s = Shape(cfg.n_src, cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.W, 0, cfg.E)
+    lay = EPLayer(s, sentinel=False)
+    lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
+    pol = pacing(X.XS_POLICY_INTERLEAVE, lead=0, claim=X.XS_CLAIM_DYNAMIC)
+    for _ in range(warmup):
+        lay.fused(pol)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        lay.fused(pol)
+    e1.record()
+    torch.cuda.synchronize()
+    eager = e0.elapsed_time(e1) * 1e3 / steps
+    graph = graph_steps(torch, lay, pol, steps)
+    status = int(lay.status.item())
+    del lay
+    torch.cuda.empty_cache()
+    if status:
+        raise RuntimeError(f"tiny layer: device status {status}")
+    flops = 6.0 * cfg.H * cfg.I * cfg.T * cfg.k
+    return {"workload": cfg.name, "us_per_step_eager": eager, "us_per_step_graph": graph["us_per_step"],
+            "graph": graph, "flops_per_step": flops}
+
+
+def zipf_line(X, torch, synth, pol, steps, warmup):
+    """The same share with Zipf(1.2) routing, this GPU the most loaded rank: step time and the
+    expert-FFN kernel's rate (FLOPs scale with the rows this rank computes)."""
+    from paper_2607_23264_amd import slow_sink as ss
+    from paper_2607_23264_amd.layer import EPLayer, Shape
+    cfg, inp = ss.share_inputs("zipf", 0)
+    experts = list(range(cfg.rank * cfg.E_local, (cfg.rank + 1) * cfg.E_local))
+    s = Shape(cfg.n_src, cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.W, experts[0], len(experts), src=cfg.rank)
+    lay = EPLayer(s, sentinel=False)
+    lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
+    lay.prefill_other_sources(inp["fill"])
+    for _ in range(warmup):
+        lay.fused(pol)
+    torch.cuda.synchronize()
+    ev = X.HipEvents(2 * steps)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(steps):
+        lay.L.events[X.XS_EV_FFN] = ev.ev[2 * i]
+        lay.L.events[X.XS_EV_FFN_END] = ev.ev[2 * i + 1]
+        lay.fused(pol)
+    e1.record()
+    torch.cuda.synchronize()
+    step_us = e0.elapsed_time(e1) * 1e3 / steps
+    ffn_us = float(np.mean([ev.elapsed_ms(2 * i, 2 * i + 1) for i in range(steps)])) * 1e3
+    rows = int(lay.dest_counts[cfg.rank].item())
+    status = int(lay.status.item())
+    del lay
+    torch.cuda.empty_cache()
+    if status:
+        raise RuntimeError(f"zipf share: device status {status}")
+    flops = 6.0 * cfg.H * cfg.I * rows
+    return {"workload": f"{cfg.name} (zipf routing, rank {cfg.rank}, the most loaded)", "us_per_step": step_us,
+            "ffn_us": ffn_us, "rows_computed": rows, "ffn_TFLOPs": flops / (ffn_us * 1e-6) / 1e12,
+            "mfma_frac": flops / (ffn_us * 1e-6) / MFMA_PEAK_BF16}
 
 
 def scatter_lines(X, torch, synth, reps=20):
@@ -202,30 +285,24 @@ def store_ceiling(X, torch):
             "frac_of_hbm_peak": nb / (span * 1e-6) / HBM_PEAK}
 
 
-def slow_sink_line(X, torch, synth, reps=7):
-    """Config 5 in brief: the tiny layer with its combine windows in host-coherent memory,
-    BURST vs paced issue at two producer caps, with the calibrated model's stall prediction
-    (the full sweep is paper_2607_23264_amd.slow_sink)."""
+def slow_sink_line(reps=5):
+    """Store pacing against the host-coherent sink (paper_2607_23264_amd.slow_sink, quick sweep):
+    the tiny layer with every combine window on the sink (c5) and the DeepSeek-V3 share with two
+    of its eight source windows there, uniform and Zipf; per policy the kernel time on the sink
+    and on the HBM control, the speedup over Expert-Wave burst issue, and the stall per producer
+    measured (issue spans and staging waits beyond the control) against the audit's prediction."""
     from paper_2607_23264_amd import slow_sink as ss
-    from paper_2607_23264_amd.calibrate import to_model
-    ch, cd = ss.calibrate_sinks(256, [16384, 65536, 262144], store_waves=8, target_bytes=256 << 20)
-    host_model = to_model(ch, capacity="knee")
-    rows = ss.sweep_layer(synth.EP_TINY, host_model, [16, 0], [8], reps, X.xs_clock_rate_hz())
-    res = {"host_sink": {k: ch.model[k] for k in ("t0_a_us", "t0_b_us_per_byte", "R_bytes_per_us",
-                                                  "Q_knee_bracket_bytes")},
-           "hbm_R_bytes_per_us": cd.model["R_bytes_per_us"], "layers": {}}
-    for cap in (16, 256):
-        host = [r for r in rows if r["sink"] == "host" and r["max_producers"] == cap]
-        burst = next(r for r in host if r["policy"] == "burst")
-        best = min((r for r in host if r["policy"] != "burst"), key=lambda r: r["kernel_us_median"])
-        res["layers"][f"cap{cap}"] = {
-            "burst_us": burst["kernel_us_median"], "best_policy": best["policy"],
-            "best_us": best["kernel_us_median"],
-            "pacing_speedup": burst["kernel_us_median"] / best["kernel_us_median"],
-            "stall_fraction_burst": burst["stall_fraction"], "stall_fraction_best": best["stall_fraction"],
-            "stall_predicted_us_burst": burst["stall_predicted_us"],
-            "stall_measured_us_burst": burst["stall_measured_us"]}
-    return res
+    rep = ss.run(quick=True, reps=reps)
+    keep = ("policy", "chunk", "kernel_us", "control_kernel_us", "speedup_over_burst",
+            "stall_measured_us_per_producer", "stall_predicted_us_per_producer",
+            "staging_wait_measured_us_per_producer", "mma_stall_predicted_us_per_producer",
+            "stall_fraction_measured", "stall_fraction_predicted", "mainloop_excess_us_per_producer",
+            "dependency_wait_excess_us_per_producer", "l2_issue_us_median", "l2_issue_us_p90", "rate_feasible_eq9")
+    return {"sink_model": rep["sink_model"], "hbm_R_bytes_per_us": rep["hbm_R_bytes_per_us"],
+            "layers": [{"layer": L["layer"], "sink_share": L["sink_share"],
+                        "control_tile_times_us": L.get("control_tile_times_us"),
+                        "policies": {k: {f: v.get(f) for f in keep} for k, v in L["policies"].items()}}
+                       for L in rep["layers"]]}
 
 
 def synth_rows(g, m, H):
@@ -625,10 +702,20 @@ def main():
                 "flops_per_launch": 4.0 * 8 * 16384 ** 2 * 128,
                 "algorithmic_bytes_per_launch": 4.0 * 8 * 16384 * 128 * 2}
         torch.cuda.empty_cache()
-    if a.slow_sink:
-        log("[bench] slow sink (host-coherent combine windows)")
-        res["slow_sink"] = slow_sink_line(X, torch, synth)
-        log("[bench] " + json.dumps(res["slow_sink"]["layers"]))
+    if not a.no_tiny:
+        log("[bench] tiny layer (eager and HIP graph replay)")
+        res["tiny_layer"] = tiny_line(X, torch, synth)
+        log(f"[bench] tiny layer: {res['tiny_layer']['us_per_step_eager']:.1f} us eager, "
+            f"{res['tiny_layer']['us_per_step_graph']} us graph")
+    if not a.no_zipf:
+        log("[bench] the share with Zipf(1.2) routing")
+        res["zipf_share"] = zipf_line(X, torch, synth, pol[a.policy], min(a.steps, 10), a.warmup)
+        log(f"[bench] zipf: {res['zipf_share']['us_per_step']:.1f} us/step, FFN {res['zipf_share']['ffn_us']:.1f} us")
+    if not a.no_slow_sink:
+        log("[bench] store pacing against the host-coherent sink")
+        res["slow_sink"] = slow_sink_line()
+        for L in res["slow_sink"]["layers"]:
+            log("[bench] " + L["layer"] + ": " + ", ".join(f"{k} {v['kernel_us']:.0f} us" for k, v in L["policies"].items()))
     if not a.no_cpu_baseline:
         log("[bench] oracle on the host (bounded sample)")
         res["cpu_baseline"] = cpu_baseline(cfg, inp, rank, a.seed)

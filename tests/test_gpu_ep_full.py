@@ -10,6 +10,7 @@ of 64 rows, dynamic claiming), through the C ABI, against the CPU oracle:
   * the whole combined output of this rank within tolerance;
   * the ready flags of every dispatch and combine window set.
 The oracle runs expert by expert, which bounds its host memory."""
+import concurrent.futures as cf
 import dataclasses
 import gc
 
@@ -119,13 +120,17 @@ def test_dsv3_share_every_row_at_bench_pacing(routing, prec):
         if mx:
             gh_codes, gh_scales = h_codes_scales(lay, cfg.I)    # the GPU's h rows (window r first)
             flips = 0
-        for i, e in enumerate(experts):
+        def check_expert(i, e):
+            """The oracle's rows of one local expert against the GPU's combine rows (and, in the MX
+            precisions, the GPU's h rows against the fp32 bound). Returns (slots of this rank,
+            y bits there, their slack, h codes that differ)."""
             r0 = int(lref["expert_offsets"][e])
             r1 = r0 + int(total[e])
             if r1 == r0:
-                continue
+                return None
             src, slot = oep.decode_row_src(lref["row_src"][r][r0:r1])
             mine = src == r
+            nflip, slack = 0, None
             if mx:
                 w1q = omx.quantize_rows(ref["w1"][i], wfmt)
                 w2q = omx.quantize_rows(ref["w2"][i], wfmt)
@@ -134,15 +139,24 @@ def test_dsv3_share_every_row_at_bench_pacing(routing, prec):
                 # h codes decided in fp32 may differ from the oracle's within the fp32 bound;
                 # y then gets the matching allowance (reading 39)
                 adm = mx_h_admissible(xr, w1q, wfmt)
-                flips += check_h_admissible(gh_codes[r0:r1], gh_scales[r0:r1], adm, f"h of expert {e}")
+                nflip = check_h_admissible(gh_codes[r0:r1], gh_scales[r0:r1], adm, f"h of expert {e}")
                 slack = mx_y_slack(adm, w2q, wfmt, hc, hs)
                 del adm
-                slack_r[slot[mine]] = slack[mine]
             else:
                 _, y64, yb = oep.expert_ffn(ref["x"][src, slot // k], ref["w1"][i], ref["w2"][i])
-                slack = None
             assert_close(comb[src, slot], y64, f"{prec} {routing} expert {e} combine rows", slack)
-            comb_r[slot[mine]] = yb[mine]
+            return slot[mine], yb[mine], (slack[mine] if mx else None), nflip
+
+        # experts are checked concurrently (their element-wise steps release the interpreter lock)
+        with cf.ThreadPoolExecutor(4) as pool:
+            for res in pool.map(lambda ie: check_expert(*ie), list(enumerate(experts))):
+                if res is None:
+                    continue
+                sl, yb, sk, nflip = res
+                comb_r[sl] = yb
+                if mx:
+                    slack_r[sl] = sk
+                    flips += nflip
         for q in range(cfg.n_src):
             if q != r:
                 assert (comb[q][~own[q]] == 0xFFFF).all(), f"combine window {q}: rows of other ranks touched"
