@@ -345,6 +345,20 @@ int xs_fused_ep_layer(const xs_ep_layer* L, const xs_pacing* pacing, const xs_tr
                       void* workspace, int64_t workspace_bytes, int32_t* dev_status,
                       void* stream);
 
+/* The same layer for callers that cannot allocate (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): no workspace argument; the layer's scratch (layout
+ * partial counts, tile tables, readiness and claim counters, MX token-row staging) lives in a
+ * library-owned device array of XS_STATIC_SCRATCH_BYTES on each GPU the library runs on, held
+ * until the process ends. Requires xs_ep_layer_workspace_bytes(L) <= XS_STATIC_SCRATCH_BYTES,
+ * else XS_EWORKSPACE and nothing is launched (the DeepSeek-V3-like share needs under 1 MiB in
+ * bf16 and about 31 MiB in the MX precisions). Calls no hipMalloc, hipFree or other allocating
+ * routine. Every call on one GPU shares that GPU's array and the kernels rewrite or clear all of
+ * it that they read, so consecutive calls on one stream are independent; calls that overlap on
+ * one GPU (other streams, other host threads) race on it. Otherwise as xs_fused_ep_layer. */
+#define XS_STATIC_SCRATCH_BYTES (48ll << 20)
+int xs_fused_ep_layer_noalloc(const xs_ep_layer* L, const xs_pacing* pacing, const xs_trace* trace,
+                              int32_t* dev_status, void* stream);
+
 /* ----------------------------------------------------------------------------- GEMM
  * C = A B^T with bf16 operands and fp32 accumulation, bf16 output.
  *   a  device bf16 [M][K] (row stride lda elements), b device bf16 [N][K] (row stride ldb;

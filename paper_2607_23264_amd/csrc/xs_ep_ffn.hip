@@ -24,6 +24,7 @@
 // so the lowest row anyone waits on always has its Linear-1 owners running.
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 
 #include "xs_gemm_mx.hpp"
 
@@ -965,9 +966,53 @@ extern "C" int xs_combine_send(const xs_ep_layer* L, const xs_pacing* pacing, in
   return xs_host::signal_windows(cws, st);
 }
 
+static int fused_ep_layer(const xs_ep_layer* L, const xs_pacing* pacing, const xs_trace* trace,
+                          void* workspace, int64_t workspace_bytes, int32_t* dev_status, void* stream);
+
 extern "C" int xs_fused_ep_layer(const xs_ep_layer* L, const xs_pacing* pacing,
                                  const xs_trace* trace, void* workspace, int64_t workspace_bytes,
                                  int32_t* dev_status, void* stream) {
+  return fused_ep_layer(L, pacing, trace, workspace, workspace_bytes, dev_status, stream);
+}
+
+// ------------------------------------------------------------------------------ no-alloc layer
+// The layer's scratch for callers that cannot allocate: one library-owned array per GPU. Host
+// code never uses the array's name as an address (on the host it names a stand-in, not device
+// memory); it uses the device address hipGetSymbolAddress gives, taken once per device with
+// that device current and kept in g_scratch.
+static __device__ __align__(256) char scratch[XS_STATIC_SCRATCH_BYTES];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch[256] = {};
+}  // namespace
+
+static int scratch_of_current_device(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 256) return XS_EHIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return XS_EHIP;
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return XS_OK;
+}
+
+extern "C" int xs_fused_ep_layer_noalloc(const xs_ep_layer* L, const xs_pacing* pacing,
+                                         const xs_trace* trace, int32_t* dev_status, void* stream) {
+  int64_t need = 0;
+  int rc = xs_ep_layer_workspace_bytes(L, &need);
+  if (rc) return rc;
+  if (need > XS_STATIC_SCRATCH_BYTES) return XS_EWORKSPACE;
+  void* ws = nullptr;
+  if ((rc = scratch_of_current_device(&ws))) return rc;
+  return fused_ep_layer(L, pacing, trace, ws, XS_STATIC_SCRATCH_BYTES, dev_status, stream);
+}
+
+static int fused_ep_layer(const xs_ep_layer* L, const xs_pacing* pacing, const xs_trace* trace,
+                          void* workspace, int64_t workspace_bytes, int32_t* dev_status, void* stream) {
   int rc = validate(L, true);
   if (rc) return rc;
   if (pacing && (pacing->policy < XS_POLICY_BURST || pacing->policy > XS_POLICY_AUTO ||

@@ -167,6 +167,9 @@ xs_model_predict = _sig("xs_model_predict", C.c_int, P(xs_model), P(xs_burst), i
 xs_model_fit = _sig("xs_model_fit", C.c_int, P(xs_calib), P(xs_model))
 xs_xstage_microbench = _sig("xs_xstage_microbench", C.c_int, P(xs_microbench_args), P(xs_trace), vp)
 xs_clock_rate_hz = _sig("xs_clock_rate_hz", C.c_double)
+XS_STATIC_SCRATCH_BYTES = 48 << 20
+xs_fused_ep_layer_noalloc = _sig("xs_fused_ep_layer_noalloc", C.c_int, P(xs_ep_layer), P(xs_pacing), P(xs_trace),
+                                 vp, vp)
 xs_grouped_gemm = _sig("xs_grouped_gemm", C.c_int, vp, i64, i32, vp, vp, i32, vp, i32, i32, vp, i64, i32, vp, vp)
 xs_drain_rate = _sig("xs_drain_rate", C.c_int, vp, vp, i32, P(f64))
 xs_calib_knee = _sig("xs_calib_knee", C.c_int, vp, vp, i32, f64, P(i32))
@@ -182,7 +185,7 @@ EXPORTED = ["xs_strerror", "xs_version", "xs_route_topk_softmax", "xs_dispatch_l
             "xs_scatter_copy", "xs_attention", "xs_ulysses_copy", "xs_quantize_mx", "xs_quantize_mx_grouped", "xs_gemm_mx", "xs_dispatch_rows",
             "xs_ring_slot_bytes", "xs_dispatch_ring_workspace_bytes", "xs_dispatch_ring",
             "xs_model_predict", "xs_model_fit", "xs_pacing_audit_run", "xs_trace_tile_times",
-            "xs_grouped_gemm", "xs_drain_rate", "xs_calib_knee", "xs_model_calibrate", "xs_burst_gap", "xs_recovery_audit",
+            "xs_grouped_gemm", "xs_fused_ep_layer_noalloc", "xs_drain_rate", "xs_calib_knee", "xs_model_calibrate", "xs_burst_gap", "xs_recovery_audit",
             "xs_xstage_microbench", "xs_clock_rate_hz"]
 
 
