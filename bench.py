@@ -294,7 +294,7 @@ def slow_sink_line(reps=5):
     from paper_2607_23264_amd import slow_sink as ss
     rep = ss.run(quick=True, reps=reps)
     keep = ("policy", "chunk", "kernel_us", "control_kernel_us", "speedup_over_burst",
-            "stall_measured_us_per_producer", "stall_predicted_us_per_producer",
+            "stall_measured_us_per_producer", "stall_predicted_us_per_producer", "time_lost_us",
             "staging_wait_measured_us_per_producer", "mma_stall_predicted_us_per_producer",
             "stall_fraction_measured", "stall_fraction_predicted", "mainloop_excess_us_per_producer",
             "dependency_wait_excess_us_per_producer", "l2_issue_us_median", "l2_issue_us_p90", "rate_feasible_eq9")

@@ -122,10 +122,11 @@ int xs_dispatch(const void* x, int32_t T, int32_t H, const int32_t* topk_idx,
                 const int32_t* slot_row, int32_t k, int32_t E, const xs_window* win, int32_t W,
                 int32_t* dev_status, void* stream);
 
-/* The same one-sided row stores for rows of any byte length (a multiple of 16, rows
- * row_stride bytes apart, 16-byte aligned): e.g. MXFP8 token rows of H codes then H / 32
- * scales (xs_quantize_mx into caller staging, then this). Windows need row_stride_bytes >=
- * row_bytes. Errors as xs_dispatch. */
+/* The same one-sided row stores (Sec. 2.1; the quantized EP runs of Sec. 5.2 dispatch quantized
+ * token rows) for rows of any byte length (a multiple of 16, rows row_stride bytes apart,
+ * 16-byte aligned): e.g. MXFP8 token rows of H codes then H / 32 scales (xs_quantize_mx into
+ * caller staging, then this). Windows need row_stride_bytes >= row_bytes. Errors as
+ * xs_dispatch. */
 int xs_dispatch_rows(const void* rows, int64_t row_stride, int32_t row_bytes, int32_t T,
                      const int32_t* topk_idx, const int32_t* slot_row, int32_t k, int32_t E,
                      const xs_window* win, int32_t W, int32_t* dev_status, void* stream);
@@ -330,7 +331,9 @@ int xs_expert_ffn(const xs_ep_layer* L, void* workspace, int64_t workspace_bytes
  * are ignored. Every setting stores the same bytes. */
 int xs_combine_send(const xs_ep_layer* L, const xs_pacing* pacing, int32_t* dev_status, void* stream);
 
-/* Combine-reduce: out[t] = bf16(sum_{j<k} w[t][j] * C[t*k + j]), fp32 sum in ascending j.
+/* Combine-reduce (the receiving side of the Combine exchange, Sec. 4.3: the source rank weighs
+ * the k expert outputs of each token by its gate weights once they are ready, Sec. 2.1):
+ * out[t] = bf16(sum_{j<k} w[t][j] * C[t*k + j]), fp32 sum in ascending j.
  *   cbuf device bf16 [T*k][H] (row stride cbuf_stride_bytes), topk_w device fp32 [T][k],
  *   out device bf16 [T][H]. Requires H % 8 == 0. */
 int xs_combine_reduce(const void* cbuf, int64_t cbuf_stride_bytes, const float* topk_w,
@@ -360,7 +363,9 @@ int xs_fused_ep_layer_noalloc(const xs_ep_layer* L, const xs_pacing* pacing, con
                               int32_t* dev_status, void* stream);
 
 /* ----------------------------------------------------------------------------- GEMM
- * C = A B^T with bf16 operands and fp32 accumulation, bf16 output.
+ * The plain local GEMM of row-parallel tensor parallelism (Sec. 4.5: each rank computes its
+ * partial Y_r = X_r W_r) without a scatter epilogue, the compute-only baseline of the fused
+ * calls: C = A B^T with bf16 operands and fp32 accumulation, bf16 output.
  *   a  device bf16 [M][K] (row stride lda elements), b device bf16 [N][K] (row stride ldb;
  *      the weight's output-major layout), c device bf16 [M][N] (row stride ldc).
  * Requires N % 256 == 0, K % 64 == 0, strides multiples of 8. */
@@ -619,11 +624,12 @@ int xs_recovery_audit(const xs_model* m, double V_bytes, int32_t n_bursts, doubl
  * XS_POLICY_AUTO makes with it (App. A.1: the average-rate bound of Eq. 9 is necessary but
  * not sufficient; the concrete order must pass the backlog recurrence and capacity guard).
  * For one order the burst sequence is rebuilt from the schedule (Sec. 4.2): producer 0's own
- * tile stream (static claiming, the grid's G producers), each of its Linear-2 epilogues one
- * burst of the fully aligned producers, V = K_act V_t with K_act = G and V_t the tile's
- * stored bytes times sink_share; G_n = the mainloops that follow before the next burst (T_L1
- * per Linear-1 tile, T_L2 for the next Linear-2 tile); cover = T0 (a workgroup issues its own
- * epilogue stores, so only the floor issue is covered). Rows per local expert come from
+ * tile stream (static claiming, the grid's G producers); its n-th Linear-2 epilogue is the n-th
+ * burst, issued together with every other producer's n-th Linear-2 epilogue (full alignment),
+ * V_n = K_act V_t summed over those producers' tiles (V_t a tile's stored bytes times
+ * sink_share; K_act < G once some producers have no n-th Linear-2 tile); G_n = producer 0's
+ * mainloops before its next burst (T_L1 per Linear-1 tile, T_L2 for the next Linear-2 tile);
+ * cover = T0 (a workgroup issues its own epilogue stores, so only the floor issue is covered). Rows per local expert come from
  * pacing->expert_rows (else the uniform expectation), split into blocks as the kernel does.
  * Candidates: the given policy alone, or for XS_POLICY_AUTO: BURST (Expert-Wave), INTERLEAVE
  * at the given lead, and CHUNK c = 1, 2, 4, ..., 32. AUTO takes the least predicted stall;

@@ -155,18 +155,21 @@ def expert_blocks(rows_per_expert: Sequence[int], equal: bool) -> Tuple[List[int
     return sizes, owner
 
 
-def audit_bursts(tiles: Sequence[Tile], block_rows: Sequence[int], G: int, sink_share: float,
+def audit_bursts(streams: Sequence[Sequence[Tile]], block_rows: Sequence[int], sink_share: float,
                  T_L1: float, T_L2: float):
-    """The burst sequence a tile stream gives under full alignment (Sec. 4.2): every
-    Linear-2 tile of the stream is one burst of the G aligned producers, V = G * V_t with
-    V_t = its rows x 256 columns x 2 bytes x sink_share; the gap after it is the mainloop
-    time of the tiles that follow up to and including the next Linear-2 tile (T_L1 or T_L2
-    each). Returns (V list, gap list, producer mainloop time)."""
+    """The burst sequence of producer 0 (streams[0]) under full alignment of all the producers'
+    streams (Sec. 4.2): its n-th Linear-2 tile is issued together with the n-th Linear-2 tile
+    of every producer that has one, so V_n is the sum of those tiles' bytes (rows x 256 columns
+    x 2 bytes x sink_share each); the gap after it is producer 0's mainloop time up to and
+    including its next Linear-2 tile (T_L1 or T_L2 per tile). Returns (V list, gap list,
+    producer 0's mainloop time)."""
     V, gaps = [], []
+    tiles = streams[0]
     compute = sum(T_L1 if kind == 1 else T_L2 for kind, _, _ in tiles)
+    l2_rows = [[row for kind, row, _ in s if kind == 2] for s in streams]
     l2_at = [i for i, t in enumerate(tiles) if t[0] == 2]
     for n, i in enumerate(l2_at):
-        V.append(G * block_rows[tiles[i][1]] * 256 * 2 * sink_share)
+        V.append(sum(block_rows[r[n]] * 256 * 2 * sink_share for r in l2_rows if len(r) > n))
         stop = l2_at[n + 1] + 1 if n + 1 < len(l2_at) else len(tiles)
         gaps.append(sum(T_L1 if tiles[j][0] == 1 else T_L2 for j in range(i + 1, stop)))
     return V, gaps, compute
@@ -193,10 +196,10 @@ def pacing_audit(rows_per_expert, equal_blocks: bool, P1: int, P2: int, G: int, 
     res = {}
     for pol, c in cands:
         if pol == "wave":
-            tiles = expert_wave_stream(0, G, P, P1, P2, waves_by_tiles(owner, P1, wave_tiles))
+            streams = all_streams("wave", G, P, P1, P2, waves=waves_by_tiles(owner, P1, wave_tiles))
         else:
-            tiles = interleave_stream(0, G, P, P1, P2, D, chunk=c)
-        V, gaps, compute = audit_bursts(tiles, sizes, G, sink_share, T_L1, T_L2)
+            streams = [interleave_stream(g, G, P, P1, P2, D, chunk=c) for g in range(G)]
+        V, gaps, compute = audit_bursts(streams, sizes, sink_share, T_L1, T_L2)
         T0 = [t0_a + t0_b * v for v in V]
         pred = xm.predict(V, T0, gaps, R, Q)
         res[(pol, c)] = (sum(p.stall for p in pred), len(pred), sum(not p.guard_ok for p in pred), compute)

@@ -635,34 +635,48 @@ __global__ __launch_bounds__(256) void ep_identity_kernel(EpArgs a, const int* _
 // Unfused combine-send: computed row -> combine window of its source. Each workgroup is one
 // producer issuing bursts of `burst_rows` consecutive computed rows (burst b of producer g is
 // rows [(g + b G) burst_rows, ... + burst_rows)), optionally followed by a non-injecting gap.
-// A wave copies one row at a time with up to 8 16-byte loads in flight per lane before their
-// stores.
+// A wave copies two rows at a time, 8 16-byte pieces of each per lane in flight before their
+// stores; the rows and their destinations are wave-uniform.
 __global__ __launch_bounds__(256) void ep_combine_send_kernel(EpArgs a, const int* __restrict__ dest_counts,
                                                               int n_cwin, int burst_rows) {
   __shared__ int base[XS_MAX_WINDOWS + 1];
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int total = window_prefix(a, dest_counts, n_cwin, base);
   const int npc = a.H / 8;   // 16-byte pieces per row
   for (int b0 = blockIdx.x * burst_rows; b0 < total; b0 += gridDim.x * burst_rows) {
     const int b1 = min(total, b0 + burst_rows);
-    for (int gr = b0 + wv; gr < b1; gr += 4) {
-      int dl = 0;
-      while (base[dl + 1] <= gr) ++dl;
-      u32x4* dst = reinterpret_cast<u32x4*>(combine_row(a, dl, gr - base[dl]));
-      if (!dst) continue;
-      const u32x4* src = reinterpret_cast<const u32x4*>(a.y + static_cast<int64_t>(gr) * a.H);
+    for (int gr = b0 + 2 * wv; gr < b1; gr += 8) {
+      u32x4* dst[2];
+      const u32x4* src[2];
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const int r = gr + q;
+        dst[q] = nullptr;
+        src[q] = nullptr;
+        if (r < b1) {
+          int dl = 0;
+          while (base[dl + 1] <= r) ++dl;
+          dst[q] = reinterpret_cast<u32x4*>(combine_row(a, dl, r - base[dl]));
+          src[q] = reinterpret_cast<const u32x4*>(a.y + static_cast<int64_t>(r) * a.H);
+        }
+      }
       for (int p0 = 0; p0 < npc; p0 += 8 * 64) {
-        u32x4 v[8];
+        u32x4 v[2][8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int pc = p0 + u * 64 + lane;
-          if (pc < npc) v[u] = __builtin_nontemporal_load(src + pc);
-        }
+        for (int q = 0; q < 2; ++q)
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int pc = p0 + u * 64 + lane;
-          if (pc < npc) dst[pc] = v[u];
-        }
+          for (int u = 0; u < 8; ++u) {
+            const int pc = p0 + u * 64 + lane;
+            if (dst[q] && pc < npc) v[q][u] = src[q][pc];
+          }
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            const int pc = p0 + u * 64 + lane;
+            if (dst[q] && pc < npc) dst[q][pc] = v[q][u];
+          }
       }
     }
     if (a.gap_ticks) {

@@ -190,15 +190,57 @@ struct Eval {
   double stall = 0, mma = 0, compute = 0;
 };
 
-Eval evaluate(const Order& o, const std::vector<int>& block_rows, const xs_model& m, int G,
-              double share, double tl1, double tl2) {
+// Aligned burst volumes: the n-th burst is every producer's n-th Linear-2 tile issued together
+// (full alignment, Sec. 4.2), V_n = the sum of those tiles' stored bytes; a producer with fewer
+// Linear-2 tiles does not take part in the later bursts (K_act < G).
+std::vector<double> aligned_volumes(bool wave, const std::vector<int>& block_rows,
+                                    const std::vector<int>& block_expert, int P1, int P2, int G,
+                                    int wave_tiles, double share) {
+  const int P = static_cast<int>(block_rows.size());
+  std::vector<double> V;
+  auto add = [&](size_t n, int row) {
+    if (V.size() <= n) V.resize(n + 1, 0.0);
+    V[n] += static_cast<double>(block_rows[row]) * kTile * 2.0 * share;
+  };
+  if (!wave) {
+    // producer g's Linear-2 tiles are its own entries g, g + G, ... in order
+    const long n2 = static_cast<long>(P) * P2;
+    for (long e = 0; e < n2; ++e) add(static_cast<size_t>(e / G), static_cast<int>(e / P2));
+    return V;
+  }
+  std::vector<int> bounds{0};
+  int wl1 = 0;
+  for (int p = 0; p < P; ++p) {
+    wl1 += P1;
+    const bool last_of_expert = p + 1 == P || block_expert[p + 1] != block_expert[p];
+    if (last_of_expert && wl1 >= wave_tiles) {
+      bounds.push_back(p + 1);
+      wl1 = 0;
+    }
+  }
+  if (bounds.back() != P) bounds.push_back(P);
+  std::vector<int> count(G, 0);   // Linear-2 tiles each producer has taken so far
+  long pos = 0;
+  for (size_t w = 0; w + 1 < bounds.size(); ++w) {
+    const int r0 = bounds[w], r1 = bounds[w + 1];
+    const long n1 = static_cast<long>(r1 - r0) * P1, n2 = static_cast<long>(r1 - r0) * P2;
+    for (long i = 0; i < n1 + n2; ++i, ++pos) {
+      if (i < n1) continue;
+      const int g = static_cast<int>(pos % G);
+      add(static_cast<size_t>(count[g]++), static_cast<int>(r0 + (i - n1) / P2));
+    }
+  }
+  return V;
+}
+
+Eval evaluate(const Order& o, const std::vector<double>& Vn, const xs_model& m, double tl1, double tl2) {
   Eval ev;
   std::vector<xs_burst> b;
   const size_t n = o.kind.size();
   for (size_t i = 0; i < n; ++i) ev.compute += o.kind[i] == 1 ? tl1 : tl2;
   for (size_t i = 0; i < n; ++i) {
     if (o.kind[i] != 2) continue;
-    const double V = static_cast<double>(G) * block_rows[o.row[i]] * kTile * 2.0 * share;
+    const double V = b.size() < Vn.size() ? Vn[b.size()] : 0.0;
     const double T0 = m.t0_a_us + m.t0_b_us_per_byte * V;
     double gap = 0;
     for (size_t j = i + 1; j < n; ++j) {
@@ -274,10 +316,11 @@ extern "C" int xs_pacing_audit_run(const xs_ep_layer* L, const xs_pacing* pc, xs
   }
   out->n_cand = static_cast<int>(cands.size());
   for (size_t i = 0; i < cands.size(); ++i) {
-    const Order o = cands[i].first == XS_POLICY_BURST
-                        ? own_wave(block_expert, P1, P2, G, wave_tiles)
-                        : own_interleave(P, P1, P2, G, D, cands[i].second);
-    const Eval ev = evaluate(o, block_rows, m, G, share, tl1, tl2);
+    const bool wave = cands[i].first == XS_POLICY_BURST;
+    const Order o = wave ? own_wave(block_expert, P1, P2, G, wave_tiles)
+                         : own_interleave(P, P1, P2, G, D, cands[i].second);
+    const Eval ev = evaluate(o, aligned_volumes(wave, block_rows, block_expert, P1, P2, G, wave_tiles, share),
+                             m, tl1, tl2);
     out->cand_policy[i] = cands[i].first;
     out->cand_chunk[i] = cands[i].second;
     out->cand_bursts[i] = ev.bursts;

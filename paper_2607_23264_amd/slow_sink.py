@@ -160,6 +160,8 @@ def evaluate(name: str, make_layer, policies: dict, model: X.xs_model, sink_shar
                    "kernel_us_p90": float(np.percentile(times, 90)),
                    "control_kernel_us": base["kernel_us"] if base else None,
                    "stall_measured_us_per_producer": float(excess.sum()) / G,
+                   # all the time the producers lose on the sink: kernel time beyond the control's
+                   "time_lost_us": k_us - base["kernel_us"] if base else None,
                    "stall_predicted_us_per_producer": au.cand_stall_us[i],
                    "mma_stall_predicted_us_per_producer": au.cand_mma_stall_us[i],
                    "staging_wait_measured_us_per_producer": float(stage.sum()) / G,
@@ -269,8 +271,9 @@ def share_inputs(routing: str, seed: int = 0):
 def run(quick=False, reps=5, routings=("zipf", "uniform"), seed=0):
     import synth
     torch.cuda.set_device(0)
-    ch, cd = calibrate_sinks(256, [16384, 65536, 262144] if quick else [4096, 16384, 65536, 131072, 262144],
-                             store_waves=8, target_bytes=256 << 20)
+    # five burst sizes (1 to 64 MiB aggregate): enough below the knee for the floor line and
+    # past it for the capacity bracket
+    ch, cd = calibrate_sinks(256, [4096, 16384, 65536, 131072, 262144], store_waves=8, target_bytes=256 << 20)
     model = to_model(ch, capacity="knee")
     report = {"sink_model": {k: ch.model[k] for k in ("t0_a_us", "t0_b_us_per_byte", "R_bytes_per_us",
                                                         "Q_knee_bracket_bytes", "Q_bytes")},

@@ -91,7 +91,7 @@ def test_audit_bursts_hand_traced():
     # Linear-2 tiles, and row 1's follow once Linear-1 is used up: L1 L2 L2 L1 L2 L2
     tiles = sc.interleave_stream(0, 1, P=2, P1=1, P2=2, D=1)
     assert [t[0] for t in tiles] == [1, 2, 2, 1, 2, 2]
-    V, gaps, comp = sc.audit_bursts(tiles, [100, 50], G=1, sink_share=0.5, T_L1=10.0, T_L2=3.0)
+    V, gaps, comp = sc.audit_bursts([tiles], [100, 50], sink_share=0.5, T_L1=10.0, T_L2=3.0)
     assert V == [100 * 256 * 2 * 0.5, 100 * 256 * 2 * 0.5, 50 * 256 * 2 * 0.5, 50 * 256 * 2 * 0.5]
     # after burst 0: the next Linear-2 mainloop; after burst 1: L1 + L2; then L2; last: nothing
     assert gaps == [3.0, 13.0, 3.0, 0.0]
@@ -112,7 +112,18 @@ def test_audit_rate_infeasible_stalls_every_order():
     # and the stall is at least the drain time the compute cannot cover, V_total / R - compute,
     # for producer 0's bursts (issue alone cannot drain faster than R)
     sizes, owner = sc.expert_blocks([1039] * 32, True)
-    tiles = sc.interleave_stream(0, 256, len(sizes), 16, 28, 16)
-    V, gaps, comp = sc.audit_bursts(tiles, sizes, 256, 1.0, 210.0, 64.0)
+    streams = [sc.interleave_stream(g, 256, len(sizes), 16, 28, 16) for g in range(256)]
+    V, gaps, comp = sc.audit_bursts(streams, sizes, 1.0, 210.0, 64.0)
     stall = res[("interleave", None)][0]
     assert stall >= sum(V) / 1000.0 - comp - 1e-6 - (1e6 / 1000.0)
+
+
+def test_aligned_volume_counts_only_producers_with_that_burst():
+    # 3 producers, 4 rows of 2 Linear-2 tiles: producer g owns entries g, g + 3, g + 6 < 8, so
+    # all three take part in the first two bursts and producers 0, 1 in the third
+    streams = [sc.interleave_stream(g, 3, P=4, P1=1, P2=2, D=1) for g in range(3)]
+    V, _, _ = sc.audit_bursts(streams, [10, 20, 30, 40], 1.0, 1.0, 1.0)
+    unit = 256 * 2
+    # burst 0: entries 0, 1, 2 -> rows 0, 0, 1; burst 1: entries 3, 4, 5 -> rows 1, 2, 2;
+    # burst 2: entries 6, 7 -> rows 3, 3 (producer 2 owns only 2 + 3 = 5 < 8 and 8 >= 8)
+    assert V == [(10 + 10 + 20) * unit, (20 + 30 + 30) * unit, (40 + 40) * unit]
