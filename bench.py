@@ -287,8 +287,8 @@ def store_ceiling(X, torch):
 
 def slow_sink_line(reps=5):
     """Store pacing against the host-coherent sink (paper_2607_23264_amd.slow_sink, quick sweep):
-    the tiny layer with every combine window on the sink (c5) and the DeepSeek-V3 share with two
-    of its eight source windows there, uniform and Zipf; per policy the kernel time on the sink
+    the tiny layer with every combine window on the sink (c5) and the DeepSeek-V3 share with one
+    and with two of its eight source windows there, uniform and Zipf; per policy the kernel time on the sink
     and on the HBM control, the speedup over Expert-Wave burst issue, and the stall per producer
     measured (issue spans and staging waits beyond the control) against the audit's prediction."""
     from paper_2607_23264_amd import slow_sink as ss
@@ -652,6 +652,14 @@ def main():
         comb_bytes = rows * cfg.H * 2
         ph["dispatch_store_GBps"] = disp_bytes / (ph["dispatch_us"] * 1e-6) / 1e9
         ph["combine_send_store_GBps"] = comb_bytes / (ph["combine_send_us"] * 1e-6) / 1e9
+        # combine-send reads every y row and stores it once: against a plain device copy of
+        # the same bytes
+        ph["combine_send_moved_GBps"] = 2 * ph["combine_send_store_GBps"]
+        cp_src = torch.empty(comb_bytes, dtype=torch.uint8, device="cuda")
+        cp_dst = torch.empty_like(cp_src)
+        ph["device_copy_same_bytes_us"] = timed(lambda: cp_dst.copy_(cp_src))
+        ph["combine_send_frac_of_device_copy"] = ph["device_copy_same_bytes_us"] / ph["combine_send_us"]
+        del cp_src, cp_dst
         ph["combine_reduce_GBps"] = (cfg.T * cfg.k * cfg.H * 2 + cfg.T * cfg.H * 2) / (ph["combine_reduce_us"] * 1e-6) / 1e9
         for name, p in pol.items():
             if a.policies or name == a.policy:

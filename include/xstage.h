@@ -326,9 +326,9 @@ int xs_expert_ffn(const xs_ep_layer* L, void* workspace, int64_t workspace_bytes
  * combine window s at row t*k+j where row_src[d][r] = (s << 24) | (t*k+j). Unfused form of
  * the Linear-2 epilogue stores; reads y_ws. pacing (nullable) shapes the bursts the combine
  * windows see: max_producers workgroups (0 = eight per CU) each store bursts of chunk_tiles
- * blocks of 256 consecutive computed rows (0 = 64 rows), burst b of producer g being block
- * g + b * producers, with a non-injecting gap of gap_ns after each burst; the other fields
- * are ignored. Every setting stores the same bytes. */
+ * blocks of 256 consecutive computed rows (chunk_tiles 0: bursts of 8 rows), burst b of
+ * producer g being burst-sized block g + b * producers, with a non-injecting gap of gap_ns
+ * after each burst; the other fields are ignored. Every setting stores the same bytes. */
 int xs_combine_send(const xs_ep_layer* L, const xs_pacing* pacing, int32_t* dev_status, void* stream);
 
 /* Combine-reduce (the receiving side of the Combine exchange, Sec. 4.3: the source rank weighs

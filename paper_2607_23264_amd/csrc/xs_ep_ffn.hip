@@ -970,9 +970,10 @@ extern "C" int xs_combine_send(const xs_ep_layer* L, const xs_pacing* pacing, in
   if (rc) return rc;
   a.status = dev_status;
   // producers: max_producers workgroups (default eight per CU); a burst is chunk_tiles blocks of
-  // 256 rows (default 64 rows)
+  // 256 rows, or by default 8 rows (one pass of the workgroup's four waves), so that the rows
+  // spread over every wave of the grid rather than over a few workgroups' long row ranges
   const int grid = pacing && pacing->max_producers > 0 ? pacing->max_producers : 8 * xs_host::persistent_grid(0);
-  const int burst_rows = pacing && pacing->chunk_tiles > 0 ? pacing->chunk_tiles * kBM : 64;
+  const int burst_rows = pacing && pacing->chunk_tiles > 0 ? pacing->chunk_tiles * kBM : 8;
   a.gap_ticks = pacing ? xs_host::ns_to_ticks(pacing->gap_ns) : 0;
   hipLaunchKernelGGL(ep_combine_send_kernel, dim3(grid), dim3(256), 0, st, a, L->dest_counts,
                      n_cwin_of(L), burst_rows);

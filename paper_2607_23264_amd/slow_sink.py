@@ -268,7 +268,7 @@ def share_inputs(routing: str, seed: int = 0):
     return cfg, inp
 
 
-def run(quick=False, reps=5, routings=("zipf", "uniform"), seed=0):
+def run(quick=False, reps=5, routings=("zipf", "uniform"), sink_windows=(1, 2), seed=0):
     import synth
     torch.cuda.set_device(0)
     # five burst sizes (1 to 64 MiB aggregate): enough below the knee for the floor line and
@@ -286,10 +286,15 @@ def run(quick=False, reps=5, routings=("zipf", "uniform"), seed=0):
                                      tiny_policies(caps, chunks), model, 1.0, reps))
     for routing in routings:
         scfg, sinp = share_inputs(routing, seed)
-        hosts = [q for q in range(scfg.n_src) if q != scfg.rank][:2]
-        report["layers"].append(evaluate(f"{scfg.name} ({routing}, rank {scfg.rank}; combine windows of sources "
-                                         f"{hosts} on the sink)", share_layer(scfg, sinp, hosts), SHARE_POLICIES,
-                                         model, len(hosts) / scfg.n_src, reps))
+        others = [q for q in range(scfg.n_src) if q != scfg.rank]
+        # one source window on the sink: the average rate leaves the sink half idle (Eq. 9 holds
+        # with room), yet aligned Linear-2 bursts can still exceed the capacity; two windows:
+        # the sink close to saturation
+        for n_host in sink_windows:
+            hosts = others[:n_host]
+            report["layers"].append(evaluate(f"{scfg.name} ({routing}, rank {scfg.rank}; combine windows of sources "
+                                             f"{hosts} on the sink)", share_layer(scfg, sinp, hosts),
+                                             SHARE_POLICIES, model, len(hosts) / scfg.n_src, reps))
         del sinp
     return report
 
