@@ -633,9 +633,9 @@ int xs_recovery_audit(const xs_model* m, double V_bytes, int32_t n_bursts, doubl
  * pacing->expert_rows (else the uniform expectation), split into blocks as the kernel does.
  * Candidates: the given policy alone, or for XS_POLICY_AUTO: BURST (Expert-Wave), INTERLEAVE
  * at the given lead, and CHUNK c = 1, 2, 4, ..., 32. AUTO takes the least predicted stall;
- * among the candidates within 1 % of BURST's mainloop time of it, BURST first (it keeps each
- * expert's weights together, the working-set side of the choice, Sec. 5.3), then INTERLEAVE,
- * then the largest chunk.
+ * among the candidates within 1 % of BURST's mainloop time of it, INTERLEAVE first, then the
+ * largest chunk, then BURST (the compute side of the choice, Sec. 5.3: Expert-Wave's Linear-2
+ * tiles wait for their wave's Linear-1 tiles, which the audit does not price).
  * Host-only and synchronous; needs the current device only for the grid size. */
 #define XS_AUDIT_MAX 16
 typedef struct xs_pacing_audit {

@@ -182,10 +182,11 @@ def pacing_audit(rows_per_expert, equal_blocks: bool, P1: int, P2: int, G: int, 
     """Audit of producer 0's tile order (Sec. 4.1 with Eqs. 3-6 via xstage_model.predict) and
     the automatic choice among "wave" (Expert-Wave), "interleave" and "chunk" c in 1, 2, 4,
     ..., 32: the least predicted stall, and among the candidates within 1 % of the Expert-Wave
-    order's mainloop time of it, Expert-Wave first (it keeps an expert's weights together),
-    then the plain interleave, then the larger chunk (a reading: the paper asks to pick the
-    order from X-Stage pressure and working-set size, Sec. 5.3). Returns (choice (policy,
-    chunk), {candidate: (stall, bursts, guard failures, mainloop time)})."""
+    order's mainloop time of it, the plain interleave first, then the larger chunk, then
+    Expert-Wave (a reading: the paper weighs X-Stage pressure against the rest of the
+    schedule, Sec. 5.3, and Expert-Wave's Linear-2 tiles wait for their whole wave's Linear-1
+    tiles, a cost the audit does not price). Returns (choice (policy, chunk), {candidate:
+    (stall, bursts, guard failures, mainloop time)})."""
     from . import xstage_model as xm
     sizes, owner = expert_blocks(rows_per_expert, equal_blocks)
     P = len(sizes)
@@ -208,7 +209,9 @@ def pacing_audit(rows_per_expert, equal_blocks: bool, P1: int, P2: int, G: int, 
     tol = 0.01 * res[("wave", None)][3]
     best = min(v[0] for v in res.values())
     near = [key for key in cands if res[key][0] <= best + tol]
-    for pref in (("wave", None), ("interleave", None)):
-        if pref in near:
-            return pref, res
-    return max(near, key=lambda key: key[1]), res
+    if ("interleave", None) in near:
+        return ("interleave", None), res
+    chunks = [key for key in near if key[0] == "chunk"]
+    if chunks:
+        return max(chunks, key=lambda key: key[1]), res
+    return ("wave", None), res

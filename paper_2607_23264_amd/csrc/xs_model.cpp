@@ -332,16 +332,17 @@ extern "C" int xs_pacing_audit_run(const xs_ep_layer* L, const xs_pacing* pc, xs
   int pick = 0;
   if (pc->policy == XS_POLICY_AUTO) {
     // the least predicted stall; among the candidates within 1 % of BURST's mainloop time of
-    // it, BURST first (it keeps each expert's weights together), then the plain interleave,
-    // then the largest chunk
+    // it, the plain interleave first, then the largest chunk, then BURST (Expert-Wave's
+    // Linear-2 tiles wait for their whole wave's Linear-1 tiles, a cost outside the audit
+    // that made it the slower order on HBM windows in every layer measured)
     double best = out->cand_stall_us[0];
     for (int i = 1; i < out->n_cand; ++i) best = std::min(best, out->cand_stall_us[i]);
     const double tol = 0.01 * out->cand_compute_us[0];
     pick = -1;
-    for (int i = 0; i < 2 && pick < 0; ++i)
-      if (out->cand_stall_us[i] <= best + tol) pick = i;
+    if (out->cand_stall_us[1] <= best + tol) pick = 1;
     for (int i = out->n_cand - 1; i >= 2 && pick < 0; --i)
       if (out->cand_stall_us[i] <= best + tol) pick = i;
+    if (pick < 0) pick = 0;
   }
   out->policy = out->cand_policy[pick];
   out->chunk = out->cand_chunk[pick];

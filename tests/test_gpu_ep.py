@@ -431,8 +431,8 @@ SKEWED = synth.EPConfig("skewed_T2048_H2048_E8_k2_I512_W4", T=2048, H=2048, E=8,
                         rank=0, compute_all=True, routing="zipf")
 
 
-@pytest.mark.parametrize("Q,want", [(1e6, "interleave"), (float("inf"), "wave")])
-def test_auto_follows_the_audited_choice(Q, want):
+@pytest.mark.parametrize("D,Q,want", [(1, 1e6, "interleave"), (1, float("inf"), "interleave"), (4, 3e6, "wave")])
+def test_auto_follows_the_audited_choice(D, Q, want):
     """AUTO with a model: the library audits every candidate order and runs the one with the least
     predicted stall; the traced tile order of every workgroup equals the schedule oracle's stream
     of the order the oracle's own audit picks."""
@@ -444,7 +444,7 @@ def test_auto_follows_the_audited_choice(Q, want):
     lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
     idx = oep.route_topk_softmax(inp["logits"][0], cfg.k)[0]
     counts = [int(c) for c in np.bincount(idx.ravel(), minlength=cfg.E)]
-    G, D, tl1, tl2 = 8, 1, 20.0, 10.0
+    G, tl1, tl2 = 8, 20.0, 10.0
     a, b, R = 1.0, 1e-7, 30000.0
     P1, P2 = cfg.I // 128, cfg.H // 256
     choice, _ = osc.pacing_audit(counts, True, P1, P2, G, D, G, 1.0, tl1, tl2, a, b, R, Q)

@@ -101,7 +101,7 @@ def test_audit_bursts_hand_traced():
 def test_audit_unbounded_capacity_and_fast_drain_predict_no_stall():
     for rows in ([1039] * 32, [30466, 128, 175, 9344] + [200] * 28):
         ch, res = sc.pacing_audit(rows, True, 16, 28, 256, 16, 256, 1.0, 210.0, 64.0, 1.0, 1e-8, 5.6e6, np.inf)
-        assert ch == ("wave", None)
+        assert ch == ("interleave", None)   # every order ties at zero: the preference decides
         assert all(v[0] == 0 and v[2] == 0 for v in res.values())
 
 
@@ -127,3 +127,17 @@ def test_aligned_volume_counts_only_producers_with_that_burst():
     # burst 0: entries 0, 1, 2 -> rows 0, 0, 1; burst 1: entries 3, 4, 5 -> rows 1, 2, 2;
     # burst 2: entries 6, 7 -> rows 3, 3 (producer 2 owns only 2 + 3 = 5 < 8 and 8 >= 8)
     assert V == [(10 + 10 + 20) * unit, (20 + 30 + 30) * unit, (40 + 40) * unit]
+
+
+def test_audit_prefers_interleave_and_takes_wave_only_when_it_stalls_less():
+    # a skewed 8-expert layer (rows per expert from Zipf routing), 8 producers, P1 = 4, P2 = 8
+    rows = [210, 177, 292, 820, 224, 497, 383, 1493]
+    args = (True, 4, 8, 8)
+    # stalls within 1 % of the compute: interleave
+    ch, res = sc.pacing_audit(rows, *args, 1, 8, 1.0, 20.0, 10.0, 1.0, 1e-7, 30000.0, 1e6)
+    assert ch == ("interleave", None)
+    # with a longer lead Expert-Wave's bursts stall clearly less than every other order's
+    ch, res = sc.pacing_audit(rows, *args, 4, 8, 1.0, 20.0, 10.0, 1.0, 1e-7, 30000.0, 3e6)
+    tol = 0.01 * res[("wave", None)][3]
+    assert all(res[("wave", None)][0] < v[0] - tol for k, v in res.items() if k != ("wave", None))
+    assert ch == ("wave", None)
