@@ -299,6 +299,7 @@ def slow_sink_line(reps=5):
             "stall_fraction_measured", "stall_fraction_predicted", "mainloop_excess_us_per_producer",
             "dependency_wait_excess_us_per_producer", "l2_issue_us_median", "l2_issue_us_p90", "rate_feasible_eq9")
     return {"sink_model": rep["sink_model"], "hbm_R_bytes_per_us": rep["hbm_R_bytes_per_us"],
+            "gap_sweep": rep["gap_sweep"], "producer_sweep": rep["producer_sweep"],
             "layers": [{"layer": L["layer"], "sink_share": L["sink_share"],
                         "control_tile_times_us": L.get("control_tile_times_us"),
                         "policies": {k: {f: v.get(f) for f in keep} for k, v in L["policies"].items()}}
@@ -660,6 +661,28 @@ def main():
         ph["device_copy_same_bytes_us"] = timed(lambda: cp_dst.copy_(cp_src))
         ph["combine_send_frac_of_device_copy"] = ph["device_copy_same_bytes_us"] / ph["combine_send_us"]
         del cp_src, cp_dst
+        # the same expert FFN as two standalone grouped GEMMs (xs_grouped_gemm): Linear-1 with
+        # the SwiGLU epilogue, then Linear-2, each local expert one segment of this rank's
+        # dispatch window; the MFMA utilisation of the GEMM phase on its own
+        e0, ne = experts[0], len(experts)
+        seg_off = lay.expert_offsets[e0:e0 + ne].contiguous()
+        seg_rows = torch.minimum(lay.expert_counts[:, e0:e0 + ne].sum(0).to(torch.int32),
+                                 lay.cap - seg_off).to(torch.int32).contiguous()
+        a_win = lay.dwin[e0 // (cfg.E // cfg.W)]
+        h_g = torch.empty((lay.cap, cfg.I), dtype=torch.int16, device="cuda")
+        y_g = torch.empty((lay.cap, cfg.H), dtype=torch.int16, device="cuda")
+        gg1 = lambda: X.check(X.xs_grouped_gemm(a_win.data_ptr(), cfg.H, lay.cap, seg_off.data_ptr(), seg_rows.data_ptr(),
+                                                ne, lay.w1.data_ptr(), 2 * cfg.I, cfg.H, h_g.data_ptr(), cfg.I,
+                                                X.XS_EPI_SWIGLU, lay.status.data_ptr(), lay.stream), "grouped_gemm")
+        gg2 = lambda: X.check(X.xs_grouped_gemm(h_g.data_ptr(), cfg.I, lay.cap, seg_off.data_ptr(), seg_rows.data_ptr(),
+                                                ne, lay.w2.data_ptr(), cfg.H, cfg.I, y_g.data_ptr(), cfg.H,
+                                                X.XS_EPI_STORE, lay.status.data_ptr(), lay.stream), "grouped_gemm")
+        ph["grouped_gemm_l1_swiglu_us"] = timed(gg1)
+        ph["grouped_gemm_l2_us"] = timed(gg2)
+        gg_us = ph["grouped_gemm_l1_swiglu_us"] + ph["grouped_gemm_l2_us"]
+        ph["grouped_gemm_TFLOPs"] = flops / (gg_us * 1e-6) / 1e12
+        ph["grouped_gemm_mfma_frac"] = flops / (gg_us * 1e-6) / MFMA_PEAK_BF16
+        del h_g, y_g
         ph["combine_reduce_GBps"] = (cfg.T * cfg.k * cfg.H * 2 + cfg.T * cfg.H * 2) / (ph["combine_reduce_us"] * 1e-6) / 1e9
         for name, p in pol.items():
             if a.policies or name == a.policy:

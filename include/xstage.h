@@ -244,11 +244,10 @@ enum { XS_EXPERT_SWIGLU = 0, XS_EXPERT_IDENTITY = 1 };
  *                        Linear-1 tiles per row.
  *   XS_POLICY_CHUNK      Alg. 1 with at most chunk_tiles consecutive Linear-2 tiles before
  *                        a ready Linear-1 tile is forced.
- *   XS_POLICY_AUTO       CHUNK with chunk_tiles chosen from `model`: the largest run of
- *                        aligned Linear-2 bursts per Linear-1 tile that meets the
- *                        average-rate bound (Eq. 9) for full alignment of the producers
- *                        (Sec. 4.2); INTERLEAVE when the bursts never outrun the drain or
- *                        without a model.
+ *   XS_POLICY_AUTO       the order xs_pacing_audit_run picks with `model` (Sec. 4.1, Eqs. 3-6
+ *                        over each candidate order's burst sequence: BURST, INTERLEAVE at
+ *                        lead_rows, CHUNK 1..32; the least predicted stall, ties to
+ *                        INTERLEAVE); INTERLEAVE without a model.
  * max_producers caps the persistent grid (0 = one workgroup per CU); wave_tiles is the
  * minimum Linear-1 tile count of an expert wave (0 = the grid size); gap_ns inserts a
  * non-injecting wait of that many nanoseconds after every Linear-2 store burst.

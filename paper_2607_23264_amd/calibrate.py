@@ -169,6 +169,35 @@ def calibrate(target_ptr: int, target_bytes: int, sink: str, K: int, Bs, knee_ex
     return Calibration(sink, K, model, rec, zg, iso, sweep)
 
 
+def producer_sweep(target_ptr: int, target_bytes: int, Ks, B: int, store_waves: int = 1,
+                   run_bytes: int = 240 << 20):
+    """The store path against the producer count K at B bytes per producer and burst (Sec. 3.1:
+    the microbenchmark's K axis): per K, the isolated burst's issue time (first start to last
+    issued store), the aggregate zero-gap drain rate K B / period, and the steady per-producer
+    period when each producer waits for its stores to complete before the next burst
+    (XS_MB_COMPLETION, the completion-coupled schedule of Sec. 3.2). Each zero-gap run stores
+    about run_bytes in all (at fresh addresses), several times what the sink absorbs before it
+    pushes back, so the period is the drain's and not the capacity's: with few producers the
+    bytes per producer and burst grow (powers of two from B) to keep a run within the
+    microbenchmark's 256 bursts."""
+    out = []
+    for K0 in Ks:
+        K, Bk = int(K0), int(B)
+        while K * Bk * 256 < run_bytes and target_bytes % (2 * Bk) == 0:
+            Bk *= 2
+        n = int(max(2, min(256, -(-run_bytes // (K * Bk)), target_bytes // (K * Bk))))
+        B_ = Bk
+        iso = float(np.median([run_bursts(target_ptr, target_bytes, K, B_, 1, 0, store_waves=store_waves)
+                               .aligned_iss_us[0] for _ in range(3)]))
+        zg = run_bursts(target_ptr, target_bytes, K, B_, n, 0, store_waves=store_waves)
+        cp = run_bursts(target_ptr, target_bytes, K, B_, n, 0, mode=X.XS_MB_COMPLETION, store_waves=store_waves)
+        period = zg.total_span_us / n
+        out.append({"K": K, "B": B_, "V": K * B_, "bursts": n, "isolated_issue_us": iso, "zero_gap_period_us": period,
+                    "drain_GBps": K * B_ / period / 1e3, "completion_period_us": cp.steady(cp.period_us),
+                    "completion_GBps": K * B_ / (cp.total_span_us / n) / 1e3})
+    return out
+
+
 def to_model(cal: Calibration, capacity: str = "fluid") -> X.xs_model:
     """xs_model from a calibration; capacity "fluid" takes the xs_model_fit Q, "knee" the lower
     end of the knee bracket (the largest volume seen absorbed without stalling)."""

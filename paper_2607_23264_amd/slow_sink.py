@@ -36,7 +36,7 @@ import numpy as np
 import torch
 
 from . import xstage as X
-from .calibrate import calibrate, to_model
+from .calibrate import calibrate, producer_sweep, to_model
 from .layer import EPLayer, HostCoherent, Shape, pacing
 
 
@@ -44,15 +44,28 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def calibrate_sinks(K, Bs, store_waves, target_bytes=1 << 30):
+SWEEP_KS = (1, 2, 4, 8, 16, 32, 64, 128, 256)
+
+
+def calibrate_sinks(K, Bs, store_waves, target_bytes=1 << 30, sweep_B=None):
+    """Burst-Gap calibration of the host-coherent sink and the HBM control at K producers; with
+    sweep_B also the producer-count sweep of both at sweep_B bytes per producer (returned as the
+    third value, {sink: rows})."""
     host = HostCoherent(target_bytes)
     hbm = torch.empty(target_bytes // 2, dtype=torch.int16, device="cuda")
+    sweeps = {}
     try:
         ch = calibrate(host.ptr, host.nbytes, "host-coherent", K, Bs, store_waves=store_waves, log=log)
         cd = calibrate(hbm.data_ptr(), hbm.numel() * 2, "hbm", K, Bs, store_waves=store_waves, log=log)
+        if sweep_B:
+            sweeps["host-coherent"] = producer_sweep(host.ptr, host.nbytes, SWEEP_KS, sweep_B, store_waves)
+            sweeps["hbm"] = producer_sweep(hbm.data_ptr(), hbm.numel() * 2, SWEEP_KS, sweep_B, store_waves)
+            for k, rows in sweeps.items():
+                log(f"[calibrate] {k} producer sweep at B = {sweep_B}: " + ", ".join(
+                    f"K={r['K']} {r['drain_GBps']:.1f} GB/s (iso {r['isolated_issue_us']:.1f} us)" for r in rows))
     finally:
         host.free()
-    return ch, cd
+    return (ch, cd, sweeps) if sweep_B else (ch, cd)
 
 
 class Traced:
@@ -273,14 +286,16 @@ def run(quick=False, reps=5, routings=("zipf", "uniform"), sink_windows=(1, 2), 
     torch.cuda.set_device(0)
     # five burst sizes (1 to 64 MiB aggregate): enough below the knee for the floor line and
     # past it for the capacity bracket
-    ch, cd = calibrate_sinks(256, [4096, 16384, 65536, 131072, 262144], store_waves=8, target_bytes=256 << 20)
+    ch, cd, sweeps = calibrate_sinks(256, [4096, 16384, 65536, 131072, 262144], store_waves=8,
+                                     target_bytes=256 << 20, sweep_B=65536)
     model = to_model(ch, capacity="knee")
     report = {"sink_model": {k: ch.model[k] for k in ("t0_a_us", "t0_b_us_per_byte", "R_bytes_per_us",
                                                         "Q_knee_bracket_bytes", "Q_bytes")},
-              "hbm_R_bytes_per_us": cd.model["R_bytes_per_us"], "layers": []}
+              "hbm_R_bytes_per_us": cd.model["R_bytes_per_us"], "gap_sweep": ch.gap_sweep,
+              "producer_sweep": sweeps, "layers": []}
     cfg = synth.EP_TINY
     inp = synth.ep_inputs(cfg, seed)
-    caps = [16, 0] if quick else [16, 64, 0]
+    caps = [16, 0] if quick else [8, 16, 32, 64, 0]
     chunks = [1, 8] if quick else [1, 2, 4, 8, 16, 32, 64]
     report["layers"].append(evaluate(cfg.name + " (every combine window on the sink)", tiny_layer(cfg, inp),
                                      tiny_policies(caps, chunks), model, 1.0, reps))
