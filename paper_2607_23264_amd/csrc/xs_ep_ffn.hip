@@ -186,8 +186,60 @@ __device__ __forceinline__ void trace_tile(const EpArgs& a, uint64_t kind, uint3
   }
 }
 
+// The rule every claim mode applies (App. A.2): Linear-2 entry e2 may run next when the first
+// Linear-1 entry not yet taken, e1, is at least the lead D rows past e2's row (or no Linear-1
+// entry is left), and the chunk cap, if set, still allows another Linear-2 tile before a
+// Linear-1 one ("run" Linear-2 tiles have run since the last Linear-1 tile).
+__device__ __forceinline__ bool l2_may_run(const EpArgs& a, int e2, int e1, int n1, int run) {
+  const bool l1_left = e1 < n1;
+  if (a.chunk > 0 && run >= a.chunk && l1_left) return false;
+  return !l1_left || e2 / a.P2 + a.lead <= e1 / a.P1;
+}
+
+// Thread 0's dynamic-claim state. The next tile is claimed ahead, during the current tile's
+// epilogue: the counters are read right after the mainloop (claim_load), their values decide
+// the next tile before the epilogue stores and at most one counter increment goes out there
+// (claim_take), and the loop top only reads its result (claim_next). The round trips to the
+// counters thus overlap the epilogue's staging and stores. The claim comes after the current
+// tile's mainloop, so after any dependency wait of that tile: a workgroup never holds a
+// claimed tile while it waits, and every Linear-1 tile a Linear-2 tile waits on still has an
+// owner that reaches it without waiting. What the early read cannot settle (a ticket not yet
+// eligible, a stream found exhausted) is left to ep_claim at the loop top. Counter values
+// read early only lag, so their eligibility tests are conservative.
+struct Claim {
+  int on;            // claim ahead (fused interleave / chunk with dynamic claiming)
+  int n1, n2;        // entries of the two streams
+  int run, ticket;   // Linear-2 tiles since the last Linear-1 tile; held ticket, -1 none, -2 no more
+  int c1, c2;        // counters as read after the mainloop
+  int kind, k;       // 0 nothing taken, 1 Linear-1 increment (k its result), 2 ticket increment,
+                     // 3 settled (k the claim value)
+};
+
+__device__ __forceinline__ void claim_load(const EpArgs& a, Claim* cl) {
+  if (!cl || !cl->on || threadIdx.x != 0) return;
+  cl->c1 = __hip_atomic_load(a.claim_ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  cl->c2 = __hip_atomic_load(a.claim_ctr + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  cl->kind = 0;
+}
+
+__device__ __forceinline__ void claim_take(const EpArgs& a, Claim* cl) {
+  if (!cl || !cl->on || threadIdx.x != 0) return;
+  if (cl->ticket >= 0 && l2_may_run(a, cl->ticket, cl->c1, cl->n1, cl->run)) {
+    cl->k = -cl->ticket - 2;
+    cl->ticket = -1;
+    ++cl->run;
+    cl->kind = 3;
+  } else if (cl->ticket == -1 && cl->c2 < cl->n2 && l2_may_run(a, cl->c2, cl->c1, cl->n1, cl->run)) {
+    cl->k = __hip_atomic_fetch_add(a.claim_ctr + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    cl->kind = 2;
+  } else if (cl->c1 < cl->n1) {
+    cl->k = __hip_atomic_fetch_add(a.claim_ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    cl->kind = 1;
+  }
+}
+
 __device__ __forceinline__ void ep_l1_tile(const EpArgs& a, int p, int nt, bool fused,
-                                           char* lds, char** rowptr) {
+                                           char* lds, char** rowptr, Claim* cl) {
   const int tid = threadIdx.x;
   const int x = a.row_expert[p];
   const int e = a.e_begin + x;
@@ -202,12 +254,14 @@ __device__ __forceinline__ void ep_l1_tile(const EpArgs& a, int p, int nt, bool 
   const uint16_t* B = a.w1 + static_cast<int64_t>(x) * 2 * a.I * a.H;
   Acc acc;
   gemm_mainloop(A, lda, rows, B, a.H, nt * (kBN / 2), a.I, true, a.H, acc, lds);
+  claim_load(a, cl);
   const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
   if (tid < rows)
     rowptr[tid] = reinterpret_cast<char*>(
         a.h + static_cast<int64_t>(a.exp_hrow[x] + m0 + tid) * a.I + nt * (kBN / 2));
   stage_swiglu(acc, lds);
   __syncthreads();
+  claim_take(a, cl);
   store_rows(lds, kEpiPitchH, kBN / 2, rows, rowptr);
   if (fused) {
     // The workgroup barrier orders every wave's h stores before thread 0's agent-scope
@@ -251,7 +305,7 @@ __device__ __forceinline__ bool ep_wait_row(const EpArgs& a, int p, int* flag) {
 }
 
 __device__ __forceinline__ void ep_l2_tile(const EpArgs& a, int p, int nt, bool fused,
-                                           char* lds, char** rowptr, int* flag) {
+                                           char* lds, char** rowptr, int* flag, Claim* cl) {
   const int tid = threadIdx.x;
   const uint64_t t0 = a.tr.buf ? wall_ticks() : 0;
   if (fused && !ep_wait_row(a, p, flag)) return;
@@ -271,6 +325,7 @@ __device__ __forceinline__ void ep_l2_tile(const EpArgs& a, int p, int nt, bool 
     code = a.row_src[static_cast<int64_t>(e / a.epw) * a.cap + a.expert_offsets[e] + m0 + tid];
   Acc acc;
   gemm_mainloop(A, a.I, rows, B, a.I, n0, 0, false, a.I, acc, lds);
+  claim_load(a, cl);
   const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
   if (tid < rows) {
     char* ptr;
@@ -290,6 +345,7 @@ __device__ __forceinline__ void ep_l2_tile(const EpArgs& a, int p, int nt, bool 
   }
   stage_tile(acc, lds);
   __syncthreads();
+  claim_take(a, cl);
   store_rows(lds, kEpiPitch, kBN, rows, rowptr);
   // The combine rows are read only after the kernel (window signal, combine-reduce): the
   // stores drain while the next tile runs.
@@ -315,7 +371,7 @@ __device__ __forceinline__ int xcd_instance_ep(int b, int G) {
 // scale groups (group nt / 4, word nt % 4).
 template <bool BF4>
 __device__ __forceinline__ void ep_l1_tile_mx(const EpArgs& a, int p, int nt, bool fused, char* lds,
-                                              char** rowptr) {
+                                              char** rowptr, Claim* cl) {
   const int tid = threadIdx.x;
   const int x = a.row_expert[p];
   const int e = a.e_begin + x;
@@ -334,11 +390,13 @@ __device__ __forceinline__ void ep_l1_tile_mx(const EpArgs& a, int p, int nt, bo
   AccMx acc;
   gemm_mainloop_mx<BF4>(A, ws, A + a.H, ws, 16, rows, B, ldb, Bs, 16, static_cast<int64_t>(a.n_experts) * 2 * a.I * 16,
                         nt * (kBN / 2), a.I, true, a.H, acc, lds);
+  claim_load(a, cl);
   const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
   const int64_t hrow0 = static_cast<int64_t>(a.exp_hrow[x] + m0);
   if (tid < rows) rowptr[tid] = reinterpret_cast<char*>(a.h) + (hrow0 + tid) * a.h_stride;
   stage_swiglu_mxq(acc, lds);
   __syncthreads();
+  claim_take(a, cl);
   typedef __attribute__((address_space(1))) u32x4 global_u32x4;
 #pragma unroll 1
   for (int i = tid; i < rows * 8; i += kMxThreads) {
@@ -363,7 +421,7 @@ __device__ __forceinline__ void ep_l1_tile_mx(const EpArgs& a, int p, int nt, bo
 // Linear-2 on MXFP8 h rows; bf16 output rows into the combine windows as in the bf16 tile.
 template <bool BF4>
 __device__ __forceinline__ void ep_l2_tile_mx(const EpArgs& a, int p, int nt, bool fused, char* lds,
-                                              char** rowptr, int* flag) {
+                                              char** rowptr, int* flag, Claim* cl) {
   const int tid = threadIdx.x;
   const uint64_t t0 = a.tr.buf ? wall_ticks() : 0;
   if (fused && !ep_wait_row(a, p, flag)) return;
@@ -387,6 +445,7 @@ __device__ __forceinline__ void ep_l2_tile_mx(const EpArgs& a, int p, int nt, bo
   AccMx acc;
   gemm_mainloop_mx<BF4>(A, a.h_stride, As, 16, a.h_rows * 16, rows, B, ldb, Bs, 16,
                         static_cast<int64_t>(a.n_experts) * a.H * 16, n0, 0, false, a.I, acc, lds);
+  claim_load(a, cl);
   const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
   if (tid < rows) {
     char* ptr = nullptr;
@@ -399,6 +458,7 @@ __device__ __forceinline__ void ep_l2_tile_mx(const EpArgs& a, int p, int nt, bo
   }
   stage_tile_mx(acc, lds);
   __syncthreads();
+  claim_take(a, cl);
   store_rows_n<kMxThreads>(lds, kEpiPitch * 2, kBN * 2 / 16, rows, rowptr);
   lds_barrier();
   if (tid == 0) {
@@ -412,25 +472,16 @@ __device__ __forceinline__ void ep_l2_tile_mx(const EpArgs& a, int p, int nt, bo
 
 // Tile dispatch by precision (PREC 0: bf16, 1: MXFP8, 2: W4A8).
 template <int PREC>
-__device__ __forceinline__ void l1_tile(const EpArgs& a, int p, int nt, bool fused, char* lds, char** rowptr) {
-  if constexpr (PREC > 0) ep_l1_tile_mx<PREC == 2>(a, p, nt, fused, lds, rowptr);
-  else ep_l1_tile(a, p, nt, fused, lds, rowptr);
+__device__ __forceinline__ void l1_tile(const EpArgs& a, int p, int nt, bool fused, char* lds, char** rowptr,
+                                        Claim* cl = nullptr) {
+  if constexpr (PREC > 0) ep_l1_tile_mx<PREC == 2>(a, p, nt, fused, lds, rowptr, cl);
+  else ep_l1_tile(a, p, nt, fused, lds, rowptr, cl);
 }
 template <int PREC>
 __device__ __forceinline__ void l2_tile(const EpArgs& a, int p, int nt, bool fused, char* lds, char** rowptr,
-                                        int* flag) {
-  if constexpr (PREC > 0) ep_l2_tile_mx<PREC == 2>(a, p, nt, fused, lds, rowptr, flag);
-  else ep_l2_tile(a, p, nt, fused, lds, rowptr, flag);
-}
-
-// The rule every claim mode applies (App. A.2): Linear-2 entry e2 may run next when the first
-// Linear-1 entry not yet taken, e1, is at least the lead D rows past e2's row (or no Linear-1
-// entry is left), and the chunk cap, if set, still allows another Linear-2 tile before a
-// Linear-1 one ("run" Linear-2 tiles have run since the last Linear-1 tile).
-__device__ __forceinline__ bool l2_may_run(const EpArgs& a, int e2, int e1, int n1, int run) {
-  const bool l1_left = e1 < n1;
-  if (a.chunk > 0 && run >= a.chunk && l1_left) return false;
-  return !l1_left || e2 / a.P2 + a.lead <= e1 / a.P1;
+                                        int* flag, Claim* cl = nullptr) {
+  if constexpr (PREC > 0) ep_l2_tile_mx<PREC == 2>(a, p, nt, fused, lds, rowptr, flag, cl);
+  else ep_l2_tile(a, p, nt, fused, lds, rowptr, flag, cl);
 }
 
 // Dynamic claiming. Thread 0 takes the next tile and broadcasts it through LDS:
@@ -441,9 +492,12 @@ __device__ __forceinline__ bool l2_may_run(const EpArgs& a, int e2, int e1, int 
 // Linear-2 tile waits on has an owner that runs it without waiting, and the holder of an
 // early ticket advances the Linear-1 frontier it waits for. The ticket is taken when the
 // shared Linear-2 counter's next entry is already eligible, so tickets are rarely held long.
-__device__ __forceinline__ int ep_claim(const EpArgs& a, int n1, int n2, int& run, int& ticket) {
+__device__ __forceinline__ int ep_claim(const EpArgs& a, Claim& cl) {
   int* c1p = a.claim_ctr;
   int* c2p = a.claim_ctr + 1;
+  const int n1 = cl.n1, n2 = cl.n2;
+  int& run = cl.run;
+  int& ticket = cl.ticket;
   for (;;) {
     const int c1 = __hip_atomic_load(c1p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (ticket == -1) {
@@ -474,11 +528,29 @@ __device__ __forceinline__ int ep_claim(const EpArgs& a, int n1, int n2, int& ru
   }
 }
 
+// The next tile: what claim_take settled or started during the last epilogue, else ep_claim.
+__device__ __forceinline__ int claim_next(const EpArgs& a, Claim& cl) {
+  const int kind = cl.kind;
+  cl.kind = 0;
+  if (kind == 3) return cl.k;
+  if (kind == 2) {
+    if (cl.k < cl.n2 && l2_may_run(a, cl.k, cl.c1, cl.n1, cl.run)) {
+      ++cl.run;
+      return -cl.k - 2;
+    }
+    cl.ticket = cl.k < cl.n2 ? cl.k : -2;
+  } else if (kind == 1 && cl.k < cl.n1) {
+    cl.run = 0;
+    return cl.k + 1;
+  }
+  return ep_claim(a, cl);
+}
+
 template <int MODE, int PREC>
 __device__ __forceinline__ void ep_dynamic(const EpArgs& a, int n1, int n2, char* lds, char** rowptr,
                                            int* flag) {
   constexpr bool fused = MODE == 3;
-  int run = 0, ticket = n2 > 0 ? -1 : -2;   // thread 0 only
+  Claim cl{fused ? 1 : 0, n1, n2, 0, n2 > 0 ? -1 : -2, 0, 0, 0, 0};   // thread 0 only
   if (fused && a.policy == XS_POLICY_BURST) {
     const int nw = a.meta[1], total = a.meta[2];
     for (;;) {
@@ -502,17 +574,17 @@ __device__ __forceinline__ void ep_dynamic(const EpArgs& a, int n1, int n2, char
     }
   }
   for (;;) {
-    if (threadIdx.x == 0) flag[1] = ep_claim(a, n1, n2, run, ticket);
+    if (threadIdx.x == 0) flag[1] = claim_next(a, cl);
     __syncthreads();
     const int t = flag[1];
     __syncthreads();
     if (t == -1) return;
     if (t > 0) {
       const int k1 = t - 1;
-      l1_tile<PREC>(a, k1 / a.P1, k1 % a.P1, fused, lds, rowptr);
+      l1_tile<PREC>(a, k1 / a.P1, k1 % a.P1, fused, lds, rowptr, &cl);
     } else {
       const int k2 = -t - 2;
-      l2_tile<PREC>(a, k2 / a.P2, k2 % a.P2, fused, lds, rowptr, flag);
+      l2_tile<PREC>(a, k2 / a.P2, k2 % a.P2, fused, lds, rowptr, flag, &cl);
     }
   }
 }
