@@ -285,7 +285,7 @@ def store_ceiling(X, torch):
             "frac_of_hbm_peak": nb / (span * 1e-6) / HBM_PEAK}
 
 
-def slow_sink_line(reps=5):
+def slow_sink_line(reps=10):
     """Store pacing against the host-coherent sink (paper_2607_23264_amd.slow_sink, quick sweep):
     the tiny layer with every combine window on the sink (c5) and the DeepSeek-V3 share with one
     and with two of its eight source windows there, uniform and Zipf; per policy the kernel time on the sink

@@ -97,14 +97,20 @@ class Traced:
         return t1.value, t2.value, t3.value
 
 
-def kernel_us(lay: EPLayer, pol: X.xs_pacing, reps: int) -> list:
+def rotated_us(lay: EPLayer, pols: list, reps: int) -> list:
+    """Kernel times of every pacing in pols, reps launches each, the order rotated from one
+    repetition to the next (round r starts at policy r mod n), so that clock drift and the
+    first-run boost fall on every policy alike. Returns one list of times per pacing."""
     ev = X.HipEvents(2)
     lay.L.events[X.XS_EV_FFN], lay.L.events[X.XS_EV_FFN_END] = ev.ev[0], ev.ev[1]
-    out = []
-    for _ in range(reps):
-        lay.fused(pol)
-        torch.cuda.synchronize()
-        out.append(X.HipEvents.elapsed_ms_pair(ev.ev[0], ev.ev[1]) * 1e3)
+    out = [[] for _ in pols]
+    n = len(pols)
+    for r in range(reps):
+        for q in range(n):
+            j = (r + q) % n
+            lay.fused(pols[j])
+            torch.cuda.synchronize()
+            out[j].append(X.HipEvents.elapsed_ms_pair(ev.ev[0], ev.ev[1]) * 1e3)
     lay.L.events[X.XS_EV_FFN], lay.L.events[X.XS_EV_FFN_END] = None, None
     if int(lay.status.item()):
         raise RuntimeError(f"device status {int(lay.status.item())}: {X.xs_strerror(int(lay.status.item())).decode()}")
@@ -133,12 +139,14 @@ def evaluate(name: str, make_layer, policies: dict, model: X.xs_model, sink_shar
         s = ctrl.s
         c = ctrl.expert_counts.sum(0).cpu().numpy()
         counts = [int(v) for v in c[s.e_begin:s.e_begin + s.n_experts]]   # the layout's rows per local expert
+        keys, pols = [], []
         for pname, (pol, lead, chunk, cap) in policies.items():
-            p = pacing(pol, lead=lead, chunk=chunk, max_producers=cap, claim=claim)
-            if pol == X.XS_POLICY_AUTO:
+            if pol == X.XS_POLICY_AUTO or (pol, lead, chunk, cap) in keys:
                 continue
-            times = kernel_us(ctrl, p, reps)
-            control[(pol, lead, chunk, cap)] = {"kernel_us": float(np.median(times)), "trace": Traced(ctrl, p)}
+            keys.append((pol, lead, chunk, cap))
+            pols.append(pacing(pol, lead=lead, chunk=chunk, max_producers=cap, claim=claim))
+        for key, p, times in zip(keys, pols, rotated_us(ctrl, pols, reps)):
+            control[key] = {"kernel_us": float(np.median(times)), "trace": Traced(ctrl, p)}
         ref = next(v for k, v in control.items() if k[0] == X.XS_POLICY_INTERLEAVE)
         tl1, tl2, _ = ref["trace"].tile_times(min_rows=0)
         out["control_tile_times_us"] = {"T_L1": tl1, "T_L2": tl2}
@@ -148,12 +156,15 @@ def evaluate(name: str, make_layer, policies: dict, model: X.xs_model, sink_shar
         torch.cuda.empty_cache()
     lay = make_layer(True)
     try:
-        for pname, (pol, lead, chunk, cap) in policies.items():
-            p = pacing(pol, lead=lead, chunk=chunk, max_producers=cap, claim=claim, model=model, t_l1_us=tl1,
+        names = list(policies)
+        pols = [pacing(pol, lead=lead, chunk=chunk, max_producers=cap, claim=claim, model=model, t_l1_us=tl1,
                        t_l2_us=tl2, expert_rows=counts, sink_share=sink_share)
+                for (pol, lead, chunk, cap) in policies.values()]
+        all_times = rotated_us(lay, pols, reps)
+        for pname, p, times in zip(names, pols, all_times):
+            pol, lead, chunk, cap = policies[pname]
             au = audit(lay, p)
             chosen = au.policy
-            times = kernel_us(lay, p, reps)
             tr = Traced(lay, p)
             G = au.producers
             base = control.get((chosen, lead, au.chunk, cap))
