@@ -166,9 +166,10 @@ def test_trace_records_every_tile_once():
     assert (rec[:, 1] <= rec[:, 2]).all() and (rec[:, 2] <= rec[:, 3]).all()
 
 
-def test_full_size_sampled_rows():
+def test_full_size_every_row():
     # the Ulysses shape of the fused-attention workload: 8 local heads, 8192 tokens, 8 windows,
-    # the launch the benchmark times (default grid); 48 sampled queries per head
+    # the launch the benchmark times (default grid); every output element against the fp64
+    # oracle (one head at a time, to bound host memory)
     cfg = synth.ATTN_UP_8K
     inp = synth.attn_inputs(cfg, 0)
     q, k, v = inp["q"], inp["k"], inp["v"]
@@ -176,10 +177,9 @@ def test_full_size_sampled_rows():
     win, flags = _fused(q, k, v, cfg.W)
     assert np.array_equal(_windows_as_heads(win, cfg.heads), oa.ulysses_scatter(o, cfg.W))
     assert (flags == 1).all()
-    rng = np.random.default_rng(7)
-    rows = np.unique(np.concatenate([rng.choice(cfg.M, 46, replace=False), [0, cfg.M - 1]]))
-    ref64, _ = oa.attention(q[:, rows], k, v)
-    assert_close(o[:, rows], ref64, "attention M=8192 sampled rows")
+    for h in range(cfg.heads):
+        ref64, _ = oa.attention(q[h:h + 1], k[h:h + 1], v[h:h + 1])
+        assert_close(o[h:h + 1], ref64, f"attention M=8192 head {h}")
 
 
 def test_bad_arguments_are_rejected():
