@@ -10,6 +10,8 @@
 // Dispatch: one wavefront per token row; every lane holds 16-byte pieces of the row in
 // registers and stores them, 128-bit and coalesced, into the k destination rows. A row is
 // contiguous on both sides, so no LDS staging is needed to coalesce.
+#include <algorithm>
+
 #include "xs_common.hpp"
 
 namespace xs {
@@ -107,16 +109,13 @@ __device__ __forceinline__ float sum_dpp(float x) {
 // all 16 lanes of a DPP row end with the reduction over the row: rotate by 8, 4, 2, 1
 constexpr int kRor8 = 0x128, kRor4 = 0x124, kRor2 = 0x122, kRor1 = 0x121;
 
+// Sixteen lanes per token, each holding VPL logits: lane sub has experts 64 q + 4 sub + c.
 template <int VPL>
-__global__ __launch_bounds__(256) void route_topk16_kernel(const float* __restrict__ logits, int T,
-                                                           int E, int k, int renorm,
-                                                           int* __restrict__ topk_idx,
-                                                           float* __restrict__ topk_w) {
-  const int sub = threadIdx.x & 15;
-  const int t = (blockIdx.x * 256 + threadIdx.x) >> 4;
-  // every lane takes part in the row reductions: tokens past T read the last row, store nothing
+__device__ __forceinline__ void route16_load(const float* __restrict__ logits, int t, int T, int E, int sub,
+                                             float (&v)[VPL]) {
+  // tokens past T read the last row (every lane takes part in the row reductions) and store
+  // nothing
   const float* row = logits + static_cast<int64_t>(t < T ? t : T - 1) * E;
-  float v[VPL];
   if ((E & 3) == 0) {
     // rows start 16-byte aligned: one 128-bit load per lane and q
 #pragma unroll
@@ -136,23 +135,31 @@ __global__ __launch_bounds__(256) void route_topk16_kernel(const float* __restri
         v[4 * q + c] = e < E ? row[e] : -INFINITY;
       }
   }
+}
+
+template <int VPL>
+__device__ __forceinline__ void route16_select(const float (&v)[VPL], int t, int T, int E, int k, int renorm,
+                                               int sub, int* __restrict__ topk_idx, float* __restrict__ topk_w) {
   uint32_t taken = 0;
   float m = 0.f, my_v = -INFINITY;
   int my_idx = 0;
   for (int j = 0; j < k; ++j) {
+    // a lane scans its experts in ascending index, so a strict > keeps the lowest index among
+    // equal values; the first untaken expert is taken even at -inf. Padding slots (index >= E,
+    // value -inf) come after every real expert of the lane and lose every tie to a real one.
     float bv = -INFINITY;
     int bi = 0x7fffffff;
 #pragma unroll
     for (int q = 0; q < VPL / 4; ++q)
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        const int e = 64 * q + 4 * sub + c;
-        // ties (equal values, or only -inf left) go to the lower expert index
-        if (e < E && !((taken >> (4 * q + c)) & 1u) && (v[4 * q + c] > bv || (v[4 * q + c] == bv && e < bi))) {
-          bv = v[4 * q + c];
-          bi = e;
+        const int s = 4 * q + c;
+        if (!((taken >> s) & 1u) && (v[s] > bv || bi == 0x7fffffff)) {
+          bv = v[s];
+          bi = 64 * q + 4 * sub + c;
         }
       }
+    // across the 16 lanes: ties (equal values, or only -inf left) go to the lower index
     argmax_dpp<kRor8>(bv, bi);
     argmax_dpp<kRor4>(bv, bi);
     argmax_dpp<kRor2>(bv, bi);
@@ -185,6 +192,31 @@ __global__ __launch_bounds__(256) void route_topk16_kernel(const float* __restri
   if (t < T && sub < k) {
     topk_idx[static_cast<int64_t>(t) * k + sub] = my_idx;
     topk_w[static_cast<int64_t>(t) * k + sub] = my_w;
+  }
+}
+
+// Persistent: a workgroup (16 tokens at a time) walks the tokens with the grid's stride and
+// loads the next group's logits while it selects the current group's experts, so the loads
+// of a cold logits tensor overlap the selection instead of preceding it.
+template <int VPL>
+__global__ __launch_bounds__(256) void route_topk16_kernel(const float* __restrict__ logits, int T,
+                                                           int E, int k, int renorm,
+                                                           int* __restrict__ topk_idx,
+                                                           float* __restrict__ topk_w) {
+  const int sub = threadIdx.x & 15;
+  const int stride = gridDim.x * 16;
+  int t = blockIdx.x * 16 + (threadIdx.x >> 4);
+  const int t_wave = blockIdx.x * 16 + (threadIdx.x >> 6) * 4;   // the wave's first token
+  float v[VPL], nv[VPL];
+  route16_load<VPL>(logits, t, T, E, sub, v);
+  for (int tw = t_wave; tw < T; tw += stride, t += stride) {
+    const bool more = tw + stride < T;
+    if (more) route16_load<VPL>(logits, t + stride, T, E, sub, nv);
+    route16_select<VPL>(v, t, T, E, k, renorm, sub, topk_idx, topk_w);
+    if (more) {
+#pragma unroll
+      for (int i = 0; i < VPL; ++i) v[i] = nv[i];
+    }
   }
 }
 
@@ -271,9 +303,17 @@ __global__ __launch_bounds__(1024) void layout_global_scan_kernel(
   __shared__ int tot[1024];
   for (int e = threadIdx.x; e < E; e += blockDim.x) {
     int run = 0;
-    for (int s = 0; s < n_src; ++s) {
-      src_base[static_cast<int64_t>(s) * E + e] = run;
-      run += expert_counts[static_cast<int64_t>(s) * E + e];
+    // eight sources' counts in flight at a time (one dependent load per source took longer)
+    for (int s0 = 0; s0 < n_src; s0 += 8) {
+      int v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        v[u] = s0 + u < n_src ? expert_counts[static_cast<int64_t>(s0 + u) * E + e] : 0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (s0 + u < n_src) src_base[static_cast<int64_t>(s0 + u) * E + e] = run;
+        run += v[u];
+      }
     }
     tot[e] = run;
   }
@@ -445,6 +485,10 @@ __global__ void signal_windows_kernel(WinSet win) {
 using namespace xs;
 
 namespace xs_host {
+int persistent_grid(int max_producers);
+}  // namespace xs_host
+
+namespace xs_host {
 int signal_windows(const WinSet& ws, hipStream_t st) {
   bool any = false;
   for (int d = 0; d < ws.n; ++d) any |= ws.flag[d] != nullptr;
@@ -462,7 +506,7 @@ extern "C" int xs_route_topk_softmax(const float* logits, int32_t T, int32_t E, 
   if (T == 0) return XS_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (E <= 256 && k <= 16) {
-    const dim3 g16((T + 15) / 16), b16(256);
+    const dim3 g16(std::min((T + 15) / 16, 2 * xs_host::persistent_grid(0))), b16(256);
     if (E <= 64)
       hipLaunchKernelGGL(route_topk16_kernel<4>, g16, b16, 0, st, logits, T, E, k, renormalize, topk_idx, topk_w);
     else if (E <= 128)

@@ -84,9 +84,17 @@ __global__ __launch_bounds__(1024) void ep_plan_kernel(const int* __restrict__ e
   const int i = threadIdx.x;
   if (i < n_experts) {
     const int e = e_begin + i;
+    const int off = expert_offsets[e];
     int m = 0;
-    for (int s = 0; s < n_src; ++s) m += expert_counts[static_cast<int64_t>(s) * E + e];
-    s_m[i] = max(0, min(m, cap - expert_offsets[e]));
+    // eight sources' counts in flight at a time
+    for (int s0 = 0; s0 < n_src; s0 += 8) {
+      int v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = s0 + u < n_src ? expert_counts[static_cast<int64_t>(s0 + u) * E + e] : 0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) m += v[u];
+    }
+    s_m[i] = max(0, min(m, cap - off));
   }
   __syncthreads();
   if (i == 0) {
