@@ -151,13 +151,26 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tiles_kernel(
         const int64_t stride = win.stride[g];
         char* plane0 = win.base[g] + (static_cast<int64_t>(p * sa.hpg + head0 - g * sa.hpg) * M + m0) * stride;
         const int64_t plane_bytes = static_cast<int64_t>(M) * stride;
-        const int n = (kBN / sa.head_dim) * rows * pph;
-        for (int i = tid; i < n; i += kThreads) {
-          const int piece = i % pph;
-          const int hr = i / pph;
-          const int hsel = hr / rows, r = hr - hsel * rows;
-          u32x4 v = *reinterpret_cast<const u32x4*>(lds + (r * kEpiPitch + hsel * sa.head_dim + piece * 8) * 2);
-          *reinterpret_cast<u32x4*>(plane0 + hsel * plane_bytes + r * stride + piece * 16) = v;
+        // head_dim divides 256, so pph divides the 512 threads: each thread keeps one piece
+        // column and walks rows with a fixed step (no division inside the loop)
+        const int rpp = kThreads / pph;
+        const int piece = tid % pph, r0 = tid / pph;
+        constexpr int U = 4;
+        typedef __attribute__((address_space(1))) u32x4 global_u32x4;   // global, not flat, stores
+        for (int hsel = 0; hsel < kBN / sa.head_dim; ++hsel) {
+          const char* src = lds + (hsel * sa.head_dim + piece * 8) * 2;
+          char* dst = plane0 + hsel * plane_bytes + piece * 16;
+#pragma unroll 1
+          for (int r = r0; r < rows; r += U * rpp) {
+            u32x4 v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+              if (r + u * rpp < rows) v[u] = *reinterpret_cast<const u32x4*>(src + (r + u * rpp) * kEpiPitch * 2);
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+              if (r + u * rpp < rows)
+                *(global_u32x4*)(dst + static_cast<int64_t>(r + u * rpp) * stride) = v[u];
+          }
         }
       } else {
         const int pc = tid & 31;
