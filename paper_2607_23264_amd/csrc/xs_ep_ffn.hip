@@ -380,7 +380,6 @@ __device__ __forceinline__ int xcd_instance_ep(int b, int G) {
 template <bool BF4>
 __device__ __forceinline__ void ep_l1_tile_mx(const EpArgs& a, int p, int nt, bool fused, char* lds,
                                               char** rowptr, Claim* cl) {
-  const int tid = threadIdx.x;
   const int x = a.row_expert[p];
   const int e = a.e_begin + x;
   const int dl = e / a.epw - a.d_first;
@@ -400,6 +399,7 @@ __device__ __forceinline__ void ep_l1_tile_mx(const EpArgs& a, int p, int nt, bo
                         nt * (kBN / 2), a.I, true, a.H, acc, lds);
   claim_load(a, cl);
   const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
+  const int tid = tid_here();   // not held across the mainloop
   const int64_t hrow0 = static_cast<int64_t>(a.exp_hrow[x] + m0);
   if (tid < rows) rowptr[tid] = reinterpret_cast<char*>(a.h) + (hrow0 + tid) * a.h_stride;
   stage_swiglu_mxq(acc, lds);
@@ -430,7 +430,6 @@ __device__ __forceinline__ void ep_l1_tile_mx(const EpArgs& a, int p, int nt, bo
 template <bool BF4>
 __device__ __forceinline__ void ep_l2_tile_mx(const EpArgs& a, int p, int nt, bool fused, char* lds,
                                               char** rowptr, int* flag, Claim* cl) {
-  const int tid = threadIdx.x;
   const uint64_t t0 = a.tr.buf ? wall_ticks() : 0;
   if (fused && !ep_wait_row(a, p, flag)) return;
   const uint64_t t_dep = a.tr.buf ? wall_ticks() : 0;
@@ -448,13 +447,14 @@ __device__ __forceinline__ void ep_l2_tile_mx(const EpArgs& a, int p, int nt, bo
   const uint8_t* Bs = a.w2s + wrows * 16;
   const int n0 = nt * kBN;
   int code = -1;
-  if (a.l2_combine && tid < rows)
-    code = a.row_src[static_cast<int64_t>(e / a.epw) * a.cap + a.expert_offsets[e] + m0 + tid];
+  if (a.l2_combine && static_cast<int>(threadIdx.x) < rows)
+    code = a.row_src[static_cast<int64_t>(e / a.epw) * a.cap + a.expert_offsets[e] + m0 + threadIdx.x];
   AccMx acc;
   gemm_mainloop_mx<BF4>(A, a.h_stride, As, 16, a.h_rows * 16, rows, B, ldb, Bs, 16,
                         static_cast<int64_t>(a.n_experts) * a.H * 16, n0, 0, false, a.I, acc, lds);
   claim_load(a, cl);
   const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
+  const int tid = tid_here();   // not held across the mainloop
   if (tid < rows) {
     char* ptr = nullptr;
     const int src = code >> 24, slot = code & 0xffffff;

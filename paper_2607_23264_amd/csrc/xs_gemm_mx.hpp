@@ -40,6 +40,21 @@
 
 namespace xs {
 
+// The lane index, computed where it is used: the asm is volatile, so the value (and the LDS
+// addresses derived from it) is not hoisted into a register kept live across the mainloop,
+// where these kernels are short of registers and would spill it to scratch.
+__device__ __forceinline__ int lane_id_here() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
+// The thread index, with its lane part computed where it is used (lane_id_here) and its wave
+// part uniform.
+__device__ __forceinline__ int tid_here() {
+  return __builtin_amdgcn_readfirstlane(threadIdx.x & ~63u) + lane_id_here();
+}
+
 constexpr int kMxThreads = 256;
 constexpr int kMxStage = 2 * kOpBytes;             // A tile and B tile of one stage: 64 KiB
 constexpr int kMxScaleBuf = 2 * kBM * 16;          // one scale group: 16 bytes per A and B row
@@ -289,7 +304,7 @@ __device__ __forceinline__ void gemm_mainloop_mx(const uint8_t* __restrict__ A, 
                                                  const uint8_t* __restrict__ Bs, int64_t b_srow,
                                                  int64_t b_sgrp, int b_n0, int b_half, bool swiglu,
                                                  int K, AccMx& acc, char* lds) {
-  const int lane = threadIdx.x & 63;
+  const int lane = lane_id_here();
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = w >> 1, wn = w & 1;
   MxTile t;
@@ -356,7 +371,7 @@ __device__ __forceinline__ void gemm_mainloop_mx(const uint8_t* __restrict__ A, 
 
 // Accumulators -> bf16 tile in LDS, row-major [256][kEpiPitch].
 __device__ __forceinline__ void stage_tile_mx(const AccMx& acc, char* lds) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = lane_id_here(), w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = w >> 1, wn = w & 1;
   const int row0 = wm * 128 + (lane & 31);
   const int col0 = wn * 128 + 4 * (lane >> 5);
@@ -405,7 +420,7 @@ constexpr int kHqScaleOff = kBM * kHqPitch;
 // and lane ^ 32 the other 16, so the block maximum takes one half swap. Codes: the exact
 // power-of-two scaling and the hardware round-to-nearest-even E4M3 conversion.
 __device__ __forceinline__ void stage_swiglu_mxq(const AccMx& acc, char* lds) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = lane_id_here(), w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = w >> 1, wn = w & 1;
   const int up = lane >> 5;
   typedef uint32_t u32x2_ __attribute__((ext_vector_type(2)));
@@ -446,7 +461,7 @@ template <int NT>
 __device__ __forceinline__ void store_rows_n(const char* lds, int pitch, int per_row, int rows,
                                              char* const* rowptr) {
   typedef __attribute__((address_space(1))) u32x4 global_u32x4;
-  const int tid = threadIdx.x;
+  const int tid = tid_here();
   const int rows_per_pass = NT / per_row;
   const int pc = tid % per_row;
 #pragma unroll 1
