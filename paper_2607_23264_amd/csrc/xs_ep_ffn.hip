@@ -406,10 +406,25 @@ __device__ __forceinline__ void ep_l1_tile_mx(const EpArgs& a, int p, int nt, bo
   __syncthreads();
   claim_take(a, cl);
   typedef __attribute__((address_space(1))) u32x4 global_u32x4;
+  // four rows' LDS reads in flight before their stores
+  constexpr int kRowsPerPass = kMxThreads / 8;
 #pragma unroll 1
-  for (int i = tid; i < rows * 8; i += kMxThreads) {
-    const int r = i >> 3, pc = i & 7;
-    *(global_u32x4*)(rowptr[r] + nt * 128 + pc * 16) = *reinterpret_cast<const u32x4*>(lds + r * kHqPitch + pc * 16);
+  for (int r = tid >> 3; r < rows; r += 4 * kRowsPerPass) {
+    const int pc = tid & 7;
+    char* dst[4];
+    u32x4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int ru = r + u * kRowsPerPass;
+      dst[u] = nullptr;
+      if (ru < rows) {
+        dst[u] = rowptr[ru];
+        v[u] = *reinterpret_cast<const u32x4*>(lds + ru * kHqPitch + pc * 16);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (dst[u]) *(global_u32x4*)(dst[u] + nt * 128 + pc * 16) = v[u];
   }
   if (tid < rows)
     *(__attribute__((address_space(1))) uint32_t*)(a.hs + ((nt >> 2) * a.h_rows + hrow0 + tid) * 16 + (nt & 3) * 4) =

@@ -457,7 +457,9 @@ __device__ __forceinline__ void stage_swiglu_mxq(const AccMx& acc, char* lds) {
 
 // Stores staged rows [0, rows) through per-row destination pointers (null rows skipped):
 // pieces of 16 bytes, per_row pieces per row, pitch bytes between staged rows; NT threads.
-template <int NT>
+// U rows' pointers and data are read from LDS before their U stores, so a pass waits for one
+// LDS round trip instead of U.
+template <int NT, int U = 4>
 __device__ __forceinline__ void store_rows_n(const char* lds, int pitch, int per_row, int rows,
                                              char* const* rowptr) {
   typedef __attribute__((address_space(1))) u32x4 global_u32x4;
@@ -465,11 +467,21 @@ __device__ __forceinline__ void store_rows_n(const char* lds, int pitch, int per
   const int rows_per_pass = NT / per_row;
   const int pc = tid % per_row;
 #pragma unroll 1
-  for (int r = tid / per_row; r < rows; r += rows_per_pass) {
-    char* p = rowptr[r];
-    if (!p) continue;
-    const u32x4 v = *reinterpret_cast<const u32x4*>(lds + r * pitch + pc * 16);
-    *(global_u32x4*)(p + pc * 16) = v;
+  for (int r = tid / per_row; r < rows; r += U * rows_per_pass) {
+    char* p[U];
+    u32x4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int ru = r + u * rows_per_pass;
+      p[u] = nullptr;
+      if (ru < rows) {
+        p[u] = rowptr[ru];
+        v[u] = *reinterpret_cast<const u32x4*>(lds + ru * pitch + pc * 16);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (p[u]) *(global_u32x4*)(p[u] + pc * 16) = v[u];
   }
 }
 
