@@ -218,6 +218,10 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
       __builtin_amdgcn_s_barrier();
     }
     __builtin_amdgcn_sched_barrier(0);
+    // Sub-step 3 runs at raised wave priority: the wave that has passed the barrier issues its
+    // MFMAs, next-stage reads and loads ahead of the SIMD's other wave (measured on the EP FFN:
+    // -1.1 %, output unchanged; placing it over sub-steps 0-2 instead was slower).
+    __builtin_amdgcn_s_setprio(1);
     constexpr int kLoads = (kIA ? 4 : 0) + (kIB ? 4 : 0);
     // sub-step 3: each MFMA followed by one read of the next stage's sub-step 0 and one load
 #pragma unroll
@@ -233,6 +237,7 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
 #pragma unroll
       for (int r = kMfma; r < kReads; ++r) read_one(na, nb, 0, 0, r);
     }
+    __builtin_amdgcn_s_setprio(0);
 #pragma unroll
     for (int n = kMfma; n < kLoads; ++n) load_one(kt, bs, kIA ? n : n + 4);
   };
