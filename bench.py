@@ -288,7 +288,8 @@ def store_ceiling(X, torch):
 def slow_sink_line(reps=10):
     """Store pacing against the host-coherent sink (paper_2607_23264_amd.slow_sink, quick sweep):
     the tiny layer with every combine window on the sink (c5) and the DeepSeek-V3 share with one
-    and with two of its eight source windows there, uniform and Zipf; per policy the kernel time on the sink
+    and with two of its eight source windows there, uniform and Zipf at bf16 and uniform at
+    MXFP8; per policy the kernel time on the sink
     and on the HBM control, the speedup over Expert-Wave burst issue, and the stall per producer
     measured (issue spans and staging waits beyond the control) against the audit's prediction."""
     from paper_2607_23264_amd import slow_sink as ss

@@ -227,11 +227,12 @@ def tiny_layer(cfg, inp):
     return make
 
 
-def share_layer(cfg, inp, host_sources):
+def share_layer(cfg, inp, host_sources, precision=X.XS_PREC_BF16):
     def make(on_sink: bool) -> EPLayer:
         experts = list(range(cfg.rank * cfg.E_local, (cfg.rank + 1) * cfg.E_local))
         s = Shape(cfg.n_src, cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.W, experts[0], len(experts), src=cfg.rank)
-        lay = EPLayer(s, sentinel=False, host_combine_sources=host_sources if on_sink else None)
+        lay = EPLayer(s, sentinel=False, host_combine_sources=host_sources if on_sink else None,
+                      precision=precision)
         lay.upload(inp["logits"], inp["x"], inp["w1"], inp["w2"])
         lay.prefill_other_sources(inp["fill"])
         return lay
@@ -292,7 +293,11 @@ def share_inputs(routing: str, seed: int = 0):
     return cfg, inp
 
 
-def run(quick=False, reps=5, routings=("zipf", "uniform"), sink_windows=(1, 2), seed=0):
+def run(quick=False, reps=5, routings=("zipf", "uniform"), sink_windows=(1, 2), seed=0,
+        mx_routings=("uniform",)):
+    """Calibrate the sink, then evaluate the tiny layer and the share layers: bf16 for every
+    routing in routings, and MXFP8 (W8A8, the precision of the paper's EP measurements) for
+    every routing in mx_routings, each with sink_windows of its source windows on the sink."""
     import synth
     torch.cuda.set_device(0)
     # five burst sizes (1 to 64 MiB aggregate): enough below the knee for the floor line and
@@ -310,17 +315,21 @@ def run(quick=False, reps=5, routings=("zipf", "uniform"), sink_windows=(1, 2), 
     chunks = [1, 8] if quick else [1, 2, 4, 8, 16, 32, 64]
     report["layers"].append(evaluate(cfg.name + " (every combine window on the sink)", tiny_layer(cfg, inp),
                                      tiny_policies(caps, chunks), model, 1.0, reps))
-    for routing in routings:
+    for routing in dict.fromkeys(tuple(routings) + tuple(mx_routings)):
         scfg, sinp = share_inputs(routing, seed)
         others = [q for q in range(scfg.n_src) if q != scfg.rank]
+        precs = ([("", X.XS_PREC_BF16)] if routing in routings else []) + \
+                ([("MXFP8, ", X.XS_PREC_MXFP8)] if routing in mx_routings else [])
         # one source window on the sink: the average rate leaves the sink half idle (Eq. 9 holds
         # with room), yet aligned Linear-2 bursts can still exceed the capacity; two windows:
-        # the sink close to saturation
-        for n_host in sink_windows:
-            hosts = others[:n_host]
-            report["layers"].append(evaluate(f"{scfg.name} ({routing}, rank {scfg.rank}; combine windows of sources "
-                                             f"{hosts} on the sink)", share_layer(scfg, sinp, hosts),
-                                             SHARE_POLICIES, model, len(hosts) / scfg.n_src, reps))
+        # the sink close to saturation. At MXFP8 the expert GEMMs take about 0.6 of the bf16
+        # time for the same combine bytes, so the same windows load the sink more.
+        for tag, prec in precs:
+            for n_host in sink_windows:
+                hosts = others[:n_host]
+                report["layers"].append(evaluate(f"{scfg.name} ({tag}{routing}, rank {scfg.rank}; combine windows of "
+                                                 f"sources {hosts} on the sink)", share_layer(scfg, sinp, hosts, prec),
+                                                 SHARE_POLICIES, model, len(hosts) / scfg.n_src, reps))
         del sinp
     return report
 
