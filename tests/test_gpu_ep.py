@@ -38,7 +38,8 @@ def _route_gpu(logits, k, renorm=0):
 
 @pytest.mark.parametrize("case", ["tiny", "dsv3_uniform", "dsv3_zipf", "ties_E1000_k32", "one_token",
                                   "k_equals_E", "renorm", "ties_E200_k16", "E100_k3_T17",
-                                  "masked_E256_k8", "masked_E300_k8"])
+                                  "masked_E256_k8", "masked_E300_k8", "loop_E256_T20001", "loop_E128_T9001",
+                                  "loop_E64_T16385"])
 def test_route_matches_oracle(case):
     g = np.random.default_rng(11)
     renorm = 0
@@ -68,6 +69,10 @@ def test_route_matches_oracle(case):
         lg[:, 5] = 0.25                 # at least one finite logit per row
         lg[4, :] = -np.inf
         lg[4, [17, 200]] = [1.0, 1.0]   # two finite ones: six slots take -inf experts
+    elif case.startswith("loop"):   # more tokens than one pass of the persistent grid covers
+        E, T = (int(v) for v in case[6:].split("_T"))   # (several groups per workgroup, ragged tail)
+        lg, k = g.standard_normal((T, E)).astype(np.float32), 8 if E > 64 else 4
+        lg[T - 1] = 0.0                  # an all-tie row in the last group
     else:
         lg, k, renorm = synth.uniform_logits(0, 2, 200, 64), 6, 1
     idx, w = _route_gpu(lg, k, renorm)
