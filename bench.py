@@ -298,7 +298,8 @@ def slow_sink_line(reps=10):
             "stall_measured_us_per_producer", "stall_predicted_us_per_producer", "time_lost_us",
             "staging_wait_measured_us_per_producer", "mma_stall_predicted_us_per_producer",
             "stall_fraction_measured", "stall_fraction_predicted", "mainloop_excess_us_per_producer",
-            "dependency_wait_excess_us_per_producer", "l2_issue_us_median", "l2_issue_us_p90", "rate_feasible_eq9")
+            "dependency_wait_excess_us_per_producer", "l2_issue_us_median", "l2_issue_us_p90", "rate_feasible_eq9",
+            "sclk_MHz_median")
     return {"sink_model": rep["sink_model"], "hbm_R_bytes_per_us": rep["hbm_R_bytes_per_us"],
             "gap_sweep": rep["gap_sweep"], "producer_sweep": rep["producer_sweep"],
             "layers": [{"layer": L["layer"], "sink_share": L["sink_share"],
@@ -554,13 +555,15 @@ def main():
     # one event per step boundary (the first and last bracket the timed region)
     bounds = [torch.cuda.Event(enable_timing=True) for _ in range(a.steps + 1)]
     torch.cuda.synchronize()
-    bounds[0].record()
-    for i in range(a.steps):
-        lay.L.events[X.XS_EV_FFN] = ev.ev[2 * i]
-        lay.L.events[X.XS_EV_FFN_END] = ev.ev[2 * i + 1]
-        lay.fused(pol[a.policy])
-        bounds[i + 1].record()
-    torch.cuda.synchronize()
+    from paper_2607_23264_amd.profiling import ClockSampler
+    with ClockSampler() as sclk:
+        bounds[0].record()
+        for i in range(a.steps):
+            lay.L.events[X.XS_EV_FFN] = ev.ev[2 * i]
+            lay.L.events[X.XS_EV_FFN_END] = ev.ev[2 * i + 1]
+            lay.fused(pol[a.policy])
+            bounds[i + 1].record()
+        torch.cuda.synchronize()
     total_ms = bounds[0].elapsed_time(bounds[-1])
     step_us = [bounds[i].elapsed_time(bounds[i + 1]) * 1e3 for i in range(a.steps)]
     ffn_ms = [ev.elapsed_ms(2 * i, 2 * i + 1) for i in range(a.steps)]
@@ -606,6 +609,11 @@ def main():
     disp_bytes = cfg.T * cfg.k * cfg.H * 2          # stored rows (plus T * H * 2 read)
     red_bytes = cfg.T * cfg.k * cfg.H * 2 + cfg.T * cfg.H * 2
     res["graph_replay"] = graph
+    # the shader clock during the timed steps (clock state differs between boxes and runs)
+    res["sclk_MHz"] = sclk.summary()
+    if res["sclk_MHz"]:
+        log(f"[bench] shader clock during the timed steps (driver's figure): median "
+            f"{res['sclk_MHz']['median']:.0f} MHz over {res['sclk_MHz']['samples']} samples")
     res["step_us_dist"] = {"median": float(np.median(step_us)), "p10": float(np.percentile(step_us, 10)),
                            "p90": float(np.percentile(step_us, 90)), "min": float(np.min(step_us)),
                            "max": float(np.max(step_us))}

@@ -51,6 +51,68 @@ def sources_hash(paths=FFN_KERNEL_SOURCES) -> str:
     return h.hexdigest()[:16]
 
 
+class ClockSampler:
+    """The shader clock the driver reports (the current entry of pp_dpm_sclk in sysfs), sampled
+    every 2 ms on a host thread while a region runs, as (host time, MHz) pairs. It is the
+    driver's running figure, not a count of the kernel's own cycles (the counter summaries give
+    that one). Without the sysfs file it samples nothing."""
+
+    def __init__(self, period_s: float = 0.002):
+        import glob
+        paths = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.path = paths[0] if paths else None
+        self.period = period_s
+        self.samples = []
+        self._stop = None
+        self._thread = None
+
+    def read(self):
+        import re
+        try:
+            with open(self.path) as f:
+                for line in f:
+                    if "*" in line:
+                        m = re.search(r"(\d+)\s*mhz", line, re.I)
+                        return int(m.group(1)) if m else None
+        except (OSError, TypeError):
+            return None
+        return None
+
+    def __enter__(self):
+        import threading
+        import time
+        if self.path is None:
+            return self
+        self._stop = threading.Event()
+
+        def run():
+            while not self._stop.is_set():
+                v = self.read()
+                if v is not None:
+                    self.samples.append((time.perf_counter(), v))
+                self._stop.wait(self.period)
+        self._thread = threading.Thread(target=run, daemon=True)
+        self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        if self._thread is not None:
+            self._stop.set()
+            self._thread.join()
+        return False
+
+    def summary(self, windows=None):
+        """Median, p10, p90, min and max of the samples, or of those inside the given
+        (start, end) host-time windows; None without samples."""
+        import numpy as np
+        v = [m for (t, m) in self.samples if windows is None or any(a <= t <= b for a, b in windows)]
+        if not v:
+            return None
+        v = np.array(v, dtype=np.float64)
+        return {"samples": int(v.size), "median": float(np.median(v)), "p10": float(np.percentile(v, 10)),
+                "p90": float(np.percentile(v, 90)), "min": float(v.min()), "max": float(v.max())}
+
+
 def read_traffic(md_path: str, kernel_hash: str | None = None):
     """The `traffic-json:` record of a traffic summary, or None if absent or stale."""
     try:

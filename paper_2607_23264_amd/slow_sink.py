@@ -97,20 +97,29 @@ class Traced:
         return t1.value, t2.value, t3.value
 
 
-def rotated_us(lay: EPLayer, pols: list, reps: int) -> list:
+def rotated_us(lay: EPLayer, pols: list, reps: int, clocks: list | None = None) -> list:
     """Kernel times of every pacing in pols, reps launches each, the order rotated from one
     repetition to the next (round r starts at policy r mod n), so that clock drift and the
-    first-run boost fall on every policy alike. Returns one list of times per pacing."""
+    first-run boost fall on every policy alike. Returns one list of times per pacing; with
+    clocks, also appends per pacing the driver's shader clock sampled during its launches."""
+    import time
+    from .profiling import ClockSampler
     ev = X.HipEvents(2)
     lay.L.events[X.XS_EV_FFN], lay.L.events[X.XS_EV_FFN_END] = ev.ev[0], ev.ev[1]
     out = [[] for _ in pols]
+    windows = [[] for _ in pols]
     n = len(pols)
-    for r in range(reps):
-        for q in range(n):
-            j = (r + q) % n
-            lay.fused(pols[j])
-            torch.cuda.synchronize()
-            out[j].append(X.HipEvents.elapsed_ms_pair(ev.ev[0], ev.ev[1]) * 1e3)
+    with ClockSampler() as sclk:
+        for r in range(reps):
+            for q in range(n):
+                j = (r + q) % n
+                t0 = time.perf_counter()
+                lay.fused(pols[j])
+                torch.cuda.synchronize()
+                windows[j].append((t0, time.perf_counter()))
+                out[j].append(X.HipEvents.elapsed_ms_pair(ev.ev[0], ev.ev[1]) * 1e3)
+    if clocks is not None:
+        clocks.extend(sclk.summary(w) for w in windows)
     lay.L.events[X.XS_EV_FFN], lay.L.events[X.XS_EV_FFN_END] = None, None
     if int(lay.status.item()):
         raise RuntimeError(f"device status {int(lay.status.item())}: {X.xs_strerror(int(lay.status.item())).decode()}")
@@ -160,8 +169,9 @@ def evaluate(name: str, make_layer, policies: dict, model: X.xs_model, sink_shar
         pols = [pacing(pol, lead=lead, chunk=chunk, max_producers=cap, claim=claim, model=model, t_l1_us=tl1,
                        t_l2_us=tl2, expert_rows=counts, sink_share=sink_share)
                 for (pol, lead, chunk, cap) in policies.values()]
-        all_times = rotated_us(lay, pols, reps)
-        for pname, p, times in zip(names, pols, all_times):
+        clocks = []
+        all_times = rotated_us(lay, pols, reps, clocks)
+        for pname, p, times, clk in zip(names, pols, all_times, clocks):
             pol, lead, chunk, cap = policies[pname]
             au = audit(lay, p)
             chosen = au.policy
@@ -196,7 +206,8 @@ def evaluate(name: str, make_layer, policies: dict, model: X.xs_model, sink_shar
                    "mainloop_excess_us_per_producer": main_excess,
                    "dependency_wait_excess_us_per_producer": dep_excess,
                    "guard_failures_predicted": au.cand_guard_fail[i], "bursts_predicted": au.cand_bursts[i],
-                   "rate_feasible_eq9": bool(au.rate_feasible)}
+                   "rate_feasible_eq9": bool(au.rate_feasible),
+                   "sclk_MHz_median": clk["median"] if clk else None}
             if pol == X.XS_POLICY_AUTO:
                 row["auto_candidates"] = [{"policy": POLICY_NAMES[au.cand_policy[j]], "chunk": au.cand_chunk[j],
                                            "stall_predicted_us": au.cand_stall_us[j]} for j in range(au.n_cand)]
