@@ -1,6 +1,6 @@
 """Host logic of the rocprofv3 summary helpers on synthetic counter files: the traffic scaling by
-the copy calibration, the staleness key of a stored traffic record, and the MFMA busy / clock /
-executed-flops arithmetic."""
+the copy calibration, the staleness key of a stored traffic record, the MFMA busy / clock /
+executed-flops arithmetic, and the shader-clock sampler's parsing and windows."""
 import csv
 import json
 import os
@@ -74,3 +74,36 @@ def test_mfma_summary_arithmetic(tmp_path):
     assert rec["clock_GHz"] == pytest.approx(1.7)
     assert rec["executed_flops"] == pytest.approx(4e12)
     assert rec["algorithmic_TFLOPs"] == pytest.approx(1500.0)
+
+
+def test_clock_sampler_reads_the_current_level_and_windows(tmp_path):
+    # the sysfs file lists DPM levels and marks the current one; the sampler takes that one
+    sys.path.insert(0, ROOT)
+    from paper_2607_23264_amd.profiling import ClockSampler
+    f = tmp_path / "pp_dpm_sclk"
+    cs = ClockSampler()
+    cs.path = str(f)
+    f.write_text("0: 500Mhz\n1: 2400Mhz *\n")
+    assert cs.read() == 2400
+    f.write_text("S: 110Mhz *\n0: 500Mhz\n1: 2400Mhz\n")
+    assert cs.read() == 110
+    f.write_text("0: 500Mhz\n1: 2400Mhz\n")         # no current level marked
+    assert cs.read() is None
+    cs.path = str(tmp_path / "missing")
+    assert cs.read() is None
+    cs.samples = [(1.0, 1800), (2.0, 1900), (3.0, 2000), (4.0, 2100)]
+    s = cs.summary()
+    assert s["samples"] == 4 and s["median"] == 1950.0 and s["min"] == 1800 and s["max"] == 2100
+    w = cs.summary([(1.5, 2.5), (3.5, 4.5)])           # samples inside either window
+    assert w["samples"] == 2 and w["median"] == 2000.0
+    assert cs.summary([(9.0, 10.0)]) is None
+
+
+def test_clock_sampler_without_sysfs_samples_nothing(monkeypatch):
+    sys.path.insert(0, ROOT)
+    import glob
+    from paper_2607_23264_amd.profiling import ClockSampler
+    monkeypatch.setattr(glob, "glob", lambda pattern: [])
+    with ClockSampler() as cs:
+        pass
+    assert cs.path is None and cs.summary() is None
