@@ -261,7 +261,7 @@ __device__ __forceinline__ void ep_l1_tile(const EpArgs& a, int p, int nt, bool 
       a.dwin.base[dl] + static_cast<int64_t>(a.expert_offsets[e] + m0) * a.dwin.stride[dl]);
   const uint16_t* B = a.w1 + static_cast<int64_t>(x) * 2 * a.I * a.H;
   Acc acc;
-  gemm_mainloop(A, lda, rows, B, a.H, nt * (kBN / 2), a.I, true, a.H, acc, lds);
+  gemm_mainloop<true>(A, lda, rows, B, a.H, nt * (kBN / 2), a.I, true, a.H, acc, lds);
   claim_load(a, cl);
   const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
   if (tid < rows)
@@ -332,7 +332,7 @@ __device__ __forceinline__ void ep_l2_tile(const EpArgs& a, int p, int nt, bool 
   if (a.l2_combine && tid < rows)
     code = a.row_src[static_cast<int64_t>(e / a.epw) * a.cap + a.expert_offsets[e] + m0 + tid];
   Acc acc;
-  gemm_mainloop(A, a.I, rows, B, a.I, n0, 0, false, a.I, acc, lds);
+  gemm_mainloop<true>(A, a.I, rows, B, a.I, n0, 0, false, a.I, acc, lds);
   claim_load(a, cl);
   const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
   if (tid < rows) {

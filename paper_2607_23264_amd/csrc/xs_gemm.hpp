@@ -103,7 +103,16 @@ struct TileAddr {
 // sub-step; the stage barrier comes before sub-step 3, whose MFMAs are each followed by one
 // fragment read of the next stage's sub-step 0 and one direct load, so the matrix pipe works
 // while the loads are issued and the next stage's first fragments arrive.
-template <int NI>
+//
+// kLateB moves the weight loads out of that burst: B(kt + 3) is issued one stage later, over
+// sub-steps 0-2 of stage kt + 1 (its slot is free from stage kt's barrier on), so sub-step 3
+// issues only the four A loads. The wait at each barrier stays vmcnt(4) (the B loads of the
+// stage after next are the only newer ones); a weight load then has 1 to 1.75 K steps to land
+// instead of about 1.75. Measured in one process on three boxes: the persistent EP FFN 1.6-1.9 %
+// faster, plain GEMMs with K of 7168 or more 0-1.5 % slower (where every CU streams weights at
+// once and the longer lead pays), K = 1024 unchanged; the EP kernels use it, the plain and
+// scatter GEMMs do not. Output is bit-identical either way.
+template <int NI, bool kLateB>
 __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc, char* lds) {
   const int lane = threadIdx.x & 63;
   const int w = ta.w;
@@ -158,7 +167,7 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
   }
   __builtin_amdgcn_s_barrier();
   if (nk > 1) issue_a(1);
-  if (nk > 2) issue_b(2, 2);
+  if (!kLateB && nk > 2) issue_b(2, 2);
   frags(lds, lds + kBBase, 0, 0);
   // One stage. NEXT: a stage follows; IA: A(kt + 2) exists (then B(kt + 2) is the only newer
   // load at the boundary: vmcnt(4)); IB: B(kt + 3) exists. Compile-time, so the steady loop
@@ -189,6 +198,12 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
                                        16, 0, 0);
     }
   };
+  // kLateB: direct load n of B(kt + 2) into its slot bs2 (that of B(kt - 1))
+  auto load_b_late = [&](int kt, int bs2, int n) {
+    char* st = lds + kBBase + bs2 * kOpBytes;
+    const char* b0 = ta.b + (kt + 2) * kBK * 2;
+    __builtin_amdgcn_global_load_lds((glob_void*)(b0 + ta.ob[n]), (lds_void*)(st + (8 * n + w) * 1024), 16, 0, 0);
+  };
   auto stage = [&](int kt, int bs, auto next_c, auto ia_c, auto ib_c) {
     constexpr bool kNext = decltype(next_c)::value;
     constexpr bool kIA = decltype(ia_c)::value;
@@ -198,6 +213,9 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
     const int bs_next = bs == 2 ? 0 : bs + 1;
     const char* na = lds + ((kt + 1) & 1) * kOpBytes;
     const char* nb = lds + kBBase + bs_next * kOpBytes;
+    // kLateB: B(kt + 2) exists exactly when A(kt + 2) does
+    constexpr bool kLate = kLateB && kIA;
+    const int bs_prev = bs == 0 ? 2 : bs - 1;
 #pragma unroll
     for (int kk = 0; kk < 3; ++kk) {
       __builtin_amdgcn_sched_barrier(0);
@@ -205,15 +223,24 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
       for (int g = 0; g < kMfma; ++g) {
         mma_one(kk & 1, g);
         if (g < kReads) read_one(ca, cb, kk + 1, (kk + 1) & 1, g);
+        if constexpr (kLate) {   // loads kk after the first MFMA of sub-step kk, load 3 mid sub-step 0
+          if (g == 0) load_b_late(kt, bs_prev, kk);
+          if (kk == 0 && g == kMfma / 2) load_b_late(kt, bs_prev, 3);
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
 #pragma unroll
       for (int r = kMfma; r < kReads; ++r) read_one(ca, cb, kk + 1, (kk + 1) & 1, r);
+      if constexpr (kLate && kMfma == 0) {
+        load_b_late(kt, bs_prev, kk);
+        if (kk == 0) load_b_late(kt, bs_prev, 3);
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (kNext) {
       // this wave's reads of stage kt are done and its loads of stage kt + 1 have landed (only
-      // B(kt + 2) may still be in flight) ... and every wave's (bare s_barrier, see above)
+      // B(kt + 2) may still be in flight) ... and every wave's (bare s_barrier, see above);
+      // kLateB issues B(kt + 2) in this stage, after A(kt + 1), so the count is the same
       __builtin_amdgcn_s_waitcnt(kIA ? 0x0074 : 0x0070);   // vmcnt(4 or 0) lgkmcnt(0)
       __builtin_amdgcn_s_barrier();
     }
@@ -222,7 +249,7 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
     // MFMAs, next-stage reads and loads ahead of the SIMD's other wave (measured on the EP FFN:
     // -1.1 %, output unchanged; placing it over sub-steps 0-2 instead was slower).
     __builtin_amdgcn_s_setprio(1);
-    constexpr int kLoads = (kIA ? 4 : 0) + (kIB ? 4 : 0);
+    constexpr int kLoads = (kIA ? 4 : 0) + (kIB && !kLateB ? 4 : 0);
     // sub-step 3: each MFMA followed by one read of the next stage's sub-step 0 and one load
 #pragma unroll
     for (int g = 0; g < kMfma; ++g) {
@@ -263,6 +290,7 @@ __device__ __forceinline__ void mainloop_ni(const TileAddr& ta, int nk, Acc& acc
 // results are zero or stale and are never stored). Ends with a block barrier, after which the
 // LDS may be reused. Accumulator layout: acc[i][j][q] is output
 //   row wm*128 + 32 i + lane % 32, column wn*64 + 32 j + 8 (q / 4) + 4 (lane / 32) + q % 4.
+template <bool kLateB = false>
 __device__ __forceinline__ void gemm_mainloop(const uint16_t* __restrict__ A, int64_t lda,
                                               int a_rows, const uint16_t* __restrict__ B,
                                               int64_t ldb, int b_n0, int b_half, bool swiglu,
@@ -297,11 +325,11 @@ __device__ __forceinline__ void gemm_mainloop(const uint16_t* __restrict__ A, in
   const int valid = a_rows - wm * 128;
   const int ni = valid >= 128 ? 4 : (valid <= 0 ? 0 : (valid + 31) >> 5);
   switch (__builtin_amdgcn_readfirstlane(ni)) {
-    case 4: mainloop_ni<4>(ta, nk, acc, lds); break;
-    case 3: mainloop_ni<3>(ta, nk, acc, lds); break;
-    case 2: mainloop_ni<2>(ta, nk, acc, lds); break;
-    case 1: mainloop_ni<1>(ta, nk, acc, lds); break;
-    default: mainloop_ni<0>(ta, nk, acc, lds); break;
+    case 4: mainloop_ni<4, kLateB>(ta, nk, acc, lds); break;
+    case 3: mainloop_ni<3, kLateB>(ta, nk, acc, lds); break;
+    case 2: mainloop_ni<2, kLateB>(ta, nk, acc, lds); break;
+    case 1: mainloop_ni<1, kLateB>(ta, nk, acc, lds); break;
+    default: mainloop_ni<0, kLateB>(ta, nk, acc, lds); break;
   }
   __syncthreads();
 }
