@@ -264,14 +264,14 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(
     const uint16_t* Bs = B + static_cast<int64_t>(sg) * N * K;
     Acc acc;
     if (SWIGLU) {
-      gemm_mainloop(A + static_cast<int64_t>(m0) * lda, lda, rows, Bs, K, nb * (kBN / 2), N / 2, true, K, acc, lds);
+      gemm_mainloop<true>(A + static_cast<int64_t>(m0) * lda, lda, rows, Bs, K, nb * (kBN / 2), N / 2, true, K, acc, lds);
       if (tid < rows)
         rowptr[tid] = C + static_cast<int64_t>(m0 + tid) * ldc_bytes + static_cast<int64_t>(nb) * (kBN / 2) * 2;
       stage_swiglu(acc, lds);
       __syncthreads();
       store_rows(lds, kEpiPitchH, kBN / 2, rows, rowptr);
     } else {
-      gemm_mainloop(A + static_cast<int64_t>(m0) * lda, lda, rows, Bs, K, nb * kBN, 0, false, K, acc, lds);
+      gemm_mainloop<true>(A + static_cast<int64_t>(m0) * lda, lda, rows, Bs, K, nb * kBN, 0, false, K, acc, lds);
       if (tid < rows)
         rowptr[tid] = C + static_cast<int64_t>(m0 + tid) * ldc_bytes + static_cast<int64_t>(nb) * kBN * 2;
       stage_tile(acc, lds);
