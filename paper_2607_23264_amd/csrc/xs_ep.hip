@@ -13,6 +13,7 @@
 #include <algorithm>
 
 #include "xs_common.hpp"
+#include "xs_plan.hpp"
 
 namespace xs {
 
@@ -229,9 +230,10 @@ __global__ __launch_bounds__(256) void layout_chunk_kernel(const int* __restrict
                                                            int k, int E, int n_chunks,
                                                            int* __restrict__ slot_row,
                                                            int* __restrict__ chunk_cnt,
-                                                           int* status) {
+                                                           int* status, int* scan_done) {
   extern __shared__ unsigned long long masks[];   // [4][E]
   const int s = blockIdx.y, c = blockIdx.x, tid = threadIdx.x;
+  if (s == 0 && c == 0 && tid == 0) *scan_done = 0;   // the next kernel's completion count
   const int lane = tid & 63, w = tid >> 6;
   for (int i = tid; i < 4 * E; i += 256) masks[i] = 0ull;
   __syncthreads();
@@ -266,10 +268,21 @@ __global__ __launch_bounds__(256) void layout_chunk_kernel(const int* __restrict
   }
 }
 
-// Per source: exclusive scan of the chunk counts of every expert, and source totals.
-__global__ __launch_bounds__(1024) void layout_source_scan_kernel(int* __restrict__ chunk_cnt,
-                                                                  int n_chunks, int E,
-                                                                  int* __restrict__ expert_counts) {
+// Per source (one block each): exclusive scan of the chunk counts of every expert, and the
+// source's expert totals. The last block to finish then scans across sources and experts:
+// src_base, expert_offsets (exclusive scan of expert totals within each window), dest_counts
+// and the capacity check; with plan args (the fused layer) it also plans the expert FFN from
+// the local experts' totals. Blocks release their counts with the counter increment (the
+// block barrier orders every wave's stores before thread 0's agent-scope release); the last
+// one acquires before it reads them.
+__global__ __launch_bounds__(1024) void layout_scan_kernel(int* __restrict__ chunk_cnt, int n_chunks,
+                                                           int n_src, int E, int W, int cap,
+                                                           int* __restrict__ expert_counts,
+                                                           int* __restrict__ src_base,
+                                                           int* __restrict__ expert_offsets,
+                                                           int* __restrict__ dest_counts, int* status,
+                                                           int* done, PlanArgs pa) {
+  __shared__ int tot[1024], s_m[1024], s_first[1024], s_rows, s_last;
   const int s = blockIdx.x;
   for (int e = threadIdx.x; e < E; e += blockDim.x) {
     int* col = chunk_cnt + static_cast<int64_t>(s) * n_chunks * E + e;
@@ -292,15 +305,14 @@ __global__ __launch_bounds__(1024) void layout_source_scan_kernel(int* __restric
     }
     expert_counts[static_cast<int64_t>(s) * E + e] = run;
   }
-}
-
-// Across sources and experts: src_base, expert_offsets (exclusive scan of expert totals
-// within each window), dest_counts and the capacity check.
-__global__ __launch_bounds__(1024) void layout_global_scan_kernel(
-    const int* __restrict__ expert_counts, int n_src, int E, int W, int cap,
-    int* __restrict__ src_base, int* __restrict__ expert_offsets, int* __restrict__ dest_counts,
-    int* status) {
-  __shared__ int tot[1024];
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    s_last = __hip_atomic_fetch_add(done, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) ==
+             static_cast<int>(gridDim.x) - 1;
+    if (s_last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  }
+  __syncthreads();
+  if (!s_last) return;
   for (int e = threadIdx.x; e < E; e += blockDim.x) {
     int run = 0;
     // eight sources' counts in flight at a time (one dependent load per source took longer)
@@ -323,6 +335,8 @@ __global__ __launch_bounds__(1024) void layout_global_scan_kernel(
     int d0 = (e / epw) * epw, off = 0;
     for (int x = d0; x < e; ++x) off += tot[x];
     expert_offsets[e] = off;
+    if (pa.meta && e >= pa.e_begin && e < pa.e_begin + pa.n_experts)
+      s_m[e - pa.e_begin] = max(0, min(tot[e], cap - off));
   }
   for (int d = threadIdx.x; d < W; d += blockDim.x) {
     int n = 0;
@@ -330,6 +344,7 @@ __global__ __launch_bounds__(1024) void layout_global_scan_kernel(
     dest_counts[d] = n;
     if (n > cap) set_status(status, XS_ECAPACITY);
   }
+  if (pa.meta) plan_rows(pa, 256, s_m, s_first, &s_rows);
 }
 
 // Every slot: final row = expert offset + source base + chunk base + rank in chunk;
@@ -357,48 +372,101 @@ __global__ __launch_bounds__(256) void layout_finalize_kernel(
 }
 
 // ------------------------------------------------------------------------------ dispatch
+// The rest of the layout, done by the dispatch launch of the fused layer (FinArgs with idx_all
+// set): the dispatch waves compute their own slots' final rows from the scan's bases (and
+// record them with the inverse map), blocks past the dispatch ones finalize every other
+// source's slots, and the last dispatch block to finish sets the windows' ready flags (done
+// set; the plan zeroed it).
+
+// Final row of slot (s, t, j) of expert e whose rank in its chunk is r.
+__device__ __forceinline__ int final_row(const FinArgs& fa, int E, int s, int t, int e, int r) {
+  return fa.expert_offsets[e] + fa.src_base[static_cast<int64_t>(s) * E + e] +
+         fa.chunk_base[(static_cast<int64_t>(s) * fa.n_chunks + t / kChunk) * E + e] + r;
+}
+
 // One wave per token (measured: a quarter row per wave, four waves per token, is slower).
 // Lanes hold up to 8 16-byte pieces of the row per round and store them into the k
 // destination rows.
 __global__ __launch_bounds__(256) void dispatch_kernel(const char* __restrict__ x, int64_t x_stride,
                                                        int nch, int T,
                                                        const int* __restrict__ idx,
-                                                       const int* __restrict__ slot_row, int k,
-                                                       int E, WinSet win, int* status) {
+                                                       int* __restrict__ slot_row, int k,
+                                                       int E, WinSet win, int* status, FinArgs fa) {
+  __shared__ int s_last;
   const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T) return;
   const int epw = E / win.n;
+  if (fa.idx_all && static_cast<int>(blockIdx.x) >= fa.n_disp_blocks) {
+    // finalize the other sources' slots
+    const int64_t per = static_cast<int64_t>(T) * k;
+    const int64_t n = static_cast<int64_t>(fa.n_src - 1) * per;
+    const int64_t step = static_cast<int64_t>(gridDim.x - fa.n_disp_blocks) * blockDim.x;
+    for (int64_t i0 = static_cast<int64_t>(blockIdx.x - fa.n_disp_blocks) * blockDim.x + threadIdx.x; i0 < n;
+         i0 += step) {
+      const int64_t i = i0 < fa.src * per ? i0 : i0 + per;
+      const int e = fa.idx_all[i];
+      if (e < 0 || e >= E) continue;
+      const int64_t st = i / k;
+      const int j = static_cast<int>(i - st * k);
+      const int s = static_cast<int>(st / T);
+      const int t = static_cast<int>(st - static_cast<int64_t>(s) * T);
+      const int r = final_row(fa, E, s, t, e, fa.slot_row_all[i]);
+      fa.slot_row_all[i] = r;
+      if (r < fa.cap) fa.row_src[static_cast<int64_t>(e / epw) * fa.cap + r] = (s << 24) | (t * k + j);
+    }
+    return;
+  }
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   // lane j < k resolves destination j; broadcast below with readlane
   char* my_dst = nullptr;
-  if (lane < k) {
-    int e = idx[static_cast<int64_t>(t) * k + lane];
-    int r = slot_row[static_cast<int64_t>(t) * k + lane];
+  if (t < T && lane < k) {
+    const int64_t si = static_cast<int64_t>(t) * k + lane;
+    int e = idx[si];
+    int r = slot_row[si];
     if (e < 0 || e >= E) {
       set_status(status, XS_EBADINPUT);
     } else {
+      if (fa.idx_all) {
+        r = final_row(fa, E, fa.src, t, e, r);
+        slot_row[si] = r;
+        if (r < fa.cap) fa.row_src[static_cast<int64_t>(e / epw) * fa.cap + r] = (fa.src << 24) | (t * k + lane);
+      }
       int d = e / epw;
       if (r < 0 || r >= win.cap[d]) set_status(status, XS_ECAPACITY);
       else my_dst = win.base[d] + static_cast<int64_t>(r) * win.stride[d];
     }
   }
-  const u32x4* src = reinterpret_cast<const u32x4*>(x + static_cast<int64_t>(t) * x_stride);
-  for (int c0 = 0; c0 < nch; c0 += 64 * 8) {
-    u32x4 v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      int c = c0 + u * 64 + lane;
-      if (c < nch) v[u] = src[c];
-    }
-    for (int j = 0; j < k; ++j) {
-      uint64_t p = __shfl(reinterpret_cast<uint64_t>(my_dst), j);
-      if (!p) continue;
-      u32x4* dst = reinterpret_cast<u32x4*>(p);
+  if (t < T) {
+    const u32x4* src = reinterpret_cast<const u32x4*>(x + static_cast<int64_t>(t) * x_stride);
+    for (int c0 = 0; c0 < nch; c0 += 64 * 8) {
+      u32x4 v[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         int c = c0 + u * 64 + lane;
-        if (c < nch) dst[c] = v[u];   // (measured: nontemporal stores here are slower)
+        if (c < nch) v[u] = src[c];
       }
+      for (int j = 0; j < k; ++j) {
+        uint64_t p = __shfl(reinterpret_cast<uint64_t>(my_dst), j);
+        if (!p) continue;
+        u32x4* dst = reinterpret_cast<u32x4*>(p);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          int c = c0 + u * 64 + lane;
+          if (c < nch) dst[c] = v[u];   // (measured: nontemporal stores here are slower)
+        }
+      }
+    }
+  }
+  if (!fa.done) return;
+  // the window signal: every block's stores are released at system scope (host-coherent
+  // windows included) before its count; the last block then sets the flags
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence_system();
+    s_last = atomicAdd(fa.done, 1) == fa.n_disp_blocks - 1;
+    if (s_last) {
+      __threadfence_system();
+      for (int d = 0; d < win.n; ++d)
+        if (win.flag[d]) __hip_atomic_store(win.flag[d], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
     }
   }
 }
@@ -534,11 +602,15 @@ extern "C" int xs_route_topk_softmax(const float* logits, int32_t T, int32_t E, 
   return xs_host::launch_status();
 }
 
-static int64_t layout_ws_bytes(int32_t n_src, int32_t T, int32_t E) {
+// The chunk counts, then 256 bytes holding the scan's completion count.
+static int64_t layout_chunk_bytes(int32_t n_src, int32_t T, int32_t E) {
   int64_t n_chunks = (static_cast<int64_t>(T) + kChunk - 1) / kChunk;
   int64_t b = static_cast<int64_t>(n_src) * n_chunks * E * 4;
   return (b + 255) & ~int64_t(255);
 }
+static int64_t layout_ws_bytes(int32_t n_src, int32_t T, int32_t E) { return layout_chunk_bytes(n_src, T, E) + 256; }
+
+__global__ void zero_int_kernel(int* p) { *p = 0; }
 
 extern "C" int xs_dispatch_layout_workspace_bytes(int32_t n_src, int32_t T, int32_t E,
                                                   int64_t* bytes) {
@@ -552,7 +624,7 @@ int dispatch_layout(const int32_t* topk_idx, int32_t n_src, int32_t T, int32_t k
                     int32_t W, int32_t cap, int32_t* expert_counts, int32_t* src_base,
                     int32_t* expert_offsets, int32_t* dest_counts, int32_t* slot_row,
                     int32_t* row_src, void* workspace, int64_t workspace_bytes,
-                    int32_t* dev_status, hipStream_t st) {
+                    int32_t* dev_status, hipStream_t st, const PlanArgs* plan) {
   if (!topk_idx || !expert_counts || !src_base || !expert_offsets || !dest_counts || !slot_row ||
       !row_src)
     return XS_EINVAL;
@@ -562,20 +634,22 @@ int dispatch_layout(const int32_t* topk_idx, int32_t n_src, int32_t T, int32_t k
   if (!workspace || workspace_bytes < layout_ws_bytes(n_src, T, E)) return XS_EWORKSPACE;
   const int n_chunks = (T + kChunk - 1) / kChunk;
   int* chunk = static_cast<int*>(workspace);
+  int* scan_done = reinterpret_cast<int*>(static_cast<char*>(workspace) + layout_chunk_bytes(n_src, T, E));
   if (n_chunks > 0) {
     hipLaunchKernelGGL(layout_chunk_kernel, dim3(n_chunks, n_src), dim3(256),
                        4 * E * sizeof(unsigned long long), st, topk_idx, T, k, E, n_chunks,
-                       slot_row, chunk, dev_status);
-    if (launch_status()) return XS_EHIP;
+                       slot_row, chunk, dev_status, scan_done);
+  } else {
+    hipLaunchKernelGGL(zero_int_kernel, dim3(1), dim3(1), 0, st, scan_done);
   }
-  hipLaunchKernelGGL(layout_source_scan_kernel, dim3(n_src), dim3(1024), 0, st, chunk, n_chunks, E,
-                     expert_counts);
   if (launch_status()) return XS_EHIP;
-  hipLaunchKernelGGL(layout_global_scan_kernel, dim3(1), dim3(1024), 0, st, expert_counts, n_src,
-                     E, W, cap, src_base, expert_offsets, dest_counts, dev_status);
+  hipLaunchKernelGGL(layout_scan_kernel, dim3(n_src), dim3(1024), 0, st, chunk, n_chunks, n_src, E, W,
+                     cap, expert_counts, src_base, expert_offsets, dest_counts, dev_status, scan_done,
+                     plan ? *plan : PlanArgs{});
   if (launch_status()) return XS_EHIP;
+  // with a plan (the fused layer), the dispatch launch finalizes the rows (FinArgs)
   const int64_t n = static_cast<int64_t>(n_src) * T * k;
-  if (n > 0) {
+  if (n > 0 && !plan) {
     int blocks = static_cast<int>(std::min<int64_t>((n + 255) / 256, 4096));
     hipLaunchKernelGGL(layout_finalize_kernel, dim3(blocks), dim3(256), 0, st, topk_idx, n_src, T,
                        k, E, W, cap, n_chunks, chunk, src_base, expert_offsets, slot_row, row_src);
@@ -586,20 +660,36 @@ int dispatch_layout(const int32_t* topk_idx, int32_t n_src, int32_t T, int32_t k
 
 // Token rows of row_bytes bytes (a multiple of 16), x_stride apart, into the window rows of
 // their slots.
+// With fin (the fused layer), the same launch finishes the layout (FinArgs) and, when the
+// windows have flags, signals them from its last dispatch block.
 int dispatch_rows(const void* x, int64_t x_stride, int32_t row_bytes, int32_t T,
                   const int32_t* topk_idx, const int32_t* slot_row, int32_t k, int32_t E,
-                  const WinSet& ws, int32_t* dev_status, hipStream_t st) {
-  if (T == 0) return signal_windows(ws, st);
-  hipLaunchKernelGGL(dispatch_kernel, dim3((T + 3) / 4), dim3(256), 0, st, static_cast<const char*>(x),
-                     x_stride, row_bytes / 16, T, topk_idx, slot_row, k, E, ws, dev_status);
-  if (launch_status()) return XS_EHIP;
-  return signal_windows(ws, st);
+                  const WinSet& ws, int32_t* dev_status, hipStream_t st, const FinArgs* fin) {
+  FinArgs fa{};
+  const int nd = (T + 3) / 4;
+  int nf = 0;
+  if (fin) {
+    fa = *fin;
+    fa.n_disp_blocks = nd;
+    const int64_t n_other = static_cast<int64_t>(fa.n_src - 1) * T * k;
+    nf = static_cast<int>(std::min<int64_t>((n_other + 255) / 256, 4096));
+    bool any = false;
+    for (int d = 0; d < ws.n; ++d) any |= ws.flag[d] != nullptr;
+    if (!any || nd == 0) fa.done = nullptr;
+  }
+  if (nd + nf > 0) {
+    hipLaunchKernelGGL(dispatch_kernel, dim3(nd + nf), dim3(256), 0, st, static_cast<const char*>(x),
+                       x_stride, row_bytes / 16, T, topk_idx, const_cast<int32_t*>(slot_row), k, E, ws,
+                       dev_status, fa);
+    if (launch_status()) return XS_EHIP;
+  }
+  return fa.done ? XS_OK : signal_windows(ws, st);
 }
 
 int dispatch(const void* x, int32_t T, int32_t H, const int32_t* topk_idx, const int32_t* slot_row,
              int32_t k, int32_t E, const WinSet& ws, int32_t* dev_status, hipStream_t st) {
   return dispatch_rows(x, static_cast<int64_t>(H) * 2, H * 2, T, topk_idx, slot_row, k, E, ws,
-                       dev_status, st);
+                       dev_status, st, nullptr);
 }
 
 int combine_reduce(const void* cbuf, int64_t cstride, const float* w, int32_t T, int32_t k,
@@ -620,7 +710,7 @@ extern "C" int xs_dispatch_layout(const int32_t* topk_idx, int32_t n_src, int32_
                                   void* stream) {
   return xs_host::dispatch_layout(topk_idx, n_src, T, k, E, W, cap, expert_counts, src_base,
                                   expert_offsets, dest_counts, slot_row, row_src, workspace,
-                                  workspace_bytes, dev_status, static_cast<hipStream_t>(stream));
+                                  workspace_bytes, dev_status, static_cast<hipStream_t>(stream), nullptr);
 }
 
 extern "C" int xs_dispatch(const void* x, int32_t T, int32_t H, const int32_t* topk_idx,
@@ -648,7 +738,7 @@ extern "C" int xs_dispatch_rows(const void* rows, int64_t row_stride, int32_t ro
   int rc = xs_host::make_winset(win, W, row_bytes, &ws);
   if (rc) return rc;
   return xs_host::dispatch_rows(rows, row_stride, row_bytes, T, topk_idx, slot_row, k, E, ws, dev_status,
-                                static_cast<hipStream_t>(stream));
+                                static_cast<hipStream_t>(stream), nullptr);
 }
 
 extern "C" int xs_combine_reduce(const void* cbuf, int64_t cbuf_stride_bytes, const float* topk_w,

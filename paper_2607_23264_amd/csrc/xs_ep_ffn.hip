@@ -27,6 +27,7 @@
 #include <mutex>
 
 #include "xs_gemm_mx.hpp"
+#include "xs_plan.hpp"
 
 namespace xs {
 
@@ -69,21 +70,15 @@ struct EpArgs {
   xs_trace tr;
 };
 
-// Per-expert row counts (clipped to the rows that fit in the window), scheduler rows,
-// Expert-Wave boundaries; clears the readiness counters. One block.
+// Per-expert row counts (clipped to the rows that fit in the window), then the plan. One block.
 __global__ __launch_bounds__(1024) void ep_plan_kernel(const int* __restrict__ expert_counts,
-                                                       int n_src, int E, int e_begin,
-                                                       int n_experts,
+                                                       int n_src, int E,
                                                        const int* __restrict__ expert_offsets,
-                                                       int cap, int P1, int P2, int wave_tiles,
-                                                       int* meta, int* row_expert, int* exp_m,
-                                                       int* exp_rowfirst, int* exp_hrow,
-                                                       int* wave_pos, int* wave_row,
-                                                       int* l1_done) {
+                                                       PlanArgs pa) {
   __shared__ int s_m[1024], s_first[1024], s_rows;
   const int i = threadIdx.x;
-  if (i < n_experts) {
-    const int e = e_begin + i;
+  if (i < pa.n_experts) {
+    const int e = pa.e_begin + i;
     const int off = expert_offsets[e];
     int m = 0;
     // eight sources' counts in flight at a time
@@ -94,48 +89,9 @@ __global__ __launch_bounds__(1024) void ep_plan_kernel(const int* __restrict__ e
 #pragma unroll
       for (int u = 0; u < 8; ++u) m += v[u];
     }
-    s_m[i] = max(0, min(m, cap - off));
+    s_m[i] = max(0, min(m, pa.cap - off));
   }
-  __syncthreads();
-  if (i == 0) {
-    int rows = 0, hrow = 0, nw = 0, wl1 = 0;
-    wave_row[0] = 0;
-    wave_pos[0] = 0;
-    for (int x = 0; x < n_experts; ++x) {
-      const int mt = (s_m[x] + kBM - 1) / kBM;
-      exp_m[x] = s_m[x];
-      exp_rowfirst[x] = rows;
-      s_first[x] = rows;
-      exp_hrow[x] = hrow;
-      rows += mt;
-      hrow += s_m[x];
-      wl1 += mt * P1;
-      if (wl1 >= wave_tiles && rows > wave_row[nw]) {
-        ++nw;
-        wave_row[nw] = rows;
-        wave_pos[nw] = rows * (P1 + P2);
-        wl1 = 0;
-      }
-    }
-    if (rows > wave_row[nw]) {
-      ++nw;
-      wave_row[nw] = rows;
-      wave_pos[nw] = rows * (P1 + P2);
-    }
-    meta[0] = rows;
-    meta[1] = nw;
-    meta[2] = rows * (P1 + P2);
-    meta[3] = hrow;
-    meta[8] = 0;   // claim counters (dynamic claiming)
-    meta[9] = 0;
-    s_rows = rows;
-  }
-  __syncthreads();
-  if (i < n_experts) {
-    const int mt = (s_m[i] + kBM - 1) / kBM;
-    for (int p = s_first[i]; p < s_first[i] + mt; ++p) row_expert[p] = i;
-  }
-  for (int p = i; p < s_rows; p += blockDim.x) l1_done[p] = 0;
+  plan_rows(pa, kBM, s_m, s_first, &s_rows);
 }
 
 // Rows [m0, m0 + rows) of local expert x covered by scheduler row p. The expert's m rows fall
@@ -789,9 +745,9 @@ using namespace xs;
 namespace xs_host {
 int dispatch_layout(const int32_t*, int32_t, int32_t, int32_t, int32_t, int32_t, int32_t, int32_t*,
                     int32_t*, int32_t*, int32_t*, int32_t*, int32_t*, void*, int64_t, int32_t*,
-                    hipStream_t);
+                    hipStream_t, const PlanArgs*);
 int dispatch_rows(const void*, int64_t, int32_t, int32_t, const int32_t*, const int32_t*, int32_t,
-                  int32_t, const WinSet&, int32_t*, hipStream_t);
+                  int32_t, const WinSet&, int32_t*, hipStream_t, const FinArgs*);
 int dispatch(const void*, int32_t, int32_t, const int32_t*, const int32_t*, int32_t, int32_t,
              const WinSet&, int32_t*, hipStream_t);
 int combine_reduce(const void*, int64_t, const float*, int32_t, int32_t, int32_t, void*,
@@ -830,7 +786,8 @@ EpWorkspace ep_workspace(const xs_ep_layer* L) {
   EpWorkspace w{};
   const int64_t n_chunks = (static_cast<int64_t>(L->T) + 255) / 256;
   w.layout_off = 0;
-  w.layout_bytes = align_up(static_cast<int64_t>(L->n_src) * n_chunks * L->E * 4);
+  // the chunk counts and the scan's completion count (xs_dispatch_layout_workspace_bytes)
+  w.layout_bytes = align_up(static_cast<int64_t>(L->n_src) * n_chunks * L->E * 4) + 256;
   const int64_t max_rows = static_cast<int64_t>(n_cwin_of(L)) * L->cap / kBM + L->n_experts + 1;
   w.max_rows = max_rows;
   int64_t o = w.layout_bytes;
@@ -950,13 +907,17 @@ int fill_args(const xs_ep_layer* L, void* workspace, EpArgs* a, WinSet* dws, Win
   return XS_OK;
 }
 
+PlanArgs plan_args(const xs_ep_layer* L, const EpArgs& a, int wave_tiles) {
+  return PlanArgs{L->e_begin, L->n_experts, L->cap, a.P1, a.P2, wave_tiles,
+                  const_cast<int*>(a.meta), const_cast<int*>(a.row_expert),
+                  const_cast<int*>(a.exp_m), const_cast<int*>(a.exp_rowfirst),
+                  const_cast<int*>(a.exp_hrow), const_cast<int*>(a.wave_pos),
+                  const_cast<int*>(a.wave_row), a.l1_done};
+}
+
 int launch_plan(const xs_ep_layer* L, const EpArgs& a, int wave_tiles, hipStream_t st) {
   hipLaunchKernelGGL(ep_plan_kernel, dim3(1), dim3(1024), 0, st, L->expert_counts, L->n_src, L->E,
-                     L->e_begin, L->n_experts, L->expert_offsets, L->cap, a.P1, a.P2, wave_tiles,
-                     const_cast<int*>(a.meta), const_cast<int*>(a.row_expert),
-                     const_cast<int*>(a.exp_m), const_cast<int*>(a.exp_rowfirst),
-                     const_cast<int*>(a.exp_hrow), const_cast<int*>(a.wave_pos),
-                     const_cast<int*>(a.wave_row), a.l1_done);
+                     L->expert_offsets, plan_args(L, a, wave_tiles));
   return xs_host::launch_status();
 }
 
@@ -1145,12 +1106,21 @@ static int fused_ep_layer(const xs_ep_layer* L, const xs_pacing* pacing, const x
                              L->topk_idx, L->topk_w, stream);
   if (rc) return rc;
   if ((rc = record_event(L, XS_EV_LAYOUT, st))) return rc;
+  // The layout's scan launch also plans the expert FFN, and the dispatch launch finishes the
+  // layout's rows and signals the dispatch windows (one launch each fewer than the
+  // standalone calls, and no plan launch).
+  const int grid = xs_host::persistent_grid(pacing ? pacing->max_producers : 0);
+  const int wave_tiles = pacing && pacing->wave_tiles > 0 ? pacing->wave_tiles : grid;
+  const PlanArgs pa = plan_args(L, a, wave_tiles);
+  char* layout_ws = static_cast<char*>(workspace) + w.layout_off;
   rc = xs_host::dispatch_layout(L->topk_idx, L->n_src, L->T, L->k, L->E, L->W, L->cap,
                                 L->expert_counts, L->src_base, L->expert_offsets, L->dest_counts,
-                                L->slot_row, L->row_src, static_cast<char*>(workspace) + w.layout_off,
-                                w.layout_bytes, dev_status, st);
+                                L->slot_row, L->row_src, layout_ws, w.layout_bytes, dev_status, st, &pa);
   if (rc) return rc;
   const int64_t so = static_cast<int64_t>(L->src) * L->T * L->k;
+  const FinArgs fin{L->src, L->n_src, L->cap, (L->T + 255) / 256, 0, L->topk_idx, L->slot_row,
+                    reinterpret_cast<const int*>(layout_ws), L->src_base, L->expert_offsets, L->row_src,
+                    const_cast<int*>(a.meta) + 11};
   if ((rc = record_event(L, XS_EV_DISPATCH, st))) return rc;
   if (is_mx(L)) {
     // quantize this source's token rows once (codes, then scales, in each staged row) and
@@ -1160,10 +1130,10 @@ static int fused_ep_layer(const xs_ep_layer* L, const xs_pacing* pacing, const x
     rc = xs_quantize_mx(L->x, L->T, L->H, L->H, XS_FMT_E4M3, xq, rb, xq + L->H, rb, stream);
     if (rc) return rc;
     rc = xs_host::dispatch_rows(xq, rb, static_cast<int32_t>(rb), L->T, L->topk_idx + so, L->slot_row + so,
-                                L->k, L->E, dws, dev_status, st);
+                                L->k, L->E, dws, dev_status, st, &fin);
   } else {
-    rc = xs_host::dispatch(L->x, L->T, L->H, L->topk_idx + so, L->slot_row + so, L->k, L->E, dws,
-                           dev_status, st);
+    rc = xs_host::dispatch_rows(L->x, static_cast<int64_t>(L->H) * 2, L->H * 2, L->T, L->topk_idx + so,
+                                L->slot_row + so, L->k, L->E, dws, dev_status, st, &fin);
   }
   if (rc) return rc;
   a.status = dev_status;
@@ -1174,10 +1144,6 @@ static int fused_ep_layer(const xs_ep_layer* L, const xs_pacing* pacing, const x
                        n_cwin_of(L), 1);
     if (xs_host::launch_status()) return XS_EHIP;
   } else {
-    const int grid = xs_host::persistent_grid(pacing ? pacing->max_producers : 0);
-    const int wave_tiles = pacing && pacing->wave_tiles > 0 ? pacing->wave_tiles : grid;
-    rc = launch_plan(L, a, wave_tiles, st);
-    if (rc) return rc;
     if ((rc = record_event(L, XS_EV_FFN, st))) return rc;
     rc = run_ffn(L, a, 3, 1, pacing, trace, dev_status, st);
     if (rc) return rc;
