@@ -444,7 +444,8 @@ int xs_scatter_copy(const void* c, int64_t ldc, int32_t M, int32_t N, const xs_s
  * online softmax in fp32 and bf16 probabilities for the second product.
  *   q, k, v  device bf16 [heads][M][head_dim]; head_dim must be 128.
  *   scale    0 = 1 / sqrt(head_dim).
- *   M        multiple of 128; with windows, M / W must be a multiple of 128 (a tile never
+ *   M        multiple of 128, at most 8,388,480 (one head's K or V rows within a 2 GiB
+ *            buffer range); with windows, M / W must be a multiple of 128 (a tile never
  *            straddles two destinations).
  * Modes:
  *   XS_ATTN_LOCAL    output o, device bf16 [heads][M][head_dim] ("FA-only").
@@ -457,7 +458,7 @@ int xs_scatter_copy(const void* c, int64_t ldc, int32_t M, int32_t N, const xs_s
  *                    waits until they are visible at system scope before its next Q-loop:
  *                    the completion-coupled issuer the paper argues against (Sec. 4.4, Fig. 7),
  *                    kept as the measured counterfactual.
- * max_producers caps the persistent grid (0 = two workgroups per CU). The optional trace
+ * max_producers caps the persistent grid (0 = three workgroups per CU). The optional trace
  * records one kind-4 record per output tile: rec[1] tile start, rec[2] end of its Q-loop,
  * rec[3] after its stores were issued. q, k, v and o are 16-byte aligned; windows as for the
  * other window calls (16-byte aligned base and row stride, stride >= heads * head_dim * 2,

@@ -62,7 +62,7 @@ def _timed(fns, reps, rounds=3):
 
 
 def default_grid() -> int:
-    return 2 * torch.cuda.get_device_properties(0).multi_processor_count
+    return 3 * torch.cuda.get_device_properties(0).multi_processor_count
 
 
 class Share:

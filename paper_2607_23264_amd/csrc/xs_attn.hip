@@ -18,11 +18,16 @@
 // lane that receives column d0 + i gets the four 16-bit values at rows kv0 .. kv0 + 3 when
 // lane j of the group points at row kv0 + j / 4, columns d0 + 4 (j % 4) .. + 3.
 //
-// LDS: per stage one K tile and one V tile of [64][128] bf16 (rows of 256 B = 16 pieces of
-// 16 B), two stages (64 KiB), two workgroups per CU. K tiles store logical piece p of row r at
-// p ^ (r & 15) (a ds_read_b128 phase reads one piece of 16 consecutive rows); V tiles at
+// LDS: two K slots and one V slot, each a tile of [64][128] bf16 (rows of 256 B = 16 pieces of
+// 16 B): 48 KiB, so that three workgroups share a CU (three waves per SIMD; two left the
+// matrix pipes idle while both waves ran their softmax). K tiles store logical piece p of row r
+// at p ^ (r & 15) (a ds_read_b128 phase reads one piece of 16 consecutive rows); V tiles at
 // p ^ 4 (r & 3) (a transposing read touches four consecutive rows, four pieces each). Both
-// tiles arrive by direct global -> LDS loads with the swizzle applied on the global side.
+// arrive by direct buffer -> LDS loads with the swizzle applied on the global side. Per K/V
+// tile j: S' from K slot j % 2, a barrier, K tile j + 2 into that slot; the softmax; V tile j
+// waited for and a barrier; O' from the V slot; K tile j + 1 waited for, a barrier, V tile
+// j + 1 into the V slot. K tiles are loaded about one and a half tiles ahead, V tiles one S'
+// and softmax ahead.
 //
 // Epilogue: O = O' / rowsum, packed to bf16 with the hardware conversion and stored four
 // columns per 8-byte store, either to the local output or, fused, into the destination
@@ -37,9 +42,7 @@ namespace xs {
 
 namespace attn {
 
-typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) char lds_char;
-typedef const __attribute__((address_space(1))) void glob_void;
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
@@ -50,12 +53,30 @@ constexpr int kBQ = 128;                   // queries per output tile (4 waves x
 constexpr int kBKV = 64;                   // keys per K/V tile
 constexpr int kRowBytes = kD * 2;          // 256
 constexpr int kTileBytes = kBKV * kRowBytes;   // 16 KiB
-constexpr int kStage = 2 * kTileBytes;     // K + V
-constexpr int kLds = 2 * kStage;           // two stages: 64 KiB
+constexpr int kLds = 3 * kTileBytes;       // two K slots and one V slot: 48 KiB
 constexpr int kThreads = 256;
 // a query's running maximum is raised (and its sums rescaled) only when a block's maximum
 // exceeds it by more than this many powers of two; until then probabilities stay <= 2^8
 constexpr float kRescaleSlack = 8.f;
+constexpr int kBufDword3 = 0x00020000;     // raw buffer resource: 32-bit data, no swizzle
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+// A raw buffer descriptor over [base, base + bytes): 32-bit data, no stride, no swizzle.
+__device__ __forceinline__ v4i buffer_rsrc(const void* base, int bytes) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  const v4i r = {static_cast<int>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b))),
+                 static_cast<int>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b >> 32)) & 0xFFFF),
+                 bytes, kBufDword3};
+  return r;
+}
+// One 16-byte piece per lane from the buffer at voff + soff into LDS at dst + 16 lane. Issued
+// from assembly so that the compiler does not count it: it would otherwise wait for every
+// load in flight before each transposing LDS read (it cannot tell the two apart), and the
+// kernel orders these loads itself, with vmcnt waits and workgroup barriers.
+__device__ __forceinline__ void load_lds16(v4i rsrc, uint32_t voff, int soff, const lds_char* dst) {
+  const uint32_t m0v = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(dst));
+  asm volatile("buffer_load_dwordx4 %0, %1, %2 offen lds" :: "v"(voff), "s"(rsrc), "s"(soff), "{m0}"(m0v) : "memory");
+}
 
 __device__ __forceinline__ int k_swz(int r) { return r & 15; }
 __device__ __forceinline__ int v_swz(int r) { return 4 * (r & 3); }
@@ -73,6 +94,7 @@ struct Args {
 };
 
 __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+__device__ __forceinline__ void wait_vm4() { __builtin_amdgcn_s_waitcnt(0x0F74); }
 
 // The two halves of a wave hold the two key halves of the same 32 queries: lanes l and
 // l + 32 combine through one half swap (v_permlane32_swap: a's upper half <-> b's lower half),
@@ -96,7 +118,7 @@ __device__ __forceinline__ float add_halves(float x) {
   return h.x + h.y;
 }
 
-__global__ __launch_bounds__(kThreads, 2) void attn_kernel(Args a) {
+__global__ __launch_bounds__(kThreads, 3) void attn_kernel(Args a) {
   __shared__ __attribute__((aligned(16))) char lds_raw[kLds];
   lds_char* const lds = (lds_char*)lds_raw;
   const int tid = threadIdx.x;
@@ -146,16 +168,20 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(Args a) {
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk)
       qf[kk] = *reinterpret_cast<const bf16x8*>(a.q + hoff + static_cast<int64_t>(qrow) * kD + 16 * kk + 8 * up);
-    auto issue = [&](int j) {
-      lds_char* st = lds + (j & 1) * kStage;
-      const char* kb = kh + static_cast<int64_t>(j) * kTileBytes;
-      const char* vb = vh + static_cast<int64_t>(j) * kTileBytes;
+    const v4i krs = buffer_rsrc(kh, a.M * kRowBytes);
+    const v4i vrs = buffer_rsrc(vh, a.M * kRowBytes);
+    // K tile j into K slot j % 2, V tile j into the V slot: four 1 KiB pieces per wave each
+    auto issue_k = [&](int j) {
+      lds_char* st = lds + (j & 1) * kTileBytes;
+      const int so = j * kTileBytes;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int off = (4 * i + w) * 1024;
-        __builtin_amdgcn_global_load_lds((glob_void*)(kb + ko[i]), (lds_void*)(st + off), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((glob_void*)(vb + vo[i]), (lds_void*)(st + kTileBytes + off), 16, 0, 0);
-      }
+      for (int i = 0; i < 4; ++i) load_lds16(krs, ko[i], so, st + (4 * i + w) * 1024);
+    };
+    auto issue_v = [&](int j) {
+      lds_char* st = lds + 2 * kTileBytes;
+      const int so = j * kTileBytes;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) load_lds16(vrs, vo[i], so, st + (4 * i + w) * 1024);
     };
     f32x16 oacc[4];
 #pragma unroll
@@ -163,13 +189,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(Args a) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) oacc[db][e] = 0.f;
     float m = -INFINITY, l = 0.f;
-    issue(0);
+    issue_k(0);
+    issue_v(0);
+    if (nkv > 1) issue_k(1);
     wait_vm0();
-    __syncthreads();
-    if (nkv > 1) issue(1);
+    asm volatile("s_barrier" ::: "memory");
     for (int j = 0; j < nkv; ++j) {
-      lds_char* const ks = lds + (j & 1) * kStage;
-      lds_char* const vs = ks + kTileBytes;
+      lds_char* const ks = lds + (j & 1) * kTileBytes;
+      lds_char* const vs = lds + 2 * kTileBytes;
       // S' = K Q^T over two 32-key blocks
       f32x16 sacc[2];
 #pragma unroll
@@ -182,11 +209,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(Args a) {
           sacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], sacc[b], 0, 0, 0);
         }
       }
-      // The softmax and the P^T permutation run at raised wave priority, so that the SIMD's other
-      // wave (of another workgroup) fills the matrix pipe around them rather than ahead of them
-      // (measured: -4 % at M = 32768, about -1 % at 16384; raising it over the products instead
-      // was slower).
-      __builtin_amdgcn_s_setprio(1);
+      // every wave is done with K slot j % 2: K tile j + 2 goes there
+      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      const bool k2 = j + 2 < nkv;
+      if (k2) issue_k(j + 2);
       // online softmax in base 2 for query lane % 32
       float mx = fmaxf(sacc[0][0], sacc[0][1]);
 #pragma unroll
@@ -231,7 +257,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(Args a) {
         const u32x4 pv = {x[0], y[0], x[1], y[1]};
         pf[s] = __builtin_bit_cast(bf16x8, pv);
       }
-      __builtin_amdgcn_s_setprio(0);
+      // V tile j has landed in every wave's share (only K tile j + 2 may still be in flight)
+      if (k2) wait_vm4(); else wait_vm0();
+      asm volatile("s_barrier" ::: "memory");
       // O' += V^T P^T
 #pragma unroll
       for (int s = 0; s < 4; ++s)
@@ -243,9 +271,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(Args a) {
           oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[s], oacc[db], 0, 0, 0);
         }
       if (j + 1 < nkv) {
-        wait_vm0();          // this wave's loads of tile j + 1 have landed
-        __syncthreads();     // every wave's have, and tile j is no longer read
-        if (j + 2 < nkv) issue(j + 2);
+        // K tile j + 1 has landed in every wave's share, and no wave reads the V slot any more
+        if (k2) wait_vm4(); else wait_vm0();
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        issue_v(j + 1);
       }
     }
     const uint64_t t1 = a.tr.buf ? wall_ticks() : 0;
@@ -273,8 +302,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(Args a) {
     if (a.mode == XS_ATTN_WINDOWS_COUPLED) __threadfence_system();
     // the next tile's loads overwrite both stages: every wave must be done with them (the
     // stores above may still drain)
-    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
-    __builtin_amdgcn_s_barrier();
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     if (a.tr.buf && tid == 0) {
       uint32_t i = atomicAdd(a.tr.count, 1u);
       if (static_cast<int64_t>(i) < a.tr.capacity) {
@@ -333,7 +361,7 @@ extern "C" int xs_attention(const xs_attn* A, int32_t mode, const xs_trace* trac
   if (mode != XS_ATTN_LOCAL && mode != XS_ATTN_WINDOWS && mode != XS_ATTN_WINDOWS_COUPLED) return XS_EINVAL;
   const auto misaligned = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) != 0; };
   if (misaligned(A->q) || misaligned(A->k) || misaligned(A->v)) return XS_EINVAL;
-  if (A->head_dim != attn::kD || A->M % attn::kBQ) return XS_EUNSUPPORTED;
+  if (A->head_dim != attn::kD || A->M % attn::kBQ || A->M > INT32_MAX / attn::kRowBytes) return XS_EUNSUPPORTED;
   attn::Args a{};
   a.q = static_cast<const uint16_t*>(A->q);
   a.k = static_cast<const uint16_t*>(A->k);
@@ -356,7 +384,7 @@ extern "C" int xs_attention(const xs_attn* A, int32_t mode, const xs_trace* trac
     if (a.chunk % attn::kBQ) return XS_EUNSUPPORTED;
   }
   const int tiles = A->heads * (A->M / attn::kBQ);
-  int grid = A->max_producers > 0 ? A->max_producers : 2 * xs_host::persistent_grid(0);
+  int grid = A->max_producers > 0 ? A->max_producers : 3 * xs_host::persistent_grid(0);
   if (grid > tiles) grid = tiles;
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipLaunchKernelGGL(attn::attn_kernel, dim3(grid), dim3(attn::kThreads), 0, st, a);

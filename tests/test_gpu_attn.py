@@ -189,8 +189,9 @@ def test_bad_arguments_are_rejected():
     o = torch.zeros_like(q)
     ok = _desc(heads, M, q, q, q, o=o)
     X.check(X.xs_attention(ok, X.XS_ATTN_LOCAL, None, _stream()))
-    # head_dim other than 128, M not a multiple of 128
-    for hd, m in ((64, 256), (128, 200)):
+    # head_dim other than 128, M not a multiple of 128, M past the kernel's buffer range
+    # (rejected before any launch)
+    for hd, m in ((64, 256), (128, 200), (128, 8388608)):
         a = _desc(heads, m, q, q, q, o=o)
         a.head_dim = hd
         assert X.xs_attention(a, X.XS_ATTN_LOCAL, None, _stream()) == X.XS_EUNSUPPORTED
