@@ -182,6 +182,27 @@ def test_full_size_every_row():
         assert_close(o[h:h + 1], ref64, f"attention M=8192 head {h}")
 
 
+@pytest.mark.parametrize("cfg", [synth.ATTN_UP_16K, synth.ATTN_UP_32K], ids=lambda c: c.name)
+def test_long_sequences_at_the_default_grid(cfg):
+    # the FA-only launch the benchmark times (default grid: several output tiles per workgroup,
+    # a last round with idle slots) stores the same bits as a 100-workgroup grid, in which every
+    # workgroup walks many tiles; sampled rows of every head (the first row of each of 16
+    # tiles, the last tile, the first and last rows) against the fp64 oracle
+    print(f"[attn long] {cfg.name}", flush=True)
+    inp = synth.attn_inputs(cfg, 0)
+    q, k, v = inp["q"], inp["k"], inp["v"]
+    o = _local(q, k, v)
+    assert np.array_equal(o, _local(q, k, v, max_producers=100))
+    M = cfg.M
+    rng = np.random.default_rng(7)
+    for h in range(cfg.heads):
+        tiles = rng.choice(M // 128, 16, replace=False)
+        rows = np.unique(np.concatenate([tiles * 128, np.arange(M - 128, M, 8), [0, M - 1],
+                                         rng.integers(0, M, 16)]))
+        ref64, _ = oa.attention(q[h:h + 1, rows], k[h:h + 1], v[h:h + 1])
+        assert_close(o[h:h + 1, rows], ref64, f"attention M={M} head {h} sampled rows")
+
+
 def test_bad_arguments_are_rejected():
     X = xs()
     heads, M = 1, 256
